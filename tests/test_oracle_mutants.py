@@ -1,0 +1,129 @@
+"""The pins have teeth: plausible slips planted in a copy of the oracle are caught.
+
+Each mutant is a one-line textual change to oracle/pld_oracle.c (a shifted
+artifact row, the query taken at the last token, a reversed tie rule, ...),
+compiled with gcc into a temporary library.  A compact run of the same pins
+as test_oracle_pins.py / test_golden_oracle.py must fail on every mutant and
+pass on the unmodified source.  CPU only; the mistakes live in the oracle.
+"""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import brute
+import golden_cases
+import oracle
+import synth
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "pld_oracle.c")
+
+MUTANTS = {
+    "artifact row j instead of j-1": ("const uint16_t *h = Hb + (j - 1) * h_row_stride;",
+                                      "const uint16_t *h = Hb + j * h_row_stride;"),
+    "query row T-1 instead of T-2": ("seq_ok ? Hb + (T - 2) * h_row_stride : Hb;",
+                                     "seq_ok ? Hb + (T - 1) * h_row_stride : Hb;"),
+    "tie goes to the earliest position": ("(v == bs && pos[c] > bj)", "(v == bs && pos[c] < bj)"),
+    "verify takes the last maximum": ("if (v == 0 || z > best) {", "if (v == 0 || z >= best) {"),
+    "shortest n-gram first": ("for (int n = ngram_max; n >= ngram_min; --n) {",
+                              "for (int n = ngram_min; n <= ngram_max; ++n) {"),
+    "last token counted as its own occurrence": ("for (int64_t j = lo; j <= T - 2; ++j) {",
+                                                 "for (int64_t j = lo; j <= T - 1; ++j) {"),
+    "draft truncation off by one": ("L = T - 1 - j;", "L = T - j;"),
+    "attention key j instead of j-1": ("a_row_stride + (j - 1)];", "a_row_stride + j];"),
+    "norm without the square": ("hh += hv * hv;", "hh += hv;"),
+    "accept counts one past the mismatch": ("a = i;\n                break;", "a = i + 1;\n                break;"),
+    "threshold taken as >=": ("!(v > threshold)", "!(v >= threshold)"),
+}
+
+
+def _pins_pass():
+    """A compact run of the pins; True when every check holds."""
+    try:
+        # golden fixtures
+        fx, toks, lens, H, A = golden_cases.load("fig1_overview.json")
+        ex = fx["expected"]
+        cp, cc, nu = oracle.find(toks, lens, 1, 1)
+        if list(cp[0, :cc[0]]) != ex["cand_pos"]:
+            return False
+        bits = synth.f32_to_bf16_bits(H)
+        sc, bp, bs = oracle.rank_hidden(bits, lens, cp, cc)
+        if bp[0] != ex["hidden_best_pos"] or not np.allclose(sc[0, :2], ex["hidden_scores"]):
+            return False
+        sc, bp, bs = oracle.rank_attn(A, lens, cp, cc, oracle.AGG_SUM)
+        if bp[0] != ex["attn_sum_best_pos"]:
+            return False
+        for K in (3, 12):
+            dr, dl = oracle.emit(toks, lens, np.array([10], np.int32), K)
+            if list(dr[0]) != ex[f"draft_K{K}"]:
+                return False
+        for vc in fx["verify_cases"]:
+            Z, dr, dl = golden_cases.verify_case(vc)
+            acc, out, cnt, ra = oracle.verify(Z, dr, dl)
+            if acc[0] != vc["expected"]["accept_len"] or list(out[0]) != vc["expected"]["out_tokens"]:
+                return False
+        fx, toks, lens, H, _ = golden_cases.load("fig3_newline.json")
+        for key, (a, b) in (("n1", (1, 1)), ("n1to4", (1, 4)), ("n7to8", (7, 8))):
+            cp, cc, nu = oracle.find(toks, lens, a, b)
+            if list(cp[0, :cc[0]]) != fx["expected"][key]["cand_pos"]:
+                return False
+        # brute force on random tiny inputs
+        rng = np.random.default_rng(0)
+        for _ in range(60):
+            T = int(rng.integers(2, 30))
+            x = rng.integers(0, 3, size=(1, T)).astype(np.int32)
+            cp, cc, nu = oracle.find(x, np.array([T], np.int32), 1, 3)
+            P, n = brute.find(x[0], T, 1, 3)
+            if list(cp[0, :cc[0]]) != P or nu[0] != n:
+                return False
+        # identical rows tie -> the most recent occurrence
+        Hr = rng.standard_normal((12, 8)).astype(np.float32)
+        Hr[2] = Hr[6]
+        Hr[10] = Hr[6] + np.float32(0.01)
+        cpos = np.full((1, 12), -1, np.int32)
+        cpos[0, :2] = [3, 7]
+        _, bp, bs = oracle.rank_hidden(synth.f32_to_bf16_bits(Hr)[None], np.array([12], np.int32),
+                                       cpos, np.array([2], np.int32))
+        if bp[0] != 7:
+            return False
+        # threshold: the top score itself is not eligible
+        sc, bp, bs = oracle.rank_hidden(synth.f32_to_bf16_bits(Hr)[None],
+                                        np.array([12], np.int32), cpos, np.array([2], np.int32),
+                                        threshold=float(bs[0]))
+        if bp[0] != -1:
+            return False
+        return True
+    except Exception:
+        return False
+
+
+def _with_lib(path):
+    saved = oracle._lib
+    oracle._lib = oracle.load_library(path)
+    try:
+        return _pins_pass()
+    finally:
+        oracle._lib = saved
+
+
+def _build(src_text, tmp_path, name):
+    c = tmp_path / f"{name}.c"
+    so = tmp_path / f"lib{name}.so"
+    c.write_text(src_text)
+    subprocess.run(["gcc", "-std=c11", "-O2", "-fPIC", "-shared", "-ffp-contract=off",
+                    str(c), "-o", str(so), "-lm"], check=True)
+    return str(so)
+
+
+def test_unmodified_oracle_passes(tmp_path):
+    assert _with_lib(_build(open(SRC).read(), tmp_path, "orig"))
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site not unique: {old!r}"
+    so = _build(src.replace(old, new), tmp_path, "mutant")
+    assert not _with_lib(so), f"pins did not catch: {name}"
