@@ -1,0 +1,189 @@
+/*
+ * pld.h -- C ABI of the PLD+ drafting step on AMD Instinct MI355X (gfx950).
+ *
+ * PLD+ (Somasundaram, Phukan, Saxena, "PLD+: Accelerating LLM inference by
+ * leveraging Language Model Artifacts", arXiv 2412.01447) drafts K future
+ * tokens by copying a span of the context: it finds the earlier occurrences
+ * of the last token (Eq. 1), ranks them by model artifacts -- the cosine
+ * similarity of hidden states (Eq. 2) or aggregated attention (Eq. 3) --
+ * copies the K tokens after the best one (Sec. 4.3), and keeps the longest
+ * prefix the model agrees with (greedy verification, Sec. 3 and 4.4).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Indexing is 0-based.  Sequence b has T = lens[b] tokens; its last token
+ *   x[T-1] is the paper's x_t and the artifact query position is T-2, the
+ *   paper's t-1 (the Fig. 1 caption calls them "t-1" and "t-2").
+ * - A candidate j is the last index of an occurrence of the query n-gram;
+ *   1 <= j <= T-2.  Its artifact row / key is j-1, its draft starts at j+1.
+ * - Every data pointer is a DEVICE pointer (memory of the GPU that `stream`
+ *   belongs to).  The caller owns all memory; inputs are never modified.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *   Calls validate their arguments on the host, enqueue kernels on the stream
+ *   and return.  They never allocate, never synchronise and keep no pointer.
+ * - Host-checkable faults return a non-zero pld_status and enqueue nothing.
+ *   Faults only visible on the device (bad lengths, positions, counts) are
+ *   reported through the outputs as documented per call.
+ * - `workspace` is device scratch of at least pld_workspace_bytes(...)
+ *   bytes.  It must be zero-filled once after allocation; every call returns
+ *   it to all-zero when its kernels complete, so one buffer serves every call
+ *   of a stream in turn.  Two calls in flight at once (on different streams)
+ *   must not share a workspace.
+ * - Results are deterministic: the same inputs give bit-identical outputs.
+ */
+#ifndef PLD_H
+#define PLD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every call. */
+enum {
+    PLD_OK = 0,
+    PLD_ERR_INVALID = 1,   /* a NULL required pointer, a size or enum out of range   */
+    PLD_ERR_ALIGN = 2,     /* a pointer or stride that breaks an alignment rule       */
+    PLD_ERR_WORKSPACE = 3, /* workspace NULL or smaller than the call needs           */
+    PLD_ERR_LAUNCH = 4     /* the HIP runtime reported an error when launching        */
+};
+
+/* Element types of the verification logits. */
+enum { PLD_F32 = 0, PLD_BF16 = 1 };
+
+/* Aggregations of the attention ranking. */
+enum { PLD_AGG_SUM = 0, PLD_AGG_MAX = 1 };
+
+/* Limits checked on the host. */
+#define PLD_MAX_NGRAM 8         /* ngram_max <= 8                                    */
+#define PLD_MAX_HIDDEN 16384    /* d <= 16384 (the query row is staged in LDS, fp32) */
+#define PLD_MAX_BATCH 4096      /* B <= 4096 for the ranking calls                   */
+
+/* Version of this ABI (major * 10000 + minor * 100 + patch). */
+int pld_version(void);
+
+/* A static, human-readable name for a status code. */
+const char *pld_status_string(int status);
+
+/*
+ * Bytes of workspace for calls with batch B, token stride tok_stride and
+ * draft length K (the largest any call on the buffer will use).  Returns 0
+ * when an argument is out of range.
+ */
+size_t pld_workspace_bytes(int B, int64_t tok_stride, int K);
+
+/*
+ * pld_find_candidates -- the occurrence set P (Eq. 1, Sec. 4.2), with
+ * n-gram queries tried longest first as prompt lookup decoding does (Sec. 2,
+ * Fig. 3 caption):
+ *   P_n = { j : max(n-1,1) <= j <= T-2, x[j-n+1+i] == x[T-n+i] for i < n }
+ * for n = ngram_max down to ngram_min; the first non-empty P_n is the result.
+ *
+ *   tokens      int32 [B][tok_stride], token ids (any values; only equality matters)
+ *   lens        int32 [B], sequence lengths
+ *   ngram_min/max  1 <= ngram_min <= ngram_max <= PLD_MAX_NGRAM
+ *   cand_pos    int32 [B][cap], cap >= tok_stride: P in ascending order in
+ *               slots [0, cand_count[b]); later slots are not written
+ *   cand_count  int32 [B], |P|
+ *   ngram_used  int32 [B], the n that produced P; 0 when no n has an occurrence;
+ *               -1 when lens[b] is outside [1, tok_stride] (then cand_count = 0)
+ * Errors: PLD_ERR_INVALID for NULL pointers, B < 1, tok_stride < 1, bad n range
+ * or cap < tok_stride; PLD_ERR_WORKSPACE; PLD_ERR_LAUNCH.
+ */
+int pld_find_candidates(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B,
+                        int ngram_min, int ngram_max, int32_t *cand_pos, int64_t cap,
+                        int32_t *cand_count, int32_t *ngram_used, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
+/*
+ * pld_rank_hidden -- hidden-state ranking, Eq. 2 (Sec. 4.2.2):
+ *   s_j = cos(H[j-1], H[T-2]) = (h.q) / sqrt(max(|h|^2 |q|^2, 1e-16)),
+ *   best_pos[b] = argmax over eligible j of (s_j, j)
+ * i.e. the highest score, ties to the most recent occurrence.  A candidate is
+ * eligible when s_j > threshold (App. B; pass -INFINITY to keep all).  The
+ * dot product and norms accumulate in fp32 from bf16 inputs.
+ *
+ *   hidden      bf16 bit patterns; row r of sequence b starts at element
+ *               b*h_seq_stride + r*h_row_stride.  Base 16-byte aligned,
+ *               both strides multiples of 8 elements.
+ *   n_rows      rows available per sequence (row T-2 must be < n_rows)
+ *   d           hidden width, 8 <= d <= PLD_MAX_HIDDEN, d % 8 == 0
+ *   lens, cand_pos [B][cap], cand_count  as written by pld_find_candidates
+ *   scores      fp32 [B][cap] or NULL: s_j per slot (NaN for an unusable candidate)
+ *   best_pos    int32 [B]: j*, or -1 when no candidate is eligible
+ *   best_score  fp32 [B]:  s_{j*}, or -INFINITY
+ * Device-side rules: a count outside [0, cap] counts as 0; a sequence with
+ * T < 2 or T-2 >= n_rows, and a slot with j outside [1, T-2], is unusable.
+ * Errors: PLD_ERR_INVALID (NULL, B outside [1, PLD_MAX_BATCH], d out of range,
+ * n_rows < 1, cap < 1, NaN threshold), PLD_ERR_ALIGN, PLD_ERR_WORKSPACE,
+ * PLD_ERR_LAUNCH.
+ */
+int pld_rank_hidden(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
+                    int64_t n_rows, int d, const int32_t *lens, const int32_t *cand_pos,
+                    int64_t cap, const int32_t *cand_count, int B, float threshold,
+                    float *scores, int32_t *best_pos, float *best_score, void *workspace,
+                    size_t workspace_bytes, void *stream);
+
+/*
+ * pld_rank_attn -- attention ranking, Eq. 3 (Sec. 4.2.1) and the all-heads
+ * aggregation of the ablation (Sec. 7.1).  The caller passes, per sequence,
+ * R rows: the attention of query position T-2 over keys 0..n_keys-1 for each
+ * selected (layer, head).
+ *   agg = PLD_AGG_SUM:  s_j = sum_{r<R} A[r][j-1], added in fp32 in r order
+ *   agg = PLD_AGG_MAX:  s_j = max_{r<R} A[r][j-1]
+ * Selection, threshold and outputs as in pld_rank_hidden.
+ *
+ *   attn        fp32; element (b, r, k) at b*a_seq_stride + r*a_row_stride + k
+ *   n_keys      keys per row; a slot with j-1 >= n_keys is unusable
+ * Errors: as pld_rank_hidden (R < 1, n_keys < 1 or a bad agg are
+ * PLD_ERR_INVALID; a base not 4-byte aligned is PLD_ERR_ALIGN).
+ */
+int pld_rank_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stride, int64_t n_keys,
+                  int R, int agg, const int32_t *lens, const int32_t *cand_pos, int64_t cap,
+                  const int32_t *cand_count, int B, float threshold, float *scores,
+                  int32_t *best_pos, float *best_score, void *workspace,
+                  size_t workspace_bytes, void *stream);
+
+/*
+ * pld_emit_draft -- draft prediction, Sec. 4.3: xhat_i = x[j*+i], i = 1..K,
+ * cut at the end of the context:
+ *   L = min(K, T-1-j*) when 0 <= j* <= T-2 and 1 <= T <= tok_stride, else 0
+ *   draft[b][i] = x[j*+1+i] for i < L, -1 for L <= i < K;  draft_len[b] = L
+ * Errors: PLD_ERR_INVALID (NULL, B < 1, K < 1, tok_stride < 1), PLD_ERR_LAUNCH.
+ */
+int pld_emit_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *lens,
+                   const int32_t *best_pos, int B, int K, int32_t *draft, int32_t *draft_len,
+                   void *stream);
+
+/*
+ * pld_verify_greedy -- greedy verification (Sec. 3 "greedy acceptance",
+ * Sec. 4.4).  One forward pass over the context plus the draft gives K+1
+ * rows of logits per sequence.  With y_i = argmax_v Z[b][i][v] (lowest v
+ * among equal maxima; -0 and +0 compare equal):
+ *   accept_len[b] = the first i < L with y_i != draft[b][i], else L
+ *   out_tokens[b] = draft[b][0..a-1], y_a, then -1 padding;  out_count[b] = a+1
+ * where L = draft_len[b].  Rows i > L are never read.
+ *
+ *   logits      PLD_F32 or PLD_BF16 (bit patterns); element (b, i, v) at
+ *               b*l_seq_stride + i*l_row_stride + v; element-aligned.
+ *   V           vocabulary size >= 1;  K >= 1 draft slots per sequence
+ *   draft       int32 [B][K], draft_len int32 [B] (from pld_emit_draft)
+ *   accept_len, out_count int32 [B];  out_tokens int32 [B][K+1]
+ * Device-side rule: draft_len outside [0, K] gives accept_len = -1,
+ * out_count = 0 and out_tokens all -1.
+ * Errors: PLD_ERR_INVALID (NULL, B < 1, K < 1, V < 1, bad dtype, strides
+ * smaller than a row / K+1 rows), PLD_ERR_ALIGN, PLD_ERR_WORKSPACE,
+ * PLD_ERR_LAUNCH.
+ */
+int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
+                      int V, int K, const int32_t *draft, const int32_t *draft_len, int B,
+                      int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PLD_H */

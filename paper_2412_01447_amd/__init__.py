@@ -1,0 +1,174 @@
+"""PLD+ drafting step on AMD Instinct MI355X (gfx950): Python binding of libpld.so.
+
+The calls carry the names and argument order of the C ABI in include/pld.h and
+only marshal arguments: every step runs in the HIP kernels of libpld.so.  Pass
+device tensors (torch is used for device memory and streams only); each call
+enqueues on ``stream`` (default: torch's current stream) and returns without
+synchronising.  A non-zero status from the library raises :class:`PLDError`.
+
+Method: arXiv 2412.01447 -- occurrences of the last token (Eq. 1), ranked by
+hidden-state cosine (Eq. 2) or aggregated attention (Eq. 3), the K tokens after
+the best occurrence as the draft (Sec. 4.3), greedy verification (Sec. 3, 4.4).
+"""
+import ctypes
+import os
+
+__all__ = [
+    "PLDError", "PLD_F32", "PLD_BF16", "PLD_AGG_SUM", "PLD_AGG_MAX", "library_path",
+    "pld_version", "pld_status_string", "pld_workspace_bytes", "pld_find_candidates",
+    "pld_rank_hidden", "pld_rank_attn", "pld_emit_draft", "pld_verify_greedy",
+]
+
+PLD_OK, PLD_ERR_INVALID, PLD_ERR_ALIGN, PLD_ERR_WORKSPACE, PLD_ERR_LAUNCH = range(5)
+PLD_F32, PLD_BF16 = 0, 1
+PLD_AGG_SUM, PLD_AGG_MAX = 0, 1
+PLD_MAX_NGRAM, PLD_MAX_HIDDEN, PLD_MAX_BATCH = 8, 16384, 4096
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+library_path = os.path.join(_HERE, "libpld.so")
+_lib = None
+
+_vp, _i64, _int, _sz, _f32 = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t,
+                              ctypes.c_float)
+
+_SIGNATURES = {
+    "pld_version": ([], _int),
+    "pld_status_string": ([_int], ctypes.c_char_p),
+    "pld_workspace_bytes": ([_int, _i64, _int], _sz),
+    "pld_find_candidates": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _vp, _vp, _vp, _sz, _vp],
+                            _int),
+    "pld_rank_hidden": ([_vp, _i64, _i64, _i64, _int, _vp, _vp, _i64, _vp, _int, _f32, _vp, _vp,
+                         _vp, _vp, _sz, _vp], _int),
+    "pld_rank_attn": ([_vp, _i64, _i64, _i64, _int, _int, _vp, _vp, _i64, _vp, _int, _f32, _vp,
+                       _vp, _vp, _vp, _sz, _vp], _int),
+    "pld_emit_draft": ([_vp, _i64, _vp, _vp, _int, _int, _vp, _vp, _vp], _int),
+    "pld_verify_greedy": ([_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int, _vp, _vp, _vp, _vp,
+                           _sz, _vp], _int),
+}
+
+
+class PLDError(RuntimeError):
+    def __init__(self, name, status):
+        super().__init__(f"{name}: {_load().pld_status_string(status).decode()} (status {status})")
+        self.status = status
+
+
+def _load():
+    """Open libpld.so; fail loudly when it has not been built (no fallback exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(library_path):
+            raise ImportError(f"{library_path} is missing: build it with "
+                              "`python -c 'import __graft_entry__ as g; g.build()'`")
+        lib = ctypes.CDLL(library_path)
+        for name, (args, res) in _SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = lib
+    return _lib
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _need(t, dtype, name, dims):
+    if t.dtype != dtype or t.dim() != dims or not t.is_cuda:
+        raise TypeError(f"{name}: expected a {dims}-d {dtype} device tensor, got "
+                        f"{tuple(t.shape)} {t.dtype} on {t.device}")
+    if t.stride(-1) != 1:
+        raise TypeError(f"{name}: the last dimension must be contiguous")
+
+
+def _call(name, *args):
+    rc = getattr(_load(), name)(*args)
+    if rc != PLD_OK:
+        raise PLDError(name, rc)
+
+
+def pld_version():
+    return _load().pld_version()
+
+
+def pld_status_string(status):
+    return _load().pld_status_string(status).decode()
+
+
+def pld_workspace_bytes(B, tok_stride, K):
+    return int(_load().pld_workspace_bytes(B, tok_stride, K))
+
+
+def pld_find_candidates(tokens, lens, ngram_min, ngram_max, cand_pos, cand_count, ngram_used,
+                        workspace, stream=None):
+    """tokens int32 [B][tok_stride]; writes cand_pos [B][cap], cand_count [B], ngram_used [B]."""
+    import torch
+    _need(tokens, torch.int32, "tokens", 2)
+    _need(cand_pos, torch.int32, "cand_pos", 2)
+    B = tokens.shape[0]
+    _call("pld_find_candidates", _ptr(tokens), tokens.stride(0), _ptr(lens), B, ngram_min,
+          ngram_max, _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), _ptr(ngram_used),
+          _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
+
+
+def pld_rank_hidden(hidden, lens, cand_pos, cand_count, best_pos, best_score, workspace,
+                    threshold=float("-inf"), scores=None, stream=None):
+    """hidden bf16 [B][n_rows][d]; writes best_pos [B], best_score [B] and optionally scores."""
+    import torch
+    _need(hidden, torch.bfloat16, "hidden", 3)
+    _need(cand_pos, torch.int32, "cand_pos", 2)
+    B, n_rows, d = hidden.shape
+    _call("pld_rank_hidden", _ptr(hidden), hidden.stride(0), hidden.stride(1), n_rows, d,
+          _ptr(lens), _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), B, float(threshold),
+          _ptr(scores), _ptr(best_pos), _ptr(best_score), _ptr(workspace),
+          workspace.numel() * workspace.element_size(), _stream(stream))
+
+
+def pld_rank_attn(attn, lens, cand_pos, cand_count, best_pos, best_score, workspace,
+                  agg=PLD_AGG_SUM, threshold=float("-inf"), scores=None, stream=None):
+    """attn fp32 [B][R][n_keys] (query row T-2 per selected head); agg SUM or MAX."""
+    import torch
+    _need(attn, torch.float32, "attn", 3)
+    _need(cand_pos, torch.int32, "cand_pos", 2)
+    B, R, n_keys = attn.shape
+    _call("pld_rank_attn", _ptr(attn), attn.stride(0), attn.stride(1), n_keys, R, int(agg),
+          _ptr(lens), _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), B, float(threshold),
+          _ptr(scores), _ptr(best_pos), _ptr(best_score), _ptr(workspace),
+          workspace.numel() * workspace.element_size(), _stream(stream))
+
+
+def pld_emit_draft(tokens, lens, best_pos, K, draft, draft_len, stream=None):
+    """Writes draft [B][K] (padded with -1) and draft_len [B]."""
+    import torch
+    _need(tokens, torch.int32, "tokens", 2)
+    _need(draft, torch.int32, "draft", 2)
+    if draft.shape[1] != K or draft.stride(0) != K:
+        raise TypeError("draft must be a contiguous [B][K] tensor")
+    _call("pld_emit_draft", _ptr(tokens), tokens.stride(0), _ptr(lens), _ptr(best_pos),
+          tokens.shape[0], K, _ptr(draft), _ptr(draft_len), _stream(stream))
+
+
+def pld_verify_greedy(logits, draft, draft_len, accept_len, out_tokens, out_count, workspace,
+                      stream=None):
+    """logits fp32 or bf16 [B][K+1][V]; writes accept_len [B], out_tokens [B][K+1], out_count [B]."""
+    import torch
+    if logits.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("logits must be float32 or bfloat16")
+    _need(logits, logits.dtype, "logits", 3)
+    B, K1, V = logits.shape
+    K = K1 - 1
+    if draft.shape != (B, K) or draft.stride(0) != K:
+        raise TypeError("draft must be a contiguous [B][K] tensor")
+    if out_tokens.shape != (B, K1) or out_tokens.stride(0) != K1:
+        raise TypeError("out_tokens must be a contiguous [B][K+1] tensor")
+    dtype = PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
+    _call("pld_verify_greedy", _ptr(logits), dtype, logits.stride(0), logits.stride(1), V, K,
+          _ptr(draft), _ptr(draft_len), B, _ptr(accept_len), _ptr(out_tokens), _ptr(out_count),
+          _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))

@@ -1,0 +1,304 @@
+// pld_verify.hip -- greedy verification (arXiv 2412.01447, Sec. 3 "greedy
+// acceptance" and Sec. 4.4) and draft emission (Sec. 4.3).
+//
+// Verification: y_i = argmax_v Z[b][i][v] for the rows i <= L = draft_len[b]
+// (lowest v among equal maxima, -0 == +0), then the accepted length is the
+// first i < L with y_i != draft[b][i] (else L), and the step emits the
+// accepted draft prefix followed by y_a.
+//
+// The argmax is a streaming read of the logits, so the kernel is shaped for
+// HBM: every row is split across S blocks (S picked on the host so that a few
+// thousand blocks are in flight), each thread issues 16-byte loads (4 fp32 or
+// 8 bf16) unrolled eight deep, keeps the first maximum of its own elements,
+// and the wave / block reduce the 64-bit key (orderable(value) << 32 |
+// ~index), whose maximum is the highest value with the lowest index.  A block
+// folds its key into the row's workspace slot with one 64-bit atomic max.
+// The last block of a sequence to finish (atomic ticket counting (L+1)*S
+// arrivals) reads the row keys back, computes the accepted length, writes the
+// outputs and returns the slots to zero.  Rows i > L are never read.
+#include <math.h>
+
+#include "pld.h"
+#include "pld_device.h"
+
+namespace pld {
+
+constexpr int kVerifyThreads = 256;
+constexpr int kVerifyWaves = kVerifyThreads / kWave;
+constexpr int kVerifyUnroll = 8;
+
+struct VerifyArgs {
+    const void *logits;
+    int64_t ls, lr;
+    int V, K, B;
+    int S;
+    const int32_t *draft;
+    const int32_t *draft_len;
+    int32_t *accept_len;
+    int32_t *out_tokens;
+    int32_t *out_count;
+    uint64_t *keys;      // [B][K+1]
+    uint32_t *tickets;   // [B]
+};
+
+template <int kBf16>
+struct Elem;
+template <>
+struct Elem<0> {
+    using T = float;
+    static constexpr int kPerVec = 4;
+    __device__ static float get(const float *p, int64_t i) { return p[i]; }
+    __device__ static void unpack(const uint4 &v, float (&o)[4]) {
+        o[0] = __uint_as_float(v.x);
+        o[1] = __uint_as_float(v.y);
+        o[2] = __uint_as_float(v.z);
+        o[3] = __uint_as_float(v.w);
+    }
+};
+template <>
+struct Elem<1> {
+    using T = uint16_t;
+    static constexpr int kPerVec = 8;
+    __device__ static float get(const uint16_t *p, int64_t i) {
+        return __uint_as_float(((uint32_t)p[i]) << 16);
+    }
+    __device__ static void unpack(const uint4 &v, float (&o)[8]) {
+        o[0] = bf16_lo(v.x);
+        o[1] = bf16_hi(v.x);
+        o[2] = bf16_lo(v.y);
+        o[3] = bf16_hi(v.y);
+        o[4] = bf16_lo(v.z);
+        o[5] = bf16_hi(v.z);
+        o[6] = bf16_lo(v.w);
+        o[7] = bf16_hi(v.w);
+    }
+};
+
+// Keeps the first maximum: a later element replaces the running best only
+// when strictly greater (so -0 after +0, or an equal value, never does).
+__device__ __forceinline__ void keep_first_max(float v, uint32_t idx, float &best, uint32_t &bi) {
+    if (v > best) {
+        best = v;
+        bi = idx;
+    }
+}
+
+template <int kBf16>
+__global__ __launch_bounds__(kVerifyThreads) void verify_kernel(VerifyArgs a) {
+    using E = Elem<kBf16>;
+    using T = typename E::T;
+    constexpr int P = E::kPerVec;
+    __shared__ uint64_t s_key[kVerifyWaves];
+    __shared__ int s_last;
+    const int split = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
+    const int L = a.draft_len[b];
+    if (L < 0 || L > a.K) {
+        if (split == 0 && i == 0) {
+            for (int t = threadIdx.x; t <= a.K; t += blockDim.x)
+                a.out_tokens[(int64_t)b * (a.K + 1) + t] = -1;
+            if (threadIdx.x == 0) {
+                a.accept_len[b] = -1;
+                a.out_count[b] = 0;
+            }
+        }
+        return;
+    }
+    if (i > L) return;
+
+    const T *row = reinterpret_cast<const T *>(a.logits) + (int64_t)b * a.ls + (int64_t)i * a.lr;
+    // The row as [head | 16-byte vectors | tail]; head and tail are scalar.
+    const int mis = (int)(((uintptr_t)row & 15) / sizeof(T));
+    int head = mis ? (P - mis) : 0;
+    if (head > a.V) head = a.V;
+    const int64_t nvec = (int64_t)(a.V - head) / P;
+    const int64_t body_end = head + nvec * P;
+    const int64_t v0 = (nvec * split) / a.S, v1 = (nvec * (split + 1)) / a.S;
+
+    float best = -INFINITY;
+    uint32_t bi = 0xffffffffu;
+    // head: elements [0, head), taken by the first block of the row
+    if (split == 0 && (int)threadIdx.x < head) {
+        best = E::get(row, threadIdx.x);
+        bi = threadIdx.x;
+    }
+    // body: vectors [v0, v1) of the row, strided over the block
+    const uint4 *vec = reinterpret_cast<const uint4 *>(row + head);
+    for (int64_t vb = v0 + threadIdx.x; vb < v1; vb += (int64_t)kVerifyThreads * kVerifyUnroll) {
+        uint4 r[kVerifyUnroll];
+#pragma unroll
+        for (int u = 0; u < kVerifyUnroll; ++u) {
+            int64_t vi = vb + (int64_t)u * kVerifyThreads;
+            if (vi < v1) r[u] = vec[vi];
+        }
+#pragma unroll
+        for (int u = 0; u < kVerifyUnroll; ++u) {
+            int64_t vi = vb + (int64_t)u * kVerifyThreads;
+            if (vi < v1) {
+                float f[P];
+                E::unpack(r[u], f);
+                const uint32_t base = (uint32_t)(head + vi * P);
+#pragma unroll
+                for (int e = 0; e < P; ++e) {
+                    if (bi == 0xffffffffu) {
+                        best = f[e];
+                        bi = base + e;
+                    } else {
+                        keep_first_max(f[e], base + e, best, bi);
+                    }
+                }
+            }
+        }
+    }
+    // tail: elements [body_end, V), taken by the last block of the row
+    if (split == a.S - 1 && body_end + threadIdx.x < a.V) {
+        const int64_t e = body_end + threadIdx.x;
+        float f = E::get(row, e);
+        if (bi == 0xffffffffu) {
+            best = f;
+            bi = (uint32_t)e;
+        } else {
+            keep_first_max(f, (uint32_t)e, best, bi);
+        }
+    }
+    uint64_t key = (bi == 0xffffffffu) ? 0ull : argmax_key(best, bi);
+    key = wave_max_u64(key);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == 0) s_key[w] = key;
+    __syncthreads();
+    uint64_t *slot = a.keys + (int64_t)b * (a.K + 1);
+    if (threadIdx.x == 0) {
+        uint64_t k = s_key[0];
+#pragma unroll
+        for (int t = 1; t < kVerifyWaves; ++t) k = s_key[t] > k ? s_key[t] : k;
+        if (k) atomicMax((unsigned long long *)&slot[i], (unsigned long long)k);
+        __threadfence();
+        uint32_t t = __hip_atomic_fetch_add(&a.tickets[b], 1u, __ATOMIC_ACQ_REL,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+        s_last = (t == (uint32_t)((L + 1) * a.S - 1));
+    }
+    __syncthreads();
+    if (!s_last || threadIdx.x != 0) return;
+    // The last block of sequence b: accept and emit, then clear the slots.
+    __threadfence();
+    int32_t *out = a.out_tokens + (int64_t)b * (a.K + 1);
+    const int32_t *dr = a.draft + (int64_t)b * a.K;
+    int acc = L;
+    int32_t y_acc = -1;
+    for (int r = 0; r <= L; ++r) {
+        uint64_t k = take_u64(&slot[r]);
+        int32_t y = (int32_t)argmax_key_index(k);
+        if (r == acc) y_acc = y;
+        if (r < acc && r < L && y != dr[r]) {
+            acc = r;
+            y_acc = y;
+        }
+    }
+    for (int r = 0; r < acc; ++r) out[r] = dr[r];
+    out[acc] = y_acc;
+    for (int r = acc + 1; r <= a.K; ++r) out[r] = -1;
+    a.accept_len[b] = acc;
+    a.out_count[b] = acc + 1;
+    __hip_atomic_store(&a.tickets[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ------------------------------------------------------------------ emit
+// draft[b][i] = x[j*+1+i] for i < L = min(K, T-1-j*), -1 after (Sec. 4.3).
+__global__ __launch_bounds__(256) void emit_kernel(const int32_t *tokens, int64_t tok_stride,
+                                                   const int32_t *lens, const int32_t *best_pos,
+                                                   int B, int K, int32_t *draft,
+                                                   int32_t *draft_len) {
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g >= (int64_t)B * K) return;
+    const int b = (int)(g / K), i = (int)(g % K);
+    const int64_t T = lens[b];
+    const int64_t j = best_pos[b];
+    int64_t L = 0;
+    if (T >= 1 && T <= tok_stride && j >= 0 && j <= T - 2) L = min((int64_t)K, T - 1 - j);
+    draft[g] = (i < L) ? tokens[(int64_t)b * tok_stride + j + 1 + i] : -1;
+    if (i == 0) draft_len[b] = (int32_t)L;
+}
+
+}  // namespace pld
+
+using namespace pld;
+
+extern "C" int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride,
+                                 int64_t l_row_stride, int V, int K, const int32_t *draft,
+                                 const int32_t *draft_len, int B, int32_t *accept_len,
+                                 int32_t *out_tokens, int32_t *out_count, void *workspace,
+                                 size_t workspace_bytes, void *stream) {
+    if (!logits || !draft || !draft_len || !accept_len || !out_tokens || !out_count)
+        return PLD_ERR_INVALID;
+    if (B < 1 || K < 1 || V < 1 || (dtype != PLD_F32 && dtype != PLD_BF16)) return PLD_ERR_INVALID;
+    if (B > 65535 || K + 1 > 65535) return PLD_ERR_INVALID;       // grid y / z limits
+    if (l_row_stride < V || l_seq_stride < (int64_t)(K + 1) * l_row_stride) return PLD_ERR_INVALID;
+    const size_t esz = dtype == PLD_F32 ? 4 : 2;
+    if ((uintptr_t)logits % esz) return PLD_ERR_ALIGN;
+    if (!workspace || workspace_bytes < verify_ws_bytes(B, K)) return PLD_ERR_WORKSPACE;
+    // Blocks per row: enough for ~2048 blocks in flight, but each block keeps
+    // at least two 16-byte vectors per thread.
+    const int64_t rows = (int64_t)B * (K + 1);
+    const int64_t nvec = (int64_t)V * esz / 16;
+    int64_t S = (2048 + rows - 1) / rows;
+    int64_t smax = nvec / (2 * kVerifyThreads);
+    if (S > smax) S = smax;
+    if (S < 1) S = 1;
+    VerifyArgs a;
+    a.logits = logits;
+    a.ls = l_seq_stride;
+    a.lr = l_row_stride;
+    a.V = V;
+    a.K = K;
+    a.B = B;
+    a.S = (int)S;
+    a.draft = draft;
+    a.draft_len = draft_len;
+    a.accept_len = accept_len;
+    a.out_tokens = out_tokens;
+    a.out_count = out_count;
+    a.keys = (uint64_t *)workspace;
+    a.tickets = (uint32_t *)((char *)workspace +
+                             align_up((size_t)B * (size_t)(K + 1) * sizeof(uint64_t), 256));
+    dim3 grid((unsigned)S, (unsigned)(K + 1), (unsigned)B);
+    if (dtype == PLD_F32)
+        hipLaunchKernelGGL(verify_kernel<0>, grid, dim3(kVerifyThreads), 0, (hipStream_t)stream, a);
+    else
+        hipLaunchKernelGGL(verify_kernel<1>, grid, dim3(kVerifyThreads), 0, (hipStream_t)stream, a);
+    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+}
+
+extern "C" int pld_emit_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *lens,
+                              const int32_t *best_pos, int B, int K, int32_t *draft,
+                              int32_t *draft_len, void *stream) {
+    if (!tokens || !lens || !best_pos || !draft || !draft_len) return PLD_ERR_INVALID;
+    if (B < 1 || K < 1 || tok_stride < 1) return PLD_ERR_INVALID;
+    const int64_t n = (int64_t)B * K;
+    const int64_t blocks = (n + 255) / 256;
+    if (blocks > 0x7fffffff) return PLD_ERR_INVALID;
+    hipLaunchKernelGGL(emit_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
+                       tokens, tok_stride, lens, best_pos, B, K, draft, draft_len);
+    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+}
+
+extern "C" int pld_version(void) { return 100; }
+
+extern "C" const char *pld_status_string(int status) {
+    switch (status) {
+    case PLD_OK: return "ok";
+    case PLD_ERR_INVALID: return "invalid argument";
+    case PLD_ERR_ALIGN: return "misaligned pointer or stride";
+    case PLD_ERR_WORKSPACE: return "workspace missing or too small";
+    case PLD_ERR_LAUNCH: return "kernel launch failed";
+    default: return "unknown status";
+    }
+}
+
+extern "C" size_t pld_workspace_bytes(int B, int64_t tok_stride, int K) {
+    if (B < 1 || tok_stride < 1 || tok_stride > kMaxTokStride || K < 1) return 0;
+    size_t n = find_ws_bytes(B, tok_stride);
+    size_t r = rank_ws_bytes(B);
+    size_t v = verify_ws_bytes(B, K);
+    if (r > n) n = r;
+    if (v > n) n = v;
+    return n;
+}

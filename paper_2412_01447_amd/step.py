@@ -1,0 +1,83 @@
+"""One drafting step (find -> rank -> emit -> verify) over preallocated device buffers.
+
+A convenience over the five calls of the binding: it owns the output and
+workspace tensors for a batch shape and enqueues the calls on one stream with
+no host synchronisation (arXiv 2412.01447, Sec. 4: retrieval Eq. 1, ranking
+Eq. 2 / Eq. 3, draft Sec. 4.3, greedy verification Sec. 4.4).
+"""
+import torch
+
+from . import (PLD_AGG_SUM, pld_emit_draft, pld_find_candidates, pld_rank_attn, pld_rank_hidden,
+               pld_verify_greedy, pld_workspace_bytes)
+
+
+class DraftStep:
+    def __init__(self, B, tok_stride, K, device="cuda", cap=None, keep_scores=False):
+        self.B, self.tok_stride, self.K = B, tok_stride, K
+        cap = tok_stride if cap is None else cap
+        i32 = dict(dtype=torch.int32, device=device)
+        self.cand_pos = torch.full((B, cap), -1, **i32)
+        self.cand_count = torch.zeros(B, **i32)
+        self.ngram_used = torch.zeros(B, **i32)
+        self.best_pos = torch.zeros(B, **i32)
+        self.best_score = torch.zeros(B, dtype=torch.float32, device=device)
+        self.best_pos_attn = torch.zeros(B, **i32)
+        self.best_score_attn = torch.zeros(B, dtype=torch.float32, device=device)
+        self.scores = torch.zeros((B, cap), dtype=torch.float32, device=device) if keep_scores else None
+        self.scores_attn = (torch.zeros((B, cap), dtype=torch.float32, device=device)
+                            if keep_scores else None)
+        self.draft = torch.zeros((B, K), **i32)
+        self.draft_len = torch.zeros(B, **i32)
+        self.accept_len = torch.zeros(B, **i32)
+        self.out_tokens = torch.zeros((B, K + 1), **i32)
+        self.out_count = torch.zeros(B, **i32)
+        nbytes = pld_workspace_bytes(B, tok_stride, K)
+        self.workspace = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+
+    def find(self, tokens, lens, ngram_min=1, ngram_max=1, stream=None):
+        pld_find_candidates(tokens, lens, ngram_min, ngram_max, self.cand_pos, self.cand_count,
+                            self.ngram_used, self.workspace, stream=stream)
+
+    def rank_hidden(self, hidden, lens, threshold=float("-inf"), stream=None):
+        pld_rank_hidden(hidden, lens, self.cand_pos, self.cand_count, self.best_pos,
+                        self.best_score, self.workspace, threshold=threshold, scores=self.scores,
+                        stream=stream)
+
+    def rank_attn(self, attn, lens, agg=PLD_AGG_SUM, threshold=float("-inf"), into_best=True,
+                  stream=None):
+        bp = self.best_pos if into_best else self.best_pos_attn
+        bs = self.best_score if into_best else self.best_score_attn
+        pld_rank_attn(attn, lens, self.cand_pos, self.cand_count, bp, bs, self.workspace, agg=agg,
+                      threshold=threshold, scores=self.scores_attn, stream=stream)
+
+    def emit(self, tokens, lens, stream=None):
+        pld_emit_draft(tokens, lens, self.best_pos, self.K, self.draft, self.draft_len,
+                       stream=stream)
+
+    def verify(self, logits, stream=None):
+        pld_verify_greedy(logits, self.draft, self.draft_len, self.accept_len, self.out_tokens,
+                          self.out_count, self.workspace, stream=stream)
+
+    def run(self, tokens, lens, logits, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
+            threshold=float("-inf"), stream=None):
+        """The whole step.  With both artifacts, the hidden-state ranking drafts and the
+        attention ranking is written to best_pos_attn / best_score_attn."""
+        self.find(tokens, lens, *ngram, stream=stream)
+        if attn is not None:
+            self.rank_attn(attn, lens, agg=agg, threshold=threshold, into_best=hidden is None,
+                           stream=stream)
+        if hidden is not None:
+            self.rank_hidden(hidden, lens, threshold=threshold, stream=stream)
+        self.emit(tokens, lens, stream=stream)
+        self.verify(logits, stream=stream)
+
+    def host(self):
+        """Copies every output to host numpy arrays (synchronises)."""
+        names = ["cand_pos", "cand_count", "ngram_used", "best_pos", "best_score",
+                 "best_pos_attn", "best_score_attn", "draft", "draft_len", "accept_len",
+                 "out_tokens", "out_count"]
+        out = {n: getattr(self, n).cpu().numpy() for n in names}
+        if self.scores is not None:
+            out["scores"] = self.scores.cpu().numpy()
+            out["scores_attn"] = self.scores_attn.cpu().numpy()
+        return out

@@ -280,3 +280,36 @@ def intended_drafts(metas, K):
         d[b, :k] = m.intended[:k]
         n[b] = k
     return d, n
+
+
+def to_device_bf16(bits, device):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(bits, np.uint16).view(np.int16))
+    return t.to(device).view(torch.bfloat16)
+
+
+def make_workload(cfg: Config, device, structured: bool = True, plant_draft=None):
+    """All inputs of one configuration.
+
+    tokens/lens (host int32), hidden (device bf16 [B][T][d] or None), attn
+    (host fp32 [B][R][T] or None).  Logits are made by `logits_for(w, draft,
+    draft_len)` once the draft to plant is known; with `plant_draft` given
+    here (a (draft, draft_len) pair) they are made at once.
+    """
+    toks, lens, metas = make_tokens(cfg)
+    w = dict(cfg=cfg, tokens=toks, lens=lens, metas=metas, hidden=None, attn=None, logits=None)
+    if cfg.rank in ("hidden", "both"):
+        plants = structured_hidden_plants(lens, metas) if structured else ()
+        w["hidden"] = make_hidden(cfg.B, cfg.T, cfg.d, cfg.seed, device=device, plants=plants)
+    if cfg.rank in ("attn", "both"):
+        w["attn"] = make_attn(cfg.B, cfg.R, cfg.T, lens, cfg.seed,
+                              metas=metas if structured else None)
+    if plant_draft is not None:
+        w["logits"] = logits_for(w, *plant_draft)
+    return w
+
+
+def logits_for(w, draft, draft_len):
+    c = w["cfg"]
+    z, _ = make_logits(c.B, c.K, c.V, c.seed, draft, draft_len, bf16=(c.logits == "bf16"))
+    return z

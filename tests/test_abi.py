@@ -1,0 +1,132 @@
+"""The C ABI library loads, exports what include/pld.h declares, and validates
+arguments on the host (CPU only; no kernel is ever launched here).
+
+Every error-path call below carries at least one argument the host check
+rejects, so it returns before any HIP call.  Those calls use placeholder
+pointers, so they run only where no GPU is visible; on a GPU machine the same
+paths are exercised with real device buffers by the GPU tests.
+"""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2412_01447_amd as pld
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pld.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pld_\w+)\s*\(", text)))
+
+
+def _no_gpu():
+    import torch
+    return torch.cuda.device_count() == 0
+
+
+def test_header_declares_the_five_calls():
+    names = _declared()
+    for n in ("pld_find_candidates", "pld_rank_hidden", "pld_rank_attn", "pld_emit_draft",
+              "pld_verify_greedy", "pld_workspace_bytes", "pld_status_string", "pld_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    assert os.path.exists(pld.library_path), "libpld.so not built"
+    out = subprocess.run(["nm", "-D", "--defined-only", pld.library_path], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (pld_\w+)$", out, flags=re.M))
+    missing = [n for n in _declared() if n not in exported]
+    assert not missing, missing
+    lib = pld._load()
+    for n in _declared():
+        assert hasattr(lib, n)
+        assert hasattr(pld, n), f"binding lacks {n}"
+
+
+def test_status_strings_and_version():
+    assert pld.pld_version() >= 100
+    assert pld.pld_status_string(0) == "ok"
+    assert "workspace" in pld.pld_status_string(3)
+    assert pld.pld_status_string(99) == "unknown status"
+
+
+def test_workspace_bytes():
+    assert pld.pld_workspace_bytes(0, 10, 4) == 0
+    assert pld.pld_workspace_bytes(1, 0, 4) == 0
+    assert pld.pld_workspace_bytes(1, 10, 0) == 0
+    a = pld.pld_workspace_bytes(8, 4096, 10)
+    assert a > 0 and a % 256 == 0
+    assert pld.pld_workspace_bytes(8, 1 << 17, 10) >= a          # multi-tile find needs more
+    assert pld.pld_workspace_bytes(64, 4096, 32) >= pld.pld_workspace_bytes(64, 4096, 16)
+    # verify keys: B*(K+1) u64 + B tickets
+    assert pld.pld_workspace_bytes(64, 16, 16) >= 64 * 17 * 8 + 64 * 4
+
+
+P = ctypes.c_void_p
+F = P(0x1000)            # placeholder pointer, never dereferenced (host check fails first)
+MIS = P(0x1002)          # misaligned placeholder
+NULL = None
+INF = float("-inf")
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="placeholder pointers are only used where no GPU is visible")
+def test_host_validation_error_codes():
+    lib = pld._load()
+    E_INV, E_AL, E_WS = pld.PLD_ERR_INVALID, pld.PLD_ERR_ALIGN, pld.PLD_ERR_WORKSPACE
+    # find: NULLs, B, n range, cap, tok_stride
+    f = lib.pld_find_candidates
+    assert f(NULL, 16, F, 1, 1, 1, F, 16, F, F, F, 1 << 20, NULL) == E_INV
+    assert f(F, 16, F, 0, 1, 1, F, 16, F, F, F, 1 << 20, NULL) == E_INV
+    assert f(F, 16, F, 1, 0, 1, F, 16, F, F, F, 1 << 20, NULL) == E_INV
+    assert f(F, 16, F, 1, 2, 1, F, 16, F, F, F, 1 << 20, NULL) == E_INV
+    assert f(F, 16, F, 1, 1, 9, F, 16, F, F, F, 1 << 20, NULL) == E_INV
+    assert f(F, 16, F, 1, 1, 1, F, 15, F, F, F, 1 << 20, NULL) == E_INV
+    assert f(F, 0, F, 1, 1, 1, F, 16, F, F, F, 1 << 20, NULL) == E_INV
+    # the multi-tile path needs a workspace of the documented size
+    big = 1 << 15
+    assert f(F, big, F, 2, 1, 1, F, big, F, F, NULL, 0, NULL) == E_WS
+    assert f(F, big, F, 2, 1, 1, F, big, F, F, F, 16, NULL) == E_WS
+    # rank hidden
+    h = lib.pld_rank_hidden
+    ok = dict()
+    assert h(NULL, 64, 8, 8, 8, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    assert h(F, 64, 8, 8, 8, F, F, 8, F, 0, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    assert h(F, 64, 8, 8, 8, F, F, 8, F, 4097, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    assert h(F, 64, 8, 8, 12, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV   # d%8
+    assert h(F, 64, 8, 8, 16392, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    assert h(F, 64, 8, 8, 8, F, F, 8, F, 1, math.nan, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    assert h(F, 64, 8, 0, 8, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    assert h(MIS, 64, 8, 8, 8, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_AL
+    assert h(F, 64, 12, 8, 8, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_AL
+    assert h(F, 64, 8, 8, 8, F, F, 8, F, 1, INF, NULL, F, F, NULL, 1 << 20, NULL) == E_WS
+    assert h(F, 64, 8, 8, 8, F, F, 8, F, 1, INF, NULL, F, F, F, 8, NULL) == E_WS
+    # rank attn
+    a = lib.pld_rank_attn
+    assert a(F, 64, 8, 8, 0, 0, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    assert a(F, 64, 8, 8, 1, 2, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    assert a(F, 64, 8, 0, 1, 0, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    assert a(MIS, 64, 8, 8, 1, 0, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_AL
+    assert a(F, 64, 8, 8, 1, 0, F, F, 8, NULL, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    # emit
+    e = lib.pld_emit_draft
+    assert e(F, 8, F, F, 1, 0, F, F, NULL) == E_INV
+    assert e(F, 8, F, F, 0, 4, F, F, NULL) == E_INV
+    assert e(F, 8, F, NULL, 1, 4, F, F, NULL) == E_INV
+    # verify
+    v = lib.pld_verify_greedy
+    assert v(F, 2, 40, 10, 10, 3, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_INV   # dtype
+    assert v(F, 0, 40, 10, 10, 0, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_INV   # K
+    assert v(F, 0, 40, 10, 0, 3, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_INV    # V
+    assert v(F, 0, 40, 9, 10, 3, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_INV    # row stride
+    assert v(F, 0, 39, 10, 10, 3, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_INV   # seq stride
+    assert v(MIS, 0, 40, 10, 10, 3, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_AL  # fp32 alignment
+    assert v(F, 0, 40, 10, 10, 3, F, F, 1, F, F, F, F, 8, NULL) == E_WS
+    assert v(F, 0, 40, 10, 10, 3, F, F, 1, F, F, F, NULL, 1 << 20, NULL) == E_WS

@@ -1,0 +1,89 @@
+"""GPU parity of the whole drafting step on the five synthetic workloads, at full
+size, in the launch configuration the benchmark times (DraftStep, one stream).
+
+For each workload the oracle runs first on the same inputs (hidden rows it
+needs are copied back from the device), its draft plants the accepted prefixes
+in the verification logits, then the GPU step runs and every stage is compared:
+positions / counts / n / draft / accept lengths / emitted tokens bit-exactly,
+scores within 1e-3 relative, near-tie flips counted.  Both the structured
+variant (the planted source of the last token is the cosine winner) and the
+plain random variant are run.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from gpu_helpers import (check_best, check_find, check_scores, check_verify, d_bf16, d_f32,
+                         d_i32, gpu_emit, gpu_verify, say, sparse_hidden_rows)
+from paper_2412_01447_amd.step import DraftStep
+
+pytestmark = pytest.mark.gpu
+
+CASES = [(1, True), (1, False), (2, True), (2, False), (3, True), (3, False), (4, True),
+         (5, True), (5, False)]
+
+
+@pytest.mark.parametrize("cid,structured", CASES, ids=[f"cfg{c}_{'structured' if s else 'random'}"
+                                                       for c, s in CASES])
+def test_config_step_parity(cid, structured):
+    cfg = synth.CONFIGS[cid]
+    say("config", cid, cfg.name, "structured" if structured else "random")
+    dev = torch.device("cuda:0")
+    w = synth.make_workload(cfg, dev, structured=structured)
+    toks, lens = w["tokens"], w["lens"]
+    # ---- oracle, stage by stage
+    cp, cc, nu = oracle.find(toks, lens, *cfg.ngram)
+    ref = {}
+    if w["hidden"] is not None:
+        hb = sparse_hidden_rows(w["hidden"], lens, cp, cc)
+        ref["h"] = oracle.rank_hidden(hb, lens, cp, cc)
+        del hb
+    if w["attn"] is not None:
+        ref["a"] = oracle.rank_attn(w["attn"], lens, cp, cc, oracle.AGG_SUM)
+    drafter = ref["h"] if "h" in ref else ref["a"]
+    rdraft, rdl = oracle.emit(toks, lens, drafter[1], cfg.K)
+    z = synth.logits_for(w, rdraft, rdl)
+    bf16 = cfg.logits == "bf16"
+    rver = oracle.verify(z, rdraft, rdl, bf16=bf16)
+    say("  oracle: counts", cc.tolist()[:8], "n", sorted(set(nu.tolist())), "accept",
+        rver[0].tolist()[:16])
+    # ---- GPU step, as the benchmark launches it
+    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, keep_scores=True)
+    zd = d_bf16(z) if bf16 else d_f32(z)
+    attn_d = d_f32(w["attn"]) if w["attn"] is not None else None
+    td, ld = d_i32(toks), d_i32(lens)
+    step.run(td, ld, zd, hidden=w["hidden"], attn=attn_d, ngram=cfg.ngram)
+    torch.cuda.synchronize()
+    g = step.host()
+    assert int(torch.count_nonzero(step.workspace).item()) == 0
+    check_find((g["cand_pos"], g["cand_count"], g["ngram_used"]), (cp, cc, nu), cfg.name)
+    flips = 0
+    if "h" in ref:
+        rsc, rbp, rbs = ref["h"]
+        check_scores(g["scores"], rsc, cc, cfg.name + " hidden")
+        flips += check_best(g["best_pos"], g["best_score"], rsc, rbp, rbs, cp, cc, cfg.name)
+    if "a" in ref:
+        rsc, rbp, rbs = ref["a"]
+        check_scores(g["scores_attn"], rsc, cc, cfg.name + " attn")
+        gbp = g["best_pos_attn"] if "h" in ref else g["best_pos"]
+        gbs = g["best_score_attn"] if "h" in ref else g["best_score"]
+        flips += check_best(gbp, gbs, rsc, rbp, rbs, cp, cc, cfg.name + " attn")
+    say("  near-tie flips:", flips)
+    if structured and "h" in ref:
+        srcs = np.array([m.query_src_end for m in w["metas"]])
+        assert np.array_equal(g["best_pos"], srcs) and np.all(g["best_score"] == 1.0)
+    if flips == 0:
+        # chained outputs equal the oracle's chain
+        assert np.array_equal(g["draft"], rdraft) and np.array_equal(g["draft_len"], rdl)
+        check_verify((g["accept_len"], g["out_tokens"], g["out_count"]), rver, cfg.name)
+    else:
+        # after a flip, the later stages are checked on the oracle's own inputs
+        gd, gl = gpu_emit(toks, lens, drafter[1], cfg.K)
+        assert np.array_equal(gd, rdraft) and np.array_equal(gl, rdl)
+        check_verify(gpu_verify(zd, rdraft, rdl), rver, cfg.name)
+    # accepted lengths cover a range (the planted prefixes work)
+    say("  accept lengths:", np.bincount(rver[0], minlength=cfg.K + 1).tolist())
+    del step, w, zd
+    torch.cuda.empty_cache()

@@ -1,0 +1,364 @@
+"""GPU parity of each call of the C ABI against the CPU oracle, on small and
+edge-case inputs (several tiles, ragged tails, empty and invalid cases).
+
+Every case prints its name before touching the GPU.  Inputs are seeded; the
+oracle sees the same bytes as the kernels; comparisons follow gpu_helpers.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import golden_cases
+import oracle
+import paper_2412_01447_amd as pld
+import synth
+from gpu_helpers import (check_best, check_find, check_scores, check_verify, d_bf16, d_f32,
+                         d_i32, gpu_emit, gpu_find, gpu_rank_attn, gpu_rank_hidden, gpu_verify,
+                         say, workspace)
+
+pytestmark = pytest.mark.gpu
+
+
+# ----------------------------------------------------------------- golden
+def _pad8(H):
+    """The library takes d % 8 == 0; zero columns leave every dot product and norm unchanged."""
+    d = H.shape[-1]
+    return np.concatenate([H, np.zeros(H.shape[:-1] + ((-d) % 8,), np.float32)], axis=-1)
+
+
+def test_golden_fig1_on_gpu():
+    say("golden fig1")
+    fx, toks, lens, H, A = golden_cases.load("fig1_overview.json")
+    H = _pad8(H)
+    ex = fx["expected"]
+    cp, cc, nu = gpu_find(toks, lens, 1, 1)
+    assert list(cp[0, :cc[0]]) == ex["cand_pos"] and nu[0] == 1
+    bits = synth.f32_to_bf16_bits(H)
+    sc, bp, bs = gpu_rank_hidden(d_bf16(bits), lens, cp, cc)
+    np.testing.assert_allclose(sc[0, :2], ex["hidden_scores"], rtol=1e-6, atol=1e-7)
+    assert bp[0] == ex["hidden_best_pos"]
+    for agg, key in ((pld.PLD_AGG_SUM, "attn_sum"), (pld.PLD_AGG_MAX, "attn_max")):
+        sc, bp, bs = gpu_rank_attn(d_f32(A), lens, cp, cc, agg)
+        assert list(sc[0, :2]) == ex[key + "_scores"] and bp[0] == ex[key + "_best_pos"]
+    for K in (3, 12):
+        dr, dl = gpu_emit(toks, lens, np.array([10], np.int32), K)
+        assert list(dr[0]) == ex[f"draft_K{K}"] and dl[0] == ex[f"draft_len_K{K}"]
+    for vc in fx["verify_cases"]:
+        Z, dr, dl = golden_cases.verify_case(vc)
+        e = vc["expected"]
+        for z in (d_f32(Z), d_bf16(synth.f32_to_bf16_bits(Z))):
+            acc, out, cnt = gpu_verify(z, dr, dl)
+            assert acc[0] == e["accept_len"] and list(out[0]) == e["out_tokens"], vc["name"]
+            assert cnt[0] == e["out_count"], vc["name"]
+
+
+def test_golden_fig3_on_gpu():
+    say("golden fig3")
+    fx, toks, lens, H, _ = golden_cases.load("fig3_newline.json")
+    bits = synth.f32_to_bf16_bits(_pad8(H))
+    for key, (a, b) in (("n1", (1, 1)), ("n1to3", (1, 3)), ("n1to4", (1, 4)), ("n5to6", (5, 6)),
+                        ("n7to8", (7, 8))):
+        e = fx["expected"][key]
+        cp, cc, nu = gpu_find(toks, lens, a, b)
+        assert list(cp[0, :cc[0]]) == e["cand_pos"] and nu[0] == e["ngram_used"], key
+        sc, bp, bs = gpu_rank_hidden(d_bf16(bits), lens, cp, cc)
+        assert bp[0] == e["best_pos"], key
+
+
+# ------------------------------------------------------------------- find
+FIND_CASES = [
+    # (B, tok_stride, V, n_min, n_max, seed)
+    (16, 1, 2, 1, 1, 0), (16, 5, 2, 1, 2, 1), (16, 64, 3, 1, 3, 2), (16, 700, 5, 1, 4, 3),
+    (12, 4096, 50, 1, 3, 4), (8, 8192, 7, 2, 5, 5), (8, 8192, 1, 1, 8, 6),
+    (6, 8193, 4, 1, 1, 7), (5, 20000, 3, 1, 3, 8), (4, 70000, 1000, 1, 2, 9),
+    (3, 131072, 2, 8, 8, 10), (3, 50000, 1, 1, 1, 11),
+]
+
+
+@pytest.mark.parametrize("case", FIND_CASES, ids=[f"B{c[0]}_S{c[1]}_V{c[2]}_n{c[3]}-{c[4]}"
+                                                  for c in FIND_CASES])
+def test_find_parity(case):
+    B, stride, V, nmin, nmax, seed = case
+    say("find", case)
+    rng = np.random.default_rng(seed)
+    toks = rng.integers(0, V, size=(B, stride)).astype(np.int32)
+    lens = rng.integers(1, stride + 1, size=B).astype(np.int32)
+    lens[0] = stride                               # full length
+    if B > 2:
+        lens[1] = 0                                # invalid: too short
+        lens[2] = stride + 1                       # invalid: too long
+    if B > 3:
+        lens[3] = min(stride, 3)
+    ref = oracle.find(toks, lens, nmin, nmax)
+    check_find(gpu_find(toks, lens, nmin, nmax), ref, str(case))
+    # a larger cap leaves the same prefix
+    check_find(gpu_find(toks, lens, nmin, nmax, cap=stride + 37), ref, str(case) + " cap")
+
+
+def test_find_planted_ngrams_multi_tile():
+    """Long sequences with planted n-gram repeats crossing tile borders."""
+    say("find planted multi-tile")
+    rng = np.random.default_rng(42)
+    B, stride = 3, 40000
+    toks = rng.integers(0, 30000, size=(B, stride)).astype(np.int32)
+    lens = np.array([40000, 39999, 12345], np.int32)
+    for b in range(B):
+        T = lens[b]
+        q = toks[b, T - 5:T].copy()
+        for p in (2046, 2047, 2048, 4095, 10000, T - 7):   # around tile borders of 2048
+            toks[b, p - 4:p + 1] = q
+    for nmin, nmax in ((1, 5), (1, 8), (3, 3), (6, 8)):
+        check_find(gpu_find(toks, lens, nmin, nmax), oracle.find(toks, lens, nmin, nmax))
+
+
+# ------------------------------------------------------------- rank hidden
+def _hidden_case(B, T, d, V, seed, nmin=1, nmax=1, plants=(), row_pad=0):
+    rng = np.random.default_rng(seed)
+    toks = rng.integers(0, V, size=(B, T)).astype(np.int32)
+    lens = rng.integers(3, T + 1, size=B).astype(np.int32)
+    lens[0] = T
+    H = rng.standard_normal((B, T, d + row_pad)).astype(np.float32)
+    for (b, dst, src) in plants:
+        H[b, dst] = H[b, src]
+    bits = synth.f32_to_bf16_bits(H)
+    cp, cc, nu = oracle.find(toks, lens, nmin, nmax)
+    return toks, lens, bits, cp, cc
+
+
+@pytest.mark.parametrize("d", [8, 40, 512, 520, 4096, 5120, 8192, 16384])
+def test_rank_hidden_parity(d):
+    say("rank_hidden d", d)
+    B, T = 6, 300
+    toks, lens, bits, cp, cc = _hidden_case(B, T, d, 12, d)
+    rsc, rbp, rbs = oracle.rank_hidden(bits, lens, cp, cc)
+    gsc, gbp, gbs = gpu_rank_hidden(d_bf16(bits), lens, cp, cc)
+    check_scores(gsc, rsc, cc, f"d={d}")
+    flips = check_best(gbp, gbs, rsc, rbp, rbs, cp, cc, f"d={d}")
+    say("near-tie flips", flips)
+
+
+def test_rank_hidden_strided_rows_and_threshold():
+    say("rank_hidden strided")
+    B, T, d, pad = 4, 200, 256, 24
+    toks, lens, bits, cp, cc = _hidden_case(B, T, d, 9, 3, row_pad=pad)
+    hd = d_bf16(bits)[:, :, :d]                    # row stride d + pad
+    assert hd.stride(1) == d + pad
+    rsc, rbp, rbs = oracle.rank_hidden(np.ascontiguousarray(bits[:, :, :d]), lens, cp, cc)
+    gsc, gbp, gbs = gpu_rank_hidden(hd, lens, cp, cc)
+    check_scores(gsc, rsc, cc, "strided")
+    check_best(gbp, gbs, rsc, rbp, rbs, cp, cc, "strided")
+    for th in (0.0, 0.05, float(np.nanmax(rsc[0, :cc[0]])), 2.0):
+        rsc2, rbp2, rbs2 = oracle.rank_hidden(np.ascontiguousarray(bits[:, :, :d]), lens, cp, cc,
+                                              threshold=th)
+        gsc2, gbp2, gbs2 = gpu_rank_hidden(hd, lens, cp, cc, threshold=th)
+        check_best(gbp2, gbs2, rsc2, rbp2, rbs2, cp, cc, f"threshold {th}", threshold=th)
+
+
+def test_rank_hidden_exact_ties_and_planted_copy():
+    """Identical and power-of-two-scaled rows tie bit-exactly on the GPU (the later j
+    wins); a copy of the query row scores exactly 1."""
+    say("rank_hidden ties")
+    T, d = 64, 1024
+    rng = np.random.default_rng(5)
+    H = rng.standard_normal((2, T, d)).astype(np.float32)
+    H[0, 9] = H[0, 19]
+    H[0, 39] = 4.0 * H[0, 19]
+    H[0, T - 2] = H[0, 19] + 0.05 * rng.standard_normal(d).astype(np.float32)
+    H[1, 30] = H[1, T - 2]
+    bits = synth.f32_to_bf16_bits(H)
+    lens = np.array([T, T], np.int32)
+    cp = np.full((2, T), -1, np.int32)
+    cp[0, :4] = [10, 20, 40, 50]
+    cp[1, :3] = [5, 31, 60]
+    cc = np.array([4, 3], np.int32)
+    gsc, gbp, gbs = gpu_rank_hidden(d_bf16(bits), lens, cp, cc)
+    assert gsc[0, 0] == gsc[0, 1] == gsc[0, 2]
+    assert gbp[0] == 40
+    assert gsc[1, 1] == 1.0 and gbp[1] == 31 and gbs[1] == 1.0
+    # the same row in another slot and another block gives the same bits
+    cp2 = np.full((2, T), -1, np.int32)
+    cp2[0, :3] = [40, 20, 10]
+    gsc2, _, _ = gpu_rank_hidden(d_bf16(bits), lens, cp2, np.array([3, 0], np.int32))
+    assert gsc2[0, 0] == gsc[0, 2] and gsc2[0, 2] == gsc[0, 0]
+
+
+def test_rank_hidden_invalid_inputs():
+    """Out-of-range candidates score NaN, bad counts count as zero, unusable
+    sequences have no best; nothing outside the buffers is read."""
+    say("rank_hidden invalid")
+    B, T, d = 5, 40, 64
+    rng = np.random.default_rng(8)
+    bits = synth.f32_to_bf16_bits(rng.standard_normal((B, T, d)).astype(np.float32))
+    lens = np.array([40, 1, 41, 40, 40], np.int32)    # seq 1 too short, seq 2 row T-2 = 39 ok
+    lens[2] = 42                                       # T-2 = 40 >= n_rows: unusable
+    cp = np.full((B, T), -1, np.int32)
+    cp[0, :5] = [0, 1, 38, 39, 100]
+    cp[1, :1] = [1]
+    cp[2, :2] = [3, 4]
+    cp[3, :2] = [5, 6]
+    cp[4, :1] = [7]
+    cc = np.array([5, 1, 2, T + 1, -3], np.int32)       # seq 3 count > cap, seq 4 negative
+    rsc, rbp, rbs = oracle.rank_hidden(bits, lens, cp, cc)
+    gsc, gbp, gbs = gpu_rank_hidden(d_bf16(bits), lens, cp, cc)
+    check_scores(gsc, rsc, np.array([5, 1, 2, 0, 0]), "invalid")
+    assert list(gbp) == list(rbp) and list(gbp[1:]) == [-1, -1, -1, -1]
+    assert math.isnan(gsc[0, 0]) and math.isnan(gsc[0, 3]) and math.isnan(gsc[0, 4])
+
+
+def test_rank_hidden_many_sequences_and_empty():
+    """A batch where most sequences have no candidate and one has thousands."""
+    say("rank_hidden skewed batch")
+    B, T, d = 40, 4000, 128
+    rng = np.random.default_rng(11)
+    toks = rng.integers(0, 100000, size=(B, T)).astype(np.int32)
+    toks[7] = rng.integers(0, 2, size=T)
+    lens = np.full(B, T, np.int32)
+    H = synth.f32_to_bf16_bits(rng.standard_normal((B, T, d)).astype(np.float32))
+    cp, cc, nu = oracle.find(toks, lens, 1, 1)
+    assert cc[7] > 1000 and (cc == 0).sum() > 20
+    rsc, rbp, rbs = oracle.rank_hidden(H, lens, cp, cc)
+    gsc, gbp, gbs = gpu_rank_hidden(d_bf16(H), lens, cp, cc)
+    check_scores(gsc, rsc, cc, "skewed")
+    check_best(gbp, gbs, rsc, rbp, rbs, cp, cc, "skewed")
+
+
+# --------------------------------------------------------------- rank attn
+@pytest.mark.parametrize("R,agg", [(1, 0), (7, 0), (40, 0), (64, 1), (9, 1)])
+def test_rank_attn_parity(R, agg):
+    say("rank_attn", R, agg)
+    B, T = 7, 900
+    rng = np.random.default_rng(R * 10 + agg)
+    toks = rng.integers(0, 15, size=(B, T)).astype(np.int32)
+    lens = rng.integers(2, T + 1, size=B).astype(np.int32)
+    lens[0] = T
+    lens[1] = 1
+    A = synth.make_attn(B, R, T, lens, seed=R)
+    cp, cc, nu = oracle.find(toks, lens, 1, 1)
+    rsc, rbp, rbs = oracle.rank_attn(A, lens, cp, cc, agg)
+    gsc, gbp, gbs = gpu_rank_attn(d_f32(A), lens, cp, cc, agg)
+    check_scores(gsc, rsc, cc, f"attn R={R}")
+    check_best(gbp, gbs, rsc, rbp, rbs, cp, cc, f"attn R={R}")
+
+
+def test_rank_attn_strided_keys_and_ties():
+    say("rank_attn strided/ties")
+    B, R, T, pad = 3, 5, 120, 13
+    A = np.zeros((B, R, T + pad), np.float32)
+    A[0, :, 9] = 0.25        # j = 10
+    A[0, :, 49] = 0.25       # j = 50 ties with j = 10 -> 50 wins
+    A[1, 2, 70] = 1.0
+    A[2, :, 5] = 0.5
+    lens = np.array([T, T, T], np.int32)
+    cp = np.full((B, T), -1, np.int32)
+    cp[0, :3] = [10, 30, 50]
+    cp[1, :3] = [10, 71, 119]          # 119 > T-2: unusable
+    cp[2, :2] = [6, 7]
+    cc = np.array([3, 3, 2], np.int32)
+    ad = d_f32(A)[:, :, :T]
+    for agg in (0, 1):
+        rsc, rbp, rbs = oracle.rank_attn(np.ascontiguousarray(A[:, :, :T]), lens, cp, cc, agg)
+        gsc, gbp, gbs = gpu_rank_attn(ad, lens, cp, cc, agg)
+        check_scores(gsc, rsc, cc)
+        assert list(gbp) == list(rbp) == [50, 71, 6]
+
+
+# ------------------------------------------------------------------- emit
+def test_emit_parity():
+    say("emit")
+    rng = np.random.default_rng(3)
+    B, stride = 64, 50
+    toks = rng.integers(0, 1000, size=(B, stride)).astype(np.int32)
+    lens = rng.integers(0, stride + 2, size=B).astype(np.int32)
+    best = np.array([rng.integers(-2, stride + 1) for _ in range(B)], np.int32)
+    best[:4] = [-1, 0, 48, 49]
+    lens[:4] = [50, 50, 50, 50]
+    for K in (1, 5, 16, 64):
+        rd, rl = oracle.emit(toks, lens, best, K)
+        gd, gl = gpu_emit(toks, lens, best, K)
+        assert np.array_equal(gd, rd) and np.array_equal(gl, rl), K
+
+
+# ----------------------------------------------------------------- verify
+VERIFY_CASES = [
+    # (B, K, V, bf16, integer_valued, seed)
+    (3, 4, 1, False, False, 0), (5, 6, 7, False, True, 1), (5, 6, 7, True, True, 2),
+    (4, 10, 1001, False, False, 3), (4, 10, 1001, True, True, 4), (2, 3, 1000003, False, False, 5),
+    (8, 10, 32000, False, False, 6), (6, 16, 128256, True, False, 7), (3, 32, 128256, False, True, 8),
+]
+
+
+@pytest.mark.parametrize("case", VERIFY_CASES, ids=[f"B{c[0]}_K{c[1]}_V{c[2]}_{'bf16' if c[3] else 'f32'}"
+                                                    for c in VERIFY_CASES])
+def test_verify_parity(case):
+    B, K, V, bf16, integer, seed = case
+    say("verify", case)
+    rng = np.random.default_rng(seed)
+    if integer:
+        Z = rng.integers(-3, 4, size=(B, K + 1, V)).astype(np.float32)
+        Z[rng.random(Z.shape) < 0.3] *= -1.0        # signed zeros
+    else:
+        Z = rng.standard_normal((B, K + 1, V)).astype(np.float32)
+    L = rng.integers(0, K + 1, size=B).astype(np.int32)
+    draft = np.full((B, K), -1, np.int32)
+    for b in range(B):
+        draft[b, :L[b]] = rng.integers(0, V, size=L[b])
+        p = rng.integers(0, L[b] + 1)
+        for i in range(p):
+            Z[b, i, draft[b, i]] = 10.0            # accepted prefix
+    if B > 2:
+        L[2] = K + 1                                # invalid draft length
+    zbits = synth.f32_to_bf16_bits(Z) if bf16 else Z
+    ref = oracle.verify(zbits, draft, L, bf16=bf16)
+    zd = d_bf16(zbits) if bf16 else d_f32(Z)
+    check_verify(gpu_verify(zd, draft, L), ref, str(case))
+
+
+def test_verify_misaligned_row_views():
+    """Rows that start off a 16-byte boundary (a view into a padded buffer)."""
+    say("verify misaligned")
+    rng = np.random.default_rng(9)
+    B, K, V = 3, 5, 3001
+    Z = rng.standard_normal((B, K + 1, V + 3)).astype(np.float32)
+    draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+    L = np.array([5, 2, 0], np.int32)
+    for off in (1, 2, 3):
+        view = np.ascontiguousarray(Z[:, :, off:off + V])
+        ref = oracle.verify(view, draft, L)
+        zd = d_f32(Z)[:, :, off:off + V]
+        check_verify(gpu_verify(zd, draft, L), ref, f"offset {off}")
+        zb = synth.f32_to_bf16_bits(Z)
+        refb = oracle.verify(np.ascontiguousarray(zb[:, :, off:off + V]), draft, L, bf16=True)
+        check_verify(gpu_verify(d_bf16(zb)[:, :, off:off + V], draft, L), refb, f"bf16 offset {off}")
+
+
+def test_verify_all_equal_rows_and_negative_infinity():
+    say("verify degenerate rows")
+    B, K, V = 2, 3, 777
+    Z = np.full((B, K + 1, V), -np.inf, np.float32)
+    Z[1] = 0.0
+    Z[1, :, ::2] = -0.0
+    draft = np.array([[0, 0, 0], [0, 0, 5]], np.int32)
+    L = np.array([3, 3], np.int32)
+    ref = oracle.verify(Z, draft, L)
+    assert list(ref[0]) == [3, 2]
+    check_verify(gpu_verify(d_f32(Z), draft, L), ref, "degenerate")
+
+
+def test_workspace_shared_across_calls_and_determinism():
+    """One workspace serves every call in turn and is zero after each; repeated
+    calls give bit-identical results."""
+    say("shared workspace")
+    cfg = synth.Config("t", 4, 3000, 500, 1.1, 0.3, (8, 32), (1, 2), 256, "hidden", 0, 8, "f32", 21)
+    toks, lens, metas = synth.make_tokens(cfg)
+    ws = workspace(cfg.B, cfg.T, cfg.K)
+    H = synth.make_hidden(cfg.B, cfg.T, cfg.d, cfg.seed, device="cuda")
+    runs = []
+    for _ in range(3):
+        cp, cc, nu = gpu_find(toks, lens, 1, 2, ws=ws)
+        sc, bp, bs = gpu_rank_hidden(H, lens, cp, cc, ws=ws)
+        runs.append((cp.copy(), cc.copy(), sc.copy(), bp.copy(), bs.copy()))
+    for r in runs[1:]:
+        for x, y in zip(r, runs[0]):
+            assert np.array_equal(x, y, equal_nan=True)
