@@ -1,0 +1,271 @@
+#!/usr/bin/env python3
+"""Benchmark of the PLD+ drafting step (find -> rank -> emit -> verify) on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config C] [--no-cpu-baseline]
+
+A step is one pass of the whole hot path over one batch of synthetic input
+already resident in HBM.  The default workload is config 2 (batch 8, context
+4096, n-grams 3..1 longest first, hidden 4096 bf16, K = 10, fp32 logits over
+32000 ids); --config picks another of the five.  To keep the caches honest the
+inputs exist in several copies at distinct addresses and consecutive steps
+rotate through them, so every step reads from HBM rather than from the 256 MB
+last-level cache.  W untimed steps run first, then exactly K steps are timed
+between two device synchronisations; HIP events on the launch stream time the
+dominant kernel inside that region.  One JSON line goes to stdout.
+
+The CPU oracle (test infrastructure) is timed on the host on the same inputs
+as a reported baseline, unless --no-cpu-baseline.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "draft+verify step latency (us) per batch; ranking-kernel HBM GB/s vs peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+MALL_BYTES = 256 << 20         # last-level (Infinity) cache
+SEG = 64                       # smallest HBM read granule counted for gathered data
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=10.0,
+                   help="CPU work the oracle baseline is given (whole steps, at least one)")
+    p.add_argument("--copy-probe", action="store_true",
+                   help="after the timed region, copy 1 GiB three times (counter calibration)")
+    p.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    return p.parse_args()
+
+
+def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits):
+    """What each kernel must move per step (never the dense work it avoids)."""
+    import numpy as np
+    B = cfg.B
+    C = cand_count.astype(np.int64)
+    out = {}
+    out["find"] = int(lens.astype(np.int64).sum() * 4 + C.sum() * 4)
+    if cfg.rank in ("hidden", "both"):
+        out["rank_hidden"] = int(((C + (C > 0)) * cfg.d * 2).sum() + C.sum() * 4)
+    if cfg.rank in ("attn", "both"):
+        # distinct 64-byte segments of each attention row that hold a key j-1
+        segs = 0
+        for b in range(B):
+            keys = cand_pos[b, :C[b]].astype(np.int64) - 1
+            segs += len(np.unique((keys * 4) // SEG))
+        out["rank_attn"] = int(segs * cfg.R * SEG + C.sum() * 4)
+    out["emit"] = int(B * cfg.K * 4 * 2)
+    out["verify"] = int(((draft_len.astype(np.int64) + 1) * cfg.V * elt_logits).sum())
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the drafting step has no cross-GPU exchange in "
+              "this build (see the sharding notes); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2412_01447_amd.step import DraftStep
+
+    cfg = synth.CONFIGS[args.config]
+    dev = torch.device("cuda:0")
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    log(f"[bench] config {args.config}: {cfg.name}")
+    t0 = time.time()
+    w = synth.make_workload(cfg, dev, structured=True)
+    toks, lens = w["tokens"], w["lens"]
+    draft_i, dlen_i = synth.intended_drafts(w["metas"], cfg.K)
+    z = synth.logits_for(w, draft_i, dlen_i)
+    bf16 = cfg.logits == "bf16"
+    elt = 2 if bf16 else 4
+    log(f"[bench] inputs generated in {time.time() - t0:.1f}s")
+
+    def dev_logits(a):
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16) if bf16 else a).to(dev)
+        return t.view(torch.bfloat16) if bf16 else t
+
+    base = dict(tokens=torch.from_numpy(toks).to(dev), lens=torch.from_numpy(lens).to(dev),
+                logits=dev_logits(z), hidden=w["hidden"],
+                attn=torch.from_numpy(w["attn"]).to(dev) if w["attn"] is not None else None)
+    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev)
+
+    def run(s):
+        step.run(s["tokens"], s["lens"], s["logits"], hidden=s["hidden"], attn=s["attn"],
+                 ngram=cfg.ngram)
+
+    # one step to learn the data-dependent byte counts
+    run(base)
+    torch.cuda.synchronize()
+    nbytes = algorithmic_bytes(cfg, lens, step.cand_count.cpu().numpy(),
+                               step.draft_len.cpu().numpy(), step.cand_pos.cpu().numpy(), elt)
+    step_bytes = sum(nbytes.values())
+    dominant = max(nbytes, key=nbytes.get)
+    # input copies at distinct addresses: the steps of one rotation touch at
+    # least four times the last-level cache
+    copies = int(min(64, max(2, math.ceil(4 * MALL_BYTES / max(step_bytes, 1)))))
+    sets = [base]
+    for _ in range(copies - 1):
+        sets.append({k: (v.clone() if v is not None else None) for k, v in base.items()})
+    torch.cuda.synchronize()
+    log(f"[bench] step bytes {step_bytes / 1e6:.2f} MB {json.dumps(nbytes)}; "
+        f"dominant {dominant}; {copies} input copies")
+
+    ops = {
+        "find": lambda s: step.find(s["tokens"], s["lens"], *cfg.ngram),
+        "rank_attn": lambda s: step.rank_attn(s["attn"], s["lens"], into_best=s["hidden"] is None),
+        "rank_hidden": lambda s: step.rank_hidden(s["hidden"], s["lens"]),
+        "emit": lambda s: step.emit(s["tokens"], s["lens"]),
+        "verify": lambda s: step.verify(s["logits"]),
+    }
+    order = ["find"] + [o for o in ("rank_attn", "rank_hidden") if o in nbytes] + ["emit", "verify"]
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+
+    def timed_step(k, s):
+        for o in order:
+            if o == dominant:
+                ev[k][0].record(stream)
+                ops[o](s)
+                ev[k][1].record(stream)
+            else:
+                ops[o](s)
+
+    graph = None
+    if args.graph:
+        # one graph per input copy; replays need no launches from the host
+        graphs = []
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            for s in sets:
+                run(s)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        for s in sets:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                run(s)
+            graphs.append(g)
+        graph = graphs
+
+    for k in range(args.warmup):
+        if graph:
+            graph[k % copies].replay()
+        else:
+            run(sets[k % copies])
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        if graph:
+            graph[k % copies].replay()
+        else:
+            timed_step(k, sets[k % copies])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    dom_ms = None
+    if not graph:
+        dom_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+    # correctness guard: the timed steps must produce what the first step did
+    torch.cuda.synchronize()
+
+    roofline = None
+    if dom_ms is not None:
+        achieved = nbytes[dominant] / (dom_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": None, "bytes_per_launch": nbytes[dominant],
+                    "avg_us": round(dom_ms * 1e3, 2)}
+        log(f"[bench] {dominant}: {dom_ms * 1e3:.2f} us avg, {achieved:.1f} GB/s")
+
+    if args.copy_probe:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] copy probe: 3 x 1 GiB device copies done")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, w, z, bf16, args.cpu_seconds, log)
+
+    line = {
+        "metric": METRIC, "value": round(ms_per_step * 1e3, 2), "unit": "us", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": cfg.B, "context": cfg.T, "vocab": cfg.V,
+                   "ngram": list(cfg.ngram), "ranking": cfg.rank, "hidden_dim": cfg.d,
+                   "attn_rows": cfg.R, "K": cfg.K, "logits": cfg.logits,
+                   "inputs": "hidden bf16, attention f32, tokens int32",
+                   "graph": bool(graph), "input_copies": copies,
+                   "step_bytes": step_bytes},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(cfg, w, z, bf16, seconds, log):
+    """The oracle's whole step on the host, single-threaded, on the same inputs."""
+    import numpy as np
+    import torch
+
+    import oracle
+    toks, lens = w["tokens"], w["lens"]
+    cp, cc, nu = oracle.find(toks, lens, *cfg.ngram)
+    hb = None
+    if w["hidden"] is not None:
+        # the rows the step reads (H[T-2] and H[j-1]); the others stay zero pages
+        B, T, d = w["hidden"].shape
+        hb = np.zeros((B, T, d), np.uint16)
+        for b in range(B):
+            rows = sorted({int(lens[b]) - 2} | {int(j) - 1 for j in cp[b, :cc[b]]})
+            idx = torch.tensor(rows, device=w["hidden"].device)
+            hb[b, rows] = w["hidden"][b].index_select(0, idx).view(torch.int16).cpu().numpy() \
+                .view(np.uint16)
+    attn = w["attn"]
+
+    def one():
+        p, c, n = oracle.find(toks, lens, *cfg.ngram)
+        if attn is not None:
+            sa, ba, _ = oracle.rank_attn(attn, lens, p, c, oracle.AGG_SUM)
+            best = ba
+        if hb is not None:
+            sh, bh, _ = oracle.rank_hidden(hb, lens, p, c)
+            best = bh
+        dr, dl = oracle.emit(toks, lens, best, cfg.K)
+        oracle.verify(z, dr, dl, bf16=bf16)
+
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        one()
+        n += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = (time.perf_counter() - t0) / n
+    log(f"[bench] cpu oracle: {n} whole steps, {dt * 1e3:.2f} ms per step")
+    return {"value": round(dt * 1e6, 1), "unit": "us", "cores": 1, "kind": "oracle",
+            "sample": f"{n} whole steps of the same workload (all {cfg.B} sequences), "
+                      f"single-threaded C oracle in fp64"}
+
+
+if __name__ == "__main__":
+    main()

@@ -24,11 +24,16 @@
  * - Host-checkable faults return a non-zero pld_status and enqueue nothing.
  *   Faults only visible on the device (bad lengths, positions, counts) are
  *   reported through the outputs as documented per call.
- * - `workspace` is device scratch of at least pld_workspace_bytes(...)
- *   bytes.  It must be zero-filled once after allocation; every call returns
- *   it to all-zero when its kernels complete, so one buffer serves every call
- *   of a stream in turn.  Two calls in flight at once (on different streams)
- *   must not share a workspace.
+ * - `workspace` (ranking and verification calls) is device memory of at
+ *   least pld_workspace_bytes(B, K) bytes.  It must be zero-filled once after
+ *   allocation; every call returns it to all-zero by the time its kernels
+ *   complete, so one buffer serves every such call of a stream in turn.
+ * - `scratch` (occurrence search) is device memory of at least
+ *   pld_find_scratch_bytes(B, tok_stride) bytes with no requirement on its
+ *   contents; it may be NULL when that size is 0.  It must not overlap a
+ *   workspace.
+ * - Two calls in flight at once (on different streams) must not share a
+ *   workspace or a scratch buffer.
  * - Results are deterministic: the same inputs give bit-identical outputs.
  */
 #ifndef PLD_H
@@ -58,7 +63,7 @@ enum { PLD_AGG_SUM = 0, PLD_AGG_MAX = 1 };
 
 /* Limits checked on the host. */
 #define PLD_MAX_NGRAM 8         /* ngram_max <= 8                                    */
-#define PLD_MAX_HIDDEN 16384    /* d <= 16384 (the query row is staged in LDS, fp32) */
+#define PLD_MAX_HIDDEN 16384    /* d <= 16384 (the query row is staged in LDS)       */
 #define PLD_MAX_BATCH 4096      /* B <= 4096 for the ranking calls                   */
 
 /* Version of this ABI (major * 10000 + minor * 100 + patch). */
@@ -68,11 +73,18 @@ int pld_version(void);
 const char *pld_status_string(int status);
 
 /*
- * Bytes of workspace for calls with batch B, token stride tok_stride and
- * draft length K (the largest any call on the buffer will use).  Returns 0
- * when an argument is out of range.
+ * Bytes of workspace for the ranking and verification calls with batch B and
+ * draft length K (size it for the largest B and K used on the buffer).
+ * Returns 0 when an argument is out of range.
  */
-size_t pld_workspace_bytes(int B, int64_t tok_stride, int K);
+size_t pld_workspace_bytes(int B, int K);
+
+/*
+ * Bytes of scratch pld_find_candidates needs for batch B and token stride
+ * tok_stride: 0 up to tok_stride = 8192 (one block per sequence), else the
+ * per-tile occurrence counts.  Returns 0 when an argument is out of range.
+ */
+size_t pld_find_scratch_bytes(int B, int64_t tok_stride);
 
 /*
  * pld_find_candidates -- the occurrence set P (Eq. 1, Sec. 4.2), with
@@ -89,13 +101,15 @@ size_t pld_workspace_bytes(int B, int64_t tok_stride, int K);
  *   cand_count  int32 [B], |P|
  *   ngram_used  int32 [B], the n that produced P; 0 when no n has an occurrence;
  *               -1 when lens[b] is outside [1, tok_stride] (then cand_count = 0)
- * Errors: PLD_ERR_INVALID for NULL pointers, B < 1, tok_stride < 1, bad n range
- * or cap < tok_stride; PLD_ERR_WORKSPACE; PLD_ERR_LAUNCH.
+ *   scratch     see the conventions above (pld_find_scratch_bytes)
+ * Errors: PLD_ERR_INVALID for NULL pointers, B outside [1, 65535], tok_stride
+ * outside [1, 2^30], a bad n range or cap < tok_stride; PLD_ERR_WORKSPACE when
+ * the scratch is missing or too small; PLD_ERR_LAUNCH.
  */
 int pld_find_candidates(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B,
                         int ngram_min, int ngram_max, int32_t *cand_pos, int64_t cap,
-                        int32_t *cand_count, int32_t *ngram_used, void *workspace,
-                        size_t workspace_bytes, void *stream);
+                        int32_t *cand_count, int32_t *ngram_used, void *scratch,
+                        size_t scratch_bytes, void *stream);
 
 /*
  * pld_rank_hidden -- hidden-state ranking, Eq. 2 (Sec. 4.2.2):

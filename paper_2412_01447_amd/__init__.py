@@ -15,7 +15,8 @@ import os
 
 __all__ = [
     "PLDError", "PLD_F32", "PLD_BF16", "PLD_AGG_SUM", "PLD_AGG_MAX", "library_path",
-    "pld_version", "pld_status_string", "pld_workspace_bytes", "pld_find_candidates",
+    "pld_version", "pld_status_string", "pld_workspace_bytes", "pld_find_scratch_bytes",
+    "pld_find_candidates",
     "pld_rank_hidden", "pld_rank_attn", "pld_emit_draft", "pld_verify_greedy",
 ]
 
@@ -34,7 +35,8 @@ _vp, _i64, _int, _sz, _f32 = (ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, cty
 _SIGNATURES = {
     "pld_version": ([], _int),
     "pld_status_string": ([_int], ctypes.c_char_p),
-    "pld_workspace_bytes": ([_int, _i64, _int], _sz),
+    "pld_workspace_bytes": ([_int, _int], _sz),
+    "pld_find_scratch_bytes": ([_int, _i64], _sz),
     "pld_find_candidates": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _vp, _vp, _vp, _sz, _vp],
                             _int),
     "pld_rank_hidden": ([_vp, _i64, _i64, _i64, _int, _vp, _vp, _i64, _vp, _int, _f32, _vp, _vp,
@@ -102,12 +104,20 @@ def pld_status_string(status):
     return _load().pld_status_string(status).decode()
 
 
-def pld_workspace_bytes(B, tok_stride, K):
-    return int(_load().pld_workspace_bytes(B, tok_stride, K))
+def pld_workspace_bytes(B, K):
+    return int(_load().pld_workspace_bytes(B, K))
+
+
+def pld_find_scratch_bytes(B, tok_stride):
+    return int(_load().pld_find_scratch_bytes(B, tok_stride))
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
 
 
 def pld_find_candidates(tokens, lens, ngram_min, ngram_max, cand_pos, cand_count, ngram_used,
-                        workspace, stream=None):
+                        scratch=None, stream=None):
     """tokens int32 [B][tok_stride]; writes cand_pos [B][cap], cand_count [B], ngram_used [B]."""
     import torch
     _need(tokens, torch.int32, "tokens", 2)
@@ -115,7 +125,7 @@ def pld_find_candidates(tokens, lens, ngram_min, ngram_max, cand_pos, cand_count
     B = tokens.shape[0]
     _call("pld_find_candidates", _ptr(tokens), tokens.stride(0), _ptr(lens), B, ngram_min,
           ngram_max, _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), _ptr(ngram_used),
-          _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
+          _ptr(scratch), _nbytes(scratch), _stream(stream))
 
 
 def pld_rank_hidden(hidden, lens, cand_pos, cand_count, best_pos, best_score, workspace,
@@ -128,7 +138,7 @@ def pld_rank_hidden(hidden, lens, cand_pos, cand_count, best_pos, best_score, wo
     _call("pld_rank_hidden", _ptr(hidden), hidden.stride(0), hidden.stride(1), n_rows, d,
           _ptr(lens), _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), B, float(threshold),
           _ptr(scores), _ptr(best_pos), _ptr(best_score), _ptr(workspace),
-          workspace.numel() * workspace.element_size(), _stream(stream))
+          _nbytes(workspace), _stream(stream))
 
 
 def pld_rank_attn(attn, lens, cand_pos, cand_count, best_pos, best_score, workspace,
@@ -141,7 +151,7 @@ def pld_rank_attn(attn, lens, cand_pos, cand_count, best_pos, best_score, worksp
     _call("pld_rank_attn", _ptr(attn), attn.stride(0), attn.stride(1), n_keys, R, int(agg),
           _ptr(lens), _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), B, float(threshold),
           _ptr(scores), _ptr(best_pos), _ptr(best_score), _ptr(workspace),
-          workspace.numel() * workspace.element_size(), _stream(stream))
+          _nbytes(workspace), _stream(stream))
 
 
 def pld_emit_draft(tokens, lens, best_pos, K, draft, draft_len, stream=None):
@@ -171,4 +181,4 @@ def pld_verify_greedy(logits, draft, draft_len, accept_len, out_tokens, out_coun
     dtype = PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
     _call("pld_verify_greedy", _ptr(logits), dtype, logits.stride(0), logits.stride(1), V, K,
           _ptr(draft), _ptr(draft_len), B, _ptr(accept_len), _ptr(out_tokens), _ptr(out_count),
-          _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
+          _ptr(workspace), _nbytes(workspace), _stream(stream))

@@ -14,26 +14,25 @@ constexpr int kWave = 64;
 constexpr int kMaxNgram = 8;                   // equals PLD_MAX_NGRAM
 constexpr int64_t kMaxTokStride = 1ll << 30;   // positions are stored as int32
 
-// Workspace layout: every call uses the buffer from offset 0 and leaves it
-// zero when its kernels finish (see pld.h).
+// Tiling of the occurrence search.
 constexpr int kFindTile = 2048;          // positions per block, multi-block find
 constexpr int kFindWavesTiled = 4;       // 256 threads, 512 positions per wave
 constexpr int kFindWavesFused = 16;      // 1024 threads, one block per sequence
-constexpr int kFindFusedMax = kFindWavesFused * 512;  // T <= 8192 takes the fused path
+constexpr int kFindFusedMax = kFindWavesFused * 512;  // tok_stride <= 8192: fused path
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-inline size_t find_ws_bytes(int B, int64_t tok_stride) {
-    int64_t ntiles = (tok_stride + kFindTile - 1) / kFindTile;
-    return align_up((size_t)B * (size_t)ntiles * 8 * sizeof(int32_t), 256) +
-           align_up((size_t)B * sizeof(uint32_t), 256);
+// Scratch of the multi-block find: per-tile occurrence counts of every n.
+inline size_t find_scratch_bytes(int B, int64_t tok_stride) {
+    if (tok_stride <= kFindFusedMax) return 0;
+    const int64_t ntiles = (tok_stride + kFindTile - 1) / kFindTile;
+    return align_up((size_t)B * (size_t)ntiles * 8 * sizeof(int32_t), 256);
 }
-inline size_t rank_ws_bytes(int B) {
-    return align_up((size_t)B * sizeof(uint64_t), 256) + 256;
-}
+// Workspace of the ranking and verification calls: 64-bit keys that must be
+// zero when a call starts and that the call leaves zero.
+inline size_t rank_ws_bytes(int B) { return align_up((size_t)B * sizeof(uint64_t), 256); }
 inline size_t verify_ws_bytes(int B, int K) {
-    return align_up((size_t)B * (size_t)(K + 1) * sizeof(uint64_t), 256) +
-           align_up((size_t)B * sizeof(uint32_t), 256);
+    return align_up((size_t)B * (size_t)(K + 1) * sizeof(uint64_t), 256);
 }
 
 // ---------------------------------------------------------------- keys
@@ -96,11 +95,5 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
-
-// Device-scope atomic read-and-clear, used by the last block of a call to
-// collect a result and leave the workspace zero.
-__device__ __forceinline__ uint64_t take_u64(uint64_t *p) {
-    return __hip_atomic_exchange(p, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 }  // namespace pld

@@ -9,14 +9,15 @@
 // ngram_max] with a non-zero count wins, and its occurrences are compacted in
 // ascending order.
 //
+// The tokens a block needs are first copied to LDS with independent loads, so
+// the backwards comparisons never wait on a chain of global loads.
 // Compaction is a wave ballot (one bit per lane, 64 positions per ballot), a
 // popcount of the lower lanes' bits for the lane's slot, and an exclusive
 // scan of per-wave and per-block counts.  Sequences up to kFindFusedMax
 // tokens take one 1024-thread block each (count, pick n, compact, in one
 // kernel); longer ones split into kFindTile-position blocks: a count kernel
-// writes per-tile counts to the workspace, and the compaction kernel derives
-// its tile's output offset from the counts of the tiles before it.  The last
-// compaction block of a sequence returns its workspace slice to zero.
+// writes per-tile counts to the scratch buffer, and the compaction kernel
+// derives its tile's output offset from the counts of the tiles before it.
 #include "pld.h"
 #include "pld_device.h"
 
@@ -32,49 +33,56 @@ struct FindArgs {
     int64_t cap;
     int32_t *cand_count;
     int32_t *ngram_used;
-    int32_t *tile_counts;   // [B][ntiles][8]
-    uint32_t *tickets;      // [B]
+    int32_t *tile_counts;   // [B][ntiles][8], scratch
     int ntiles;
 };
 
-// The query read backwards: qry[k] = x[T-1-k] (only read where it exists).
+// Copies x[lo, hi) of one sequence into s[0, hi-lo) (block-wide).
+__device__ __forceinline__ void stage_tokens(const int32_t *x, int64_t lo, int64_t hi, int32_t *s) {
+    const int n = (int)(hi - lo);
+    constexpr int U = 8;
+    for (int i0 = threadIdx.x; i0 < n; i0 += blockDim.x * U) {
+        int32_t v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            int i = i0 + u * blockDim.x;
+            v[u] = i < n ? x[lo + i] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            int i = i0 + u * blockDim.x;
+            if (i < n) s[i] = v[u];
+        }
+    }
+}
+
+// The query read backwards: q.v[k] = x[T-1-k] for k < nmax (0 beyond T).
 struct Query {
     int32_t v[kMaxNgram];
 };
 
-__device__ __forceinline__ Query load_query(const int32_t *x, int64_t T, int nmax) {
-    Query q;
-#pragma unroll
-    for (int k = 0; k < kMaxNgram; ++k) q.v[k] = (k < nmax && T - 1 - k >= 0) ? x[T - 1 - k] : 0;
-    return q;
-}
-
-// m(p) for an in-range position (1 <= p <= T-2): the loop stops at the first
-// disagreement, at the start of the sequence, or at nmax.  p - k >= 0 with
-// p <= T-2 implies T-1-k >= 1, so q.v[k] is always a real query token.
-__device__ __forceinline__ int match_len(const int32_t *x, int64_t p, const Query &q, int nmax) {
-    int m = 0;
-    bool go = true;
-#pragma unroll
-    for (int k = 0; k < kMaxNgram; ++k) {
-        if (k < nmax && go) {
-            int64_t s = p - k;
-            go = (s >= 0) && (x[s] == q.v[k]);
-            m += go ? 1 : 0;
-        }
-    }
-    return m;
-}
-
-// Match lengths of the 512 positions of one wave: m[it] belongs to position
-// base + it*64 + lane (0 when the position is not a possible occurrence).
-__device__ __forceinline__ void wave_match(const int32_t *x, int64_t T, int64_t base,
+// m(p) for the 512 positions of one wave: m[it] belongs to position
+// base + it*64 + lane (0 when p is not in [1, T-2]).  `s` holds x[s0 ...].
+// p - k >= 0 with p <= T-2 implies T-1-k >= 1, so q.v[k] is a real token.
+__device__ __forceinline__ void wave_match(const int32_t *s, int64_t s0, int64_t T, int64_t base,
                                            const Query &q, int nmax, int (&m)[8]) {
     const int lane = lane_id();
 #pragma unroll
     for (int it = 0; it < 8; ++it) {
-        int64_t p = base + it * kWave + lane;
-        m[it] = (p >= 1 && p <= T - 2) ? match_len(x, p, q, nmax) : 0;
+        const int64_t p = base + it * kWave + lane;
+        int len = 0;
+        if (p >= 1 && p <= T - 2) {
+            bool go = true;
+#pragma unroll
+            for (int k = 0; k < kMaxNgram; ++k) {
+                if (k < nmax && go) {
+                    const int64_t t = p - k;
+                    go = (t >= 0) && (s[t - s0] == q.v[k]);
+                    len += go ? 1 : 0;
+                }
+            }
+        }
+        m[it] = len;
     }
 }
 
@@ -91,6 +99,13 @@ __device__ __forceinline__ void wave_level_counts(const int (&m)[8], int nmax, i
     }
 }
 
+__device__ __forceinline__ int wave_hits(const int (&m)[8], int n) {
+    int c = 0;
+#pragma unroll
+    for (int it = 0; it < 8; ++it) c += __popcll(__ballot(m[it] >= n));
+    return c;
+}
+
 // Writes the occurrences (m >= n) of one wave's positions to out + start, in
 // ascending order.
 __device__ __forceinline__ void wave_emit(const int (&m)[8], int n, int64_t base, int32_t *out,
@@ -100,22 +115,16 @@ __device__ __forceinline__ void wave_emit(const int (&m)[8], int n, int64_t base
     int64_t run = start;
 #pragma unroll
     for (int it = 0; it < 8; ++it) {
-        uint64_t mk = __ballot(m[it] >= n);
+        const uint64_t mk = __ballot(m[it] >= n);
         if ((mk >> lane) & 1ull) out[run + __popcll(mk & lt)] = (int32_t)(base + it * kWave + lane);
         run += __popcll(mk);
     }
 }
 
-__device__ __forceinline__ int wave_hits(const int (&m)[8], int n) {
-    int c = 0;
-#pragma unroll
-    for (int it = 0; it < 8; ++it) c += __popcll(__ballot(m[it] >= n));
-    return c;
-}
-
 // ---------------------------------------------------------------- fused
 // One 1024-thread block per sequence, tok_stride <= kFindFusedMax.
 __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(FindArgs a) {
+    __shared__ int32_t s_x[kFindFusedMax];
     __shared__ int s_lvl[kFindWavesFused][kMaxNgram];
     __shared__ int s_wc[kFindWavesFused];
     const int b = blockIdx.x;
@@ -130,10 +139,14 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
         }
         return;
     }
-    const Query q = load_query(x, T, a.nmax);
+    stage_tokens(x, 0, T, s_x);
+    __syncthreads();
+    Query q;
+#pragma unroll
+    for (int k = 0; k < kMaxNgram; ++k) q.v[k] = (k < a.nmax && T - 1 - k >= 0) ? s_x[T - 1 - k] : 0;
     const int64_t base = (int64_t)w * 512;
     int m[8];
-    wave_match(x, T, base, q, a.nmax, m);
+    wave_match(s_x, 0, T, base, q, a.nmax, m);
     int cnt[8];
     wave_level_counts(m, a.nmax, cnt);
     if (lane == 0) {
@@ -141,7 +154,7 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
         for (int k = 0; k < kMaxNgram; ++k) s_lvl[w][k] = cnt[k];
     }
     __syncthreads();
-    // pick the longest n with an occurrence (every thread, same answer)
+    // the longest n with an occurrence (every thread, same answer)
     int n_used = 0, total = 0;
     for (int n = a.nmax; n >= a.nmin; --n) {
         int t = 0;
@@ -153,7 +166,7 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
         }
     }
     if (n_used > 0) {
-        int wc = wave_hits(m, n_used);
+        const int wc = wave_hits(m, n_used);
         if (lane == 0) s_wc[w] = wc;
         __syncthreads();
         int64_t start = 0;
@@ -167,21 +180,39 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
 }
 
 // ---------------------------------------------------------------- tiled
+// A tile covers positions [tile*kFindTile, (tile+1)*kFindTile); its LDS copy
+// starts kMaxNgram-1 tokens earlier so the backwards comparisons stay inside.
+constexpr int kHalo = kMaxNgram - 1;
+
+__device__ __forceinline__ int64_t tile_lo(int tile) {
+    int64_t lo = (int64_t)tile * kFindTile - kHalo;
+    return lo < 0 ? 0 : lo;
+}
+
 __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_count_kernel(FindArgs a) {
+    __shared__ int32_t s_x[kFindTile + kHalo];
     __shared__ int s_lvl[kFindWavesTiled][kMaxNgram];
     const int tile = blockIdx.x, b = blockIdx.y;
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
     const int64_t T = a.lens[b];
-    const int64_t base = (int64_t)tile * kFindTile + (int64_t)w * 512;
+    const int64_t t0 = (int64_t)tile * kFindTile;
+    const bool live = (T >= 1 && T <= a.tok_stride && t0 <= T - 2);
     int cnt[8];
 #pragma unroll
     for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
-    if (T >= 1 && T <= a.tok_stride && base <= T - 2) {
-        const Query q = load_query(x, T, a.nmax);
+    if (live) {   // block-uniform
+        const int64_t lo = tile_lo(tile);
+        const int64_t hi = (t0 + kFindTile < T - 1) ? t0 + kFindTile : T - 1;
+        stage_tokens(x, lo, hi, s_x);
+        Query q;
+#pragma unroll
+        for (int k = 0; k < kMaxNgram; ++k)
+            q.v[k] = (k < a.nmax && T - 1 - k >= 0) ? x[T - 1 - k] : 0;
+        __syncthreads();
         int m[8];
-        wave_match(x, T, base, q, a.nmax, m);
+        wave_match(s_x, lo, T, t0 + (int64_t)w * 512, q, a.nmax, m);
         wave_level_counts(m, a.nmax, cnt);
     }
     if (lane == 0) {
@@ -197,23 +228,29 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_count_kernel(Fin
 }
 
 __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_compact_kernel(FindArgs a) {
+    __shared__ int32_t s_x[kFindTile + kHalo];
     __shared__ int s_tot[kMaxNgram];
     __shared__ int s_pre[kMaxNgram];
     __shared__ int s_wc[kFindWavesTiled];
-    __shared__ int s_last;
     const int tile = blockIdx.x, b = blockIdx.y;
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
     const int64_t T = a.lens[b];
+    if (T < 1 || T > a.tok_stride) {   // block-uniform
+        if (tile == 0 && threadIdx.x == 0) {
+            a.cand_count[b] = 0;
+            a.ngram_used[b] = -1;
+        }
+        return;
+    }
     const int32_t *tc = a.tile_counts + (int64_t)b * a.ntiles * kMaxNgram;
     if (threadIdx.x < kMaxNgram) {
         s_tot[threadIdx.x] = 0;
         s_pre[threadIdx.x] = 0;
     }
     __syncthreads();
-    const bool valid = (T >= 1 && T <= a.tok_stride);
-    if (valid) {
+    {
         // totals over all tiles, and over the tiles before this one
         int tot[8], pre[8];
 #pragma unroll
@@ -221,7 +258,7 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_compact_kernel(F
         for (int t = threadIdx.x; t < a.ntiles; t += blockDim.x) {
 #pragma unroll
             for (int k = 0; k < kMaxNgram; ++k) {
-                int v = tc[(int64_t)t * kMaxNgram + k];
+                const int v = tc[(int64_t)t * kMaxNgram + k];
                 tot[k] += v;
                 if (t < tile) pre[k] += v;
             }
@@ -241,50 +278,36 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_compact_kernel(F
         }
     }
     __syncthreads();
-    if (valid) {
-        int n_used = 0;
-        for (int n = a.nmax; n >= a.nmin; --n) {
-            if (s_tot[n - 1] > 0) {
-                n_used = n;
-                break;
-            }
+    int n_used = 0;
+    for (int n = a.nmax; n >= a.nmin; --n) {
+        if (s_tot[n - 1] > 0) {
+            n_used = n;
+            break;
         }
-        const int64_t base = (int64_t)tile * kFindTile + (int64_t)w * 512;
+    }
+    const int64_t t0 = (int64_t)tile * kFindTile;
+    if (n_used > 0 && t0 <= T - 2) {   // block-uniform
+        const int64_t lo = tile_lo(tile);
+        const int64_t hi = (t0 + kFindTile < T - 1) ? t0 + kFindTile : T - 1;
+        stage_tokens(x, lo, hi, s_x);
+        Query q;
+#pragma unroll
+        for (int k = 0; k < kMaxNgram; ++k)
+            q.v[k] = (k < a.nmax && T - 1 - k >= 0) ? x[T - 1 - k] : 0;
+        __syncthreads();
+        const int64_t base = t0 + (int64_t)w * 512;
         int m[8];
-        int wc = 0;
-        if (n_used > 0 && (int64_t)tile * kFindTile <= T - 2) {
-            const Query q = load_query(x, T, a.nmax);
-            wave_match(x, T, base, q, a.nmax, m);
-            wc = wave_hits(m, n_used);
-        }
+        wave_match(s_x, lo, T, base, q, a.nmax, m);
+        const int wc = wave_hits(m, n_used);
         if (lane == 0) s_wc[w] = wc;
         __syncthreads();
-        if (wc > 0) {
-            int64_t start = s_pre[n_used - 1];
-            for (int i = 0; i < w; ++i) start += s_wc[i];
-            wave_emit(m, n_used, base, a.cand_pos + (int64_t)b * a.cap, start);
-        }
-        if (tile == 0 && threadIdx.x == 0) {
-            a.cand_count[b] = n_used > 0 ? s_tot[n_used - 1] : 0;
-            a.ngram_used[b] = n_used;
-        }
-    } else if (tile == 0 && threadIdx.x == 0) {
-        a.cand_count[b] = 0;
-        a.ngram_used[b] = -1;
+        int64_t start = s_pre[n_used - 1];
+        for (int i = 0; i < w; ++i) start += s_wc[i];
+        wave_emit(m, n_used, base, a.cand_pos + (int64_t)b * a.cap, start);
     }
-    // The last block of this sequence to finish clears its workspace slice.
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t t = __hip_atomic_fetch_add(&a.tickets[b], 1u, __ATOMIC_ACQ_REL,
-                                            __HIP_MEMORY_SCOPE_AGENT);
-        s_last = (t == (uint32_t)a.ntiles - 1u);
-    }
-    __syncthreads();
-    if (s_last) {
-        int32_t *mine = a.tile_counts + (int64_t)b * a.ntiles * kMaxNgram;
-        for (int i = threadIdx.x; i < a.ntiles * kMaxNgram; i += blockDim.x) mine[i] = 0;
-        if (threadIdx.x == 0) a.tickets[b] = 0u;
+    if (tile == 0 && threadIdx.x == 0) {
+        a.cand_count[b] = n_used > 0 ? s_tot[n_used - 1] : 0;
+        a.ngram_used[b] = n_used;
     }
 }
 
@@ -292,12 +315,17 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_compact_kernel(F
 
 using namespace pld;
 
+extern "C" size_t pld_find_scratch_bytes(int B, int64_t tok_stride) {
+    if (B < 1 || tok_stride < 1 || tok_stride > kMaxTokStride) return 0;
+    return find_scratch_bytes(B, tok_stride);
+}
+
 extern "C" int pld_find_candidates(const int32_t *tokens, int64_t tok_stride, const int32_t *lens,
                                    int B, int ngram_min, int ngram_max, int32_t *cand_pos,
                                    int64_t cap, int32_t *cand_count, int32_t *ngram_used,
-                                   void *workspace, size_t workspace_bytes, void *stream) {
+                                   void *scratch, size_t scratch_bytes, void *stream) {
     if (!tokens || !lens || !cand_pos || !cand_count || !ngram_used) return PLD_ERR_INVALID;
-    if (B < 1 || tok_stride < 1 || tok_stride > kMaxTokStride) return PLD_ERR_INVALID;
+    if (B < 1 || B > 65535 || tok_stride < 1 || tok_stride > kMaxTokStride) return PLD_ERR_INVALID;
     if (ngram_min < 1 || ngram_max < ngram_min || ngram_max > PLD_MAX_NGRAM) return PLD_ERR_INVALID;
     if (cap < tok_stride) return PLD_ERR_INVALID;
     FindArgs a;
@@ -312,17 +340,13 @@ extern "C" int pld_find_candidates(const int32_t *tokens, int64_t tok_stride, co
     a.cand_count = cand_count;
     a.ngram_used = ngram_used;
     a.tile_counts = nullptr;
-    a.tickets = nullptr;
     a.ntiles = (int)((tok_stride + kFindTile - 1) / kFindTile);
     hipStream_t s = (hipStream_t)stream;
     if (tok_stride <= kFindFusedMax) {
         hipLaunchKernelGGL(find_fused_kernel, dim3(B), dim3(kFindWavesFused * kWave), 0, s, a);
     } else {
-        if (!workspace) return PLD_ERR_WORKSPACE;
-        if (workspace_bytes < find_ws_bytes(B, tok_stride)) return PLD_ERR_WORKSPACE;
-        a.tile_counts = (int32_t *)workspace;
-        a.tickets = (uint32_t *)((char *)workspace +
-                                 align_up((size_t)B * a.ntiles * kMaxNgram * sizeof(int32_t), 256));
+        if (!scratch || scratch_bytes < find_scratch_bytes(B, tok_stride)) return PLD_ERR_WORKSPACE;
+        a.tile_counts = (int32_t *)scratch;
         dim3 grid(a.ntiles, B);
         hipLaunchKernelGGL(find_count_kernel, grid, dim3(kFindWavesTiled * kWave), 0, s, a);
         hipLaunchKernelGGL(find_compact_kernel, grid, dim3(kFindWavesTiled * kWave), 0, s, a);

@@ -24,8 +24,10 @@
 //
 // Selection: a candidate with s > threshold contributes the 64-bit key
 // (orderable(s) << 32 | j); waves reduce keys and atomically max them into the
-// per-sequence workspace slot.  The last block to finish (atomic ticket)
-// turns the keys into best_pos / best_score and zeroes the slots and ticket.
+// per-sequence workspace slot.  A small finishing kernel, launched right
+// after on the same stream, turns the keys into best_pos / best_score and
+// zeroes the slots (the kernel boundary orders the two; no block of the
+// ranking kernel ever waits for, or fences against, another).
 #include <math.h>
 
 #include "pld.h"
@@ -46,8 +48,7 @@ struct RankCommon {
     float *scores;
     int32_t *best_pos;
     float *best_score;
-    uint64_t *keys;     // [B]
-    uint32_t *ticket;   // [1]
+    uint64_t *keys;     // [B], zero on entry
 };
 
 struct RankHiddenArgs {
@@ -67,33 +68,42 @@ struct RankAttnArgs {
 
 // pre[b] = number of candidates before sequence b; pre[B] = total.  Counts
 // outside [0, cap] count as 0.  Block-wide: each thread sums a contiguous run
-// of sequences, the per-thread sums are scanned in LDS.
+// of sequences; the thread sums are scanned with wave shuffles and one LDS
+// exchange of the wave totals.
+__device__ __forceinline__ uint32_t clamped_count(const RankCommon &c, int b) {
+    const int32_t n = c.cand_count[b];
+    return (n >= 0 && (int64_t)n <= c.cap) ? (uint32_t)n : 0u;
+}
+
 __device__ void candidate_prefix(const RankCommon &c, uint32_t *pre) {
-    __shared__ uint32_t s_part[kRankThreads];
+    __shared__ uint32_t s_wave[kRankWaves];
     const int per = (c.B + kRankThreads - 1) / kRankThreads;
     const int b0 = threadIdx.x * per;
     const int b1 = min(b0 + per, c.B);
     uint32_t sum = 0;
-    for (int b = b0; b < b1; ++b) {
-        int32_t n = c.cand_count[b];
-        sum += (n >= 0 && (int64_t)n <= c.cap) ? (uint32_t)n : 0u;
+    for (int b = b0; b < b1; ++b) sum += clamped_count(c, b);
+    // inclusive scan across the wave
+    uint32_t inc = sum;
+    const int lane = lane_id();
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const uint32_t v = (uint32_t)__shfl_up((int)inc, off);
+        if (lane >= off) inc += v;
     }
-    s_part[threadIdx.x] = sum;
+    const int w = threadIdx.x / kWave;
+    if (lane == kWave - 1) s_wave[w] = inc;
     __syncthreads();
-    // inclusive scan of the thread sums (Hillis-Steele, 8 steps)
-    for (int off = 1; off < kRankThreads; off <<= 1) {
-        uint32_t v = threadIdx.x >= off ? s_part[threadIdx.x - off] : 0u;
-        __syncthreads();
-        s_part[threadIdx.x] += v;
-        __syncthreads();
-    }
-    uint32_t run = threadIdx.x == 0 ? 0u : s_part[threadIdx.x - 1];
+    uint32_t run = inc - sum;
+    for (int i = 0; i < w; ++i) run += s_wave[i];
     for (int b = b0; b < b1; ++b) {
         pre[b] = run;
-        int32_t n = c.cand_count[b];
-        run += (n >= 0 && (int64_t)n <= c.cap) ? (uint32_t)n : 0u;
+        run += clamped_count(c, b);
     }
-    if (threadIdx.x == kRankThreads - 1) pre[c.B] = s_part[kRankThreads - 1];
+    if (threadIdx.x == 0) {
+        uint32_t t = 0;
+        for (int i = 0; i < kRankWaves; ++i) t += s_wave[i];
+        pre[c.B] = t;
+    }
     __syncthreads();
 }
 
@@ -107,32 +117,19 @@ __device__ __forceinline__ int seq_of(const uint32_t *pre, int B, uint32_t i) {
     return lo;
 }
 
-// Called by every block after its atomics: the last block to arrive writes
-// best_pos / best_score for all sequences and clears the workspace.
-__device__ void finish_selection(const RankCommon &c) {
-    __shared__ int s_last;
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        uint32_t t = __hip_atomic_fetch_add(c.ticket, 1u, __ATOMIC_ACQ_REL,
-                                            __HIP_MEMORY_SCOPE_AGENT);
-        s_last = (t == gridDim.x - 1);
+// best_pos / best_score from the keys, which are returned to zero.
+__global__ __launch_bounds__(256) void rank_finish_kernel(RankCommon c) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= c.B) return;
+    const uint64_t k = c.keys[b];
+    c.keys[b] = 0;
+    if (k == 0) {
+        c.best_pos[b] = -1;
+        c.best_score[b] = -INFINITY;
+    } else {
+        c.best_pos[b] = (int32_t)(uint32_t)(k & 0xffffffffu);
+        c.best_score[b] = unord_f32((uint32_t)(k >> 32));
     }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    for (int b = threadIdx.x; b < c.B; b += blockDim.x) {
-        uint64_t k = take_u64(&c.keys[b]);
-        if (k == 0) {
-            c.best_pos[b] = -1;
-            c.best_score[b] = -INFINITY;
-        } else {
-            c.best_pos[b] = (int32_t)(uint32_t)(k & 0xffffffffu);
-            c.best_score[b] = unord_f32((uint32_t)(k >> 32));
-        }
-    }
-    if (threadIdx.x == 0)
-        __hip_atomic_store(c.ticket, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ---------------------------------------------------------------- hidden
@@ -142,7 +139,7 @@ __device__ void finish_selection(const RankCommon &c) {
 // then summed across the wave.  `row` may point to LDS (query norm) or HBM.
 __device__ __forceinline__ void row_dot(const uint4 *row, const uint4 *q, int nch, float &dot,
                                         float &nrm) {
-    constexpr int U = 8;
+    constexpr int U = 16;   // every 16-byte load of a row up to d = 8192 in flight at once
     const int lane = lane_id();
     float ad[8], an[8];
 #pragma unroll
@@ -230,7 +227,6 @@ __global__ __launch_bounds__(kRankThreads) void rank_hidden_kernel(RankHiddenArg
             lo = seg_hi;
         }
     }
-    finish_selection(c);
 }
 
 // ------------------------------------------------------------------ attn
@@ -292,7 +288,6 @@ __global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a)
             atomicMax((unsigned long long *)&c.keys[b], (unsigned long long)key);
         }
     }
-    finish_selection(c);
 }
 
 // Blocks of the persistent ranking grids: a few per CU keeps enough rows in
@@ -323,7 +318,6 @@ static RankCommon make_common(const int32_t *lens, const int32_t *cand_pos, int6
     c.best_pos = best_pos;
     c.best_score = best_score;
     c.keys = (uint64_t *)workspace;
-    c.ticket = (uint32_t *)((char *)workspace + align_up((size_t)B * sizeof(uint64_t), 256));
     return c;
 }
 
@@ -354,6 +348,8 @@ extern "C" int pld_rank_hidden(const uint16_t *hidden, int64_t h_seq_stride, int
     size_t lds = (size_t)(d / 8) * sizeof(uint4) + (size_t)(B + 1) * sizeof(uint32_t);
     hipLaunchKernelGGL(rank_hidden_kernel, dim3(kRankBlocks), dim3(kRankThreads), lds,
                        (hipStream_t)stream, a);
+    hipLaunchKernelGGL(rank_finish_kernel, dim3((B + 255) / 256), dim3(256), 0, (hipStream_t)stream,
+                       a.c);
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }
 
@@ -380,5 +376,7 @@ extern "C" int pld_rank_attn(const float *attn, int64_t a_seq_stride, int64_t a_
     a.agg = agg;
     hipLaunchKernelGGL(rank_attn_kernel, dim3(kRankBlocks), dim3(kRankThreads), 0,
                        (hipStream_t)stream, a);
+    hipLaunchKernelGGL(rank_finish_kernel, dim3((B + 255) / 256), dim3(256), 0, (hipStream_t)stream,
+                       a.c);
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }

@@ -13,9 +13,10 @@
 // and the wave / block reduce the 64-bit key (orderable(value) << 32 |
 // ~index), whose maximum is the highest value with the lowest index.  A block
 // folds its key into the row's workspace slot with one 64-bit atomic max.
-// The last block of a sequence to finish (atomic ticket counting (L+1)*S
-// arrivals) reads the row keys back, computes the accepted length, writes the
-// outputs and returns the slots to zero.  Rows i > L are never read.
+// A small acceptance kernel, launched right after on the same stream (the
+// kernel boundary orders the two), reads the row keys back with one thread
+// per sequence, computes the accepted length, writes the outputs and returns
+// the slots to zero.  Rows i > L are never read.
 #include <math.h>
 
 #include "pld.h"
@@ -37,8 +38,7 @@ struct VerifyArgs {
     int32_t *accept_len;
     int32_t *out_tokens;
     int32_t *out_count;
-    uint64_t *keys;      // [B][K+1]
-    uint32_t *tickets;   // [B]
+    uint64_t *keys;      // [B][K+1], zero on entry
 };
 
 template <int kBf16>
@@ -74,36 +74,15 @@ struct Elem<1> {
     }
 };
 
-// Keeps the first maximum: a later element replaces the running best only
-// when strictly greater (so -0 after +0, or an equal value, never does).
-__device__ __forceinline__ void keep_first_max(float v, uint32_t idx, float &best, uint32_t &bi) {
-    if (v > best) {
-        best = v;
-        bi = idx;
-    }
-}
-
 template <int kBf16>
-__global__ __launch_bounds__(kVerifyThreads) void verify_kernel(VerifyArgs a) {
+__global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArgs a) {
     using E = Elem<kBf16>;
     using T = typename E::T;
     constexpr int P = E::kPerVec;
     __shared__ uint64_t s_key[kVerifyWaves];
-    __shared__ int s_last;
     const int split = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
     const int L = a.draft_len[b];
-    if (L < 0 || L > a.K) {
-        if (split == 0 && i == 0) {
-            for (int t = threadIdx.x; t <= a.K; t += blockDim.x)
-                a.out_tokens[(int64_t)b * (a.K + 1) + t] = -1;
-            if (threadIdx.x == 0) {
-                a.accept_len[b] = -1;
-                a.out_count[b] = 0;
-            }
-        }
-        return;
-    }
-    if (i > L) return;
+    if (L < 0 || L > a.K || i > L) return;   // rows past the draft are never read
 
     const T *row = reinterpret_cast<const T *>(a.logits) + (int64_t)b * a.ls + (int64_t)i * a.lr;
     // The row as [head | 16-byte vectors | tail]; head and tail are scalar.
@@ -114,91 +93,106 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_kernel(VerifyArgs a) {
     const int64_t body_end = head + nvec * P;
     const int64_t v0 = (nvec * split) / a.S, v1 = (nvec * (split + 1)) / a.S;
 
+    // Each thread keeps the first maximum of its own elements, which it visits
+    // in increasing index order: a later element replaces the best only when
+    // strictly greater (so an equal value, or -0 after +0, never does).  The
+    // index starts at the thread's first element, so a thread whose elements
+    // are all -inf still reports its first one.
+    constexpr uint32_t kNone = 0xffffffffu;
     float best = -INFINITY;
-    uint32_t bi = 0xffffffffu;
-    // head: elements [0, head), taken by the first block of the row
-    if (split == 0 && (int)threadIdx.x < head) {
-        best = E::get(row, threadIdx.x);
-        bi = threadIdx.x;
+    uint32_t bi = kNone;
+    const bool has_head = split == 0 && (int)threadIdx.x < head;
+    const int64_t my_v = v0 + threadIdx.x;
+    const bool has_tail = split == a.S - 1 && body_end + threadIdx.x < a.V;
+    if (has_head) bi = threadIdx.x;
+    else if (my_v < v1) bi = (uint32_t)(head + my_v * P);
+    else if (has_tail) bi = (uint32_t)(body_end + threadIdx.x);
+    if (has_head) {
+        const float f = E::get(row, threadIdx.x);
+        if (f > best) best = f;
     }
-    // body: vectors [v0, v1) of the row, strided over the block
     const uint4 *vec = reinterpret_cast<const uint4 *>(row + head);
-    for (int64_t vb = v0 + threadIdx.x; vb < v1; vb += (int64_t)kVerifyThreads * kVerifyUnroll) {
+    for (int64_t vb = my_v; vb < v1; vb += (int64_t)kVerifyThreads * kVerifyUnroll) {
         uint4 r[kVerifyUnroll];
 #pragma unroll
         for (int u = 0; u < kVerifyUnroll; ++u) {
-            int64_t vi = vb + (int64_t)u * kVerifyThreads;
+            const int64_t vi = vb + (int64_t)u * kVerifyThreads;
             if (vi < v1) r[u] = vec[vi];
         }
 #pragma unroll
         for (int u = 0; u < kVerifyUnroll; ++u) {
-            int64_t vi = vb + (int64_t)u * kVerifyThreads;
+            const int64_t vi = vb + (int64_t)u * kVerifyThreads;
             if (vi < v1) {
                 float f[P];
                 E::unpack(r[u], f);
                 const uint32_t base = (uint32_t)(head + vi * P);
 #pragma unroll
                 for (int e = 0; e < P; ++e) {
-                    if (bi == 0xffffffffu) {
+                    if (f[e] > best) {
                         best = f[e];
                         bi = base + e;
-                    } else {
-                        keep_first_max(f[e], base + e, best, bi);
                     }
                 }
             }
         }
     }
-    // tail: elements [body_end, V), taken by the last block of the row
-    if (split == a.S - 1 && body_end + threadIdx.x < a.V) {
+    if (has_tail) {
         const int64_t e = body_end + threadIdx.x;
-        float f = E::get(row, e);
-        if (bi == 0xffffffffu) {
+        const float f = E::get(row, e);
+        if (f > best) {
             best = f;
             bi = (uint32_t)e;
-        } else {
-            keep_first_max(f, (uint32_t)e, best, bi);
         }
     }
-    uint64_t key = (bi == 0xffffffffu) ? 0ull : argmax_key(best, bi);
+    uint64_t key = (bi == kNone) ? 0ull : argmax_key(best, bi);
     key = wave_max_u64(key);
     const int w = threadIdx.x / kWave;
     if (lane_id() == 0) s_key[w] = key;
     __syncthreads();
-    uint64_t *slot = a.keys + (int64_t)b * (a.K + 1);
     if (threadIdx.x == 0) {
         uint64_t k = s_key[0];
 #pragma unroll
         for (int t = 1; t < kVerifyWaves; ++t) k = s_key[t] > k ? s_key[t] : k;
-        if (k) atomicMax((unsigned long long *)&slot[i], (unsigned long long)k);
-        __threadfence();
-        uint32_t t = __hip_atomic_fetch_add(&a.tickets[b], 1u, __ATOMIC_ACQ_REL,
-                                            __HIP_MEMORY_SCOPE_AGENT);
-        s_last = (t == (uint32_t)((L + 1) * a.S - 1));
+        if (k)
+            atomicMax((unsigned long long *)&a.keys[(int64_t)b * (a.K + 1) + i],
+                      (unsigned long long)k);
     }
-    __syncthreads();
-    if (!s_last || threadIdx.x != 0) return;
-    // The last block of sequence b: accept and emit, then clear the slots.
-    __threadfence();
-    int32_t *out = a.out_tokens + (int64_t)b * (a.K + 1);
-    const int32_t *dr = a.draft + (int64_t)b * a.K;
+}
+
+// One thread per sequence: y_i from the row keys, the accepted length, the
+// emitted tokens; the keys are returned to zero.
+__global__ __launch_bounds__(64) void verify_accept_kernel(VerifyArgs a) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= a.B) return;
+    const int K = a.K;
+    const int L = a.draft_len[b];
+    int32_t *out = a.out_tokens + (int64_t)b * (K + 1);
+    if (L < 0 || L > K) {
+        for (int r = 0; r <= K; ++r) out[r] = -1;
+        a.accept_len[b] = -1;
+        a.out_count[b] = 0;
+        return;
+    }
+    uint64_t *slot = a.keys + (int64_t)b * (K + 1);
+    const int32_t *dr = a.draft + (int64_t)b * K;
     int acc = L;
     int32_t y_acc = -1;
     for (int r = 0; r <= L; ++r) {
-        uint64_t k = take_u64(&slot[r]);
-        int32_t y = (int32_t)argmax_key_index(k);
-        if (r == acc) y_acc = y;
+        const uint64_t k = slot[r];
+        slot[r] = 0;
+        const int32_t y = (int32_t)argmax_key_index(k);
         if (r < acc && r < L && y != dr[r]) {
             acc = r;
+            y_acc = y;
+        } else if (r == acc) {
             y_acc = y;
         }
     }
     for (int r = 0; r < acc; ++r) out[r] = dr[r];
     out[acc] = y_acc;
-    for (int r = acc + 1; r <= a.K; ++r) out[r] = -1;
+    for (int r = acc + 1; r <= K; ++r) out[r] = -1;
     a.accept_len[b] = acc;
     a.out_count[b] = acc + 1;
-    __hip_atomic_store(&a.tickets[b], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ------------------------------------------------------------------ emit
@@ -257,13 +251,13 @@ extern "C" int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_st
     a.out_tokens = out_tokens;
     a.out_count = out_count;
     a.keys = (uint64_t *)workspace;
-    a.tickets = (uint32_t *)((char *)workspace +
-                             align_up((size_t)B * (size_t)(K + 1) * sizeof(uint64_t), 256));
     dim3 grid((unsigned)S, (unsigned)(K + 1), (unsigned)B);
+    hipStream_t s = (hipStream_t)stream;
     if (dtype == PLD_F32)
-        hipLaunchKernelGGL(verify_kernel<0>, grid, dim3(kVerifyThreads), 0, (hipStream_t)stream, a);
+        hipLaunchKernelGGL(verify_argmax_kernel<0>, grid, dim3(kVerifyThreads), 0, s, a);
     else
-        hipLaunchKernelGGL(verify_kernel<1>, grid, dim3(kVerifyThreads), 0, (hipStream_t)stream, a);
+        hipLaunchKernelGGL(verify_argmax_kernel<1>, grid, dim3(kVerifyThreads), 0, s, a);
+    hipLaunchKernelGGL(verify_accept_kernel, dim3((B + 63) / 64), dim3(64), 0, s, a);
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }
 
@@ -293,12 +287,9 @@ extern "C" const char *pld_status_string(int status) {
     }
 }
 
-extern "C" size_t pld_workspace_bytes(int B, int64_t tok_stride, int K) {
-    if (B < 1 || tok_stride < 1 || tok_stride > kMaxTokStride || K < 1) return 0;
-    size_t n = find_ws_bytes(B, tok_stride);
-    size_t r = rank_ws_bytes(B);
-    size_t v = verify_ws_bytes(B, K);
-    if (r > n) n = r;
-    if (v > n) n = v;
-    return n;
+extern "C" size_t pld_workspace_bytes(int B, int K) {
+    if (B < 1 || K < 1) return 0;
+    const size_t r = rank_ws_bytes(B);
+    const size_t v = verify_ws_bytes(B, K);
+    return r > v ? r : v;
 }

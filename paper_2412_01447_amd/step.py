@@ -7,8 +7,8 @@ Eq. 2 / Eq. 3, draft Sec. 4.3, greedy verification Sec. 4.4).
 """
 import torch
 
-from . import (PLD_AGG_SUM, pld_emit_draft, pld_find_candidates, pld_rank_attn, pld_rank_hidden,
-               pld_verify_greedy, pld_workspace_bytes)
+from . import (PLD_AGG_SUM, pld_emit_draft, pld_find_candidates, pld_find_scratch_bytes,
+               pld_rank_attn, pld_rank_hidden, pld_verify_greedy, pld_workspace_bytes)
 
 
 class DraftStep:
@@ -31,12 +31,15 @@ class DraftStep:
         self.accept_len = torch.zeros(B, **i32)
         self.out_tokens = torch.zeros((B, K + 1), **i32)
         self.out_count = torch.zeros(B, **i32)
-        nbytes = pld_workspace_bytes(B, tok_stride, K)
-        self.workspace = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+        # ranking / verification keys: zero once here, left zero by every call
+        self.workspace = torch.zeros(pld_workspace_bytes(B, K), dtype=torch.uint8, device=device)
+        nscratch = pld_find_scratch_bytes(B, tok_stride)
+        self.scratch = (torch.empty(nscratch, dtype=torch.uint8, device=device)
+                        if nscratch else None)
 
     def find(self, tokens, lens, ngram_min=1, ngram_max=1, stream=None):
         pld_find_candidates(tokens, lens, ngram_min, ngram_max, self.cand_pos, self.cand_count,
-                            self.ngram_used, self.workspace, stream=stream)
+                            self.ngram_used, self.scratch, stream=stream)
 
     def rank_hidden(self, hidden, lens, threshold=float("-inf"), stream=None):
         pld_rank_hidden(hidden, lens, self.cand_pos, self.cand_count, self.best_pos,

@@ -50,8 +50,14 @@ def h_bits(t):
     return t.view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def workspace(B, tok_stride, K):
-    return torch.zeros(pld.pld_workspace_bytes(B, tok_stride, K), dtype=torch.uint8, device=dev())
+def workspace(B, K):
+    return torch.zeros(pld.pld_workspace_bytes(B, K), dtype=torch.uint8, device=dev())
+
+
+def scratch(B, tok_stride, fill=0x5A):
+    """Find scratch, deliberately filled with garbage: its contents must not matter."""
+    n = pld.pld_find_scratch_bytes(B, tok_stride)
+    return torch.full((n,), fill, dtype=torch.uint8, device=dev()) if n else None
 
 
 def assert_ws_zero(ws):
@@ -61,17 +67,16 @@ def assert_ws_zero(ws):
 
 
 # ------------------------------------------------------------------ stages
-def gpu_find(tokens, lens, nmin, nmax, cap=None, ws=None):
+def gpu_find(tokens, lens, nmin, nmax, cap=None, scr=None):
     B, stride = tokens.shape
     cap = stride if cap is None else cap
     t, l = d_i32(tokens), d_i32(lens)
     cp = torch.full((B, cap), -1, dtype=torch.int32, device=dev())
     cc = torch.full((B,), -7, dtype=torch.int32, device=dev())
     nu = torch.full((B,), -7, dtype=torch.int32, device=dev())
-    ws = workspace(B, stride, 1) if ws is None else ws
-    pld.pld_find_candidates(t, l, nmin, nmax, cp, cc, nu, ws)
+    scr = scratch(B, stride) if scr is None else scr
+    pld.pld_find_candidates(t, l, nmin, nmax, cp, cc, nu, scr)
     torch.cuda.synchronize()
-    assert_ws_zero(ws)
     return cp.cpu().numpy(), cc.cpu().numpy(), nu.cpu().numpy()
 
 
@@ -90,7 +95,7 @@ def gpu_rank_hidden(hidden_dev, lens, cp, cc, threshold=-math.inf, ws=None):
     bp = torch.full((B,), -7, dtype=torch.int32, device=dev())
     bs = torch.zeros(B, dtype=torch.float32, device=dev())
     sc = torch.full((B, cap), 12345.0, dtype=torch.float32, device=dev())
-    ws = workspace(B, 1, 1) if ws is None else ws
+    ws = workspace(B, 1) if ws is None else ws
     pld.pld_rank_hidden(hidden_dev, d_i32(lens), d_i32(cp), d_i32(cc), bp, bs, ws,
                         threshold=threshold, scores=sc)
     torch.cuda.synchronize()
@@ -104,7 +109,7 @@ def gpu_rank_attn(attn_dev, lens, cp, cc, agg, threshold=-math.inf, ws=None):
     bp = torch.full((B,), -7, dtype=torch.int32, device=dev())
     bs = torch.zeros(B, dtype=torch.float32, device=dev())
     sc = torch.full((B, cap), 12345.0, dtype=torch.float32, device=dev())
-    ws = workspace(B, 1, 1) if ws is None else ws
+    ws = workspace(B, 1) if ws is None else ws
     pld.pld_rank_attn(attn_dev, d_i32(lens), d_i32(cp), d_i32(cc), bp, bs, ws, agg=agg,
                       threshold=threshold, scores=sc)
     torch.cuda.synchronize()
@@ -163,7 +168,7 @@ def gpu_verify(logits_dev, draft, draft_len, ws=None):
     acc = torch.full((B,), -7, dtype=torch.int32, device=dev())
     out = torch.full((B, K1), -7, dtype=torch.int32, device=dev())
     cnt = torch.full((B,), -7, dtype=torch.int32, device=dev())
-    ws = workspace(B, 1, K1 - 1) if ws is None else ws
+    ws = workspace(B, K1 - 1) if ws is None else ws
     pld.pld_verify_greedy(logits_dev, d_i32(draft), d_i32(draft_len), acc, out, cnt, ws)
     torch.cuda.synchronize()
     assert_ws_zero(ws)

@@ -58,16 +58,19 @@ def test_status_strings_and_version():
     assert pld.pld_status_string(99) == "unknown status"
 
 
-def test_workspace_bytes():
-    assert pld.pld_workspace_bytes(0, 10, 4) == 0
-    assert pld.pld_workspace_bytes(1, 0, 4) == 0
-    assert pld.pld_workspace_bytes(1, 10, 0) == 0
-    a = pld.pld_workspace_bytes(8, 4096, 10)
+def test_workspace_and_scratch_bytes():
+    assert pld.pld_workspace_bytes(0, 4) == 0
+    assert pld.pld_workspace_bytes(1, 0) == 0
+    a = pld.pld_workspace_bytes(8, 10)
     assert a > 0 and a % 256 == 0
-    assert pld.pld_workspace_bytes(8, 1 << 17, 10) >= a          # multi-tile find needs more
-    assert pld.pld_workspace_bytes(64, 4096, 32) >= pld.pld_workspace_bytes(64, 4096, 16)
-    # verify keys: B*(K+1) u64 + B tickets
-    assert pld.pld_workspace_bytes(64, 16, 16) >= 64 * 17 * 8 + 64 * 4
+    assert pld.pld_workspace_bytes(64, 32) >= pld.pld_workspace_bytes(64, 16)
+    assert pld.pld_workspace_bytes(64, 16) >= 64 * 17 * 8      # verify keys: B*(K+1) u64
+    assert pld.pld_workspace_bytes(4096, 1) >= 4096 * 8        # ranking keys: B u64
+    # find: no scratch up to 8192 tokens, per-tile counts beyond
+    assert pld.pld_find_scratch_bytes(8, 8192) == 0
+    assert pld.pld_find_scratch_bytes(8, 8193) >= 8 * 5 * 8 * 4
+    assert pld.pld_find_scratch_bytes(4, 131072) >= 4 * 64 * 8 * 4
+    assert pld.pld_find_scratch_bytes(0, 9000) == 0
 
 
 P = ctypes.c_void_p
@@ -90,7 +93,7 @@ def test_host_validation_error_codes():
     assert f(F, 16, F, 1, 1, 9, F, 16, F, F, F, 1 << 20, NULL) == E_INV
     assert f(F, 16, F, 1, 1, 1, F, 15, F, F, F, 1 << 20, NULL) == E_INV
     assert f(F, 0, F, 1, 1, 1, F, 16, F, F, F, 1 << 20, NULL) == E_INV
-    # the multi-tile path needs a workspace of the documented size
+    # the multi-tile path needs a scratch buffer of the documented size
     big = 1 << 15
     assert f(F, big, F, 2, 1, 1, F, big, F, F, NULL, 0, NULL) == E_WS
     assert f(F, big, F, 2, 1, 1, F, big, F, F, F, 16, NULL) == E_WS
@@ -107,7 +110,7 @@ def test_host_validation_error_codes():
     assert h(MIS, 64, 8, 8, 8, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_AL
     assert h(F, 64, 12, 8, 8, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_AL
     assert h(F, 64, 8, 8, 8, F, F, 8, F, 1, INF, NULL, F, F, NULL, 1 << 20, NULL) == E_WS
-    assert h(F, 64, 8, 8, 8, F, F, 8, F, 1, INF, NULL, F, F, F, 8, NULL) == E_WS
+    assert h(F, 64, 8, 8, 8, F, F, 8, F, 1, INF, NULL, F, F, F, 7, NULL) == E_WS
     # rank attn
     a = lib.pld_rank_attn
     assert a(F, 64, 8, 8, 0, 0, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV

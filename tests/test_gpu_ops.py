@@ -352,11 +352,11 @@ def test_workspace_shared_across_calls_and_determinism():
     say("shared workspace")
     cfg = synth.Config("t", 4, 3000, 500, 1.1, 0.3, (8, 32), (1, 2), 256, "hidden", 0, 8, "f32", 21)
     toks, lens, metas = synth.make_tokens(cfg)
-    ws = workspace(cfg.B, cfg.T, cfg.K)
+    ws = workspace(cfg.B, cfg.K)
     H = synth.make_hidden(cfg.B, cfg.T, cfg.d, cfg.seed, device="cuda")
     runs = []
     for _ in range(3):
-        cp, cc, nu = gpu_find(toks, lens, 1, 2, ws=ws)
+        cp, cc, nu = gpu_find(toks, lens, 1, 2)
         sc, bp, bs = gpu_rank_hidden(H, lens, cp, cc, ws=ws)
         runs.append((cp.copy(), cc.copy(), sc.copy(), bp.copy(), bs.copy()))
     for r in runs[1:]:
