@@ -43,28 +43,36 @@ def parse():
                    help="CPU work the oracle baseline is given (whole steps, at least one)")
     p.add_argument("--copy-probe", action="store_true",
                    help="after the timed region, copy 1 GiB three times (counter calibration)")
-    p.add_argument("--graph", action="store_true", help="replay the step as a captured HIP graph")
+    p.add_argument("--mode", choices=["auto", "fused", "split"], default="auto",
+                   help="drafting: one-launch call (fused), separate calls (split), or auto")
     return p.parse_args()
 
 
-def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits):
+def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fused):
     """What each kernel must move per step (never the dense work it avoids)."""
     import numpy as np
-    B = cfg.B
+    B, K = cfg.B, cfg.K
     C = cand_count.astype(np.int64)
     out = {}
     out["find"] = int(lens.astype(np.int64).sum() * 4 + C.sum() * 4)
-    if cfg.rank in ("hidden", "both"):
-        out["rank_hidden"] = int(((C + (C > 0)) * cfg.d * 2).sum() + C.sum() * 4)
     if cfg.rank in ("attn", "both"):
         # distinct 64-byte segments of each attention row that hold a key j-1
         segs = 0
         for b in range(B):
             keys = cand_pos[b, :C[b]].astype(np.int64) - 1
             segs += len(np.unique((keys * 4) // SEG))
-        out["rank_attn"] = int(segs * cfg.R * SEG + C.sum() * 4)
-    out["emit"] = int(B * cfg.K * 4 * 2)
-    out["verify"] = int(((draft_len.astype(np.int64) + 1) * cfg.V * elt_logits).sum())
+        out["score_attn"] = int(segs * cfg.R * SEG + C.sum() * 4)
+        out["select_attn"] = B * 8 * 2 + B * 8
+    if cfg.rank in ("hidden", "both"):
+        out["score_hidden"] = int(((C + (C > 0)) * cfg.d * 2).sum() + C.sum() * 4)
+        out["select"] = B * 8 * 2 + B * 8
+    out["emit"] = int(B * K * 4 * 2)
+    out["verify_argmax"] = int(((draft_len.astype(np.int64) + 1) * cfg.V * elt_logits).sum())
+    out["verify_accept"] = int(((draft_len.astype(np.int64) + 1) * 8 * 2).sum() + B * K * 4 +
+                               B * (K + 1) * 4)
+    if fused:   # one launch does find, rank, select and emit
+        out["draft"] = sum(out.pop(k) for k in ("find", "score_hidden", "score_attn", "select",
+                                                "select_attn", "emit") if k in out)
     return out
 
 
@@ -100,7 +108,8 @@ def main():
     base = dict(tokens=torch.from_numpy(toks).to(dev), lens=torch.from_numpy(lens).to(dev),
                 logits=dev_logits(z), hidden=w["hidden"],
                 attn=torch.from_numpy(w["attn"]).to(dev) if w["attn"] is not None else None)
-    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev)
+    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, mode=args.mode)
+    fused = step.uses_fused(base["hidden"], base["attn"])
 
     def run(s):
         step.run(s["tokens"], s["lens"], s["logits"], hidden=s["hidden"], attn=s["attn"],
@@ -110,12 +119,13 @@ def main():
     run(base)
     torch.cuda.synchronize()
     nbytes = algorithmic_bytes(cfg, lens, step.cand_count.cpu().numpy(),
-                               step.draft_len.cpu().numpy(), step.cand_pos.cpu().numpy(), elt)
+                               step.draft_len.cpu().numpy(), step.cand_pos.cpu().numpy(), elt,
+                               fused)
     step_bytes = sum(nbytes.values())
     dominant = max(nbytes, key=nbytes.get)
     # input copies at distinct addresses: the steps of one rotation touch at
-    # least four times the last-level cache
-    copies = int(min(64, max(2, math.ceil(4 * MALL_BYTES / max(step_bytes, 1)))))
+    # least twice the last-level cache
+    copies = int(min(64, max(2, math.ceil(2 * MALL_BYTES / max(step_bytes, 1)))))
     sets = [base]
     for _ in range(copies - 1):
         sets.append({k: (v.clone() if v is not None else None) for k, v in base.items()})
@@ -123,69 +133,36 @@ def main():
     log(f"[bench] step bytes {step_bytes / 1e6:.2f} MB {json.dumps(nbytes)}; "
         f"dominant {dominant}; {copies} input copies")
 
-    ops = {
-        "find": lambda s: step.find(s["tokens"], s["lens"], *cfg.ngram),
-        "rank_attn": lambda s: step.rank_attn(s["attn"], s["lens"], into_best=s["hidden"] is None),
-        "rank_hidden": lambda s: step.rank_hidden(s["hidden"], s["lens"]),
-        "emit": lambda s: step.emit(s["tokens"], s["lens"]),
-        "verify": lambda s: step.verify(s["logits"]),
-    }
-    order = ["find"] + [o for o in ("rank_attn", "rank_hidden") if o in nbytes] + ["emit", "verify"]
+    # every step as prepared calls (arguments marshalled once, one kernel each)
     stream = torch.cuda.current_stream()
+    plans = [step.plan(s_["tokens"], s_["lens"], s_["logits"], hidden=s_["hidden"],
+                       attn=s_["attn"], ngram=cfg.ngram, stream=stream) for s_ in sets]
+    names = [n for n, _ in plans[0]]
+    assert set(names) == set(nbytes), (names, list(nbytes))
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
 
-    def timed_step(k, s):
-        for o in order:
-            if o == dominant:
-                ev[k][0].record(stream)
-                ops[o](s)
-                ev[k][1].record(stream)
-            else:
-                ops[o](s)
-
-    graph = None
-    if args.graph:
-        # one graph per input copy; replays need no launches from the host
-        graphs = []
-        side = torch.cuda.Stream()
-        side.wait_stream(stream)
-        with torch.cuda.stream(side):
-            for s in sets:
-                run(s)
-        stream.wait_stream(side)
-        torch.cuda.synchronize()
-        for s in sets:
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                run(s)
-            graphs.append(g)
-        graph = graphs
-
     for k in range(args.warmup):
-        if graph:
-            graph[k % copies].replay()
-        else:
-            run(sets[k % copies])
+        for _, call in plans[k % copies]:
+            call()
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for k in range(args.steps):
-        if graph:
-            graph[k % copies].replay()
-        else:
-            timed_step(k, sets[k % copies])
+        e0, e1 = ev[k]
+        for name, call in plans[k % copies]:
+            if name == dominant:
+                e0.record(stream)
+                call()
+                e1.record(stream)
+            else:
+                call()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ms_per_step = elapsed * 1e3 / args.steps
-
-    dom_ms = None
-    if not graph:
-        dom_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
-    # correctness guard: the timed steps must produce what the first step did
-    torch.cuda.synchronize()
+    dom_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
 
     roofline = None
-    if dom_ms is not None:
+    if dom_ms:
         achieved = nbytes[dominant] / (dom_ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
@@ -214,7 +191,8 @@ def main():
                    "ngram": list(cfg.ngram), "ranking": cfg.rank, "hidden_dim": cfg.d,
                    "attn_rows": cfg.R, "K": cfg.K, "logits": cfg.logits,
                    "inputs": "hidden bf16, attention f32, tokens int32",
-                   "graph": bool(graph), "input_copies": copies,
+                   "drafting": "one launch" if fused else "separate calls",
+                   "input_copies": copies,
                    "step_bytes": step_bytes},
         "roofline": roofline,
         "cpu_baseline": cpu,

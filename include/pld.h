@@ -196,6 +196,69 @@ int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride, int64
                       int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
                       void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * The two halves of the ranking calls and of verification, for callers that
+ * schedule (or time) the phases separately.  Run in order on one stream with
+ * the same workspace, they produce exactly what the combined call produces.
+ *
+ * pld_score_hidden / pld_score_attn -- the scoring half of pld_rank_hidden /
+ *   pld_rank_attn (Eq. 2 / Eq. 3): writes `scores` (may be NULL) and folds
+ *   every eligible candidate into per-sequence keys held in the workspace.
+ * pld_select_best -- the selection (argmax over the occurrences, highest
+ *   score then most recent position): turns those keys into best_pos /
+ *   best_score and returns the workspace to zero.
+ * pld_verify_argmax -- y_i = argmax_v Z[b][i][v] for the rows i <= draft_len[b],
+ *   kept in the workspace.
+ * pld_verify_accept -- the accepted length and emitted tokens from those
+ *   row maxima (Sec. 4.4); returns the workspace to zero.
+ * Arguments and errors as in the combined calls.
+ */
+int pld_score_hidden(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
+                     int64_t n_rows, int d, const int32_t *lens, const int32_t *cand_pos,
+                     int64_t cap, const int32_t *cand_count, int B, float threshold,
+                     float *scores, void *workspace, size_t workspace_bytes, void *stream);
+
+int pld_score_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stride, int64_t n_keys,
+                   int R, int agg, const int32_t *lens, const int32_t *cand_pos, int64_t cap,
+                   const int32_t *cand_count, int B, float threshold, float *scores,
+                   void *workspace, size_t workspace_bytes, void *stream);
+
+int pld_select_best(int B, int32_t *best_pos, float *best_score, void *workspace,
+                    size_t workspace_bytes, void *stream);
+
+int pld_verify_argmax(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
+                      int V, int K, const int32_t *draft_len, int B, void *workspace,
+                      size_t workspace_bytes, void *stream);
+
+int pld_verify_accept(const int32_t *draft, const int32_t *draft_len, int B, int K,
+                      int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * pld_draft_hidden / pld_draft_attn -- the drafting half of a step in one
+ * launch: pld_find_candidates, then pld_rank_hidden (or pld_rank_attn), then
+ * pld_emit_draft, with the same definitions, outputs and device-side rules
+ * (Eq. 1, Eq. 2 / Eq. 3 and Sec. 4.3).  One block owns one sequence, so
+ * the scores, choices and drafts are bit-identical to the separate calls;
+ * it needs tok_stride <= 8192 and its time grows with a sequence's own
+ * candidate count, so it suits short candidate lists (small batches, the
+ * latency regime).  `scores` may be NULL.  No workspace is used.
+ * Errors: as the separate calls; tok_stride > 8192 is PLD_ERR_INVALID.
+ */
+int pld_draft_hidden(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B,
+                     int ngram_min, int ngram_max, const uint16_t *hidden, int64_t h_seq_stride,
+                     int64_t h_row_stride, int64_t n_rows, int d, float threshold, int K,
+                     int32_t *cand_pos, int64_t cap, int32_t *cand_count, int32_t *ngram_used,
+                     float *scores, int32_t *best_pos, float *best_score, int32_t *draft,
+                     int32_t *draft_len, void *stream);
+
+int pld_draft_attn(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B,
+                   int ngram_min, int ngram_max, const float *attn, int64_t a_seq_stride,
+                   int64_t a_row_stride, int64_t n_keys, int R, int agg, float threshold, int K,
+                   int32_t *cand_pos, int64_t cap, int32_t *cand_count, int32_t *ngram_used,
+                   float *scores, int32_t *best_pos, float *best_score, int32_t *draft,
+                   int32_t *draft_len, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -18,12 +18,15 @@ __all__ = [
     "pld_version", "pld_status_string", "pld_workspace_bytes", "pld_find_scratch_bytes",
     "pld_find_candidates",
     "pld_rank_hidden", "pld_rank_attn", "pld_emit_draft", "pld_verify_greedy",
+    "pld_draft_hidden", "pld_draft_attn", "DRAFT_MAX_TOK_STRIDE", "pld_score_hidden",
+    "pld_score_attn", "pld_select_best", "pld_verify_argmax", "pld_verify_accept",
 ]
 
 PLD_OK, PLD_ERR_INVALID, PLD_ERR_ALIGN, PLD_ERR_WORKSPACE, PLD_ERR_LAUNCH = range(5)
 PLD_F32, PLD_BF16 = 0, 1
 PLD_AGG_SUM, PLD_AGG_MAX = 0, 1
 PLD_MAX_NGRAM, PLD_MAX_HIDDEN, PLD_MAX_BATCH = 8, 16384, 4096
+DRAFT_MAX_TOK_STRIDE = 8192     # one-launch drafting: one block per sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 library_path = os.path.join(_HERE, "libpld.so")
@@ -46,6 +49,17 @@ _SIGNATURES = {
     "pld_emit_draft": ([_vp, _i64, _vp, _vp, _int, _int, _vp, _vp, _vp], _int),
     "pld_verify_greedy": ([_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int, _vp, _vp, _vp, _vp,
                            _sz, _vp], _int),
+    "pld_score_hidden": ([_vp, _i64, _i64, _i64, _int, _vp, _vp, _i64, _vp, _int, _f32, _vp, _vp,
+                          _sz, _vp], _int),
+    "pld_score_attn": ([_vp, _i64, _i64, _i64, _int, _int, _vp, _vp, _i64, _vp, _int, _f32, _vp,
+                        _vp, _sz, _vp], _int),
+    "pld_select_best": ([_int, _vp, _vp, _vp, _sz, _vp], _int),
+    "pld_verify_argmax": ([_vp, _int, _i64, _i64, _int, _int, _vp, _int, _vp, _sz, _vp], _int),
+    "pld_verify_accept": ([_vp, _vp, _int, _int, _vp, _vp, _vp, _vp, _sz, _vp], _int),
+    "pld_draft_hidden": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _i64, _i64, _int, _f32, _int,
+                          _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _int),
+    "pld_draft_attn": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _i64, _i64, _int, _int, _f32,
+                        _int, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _int),
 }
 
 
@@ -96,6 +110,32 @@ def _call(name, *args):
         raise PLDError(name, rc)
 
 
+class Prepared:
+    """One library call with its arguments marshalled once.  Calling it only
+    enqueues the kernels (the lowest-overhead way to issue a step from Python);
+    the tensors it points to must stay alive and in place."""
+    __slots__ = ("name", "fn", "args")
+
+    def __init__(self, name, args):
+        self.name = name
+        self.fn = getattr(_load(), name)
+        conv = []
+        for a, t in zip(args, self.fn.argtypes):
+            conv.append(a if isinstance(a, (ctypes.c_void_p,)) or a is None else t(a))
+        self.args = tuple(conv)
+
+    def __call__(self):
+        rc = self.fn(*self.args)
+        if rc != PLD_OK:
+            raise PLDError(self.name, rc)
+
+
+def _run(name, args, prepare):
+    if prepare:
+        return Prepared(name, args)
+    _call(name, *args)
+
+
 def pld_version():
     return _load().pld_version()
 
@@ -117,56 +157,56 @@ def _nbytes(t):
 
 
 def pld_find_candidates(tokens, lens, ngram_min, ngram_max, cand_pos, cand_count, ngram_used,
-                        scratch=None, stream=None):
+                        scratch=None, stream=None, prepare=False):
     """tokens int32 [B][tok_stride]; writes cand_pos [B][cap], cand_count [B], ngram_used [B]."""
     import torch
     _need(tokens, torch.int32, "tokens", 2)
     _need(cand_pos, torch.int32, "cand_pos", 2)
     B = tokens.shape[0]
-    _call("pld_find_candidates", _ptr(tokens), tokens.stride(0), _ptr(lens), B, ngram_min,
+    return _run("pld_find_candidates", (_ptr(tokens), tokens.stride(0), _ptr(lens), B, ngram_min,
           ngram_max, _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), _ptr(ngram_used),
-          _ptr(scratch), _nbytes(scratch), _stream(stream))
+          _ptr(scratch), _nbytes(scratch), _stream(stream),), prepare)
 
 
 def pld_rank_hidden(hidden, lens, cand_pos, cand_count, best_pos, best_score, workspace,
-                    threshold=float("-inf"), scores=None, stream=None):
+                    threshold=float("-inf"), scores=None, stream=None, prepare=False):
     """hidden bf16 [B][n_rows][d]; writes best_pos [B], best_score [B] and optionally scores."""
     import torch
     _need(hidden, torch.bfloat16, "hidden", 3)
     _need(cand_pos, torch.int32, "cand_pos", 2)
     B, n_rows, d = hidden.shape
-    _call("pld_rank_hidden", _ptr(hidden), hidden.stride(0), hidden.stride(1), n_rows, d,
+    return _run("pld_rank_hidden", (_ptr(hidden), hidden.stride(0), hidden.stride(1), n_rows, d,
           _ptr(lens), _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), B, float(threshold),
           _ptr(scores), _ptr(best_pos), _ptr(best_score), _ptr(workspace),
-          _nbytes(workspace), _stream(stream))
+          _nbytes(workspace), _stream(stream),), prepare)
 
 
 def pld_rank_attn(attn, lens, cand_pos, cand_count, best_pos, best_score, workspace,
-                  agg=PLD_AGG_SUM, threshold=float("-inf"), scores=None, stream=None):
+                  agg=PLD_AGG_SUM, threshold=float("-inf"), scores=None, stream=None, prepare=False):
     """attn fp32 [B][R][n_keys] (query row T-2 per selected head); agg SUM or MAX."""
     import torch
     _need(attn, torch.float32, "attn", 3)
     _need(cand_pos, torch.int32, "cand_pos", 2)
     B, R, n_keys = attn.shape
-    _call("pld_rank_attn", _ptr(attn), attn.stride(0), attn.stride(1), n_keys, R, int(agg),
+    return _run("pld_rank_attn", (_ptr(attn), attn.stride(0), attn.stride(1), n_keys, R, int(agg),
           _ptr(lens), _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), B, float(threshold),
           _ptr(scores), _ptr(best_pos), _ptr(best_score), _ptr(workspace),
-          _nbytes(workspace), _stream(stream))
+          _nbytes(workspace), _stream(stream),), prepare)
 
 
-def pld_emit_draft(tokens, lens, best_pos, K, draft, draft_len, stream=None):
+def pld_emit_draft(tokens, lens, best_pos, K, draft, draft_len, stream=None, prepare=False):
     """Writes draft [B][K] (padded with -1) and draft_len [B]."""
     import torch
     _need(tokens, torch.int32, "tokens", 2)
     _need(draft, torch.int32, "draft", 2)
     if draft.shape[1] != K or draft.stride(0) != K:
         raise TypeError("draft must be a contiguous [B][K] tensor")
-    _call("pld_emit_draft", _ptr(tokens), tokens.stride(0), _ptr(lens), _ptr(best_pos),
-          tokens.shape[0], K, _ptr(draft), _ptr(draft_len), _stream(stream))
+    return _run("pld_emit_draft", (_ptr(tokens), tokens.stride(0), _ptr(lens), _ptr(best_pos),
+          tokens.shape[0], K, _ptr(draft), _ptr(draft_len), _stream(stream),), prepare)
 
 
 def pld_verify_greedy(logits, draft, draft_len, accept_len, out_tokens, out_count, workspace,
-                      stream=None):
+                      stream=None, prepare=False):
     """logits fp32 or bf16 [B][K+1][V]; writes accept_len [B], out_tokens [B][K+1], out_count [B]."""
     import torch
     if logits.dtype not in (torch.float32, torch.bfloat16):
@@ -179,6 +219,95 @@ def pld_verify_greedy(logits, draft, draft_len, accept_len, out_tokens, out_coun
     if out_tokens.shape != (B, K1) or out_tokens.stride(0) != K1:
         raise TypeError("out_tokens must be a contiguous [B][K+1] tensor")
     dtype = PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
-    _call("pld_verify_greedy", _ptr(logits), dtype, logits.stride(0), logits.stride(1), V, K,
+    return _run("pld_verify_greedy", (_ptr(logits), dtype, logits.stride(0), logits.stride(1), V, K,
           _ptr(draft), _ptr(draft_len), B, _ptr(accept_len), _ptr(out_tokens), _ptr(out_count),
-          _ptr(workspace), _nbytes(workspace), _stream(stream))
+          _ptr(workspace), _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_draft_hidden(tokens, lens, ngram_min, ngram_max, hidden, K, cand_pos, cand_count,
+                     ngram_used, best_pos, best_score, draft, draft_len, threshold=float("-inf"),
+                     scores=None, stream=None, prepare=False):
+    """find + hidden-state ranking + emit in one launch (tok_stride <= 8192)."""
+    import torch
+    _need(tokens, torch.int32, "tokens", 2)
+    _need(hidden, torch.bfloat16, "hidden", 3)
+    _need(cand_pos, torch.int32, "cand_pos", 2)
+    if draft.shape[1] != K or draft.stride(0) != K:
+        raise TypeError("draft must be a contiguous [B][K] tensor")
+    B, n_rows, d = hidden.shape
+    return _run("pld_draft_hidden", (_ptr(tokens), tokens.stride(0), _ptr(lens), tokens.shape[0],
+          ngram_min, ngram_max, _ptr(hidden), hidden.stride(0), hidden.stride(1), n_rows, d,
+          float(threshold), K, _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count),
+          _ptr(ngram_used), _ptr(scores), _ptr(best_pos), _ptr(best_score), _ptr(draft),
+          _ptr(draft_len), _stream(stream),), prepare)
+
+
+def pld_draft_attn(tokens, lens, ngram_min, ngram_max, attn, K, cand_pos, cand_count, ngram_used,
+                   best_pos, best_score, draft, draft_len, agg=PLD_AGG_SUM,
+                   threshold=float("-inf"), scores=None, stream=None, prepare=False):
+    """find + attention ranking + emit in one launch (tok_stride <= 8192)."""
+    import torch
+    _need(tokens, torch.int32, "tokens", 2)
+    _need(attn, torch.float32, "attn", 3)
+    _need(cand_pos, torch.int32, "cand_pos", 2)
+    if draft.shape[1] != K or draft.stride(0) != K:
+        raise TypeError("draft must be a contiguous [B][K] tensor")
+    B, R, n_keys = attn.shape
+    return _run("pld_draft_attn", (_ptr(tokens), tokens.stride(0), _ptr(lens), tokens.shape[0],
+          ngram_min, ngram_max, _ptr(attn), attn.stride(0), attn.stride(1), n_keys, R, int(agg),
+          float(threshold), K, _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count),
+          _ptr(ngram_used), _ptr(scores), _ptr(best_pos), _ptr(best_score), _ptr(draft),
+          _ptr(draft_len), _stream(stream),), prepare)
+
+
+def pld_score_hidden(hidden, lens, cand_pos, cand_count, workspace, threshold=float("-inf"),
+                     scores=None, stream=None, prepare=False):
+    """Scoring half of pld_rank_hidden: per-sequence best keys into the workspace."""
+    import torch
+    _need(hidden, torch.bfloat16, "hidden", 3)
+    _need(cand_pos, torch.int32, "cand_pos", 2)
+    B, n_rows, d = hidden.shape
+    return _run("pld_score_hidden", (_ptr(hidden), hidden.stride(0), hidden.stride(1), n_rows, d,
+          _ptr(lens), _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), B, float(threshold),
+          _ptr(scores), _ptr(workspace), _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_score_attn(attn, lens, cand_pos, cand_count, workspace, agg=PLD_AGG_SUM,
+                   threshold=float("-inf"), scores=None, stream=None, prepare=False):
+    """Scoring half of pld_rank_attn."""
+    import torch
+    _need(attn, torch.float32, "attn", 3)
+    _need(cand_pos, torch.int32, "cand_pos", 2)
+    B, R, n_keys = attn.shape
+    return _run("pld_score_attn", (_ptr(attn), attn.stride(0), attn.stride(1), n_keys, R, int(agg),
+          _ptr(lens), _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), B, float(threshold),
+          _ptr(scores), _ptr(workspace), _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_select_best(B, best_pos, best_score, workspace, stream=None, prepare=False):
+    """Selection half of the ranking calls: keys -> best_pos / best_score."""
+    return _run("pld_select_best", (B, _ptr(best_pos), _ptr(best_score), _ptr(workspace),
+          _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_verify_argmax(logits, draft_len, workspace, stream=None, prepare=False):
+    """Row maxima of the K+1 logits rows (rows past each draft skipped) into the workspace."""
+    import torch
+    if logits.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("logits must be float32 or bfloat16")
+    _need(logits, logits.dtype, "logits", 3)
+    B, K1, V = logits.shape
+    dtype = PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
+    return _run("pld_verify_argmax", (_ptr(logits), dtype, logits.stride(0), logits.stride(1), V, K1 - 1,
+          _ptr(draft_len), B, _ptr(workspace), _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_verify_accept(draft, draft_len, accept_len, out_tokens, out_count, workspace,
+                      stream=None, prepare=False):
+    """Accepted length and emitted tokens from the row maxima in the workspace."""
+    B, K = draft.shape
+    if draft.stride(0) != K or out_tokens.shape != (B, K + 1) or out_tokens.stride(0) != K + 1:
+        raise TypeError("draft [B][K] and out_tokens [B][K+1] must be contiguous")
+    return _run("pld_verify_accept", (_ptr(draft), _ptr(draft_len), B, K, _ptr(accept_len),
+          _ptr(out_tokens), _ptr(out_count), _ptr(workspace), _nbytes(workspace),
+          _stream(stream),), prepare)

@@ -2,7 +2,10 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
+
+#include <mutex>
 
 #if defined(__HIP_DEVICE_COMPILE__) && !defined(__gfx950__)
 #error "this library is written for gfx950 (MI355X) only"
@@ -22,6 +25,41 @@ constexpr int kFindFusedMax = kFindWavesFused * 512;  // tok_stride <= 8192: fus
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Blocks of `kernel` that fit on the current device at once (CUs x resident
+// blocks per CU): the grid of the persistent kernels, whose equal contiguous
+// work ranges then finish in a single round.  Cached per device, kernel and
+// dynamic LDS size.
+inline int resident_blocks(const void *kernel, int threads, size_t dyn_lds) {
+    struct Entry {
+        int dev;
+        const void *k;
+        size_t lds;
+        int blocks;
+    };
+    static std::mutex mu;
+    static Entry cache[64];
+    static int used = 0;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+    {
+        std::lock_guard<std::mutex> g(mu);
+        for (int i = 0; i < used; ++i)
+            if (cache[i].dev == dev && cache[i].k == kernel && cache[i].lds == dyn_lds)
+                return cache[i].blocks;
+    }
+    int cus = 0, per = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus < 1)
+        cus = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kernel, threads, dyn_lds) != hipSuccess ||
+        per < 1)
+        per = 1;
+    const int blocks = cus * per;
+    std::lock_guard<std::mutex> g(mu);
+    if (used < 64) cache[used++] = Entry{dev, kernel, dyn_lds, blocks};
+    return blocks;
+}
+
 // Scratch of the multi-block find: per-tile occurrence counts of every n.
 inline size_t find_scratch_bytes(int B, int64_t tok_stride) {
     if (tok_stride <= kFindFusedMax) return 0;
@@ -29,8 +67,13 @@ inline size_t find_scratch_bytes(int B, int64_t tok_stride) {
     return align_up((size_t)B * (size_t)ntiles * 8 * sizeof(int32_t), 256);
 }
 // Workspace of the ranking and verification calls: 64-bit keys that must be
-// zero when a call starts and that the call leaves zero.
-inline size_t rank_ws_bytes(int B) { return align_up((size_t)B * sizeof(uint64_t), 256); }
+// zero when a call starts and that the call leaves zero.  The ranking keys of
+// a sequence are spread over kKeySlots slots (a block folds into slot
+// blockIdx % kKeySlots), so that few atomics ever queue on one address.
+constexpr int kKeySlots = 16;
+inline size_t rank_ws_bytes(int B) {
+    return align_up((size_t)B * kKeySlots * sizeof(uint64_t), 256);
+}
 inline size_t verify_ws_bytes(int B, int K) {
     return align_up((size_t)B * (size_t)(K + 1) * sizeof(uint64_t), 256);
 }
@@ -93,7 +136,129 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
     return l == 0 ? 0ull : (~0ull >> (64 - l));
 }
 
+// Loads of data read exactly once per call (logits rows, candidate hidden
+// rows, gathered attention weights): the nontemporal hint streams them past
+// the caches, which measurably raises the HBM read rate on gfx950.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ld_stream(const uint4 *p) {
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float ld_stream(const float *p) { return __builtin_nontemporal_load(p); }
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// ------------------------------------------------------- cosine pieces
+// Dot products and squared norms of bf16 rows against the bf16 query row in
+// LDS, with the gfx950 bf16 dot instruction (v_dot2c_f32_bf16: two bf16
+// products added to an fp32 accumulator).  Lane l owns the 8-element chunks
+// l, l+64, l+128, ... of a row, in that order; pair p of a chunk accumulates
+// into acc[p]; the four accumulators are added as (a0+a1)+(a2+a3) and then
+// summed across the wave by a butterfly.  The order depends only on d, so a
+// row gives the same bits whichever slot, wave, block or kernel scores it,
+// and a row equal to the query gives a dot product equal to both norms.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                           __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+__device__ __forceinline__ void accum_chunk(const uint4 &h, const uint4 &q, float (&ad)[4],
+                                            float (&an)[4]) {
+    ad[0] = dot2(h.x, q.x, ad[0]);
+    ad[1] = dot2(h.y, q.y, ad[1]);
+    ad[2] = dot2(h.z, q.z, ad[2]);
+    ad[3] = dot2(h.w, q.w, ad[3]);
+    an[0] = dot2(h.x, h.x, an[0]);
+    an[1] = dot2(h.y, h.y, an[1]);
+    an[2] = dot2(h.z, h.z, an[2]);
+    an[3] = dot2(h.w, h.w, an[3]);
+}
+
+__device__ __forceinline__ void finish_row(const float (&ad)[4], const float (&an)[4], float &dot,
+                                           float &nrm) {
+    dot = wave_sum_f32((ad[0] + ad[1]) + (ad[2] + ad[3]));
+    nrm = wave_sum_f32((an[0] + an[1]) + (an[2] + an[3]));
+}
+
+// One row of any width: up to 16 chunks per lane requested at once.  `row`
+// is either the LDS copy of the query (kStream false) or a candidate row in
+// HBM read once (kStream true).
+template <bool kStream>
+__device__ __forceinline__ void row_dot(const uint4 *row, const uint4 *q, int nch, float &dot,
+                                        float &nrm) {
+    constexpr int U = 16;
+    const int lane = lane_id();
+    float ad[4] = {0.f, 0.f, 0.f, 0.f}, an[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int c0 = lane; c0 < nch; c0 += kWave * U) {
+        uint4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int ch = c0 + u * kWave;
+            if (ch < nch) v[u] = kStream ? ld_stream(row + ch) : row[ch];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int ch = c0 + u * kWave;
+            if (ch < nch) accum_chunk(v[u], q[ch], ad, an);
+        }
+    }
+    finish_row(ad, an, dot, nrm);
+}
+
+// G rows of width nch <= 64 * (16 / G) chunks, all their loads requested at
+// once; a row whose pointer is null is skipped (its results are 0).
+template <int G>
+__device__ __forceinline__ void rows_dot(const uint4 *const (&rows)[G], const uint4 *q, int nch,
+                                         float (&dot)[G], float (&nrm)[G]) {
+    constexpr int U = 16 / G;
+    const int lane = lane_id();
+    uint4 v[G][U];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int ch = lane + u * kWave;
+            if (rows[g] && ch < nch) v[g][u] = ld_stream(rows[g] + ch);
+        }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        float ad[4] = {0.f, 0.f, 0.f, 0.f}, an[4] = {0.f, 0.f, 0.f, 0.f};
+        if (rows[g]) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int ch = lane + u * kWave;
+                if (ch < nch) accum_chunk(v[g][u], q[ch], ad, an);
+            }
+        }
+        finish_row(ad, an, dot[g], nrm[g]);
+    }
+}
+
+// Aggregated attention of one candidate (Eq. 3 / Sec. 7.1): the R weights
+// A[r][j-1] (col = &A[0][j-1], rows ar apart) summed in r order in fp32, or
+// their maximum.  Up to 32 weights are requested at once.
+__device__ __forceinline__ float attn_gather(const float *col, int64_t ar, int R, bool sum) {
+    float acc = sum ? 0.f : -INFINITY;
+    for (int r0 = 0; r0 < R; r0 += 32) {
+        float v[32];
+#pragma unroll
+        for (int u = 0; u < 32; ++u)
+            if (r0 + u < R) v[u] = ld_stream(col + (int64_t)(r0 + u) * ar);
+#pragma unroll
+        for (int u = 0; u < 32; ++u)
+            if (r0 + u < R) acc = sum ? acc + v[u] : fmaxf(acc, v[u]);
+    }
+    return acc;
+}
+
+// Eq. 2's cosine from the dot product and the two squared norms; the clamp
+// is the usual eps = 1e-8 guard (eps^2 on the product of squared norms).
+__device__ __forceinline__ float cosine(float dot, float hh, float qq) {
+    return dot / sqrtf(fmaxf(hh * qq, 1e-16f));
+}
 
 }  // namespace pld

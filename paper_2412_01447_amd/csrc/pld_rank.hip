@@ -23,8 +23,10 @@
 // neighbouring keys).
 //
 // Selection: a candidate with s > threshold contributes the 64-bit key
-// (orderable(s) << 32 | j); waves reduce keys and atomically max them into the
-// per-sequence workspace slot.  A small finishing kernel, launched right
+// (orderable(s) << 32 | j); a block reduces its keys per sequence and folds
+// them with one 64-bit atomic max into one of kKeySlots workspace slots of the
+// sequence (the slot is picked by block index, so an atomic never waits
+// behind more than a handful of others on the same address).  A small finishing kernel, launched right
 // after on the same stream, turns the keys into best_pos / best_score and
 // zeroes the slots (the kernel boundary orders the two; no block of the
 // ranking kernel ever waits for, or fences against, another).
@@ -34,6 +36,10 @@
 #include "pld_device.h"
 
 namespace pld {
+
+#ifndef PLD_RANK_OVERSUB
+#define PLD_RANK_OVERSUB 1           // ranking grid = resident blocks x this (tuning builds)
+#endif
 
 constexpr int kRankThreads = 256;
 constexpr int kRankWaves = kRankThreads / kWave;
@@ -48,7 +54,7 @@ struct RankCommon {
     float *scores;
     int32_t *best_pos;
     float *best_score;
-    uint64_t *keys;     // [B], zero on entry
+    uint64_t *keys;     // [B][kKeySlots], zero on entry
 };
 
 struct RankHiddenArgs {
@@ -107,6 +113,14 @@ __device__ void candidate_prefix(const RankCommon &c, uint32_t *pre) {
     __syncthreads();
 }
 
+// Block k's share [lo, hi) of n items split evenly over the grid (32-bit).
+__device__ __forceinline__ void block_share(uint32_t n, uint32_t &lo, uint32_t &hi) {
+    const uint32_t g = gridDim.x, k = blockIdx.x;
+    const uint32_t q = n / g, r = n % g;
+    lo = k * q + min(k, r);
+    hi = lo + q + (k < r ? 1u : 0u);
+}
+
 // Largest b with pre[b] <= i (i < pre[B]); lands on a non-empty sequence.
 __device__ __forceinline__ int seq_of(const uint32_t *pre, int B, uint32_t i) {
     int lo = 0, hi = B;   // invariant: pre[lo] <= i < pre[hi]
@@ -121,8 +135,15 @@ __device__ __forceinline__ int seq_of(const uint32_t *pre, int B, uint32_t i) {
 __global__ __launch_bounds__(256) void rank_finish_kernel(RankCommon c) {
     const int b = blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= c.B) return;
-    const uint64_t k = c.keys[b];
-    c.keys[b] = 0;
+    uint64_t k = 0;
+    uint64_t *slots = c.keys + (int64_t)b * kKeySlots;
+#pragma unroll
+    for (int i = 0; i < kKeySlots; ++i) {
+        const uint64_t v = slots[i];
+        k = v > k ? v : k;
+    }
+#pragma unroll
+    for (int i = 0; i < kKeySlots; ++i) slots[i] = 0;
     if (k == 0) {
         c.best_pos[b] = -1;
         c.best_score[b] = -INFINITY;
@@ -133,99 +154,105 @@ __global__ __launch_bounds__(256) void rank_finish_kernel(RankCommon c) {
 }
 
 // ---------------------------------------------------------------- hidden
-// Dot product and squared norm of one bf16 row against the bf16 query in LDS.
-// Lane l owns the 8-element chunks l, l+64, l+128, ...; element t of a chunk
-// accumulates into acc[t]; the eight accumulators are added in a fixed tree,
-// then summed across the wave.  `row` may point to LDS (query norm) or HBM.
-__device__ __forceinline__ void row_dot(const uint4 *row, const uint4 *q, int nch, float &dot,
-                                        float &nrm) {
-    constexpr int U = 16;   // every 16-byte load of a row up to d = 8192 in flight at once
+// Scores the rows i = first, first + kRankWaves, ... < end of sequence b (one
+// wave's share of a segment).  The wave fetches the candidate positions of up
+// to 64 rows with one load, then scores G rows at a time with all their loads
+// in flight.  `best` collects the wave's best key.
+template <int G>
+__device__ void score_rows(const RankHiddenArgs &a, int b, int64_t T, bool seq_ok,
+                           const uint16_t *Hb, const uint4 *q_s, float qq, uint32_t first,
+                           uint32_t end, uint32_t seq_start, uint64_t &best) {
+    const RankCommon &c = a.c;
     const int lane = lane_id();
-    float ad[8], an[8];
+    const int nch = a.d / 8;
+    const uint32_t n = end > first ? (end - first + kRankWaves - 1) / kRankWaves : 0;
+    for (uint32_t base = 0; base < n; base += kWave) {
+        const uint32_t nb = min((uint32_t)kWave, n - base);
+        const uint32_t mine = base + lane;
+        int32_t jv = 0;
+        if (mine < n)
+            jv = c.cand_pos[(int64_t)b * c.cap + (first + mine * kRankWaves - seq_start)];
+        for (uint32_t r = 0; r < nb; r += G) {
+            const uint4 *rows[G];
+            int32_t js[G];
 #pragma unroll
-    for (int t = 0; t < 8; ++t) ad[t] = an[t] = 0.f;
-    for (int c0 = lane; c0 < nch; c0 += kWave * U) {
-        uint4 v[U];
+            for (int g = 0; g < G; ++g) {
+                js[g] = (r + g < nb) ? __builtin_amdgcn_readlane(jv, r + g) : 0;
+                const bool ok = (r + g < nb) && seq_ok && js[g] >= 1 && (int64_t)js[g] <= T - 2;
+                rows[g] = ok ? reinterpret_cast<const uint4 *>(Hb + (int64_t)(js[g] - 1) * a.hr)
+                             : nullptr;
+            }
+            float dot[G], nrm[G];
+            if (G == 1 && nch > 16 * kWave) {
+                if (rows[0]) row_dot<true>(rows[0], q_s, nch, dot[0], nrm[0]);
+            } else {
+                rows_dot<G>(rows, q_s, nch, dot, nrm);
+            }
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            int ch = c0 + u * kWave;
-            v[u] = ch < nch ? row[ch] : make_uint4(0u, 0u, 0u, 0u);
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            int ch = c0 + u * kWave;
-            if (ch < nch) {
-                uint4 qq = q[ch];
-                const uint32_t hw[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-                const uint32_t qw[4] = {qq.x, qq.y, qq.z, qq.w};
-#pragma unroll
-                for (int p = 0; p < 4; ++p) {
-                    float h0 = bf16_lo(hw[p]), h1 = bf16_hi(hw[p]);
-                    float q0 = bf16_lo(qw[p]), q1 = bf16_hi(qw[p]);
-                    ad[2 * p] = __builtin_fmaf(h0, q0, ad[2 * p]);
-                    ad[2 * p + 1] = __builtin_fmaf(h1, q1, ad[2 * p + 1]);
-                    an[2 * p] = __builtin_fmaf(h0, h0, an[2 * p]);
-                    an[2 * p + 1] = __builtin_fmaf(h1, h1, an[2 * p + 1]);
+            for (int g = 0; g < G; ++g) {
+                if (r + g >= nb) break;
+                float s = __builtin_nanf("");
+                if (rows[g]) {
+                    s = cosine(dot[g], nrm[g], qq);
+                    if (s > c.threshold) {
+                        const uint64_t k = rank_key(s, js[g]);
+                        best = k > best ? k : best;
+                    }
                 }
+                if (c.scores && lane == 0)
+                    c.scores[(int64_t)b * c.cap +
+                             (first + (base + r + g) * kRankWaves - seq_start)] = s;
             }
         }
     }
-    float d = ((ad[0] + ad[1]) + (ad[2] + ad[3])) + ((ad[4] + ad[5]) + (ad[6] + ad[7]));
-    float n = ((an[0] + an[1]) + (an[2] + an[3])) + ((an[4] + an[5]) + (an[6] + an[7]));
-    dot = wave_sum_f32(d);
-    nrm = wave_sum_f32(n);
 }
 
 __global__ __launch_bounds__(kRankThreads) void rank_hidden_kernel(RankHiddenArgs a) {
     extern __shared__ uint4 smem[];
+    __shared__ uint64_t s_best[kRankWaves];
     const RankCommon &c = a.c;
     const int nch = a.d / 8;
-    uint4 *q_s = smem;                                     // nch chunks of 8 bf16
+    uint4 *q_s = smem;                                         // nch chunks of 8 bf16
     uint32_t *pre = reinterpret_cast<uint32_t *>(smem + nch);  // B + 1
     candidate_prefix(c, pre);
-    const uint32_t total = pre[c.B];
-    const uint32_t lo0 = (uint32_t)(((uint64_t)blockIdx.x * total) / gridDim.x);
-    const uint32_t hi = (uint32_t)(((uint64_t)(blockIdx.x + 1) * total) / gridDim.x);
+    uint32_t lo0, hi;
+    block_share(pre[c.B], lo0, hi);
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
-    if (lo0 < hi) {
-        int b = seq_of(pre, c.B, lo0);
-        uint32_t lo = lo0;
-        while (lo < hi) {
-            while (pre[b + 1] <= lo) ++b;                  // skip empty sequences
-            const uint32_t seg_hi = min(hi, pre[b + 1]);
-            const int64_t T = c.lens[b];
-            const bool seq_ok = (T >= 2 && T - 2 < a.n_rows);
-            const uint16_t *Hb = a.hidden + (int64_t)b * a.hs;
-            if (seq_ok) {
-                const uint4 *qg = reinterpret_cast<const uint4 *>(Hb + (T - 2) * a.hr);
-                for (int i = threadIdx.x; i < nch; i += kRankThreads) q_s[i] = qg[i];
-            }
-            __syncthreads();
-            float qdot = 0.f, qq = 0.f;
-            if (seq_ok) row_dot(q_s, q_s, nch, qdot, qq);
-            uint64_t best = 0;
-            for (uint32_t i = lo + w; i < seg_hi; i += kRankWaves) {
-                const int64_t slot = (int64_t)(i - pre[b]);
-                const int32_t j = c.cand_pos[(int64_t)b * c.cap + slot];
-                float s = __builtin_nanf("");
-                const bool ok = seq_ok && j >= 1 && (int64_t)j <= T - 2;
-                if (ok) {
-                    const uint4 *row = reinterpret_cast<const uint4 *>(Hb + (int64_t)(j - 1) * a.hr);
-                    float dot, hh;
-                    row_dot(row, q_s, nch, dot, hh);
-                    s = dot / sqrtf(fmaxf(hh * qq, 1e-16f));
-                    if (s > c.threshold) {
-                        uint64_t k = rank_key(s, j);
-                        best = k > best ? k : best;
-                    }
-                }
-                if (c.scores && lane == 0) c.scores[(int64_t)b * c.cap + slot] = s;
-            }
-            if (best && lane == 0) atomicMax((unsigned long long *)&c.keys[b], (unsigned long long)best);
-            __syncthreads();                               // q_s is restaged next
-            lo = seg_hi;
+    if (lo0 >= hi) return;   // block-uniform: nothing to score
+    int b = seq_of(pre, c.B, lo0);
+    uint32_t lo = lo0;
+    while (lo < hi) {
+        while (pre[b + 1] <= lo) ++b;                          // skip empty sequences
+        const uint32_t seg_hi = min(hi, pre[b + 1]);
+        const int64_t T = c.lens[b];
+        const bool seq_ok = (T >= 2 && T - 2 < a.n_rows);
+        const uint16_t *Hb = a.hidden + (int64_t)b * a.hs;
+        if (seq_ok) {
+            const uint4 *qg = reinterpret_cast<const uint4 *>(Hb + (T - 2) * a.hr);
+            for (int i = threadIdx.x; i < nch; i += kRankThreads) q_s[i] = qg[i];
         }
+        __syncthreads();
+        float qdot = 0.f, qq = 0.f;
+        if (seq_ok) row_dot<false>(q_s, q_s, nch, qdot, qq);
+        uint64_t best = 0;
+        if (nch <= 4 * kWave)
+            score_rows<4>(a, b, T, seq_ok, Hb, q_s, qq, lo + w, seg_hi, pre[b], best);
+        else if (nch <= 8 * kWave)
+            score_rows<2>(a, b, T, seq_ok, Hb, q_s, qq, lo + w, seg_hi, pre[b], best);
+        else
+            score_rows<1>(a, b, T, seq_ok, Hb, q_s, qq, lo + w, seg_hi, pre[b], best);
+        if (lane == 0) s_best[w] = best;
+        __syncthreads();                                       // also: q_s is restaged next
+        if (threadIdx.x == 0) {
+            uint64_t k = s_best[0];
+            for (int i = 1; i < kRankWaves; ++i) k = s_best[i] > k ? s_best[i] : k;
+            if (k)
+                atomicMax((unsigned long long *)&c.keys[(int64_t)b * kKeySlots +
+                                                        (blockIdx.x % kKeySlots)],
+                          (unsigned long long)k);
+        }
+        lo = seg_hi;
     }
 }
 
@@ -234,9 +261,8 @@ __global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a)
     __shared__ uint32_t pre[PLD_MAX_BATCH + 1];
     const RankCommon &c = a.c;
     candidate_prefix(c, pre);
-    const uint32_t total = pre[c.B];
-    const uint32_t lo = (uint32_t)(((uint64_t)blockIdx.x * total) / gridDim.x);
-    const uint32_t hi = (uint32_t)(((uint64_t)(blockIdx.x + 1) * total) / gridDim.x);
+    uint32_t lo, hi;
+    block_share(pre[c.B], lo, hi);
     for (uint32_t base = lo; base < hi; base += kRankThreads) {
         const uint32_t i = base + threadIdx.x;
         const bool active = i < hi;
@@ -249,31 +275,7 @@ __global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a)
             float s = __builtin_nanf("");
             if (T >= 2 && j >= 1 && (int64_t)j <= T - 2 && (int64_t)(j - 1) < a.n_keys) {
                 const float *col = a.attn + (int64_t)b * a.as + (j - 1);
-                if (a.agg == PLD_AGG_SUM) {
-                    float acc = 0.f;
-                    int r = 0;
-                    for (; r + 8 <= a.R; r += 8) {
-                        float v[8];
-#pragma unroll
-                        for (int u = 0; u < 8; ++u) v[u] = col[(int64_t)(r + u) * a.ar];
-#pragma unroll
-                        for (int u = 0; u < 8; ++u) acc += v[u];
-                    }
-                    for (; r < a.R; ++r) acc += col[(int64_t)r * a.ar];
-                    s = acc;
-                } else {
-                    float acc = -INFINITY;
-                    int r = 0;
-                    for (; r + 8 <= a.R; r += 8) {
-                        float v[8];
-#pragma unroll
-                        for (int u = 0; u < 8; ++u) v[u] = col[(int64_t)(r + u) * a.ar];
-#pragma unroll
-                        for (int u = 0; u < 8; ++u) acc = fmaxf(acc, v[u]);
-                    }
-                    for (; r < a.R; ++r) acc = fmaxf(acc, col[(int64_t)r * a.ar]);
-                    s = acc;
-                }
+                s = attn_gather(col, a.ar, a.R, a.agg == PLD_AGG_SUM);
                 if (s > c.threshold) key = rank_key(s, j);
             }
             if (c.scores) c.scores[(int64_t)b * c.cap + slot] = s;
@@ -281,27 +283,17 @@ __global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a)
         // one atomic per wave when all its lanes share a sequence
         const int b0 = __shfl(b, 0);
         const bool same = __ballot(active && b != b0) == 0ull;
+        const int slot = (int)((blockIdx.x * kRankWaves + threadIdx.x / kWave) % kKeySlots);
         if (same) {
             uint64_t m = wave_max_u64(key);
-            if (lane_id() == 0 && m) atomicMax((unsigned long long *)&c.keys[b0], (unsigned long long)m);
+            if (lane_id() == 0 && m)
+                atomicMax((unsigned long long *)&c.keys[(int64_t)b0 * kKeySlots + slot],
+                          (unsigned long long)m);
         } else if (key) {
-            atomicMax((unsigned long long *)&c.keys[b], (unsigned long long)key);
+            atomicMax((unsigned long long *)&c.keys[(int64_t)b * kKeySlots + slot],
+                      (unsigned long long)key);
         }
     }
-}
-
-// Blocks of the persistent ranking grids: a few per CU keeps enough rows in
-// flight; the ranges are equal, so the grid size does not affect balance.
-constexpr int kRankBlocks = 1024;
-
-static int check_common(const int32_t *lens, const int32_t *cand_pos, int64_t cap,
-                        const int32_t *cand_count, int B, float threshold, int32_t *best_pos,
-                        float *best_score, void *workspace, size_t workspace_bytes) {
-    if (!lens || !cand_pos || !cand_count || !best_pos || !best_score) return PLD_ERR_INVALID;
-    if (B < 1 || B > PLD_MAX_BATCH || cap < 1 || isnan(threshold)) return PLD_ERR_INVALID;
-    if ((uint64_t)B * (uint64_t)cap >= (1ull << 32)) return PLD_ERR_INVALID;
-    if (!workspace || workspace_bytes < rank_ws_bytes(B)) return PLD_ERR_WORKSPACE;
-    return PLD_OK;
 }
 
 static RankCommon make_common(const int32_t *lens, const int32_t *cand_pos, int64_t cap,
@@ -321,52 +313,40 @@ static RankCommon make_common(const int32_t *lens, const int32_t *cand_pos, int6
     return c;
 }
 
-}  // namespace pld
-
-using namespace pld;
-
-extern "C" int pld_rank_hidden(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
-                               int64_t n_rows, int d, const int32_t *lens, const int32_t *cand_pos,
-                               int64_t cap, const int32_t *cand_count, int B, float threshold,
-                               float *scores, int32_t *best_pos, float *best_score,
-                               void *workspace, size_t workspace_bytes, void *stream) {
-    if (!hidden) return PLD_ERR_INVALID;
-    int rc = check_common(lens, cand_pos, cap, cand_count, B, threshold, best_pos, best_score,
-                          workspace, workspace_bytes);
-    if (rc != PLD_OK) return rc;
+static int prep_hidden(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
+                       int64_t n_rows, int d, const int32_t *lens, const int32_t *cand_pos,
+                       int64_t cap, const int32_t *cand_count, int B, float threshold,
+                       float *scores, void *workspace, size_t workspace_bytes,
+                       RankHiddenArgs &a) {
+    if (!hidden || !lens || !cand_pos || !cand_count) return PLD_ERR_INVALID;
+    if (B < 1 || B > PLD_MAX_BATCH || cap < 1 || isnan(threshold)) return PLD_ERR_INVALID;
+    if ((uint64_t)B * (uint64_t)cap >= (1ull << 32)) return PLD_ERR_INVALID;
     if (d < 8 || d > PLD_MAX_HIDDEN || d % 8 != 0 || n_rows < 1) return PLD_ERR_INVALID;
     if (h_row_stride < d || h_seq_stride < 0) return PLD_ERR_INVALID;
     if (((uintptr_t)hidden & 15) || (h_row_stride % 8) || (h_seq_stride % 8)) return PLD_ERR_ALIGN;
-    RankHiddenArgs a;
-    a.c = make_common(lens, cand_pos, cap, cand_count, B, threshold, scores, best_pos, best_score,
+    if (!workspace || workspace_bytes < rank_ws_bytes(B)) return PLD_ERR_WORKSPACE;
+    a.c = make_common(lens, cand_pos, cap, cand_count, B, threshold, scores, nullptr, nullptr,
                       workspace);
     a.hidden = hidden;
     a.hs = h_seq_stride;
     a.hr = h_row_stride;
     a.n_rows = n_rows;
     a.d = d;
-    size_t lds = (size_t)(d / 8) * sizeof(uint4) + (size_t)(B + 1) * sizeof(uint32_t);
-    hipLaunchKernelGGL(rank_hidden_kernel, dim3(kRankBlocks), dim3(kRankThreads), lds,
-                       (hipStream_t)stream, a);
-    hipLaunchKernelGGL(rank_finish_kernel, dim3((B + 255) / 256), dim3(256), 0, (hipStream_t)stream,
-                       a.c);
-    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+    return PLD_OK;
 }
 
-extern "C" int pld_rank_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stride,
-                             int64_t n_keys, int R, int agg, const int32_t *lens,
-                             const int32_t *cand_pos, int64_t cap, const int32_t *cand_count, int B,
-                             float threshold, float *scores, int32_t *best_pos, float *best_score,
-                             void *workspace, size_t workspace_bytes, void *stream) {
-    if (!attn) return PLD_ERR_INVALID;
-    int rc = check_common(lens, cand_pos, cap, cand_count, B, threshold, best_pos, best_score,
-                          workspace, workspace_bytes);
-    if (rc != PLD_OK) return rc;
+static int prep_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stride,
+                     int64_t n_keys, int R, int agg, const int32_t *lens, const int32_t *cand_pos,
+                     int64_t cap, const int32_t *cand_count, int B, float threshold, float *scores,
+                     void *workspace, size_t workspace_bytes, RankAttnArgs &a) {
+    if (!attn || !lens || !cand_pos || !cand_count) return PLD_ERR_INVALID;
+    if (B < 1 || B > PLD_MAX_BATCH || cap < 1 || isnan(threshold)) return PLD_ERR_INVALID;
+    if ((uint64_t)B * (uint64_t)cap >= (1ull << 32)) return PLD_ERR_INVALID;
     if (R < 1 || n_keys < 1 || (agg != PLD_AGG_SUM && agg != PLD_AGG_MAX)) return PLD_ERR_INVALID;
     if (a_row_stride < 0 || a_seq_stride < 0) return PLD_ERR_INVALID;
     if ((uintptr_t)attn & 3) return PLD_ERR_ALIGN;
-    RankAttnArgs a;
-    a.c = make_common(lens, cand_pos, cap, cand_count, B, threshold, scores, best_pos, best_score,
+    if (!workspace || workspace_bytes < rank_ws_bytes(B)) return PLD_ERR_WORKSPACE;
+    a.c = make_common(lens, cand_pos, cap, cand_count, B, threshold, scores, nullptr, nullptr,
                       workspace);
     a.attn = attn;
     a.as = a_seq_stride;
@@ -374,9 +354,101 @@ extern "C" int pld_rank_attn(const float *attn, int64_t a_seq_stride, int64_t a_
     a.n_keys = n_keys;
     a.R = R;
     a.agg = agg;
-    hipLaunchKernelGGL(rank_attn_kernel, dim3(kRankBlocks), dim3(kRankThreads), 0,
-                       (hipStream_t)stream, a);
-    hipLaunchKernelGGL(rank_finish_kernel, dim3((B + 255) / 256), dim3(256), 0, (hipStream_t)stream,
-                       a.c);
-    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+    return PLD_OK;
+}
+
+// The ranking grids are persistent: as many blocks as fit on the device at
+// once, each taking an equal contiguous share of the flattened candidates.
+static void launch_hidden(const RankHiddenArgs &a, hipStream_t s) {
+    const size_t lds = (size_t)(a.d / 8) * sizeof(uint4) + (size_t)(a.c.B + 1) * sizeof(uint32_t);
+    const int grid = resident_blocks(reinterpret_cast<const void *>(&rank_hidden_kernel),
+                                     kRankThreads, lds) * PLD_RANK_OVERSUB;
+    hipLaunchKernelGGL(rank_hidden_kernel, dim3(grid), dim3(kRankThreads), lds, s, a);
+}
+
+static void launch_attn(const RankAttnArgs &a, hipStream_t s) {
+    const int grid = resident_blocks(reinterpret_cast<const void *>(&rank_attn_kernel),
+                                     kRankThreads, 0) * PLD_RANK_OVERSUB;
+    hipLaunchKernelGGL(rank_attn_kernel, dim3(grid), dim3(kRankThreads), 0, s, a);
+}
+
+static int launch_select(RankCommon c, int32_t *best_pos, float *best_score, hipStream_t s) {
+    if (!best_pos || !best_score) return PLD_ERR_INVALID;
+    c.best_pos = best_pos;
+    c.best_score = best_score;
+    hipLaunchKernelGGL(rank_finish_kernel, dim3((c.B + 255) / 256), dim3(256), 0, s, c);
+    return PLD_OK;
+}
+
+static int launched() { return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH; }
+
+}  // namespace pld
+
+using namespace pld;
+
+extern "C" int pld_score_hidden(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
+                                int64_t n_rows, int d, const int32_t *lens,
+                                const int32_t *cand_pos, int64_t cap, const int32_t *cand_count,
+                                int B, float threshold, float *scores, void *workspace,
+                                size_t workspace_bytes, void *stream) {
+    RankHiddenArgs a;
+    int rc = prep_hidden(hidden, h_seq_stride, h_row_stride, n_rows, d, lens, cand_pos, cap,
+                         cand_count, B, threshold, scores, workspace, workspace_bytes, a);
+    if (rc != PLD_OK) return rc;
+    launch_hidden(a, (hipStream_t)stream);
+    return launched();
+}
+
+extern "C" int pld_score_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stride,
+                              int64_t n_keys, int R, int agg, const int32_t *lens,
+                              const int32_t *cand_pos, int64_t cap, const int32_t *cand_count,
+                              int B, float threshold, float *scores, void *workspace,
+                              size_t workspace_bytes, void *stream) {
+    RankAttnArgs a;
+    int rc = prep_attn(attn, a_seq_stride, a_row_stride, n_keys, R, agg, lens, cand_pos, cap,
+                       cand_count, B, threshold, scores, workspace, workspace_bytes, a);
+    if (rc != PLD_OK) return rc;
+    launch_attn(a, (hipStream_t)stream);
+    return launched();
+}
+
+extern "C" int pld_select_best(int B, int32_t *best_pos, float *best_score, void *workspace,
+                               size_t workspace_bytes, void *stream) {
+    if (B < 1 || B > PLD_MAX_BATCH || !best_pos || !best_score) return PLD_ERR_INVALID;
+    if (!workspace || workspace_bytes < rank_ws_bytes(B)) return PLD_ERR_WORKSPACE;
+    RankCommon c{};
+    c.B = B;
+    c.keys = (uint64_t *)workspace;
+    int rc = launch_select(c, best_pos, best_score, (hipStream_t)stream);
+    return rc != PLD_OK ? rc : launched();
+}
+
+extern "C" int pld_rank_hidden(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
+                               int64_t n_rows, int d, const int32_t *lens, const int32_t *cand_pos,
+                               int64_t cap, const int32_t *cand_count, int B, float threshold,
+                               float *scores, int32_t *best_pos, float *best_score,
+                               void *workspace, size_t workspace_bytes, void *stream) {
+    if (!best_pos || !best_score) return PLD_ERR_INVALID;
+    RankHiddenArgs a;
+    int rc = prep_hidden(hidden, h_seq_stride, h_row_stride, n_rows, d, lens, cand_pos, cap,
+                         cand_count, B, threshold, scores, workspace, workspace_bytes, a);
+    if (rc != PLD_OK) return rc;
+    launch_hidden(a, (hipStream_t)stream);
+    launch_select(a.c, best_pos, best_score, (hipStream_t)stream);
+    return launched();
+}
+
+extern "C" int pld_rank_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stride,
+                             int64_t n_keys, int R, int agg, const int32_t *lens,
+                             const int32_t *cand_pos, int64_t cap, const int32_t *cand_count, int B,
+                             float threshold, float *scores, int32_t *best_pos, float *best_score,
+                             void *workspace, size_t workspace_bytes, void *stream) {
+    if (!best_pos || !best_score) return PLD_ERR_INVALID;
+    RankAttnArgs a;
+    int rc = prep_attn(attn, a_seq_stride, a_row_stride, n_keys, R, agg, lens, cand_pos, cap,
+                       cand_count, B, threshold, scores, workspace, workspace_bytes, a);
+    if (rc != PLD_OK) return rc;
+    launch_attn(a, (hipStream_t)stream);
+    launch_select(a.c, best_pos, best_score, (hipStream_t)stream);
+    return launched();
 }

@@ -24,15 +24,24 @@
 
 namespace pld {
 
+// Launch tunables (compile-time; -D overrides serve tuning builds only).
+#ifndef PLD_VERIFY_UNROLL
+#define PLD_VERIFY_UNROLL 8          // 16-byte loads in flight per thread
+#endif
+#ifndef PLD_VERIFY_TARGET_BLOCKS
+#define PLD_VERIFY_TARGET_BLOCKS 2048    // split-row kernel: blocks to aim for
+#endif
+
 constexpr int kVerifyThreads = 256;
 constexpr int kVerifyWaves = kVerifyThreads / kWave;
-constexpr int kVerifyUnroll = 8;
+constexpr int kVerifyUnroll = PLD_VERIFY_UNROLL;
 
 struct VerifyArgs {
     const void *logits;
     int64_t ls, lr;
     int V, K, B;
-    int S;
+    int S;         // blocks per row (general kernel)
+    int chunk;     // 16-byte vectors per block (the last block of a row takes the rest)
     const int32_t *draft;
     const int32_t *draft_len;
     int32_t *accept_len;
@@ -81,17 +90,30 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArg
     constexpr int P = E::kPerVec;
     __shared__ uint64_t s_key[kVerifyWaves];
     const int split = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
-    const int L = a.draft_len[b];
-    if (L < 0 || L > a.K || i > L) return;   // rows past the draft are never read
 
     const T *row = reinterpret_cast<const T *>(a.logits) + (int64_t)b * a.ls + (int64_t)i * a.lr;
     // The row as [head | 16-byte vectors | tail]; head and tail are scalar.
     const int mis = (int)(((uintptr_t)row & 15) / sizeof(T));
     int head = mis ? (P - mis) : 0;
     if (head > a.V) head = a.V;
-    const int64_t nvec = (int64_t)(a.V - head) / P;
-    const int64_t body_end = head + nvec * P;
-    const int64_t v0 = (nvec * split) / a.S, v1 = (nvec * (split + 1)) / a.S;
+    const int nvec = (a.V - head) / P;
+    const int64_t body_end = head + (int64_t)nvec * P;
+    const int v0 = min(split * a.chunk, nvec);
+    const int v1 = (split == a.S - 1) ? nvec : min(v0 + a.chunk, nvec);
+    const uint4 *vec = reinterpret_cast<const uint4 *>(row + head);
+    const int64_t my_v = v0 + threadIdx.x;
+
+    // The first batch of this thread's vectors is requested together with the
+    // draft length (every row of the buffer exists, so the loads are in
+    // bounds); a row past the draft then returns without reading further.
+    uint4 r[kVerifyUnroll];
+#pragma unroll
+    for (int u = 0; u < kVerifyUnroll; ++u) {
+        const int64_t vi = my_v + (int64_t)u * kVerifyThreads;
+        if (vi < v1) r[u] = ld_stream(vec + vi);
+    }
+    const int L = a.draft_len[b];
+    if (L < 0 || L > a.K || i > L) return;   // rows past the draft are not used
 
     // Each thread keeps the first maximum of its own elements, which it visits
     // in increasing index order: a later element replaces the best only when
@@ -102,7 +124,6 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArg
     float best = -INFINITY;
     uint32_t bi = kNone;
     const bool has_head = split == 0 && (int)threadIdx.x < head;
-    const int64_t my_v = v0 + threadIdx.x;
     const bool has_tail = split == a.S - 1 && body_end + threadIdx.x < a.V;
     if (has_head) bi = threadIdx.x;
     else if (my_v < v1) bi = (uint32_t)(head + my_v * P);
@@ -111,13 +132,13 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArg
         const float f = E::get(row, threadIdx.x);
         if (f > best) best = f;
     }
-    const uint4 *vec = reinterpret_cast<const uint4 *>(row + head);
     for (int64_t vb = my_v; vb < v1; vb += (int64_t)kVerifyThreads * kVerifyUnroll) {
-        uint4 r[kVerifyUnroll];
+        if (vb != my_v) {
 #pragma unroll
-        for (int u = 0; u < kVerifyUnroll; ++u) {
-            const int64_t vi = vb + (int64_t)u * kVerifyThreads;
-            if (vi < v1) r[u] = vec[vi];
+            for (int u = 0; u < kVerifyUnroll; ++u) {
+                const int64_t vi = vb + (int64_t)u * kVerifyThreads;
+                if (vi < v1) r[u] = ld_stream(vec + vi);
+            }
         }
 #pragma unroll
         for (int u = 0; u < kVerifyUnroll; ++u) {
@@ -159,40 +180,52 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArg
     }
 }
 
-// One thread per sequence: y_i from the row keys, the accepted length, the
-// emitted tokens; the keys are returned to zero.
-__global__ __launch_bounds__(64) void verify_accept_kernel(VerifyArgs a) {
-    const int b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= a.B) return;
+// One wave per sequence, one lane per row: y_i from the row keys, the first
+// mismatch by a ballot, the emitted tokens; the keys are returned to zero.
+__global__ __launch_bounds__(256) void verify_accept_kernel(VerifyArgs a) {
+    const int b = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave);
+    const int lane = lane_id();
+    if (b >= a.B) return;   // wave-uniform
     const int K = a.K;
     const int L = a.draft_len[b];
     int32_t *out = a.out_tokens + (int64_t)b * (K + 1);
     if (L < 0 || L > K) {
-        for (int r = 0; r <= K; ++r) out[r] = -1;
-        a.accept_len[b] = -1;
-        a.out_count[b] = 0;
+        for (int r = lane; r <= K; r += kWave) out[r] = -1;
+        if (lane == 0) {
+            a.accept_len[b] = -1;
+            a.out_count[b] = 0;
+        }
         return;
     }
     uint64_t *slot = a.keys + (int64_t)b * (K + 1);
     const int32_t *dr = a.draft + (int64_t)b * K;
-    int acc = L;
-    int32_t y_acc = -1;
-    for (int r = 0; r <= L; ++r) {
-        const uint64_t k = slot[r];
-        slot[r] = 0;
-        const int32_t y = (int32_t)argmax_key_index(k);
-        if (r < acc && r < L && y != dr[r]) {
-            acc = r;
-            y_acc = y;
-        } else if (r == acc) {
-            y_acc = y;
+    int acc = L;           // accepted length: first mismatch, else L
+    int32_t y_acc = -1;    // the model's token at position acc
+    bool found = false;
+    for (int base = 0; base <= L; base += kWave) {
+        const int r = base + lane;
+        int32_t y = -1;
+        bool mism = false;
+        if (r <= L) {
+            const uint64_t k = slot[r];
+            slot[r] = 0;
+            y = (int32_t)argmax_key_index(k);
+            mism = (r < L) && (y != dr[r]);
         }
+        const uint64_t mk = __ballot(mism);
+        if (!found && mk) {
+            const int f = __ffsll((unsigned long long)mk) - 1;
+            acc = base + f;
+            y_acc = __shfl(y, f);
+            found = true;
+        }
+        if (!found && L >= base && L < base + kWave) y_acc = __shfl(y, L - base);
     }
-    for (int r = 0; r < acc; ++r) out[r] = dr[r];
-    out[acc] = y_acc;
-    for (int r = acc + 1; r <= K; ++r) out[r] = -1;
-    a.accept_len[b] = acc;
-    a.out_count[b] = acc + 1;
+    for (int r = lane; r <= K; r += kWave) out[r] = r < acc ? dr[r] : (r == acc ? y_acc : -1);
+    if (lane == 0) {
+        a.accept_len[b] = acc;
+        a.out_count[b] = acc + 1;
+    }
 }
 
 // ------------------------------------------------------------------ emit
@@ -212,17 +245,10 @@ __global__ __launch_bounds__(256) void emit_kernel(const int32_t *tokens, int64_
     if (i == 0) draft_len[b] = (int32_t)L;
 }
 
-}  // namespace pld
-
-using namespace pld;
-
-extern "C" int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride,
-                                 int64_t l_row_stride, int V, int K, const int32_t *draft,
-                                 const int32_t *draft_len, int B, int32_t *accept_len,
-                                 int32_t *out_tokens, int32_t *out_count, void *workspace,
-                                 size_t workspace_bytes, void *stream) {
-    if (!logits || !draft || !draft_len || !accept_len || !out_tokens || !out_count)
-        return PLD_ERR_INVALID;
+static int prep_verify(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
+                       int V, int K, const int32_t *draft_len, int B, void *workspace,
+                       size_t workspace_bytes, VerifyArgs &a) {
+    if (!logits || !draft_len) return PLD_ERR_INVALID;
     if (B < 1 || K < 1 || V < 1 || (dtype != PLD_F32 && dtype != PLD_BF16)) return PLD_ERR_INVALID;
     if (B > 65535 || K + 1 > 65535) return PLD_ERR_INVALID;       // grid y / z limits
     if (l_row_stride < V || l_seq_stride < (int64_t)(K + 1) * l_row_stride) return PLD_ERR_INVALID;
@@ -233,11 +259,11 @@ extern "C" int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_st
     // at least two 16-byte vectors per thread.
     const int64_t rows = (int64_t)B * (K + 1);
     const int64_t nvec = (int64_t)V * esz / 16;
-    int64_t S = (2048 + rows - 1) / rows;
-    int64_t smax = nvec / (2 * kVerifyThreads);
+    int64_t S = (PLD_VERIFY_TARGET_BLOCKS + rows - 1) / rows;
+    const int64_t smax = nvec / (2 * kVerifyThreads);
     if (S > smax) S = smax;
     if (S < 1) S = 1;
-    VerifyArgs a;
+    a = VerifyArgs{};
     a.logits = logits;
     a.ls = l_seq_stride;
     a.lr = l_row_stride;
@@ -245,19 +271,74 @@ extern "C" int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_st
     a.K = K;
     a.B = B;
     a.S = (int)S;
+    a.chunk = (int)((nvec + S - 1) / S);
+    a.draft_len = draft_len;
+    a.keys = (uint64_t *)workspace;
+    return PLD_OK;
+}
+
+static void launch_argmax(const VerifyArgs &a, int dtype, hipStream_t s) {
+    dim3 grid((unsigned)a.S, (unsigned)(a.K + 1), (unsigned)a.B);
+    if (dtype == PLD_F32)
+        hipLaunchKernelGGL(verify_argmax_kernel<0>, grid, dim3(kVerifyThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(verify_argmax_kernel<1>, grid, dim3(kVerifyThreads), 0, s, a);
+}
+
+static void launch_accept(const VerifyArgs &a, hipStream_t s) {
+    hipLaunchKernelGGL(verify_accept_kernel, dim3((a.B + 3) / 4), dim3(256), 0, s, a);
+}
+
+}  // namespace pld
+
+using namespace pld;
+
+extern "C" int pld_verify_argmax(const void *logits, int dtype, int64_t l_seq_stride,
+                                 int64_t l_row_stride, int V, int K, const int32_t *draft_len,
+                                 int B, void *workspace, size_t workspace_bytes, void *stream) {
+    VerifyArgs a;
+    int rc = prep_verify(logits, dtype, l_seq_stride, l_row_stride, V, K, draft_len, B, workspace,
+                         workspace_bytes, a);
+    if (rc != PLD_OK) return rc;
+    launch_argmax(a, dtype, (hipStream_t)stream);
+    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+}
+
+extern "C" int pld_verify_accept(const int32_t *draft, const int32_t *draft_len, int B, int K,
+                                 int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
+                                 void *workspace, size_t workspace_bytes, void *stream) {
+    if (!draft || !draft_len || !accept_len || !out_tokens || !out_count) return PLD_ERR_INVALID;
+    if (B < 1 || K < 1 || B > 65535 || K + 1 > 65535) return PLD_ERR_INVALID;
+    if (!workspace || workspace_bytes < verify_ws_bytes(B, K)) return PLD_ERR_WORKSPACE;
+    VerifyArgs a{};
+    a.K = K;
+    a.B = B;
     a.draft = draft;
     a.draft_len = draft_len;
     a.accept_len = accept_len;
     a.out_tokens = out_tokens;
     a.out_count = out_count;
     a.keys = (uint64_t *)workspace;
-    dim3 grid((unsigned)S, (unsigned)(K + 1), (unsigned)B);
-    hipStream_t s = (hipStream_t)stream;
-    if (dtype == PLD_F32)
-        hipLaunchKernelGGL(verify_argmax_kernel<0>, grid, dim3(kVerifyThreads), 0, s, a);
-    else
-        hipLaunchKernelGGL(verify_argmax_kernel<1>, grid, dim3(kVerifyThreads), 0, s, a);
-    hipLaunchKernelGGL(verify_accept_kernel, dim3((B + 63) / 64), dim3(64), 0, s, a);
+    launch_accept(a, (hipStream_t)stream);
+    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+}
+
+extern "C" int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride,
+                                 int64_t l_row_stride, int V, int K, const int32_t *draft,
+                                 const int32_t *draft_len, int B, int32_t *accept_len,
+                                 int32_t *out_tokens, int32_t *out_count, void *workspace,
+                                 size_t workspace_bytes, void *stream) {
+    if (!draft || !accept_len || !out_tokens || !out_count) return PLD_ERR_INVALID;
+    VerifyArgs a;
+    int rc = prep_verify(logits, dtype, l_seq_stride, l_row_stride, V, K, draft_len, B, workspace,
+                         workspace_bytes, a);
+    if (rc != PLD_OK) return rc;
+    a.draft = draft;
+    a.accept_len = accept_len;
+    a.out_tokens = out_tokens;
+    a.out_count = out_count;
+    launch_argmax(a, dtype, (hipStream_t)stream);
+    launch_accept(a, (hipStream_t)stream);
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }
 

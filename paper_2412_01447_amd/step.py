@@ -7,13 +7,20 @@ Eq. 2 / Eq. 3, draft Sec. 4.3, greedy verification Sec. 4.4).
 """
 import torch
 
-from . import (PLD_AGG_SUM, pld_emit_draft, pld_find_candidates, pld_find_scratch_bytes,
-               pld_rank_attn, pld_rank_hidden, pld_verify_greedy, pld_workspace_bytes)
+from . import (DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, pld_draft_attn, pld_draft_hidden,
+               pld_emit_draft, pld_find_candidates, pld_find_scratch_bytes, pld_rank_attn,
+               pld_rank_hidden, pld_score_attn, pld_score_hidden, pld_select_best,
+               pld_verify_accept, pld_verify_argmax, pld_verify_greedy, pld_workspace_bytes)
 
 
 class DraftStep:
-    def __init__(self, B, tok_stride, K, device="cuda", cap=None, keep_scores=False):
-        self.B, self.tok_stride, self.K = B, tok_stride, K
+    """mode: "split" runs the separate calls (find, rank, emit), "fused" the one-launch
+    drafting call (tok_stride <= 8192, one ranking), "auto" picks fused when it applies."""
+
+    def __init__(self, B, tok_stride, K, device="cuda", cap=None, keep_scores=False, mode="auto"):
+        if mode not in ("auto", "fused", "split"):
+            raise ValueError(mode)
+        self.B, self.tok_stride, self.K, self.mode = B, tok_stride, K, mode
         cap = tok_stride if cap is None else cap
         i32 = dict(dtype=torch.int32, device=device)
         self.cand_pos = torch.full((B, cap), -1, **i32)
@@ -61,10 +68,58 @@ class DraftStep:
         pld_verify_greedy(logits, self.draft, self.draft_len, self.accept_len, self.out_tokens,
                           self.out_count, self.workspace, stream=stream)
 
+    # the halves of the ranking and verification calls (same results, one kernel each)
+    def score_hidden(self, hidden, lens, threshold=float("-inf"), stream=None):
+        pld_score_hidden(hidden, lens, self.cand_pos, self.cand_count, self.workspace,
+                         threshold=threshold, scores=self.scores, stream=stream)
+
+    def score_attn(self, attn, lens, agg=PLD_AGG_SUM, threshold=float("-inf"), stream=None):
+        pld_score_attn(attn, lens, self.cand_pos, self.cand_count, self.workspace, agg=agg,
+                       threshold=threshold, scores=self.scores_attn, stream=stream)
+
+    def select(self, into_best=True, stream=None):
+        bp = self.best_pos if into_best else self.best_pos_attn
+        bs = self.best_score if into_best else self.best_score_attn
+        pld_select_best(self.B, bp, bs, self.workspace, stream=stream)
+
+    def verify_argmax(self, logits, stream=None):
+        pld_verify_argmax(logits, self.draft_len, self.workspace, stream=stream)
+
+    def verify_accept(self, stream=None):
+        pld_verify_accept(self.draft, self.draft_len, self.accept_len, self.out_tokens,
+                          self.out_count, self.workspace, stream=stream)
+
+    def uses_fused(self, hidden, attn):
+        one = (hidden is None) != (attn is None)
+        if self.mode == "fused":
+            if not one or self.tok_stride > DRAFT_MAX_TOK_STRIDE:
+                raise ValueError("the one-launch drafting call takes one artifact and "
+                                 "tok_stride <= 8192")
+            return True
+        return self.mode == "auto" and one and self.tok_stride <= DRAFT_MAX_TOK_STRIDE
+
+    def draft_fused(self, tokens, lens, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
+                    threshold=float("-inf"), stream=None):
+        """find + rank + emit with the one-launch call."""
+        if hidden is not None:
+            pld_draft_hidden(tokens, lens, ngram[0], ngram[1], hidden, self.K, self.cand_pos,
+                             self.cand_count, self.ngram_used, self.best_pos, self.best_score,
+                             self.draft, self.draft_len, threshold=threshold, scores=self.scores,
+                             stream=stream)
+        else:
+            pld_draft_attn(tokens, lens, ngram[0], ngram[1], attn, self.K, self.cand_pos,
+                           self.cand_count, self.ngram_used, self.best_pos, self.best_score,
+                           self.draft, self.draft_len, agg=agg, threshold=threshold,
+                           scores=self.scores_attn, stream=stream)
+
     def run(self, tokens, lens, logits, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
             threshold=float("-inf"), stream=None):
         """The whole step.  With both artifacts, the hidden-state ranking drafts and the
         attention ranking is written to best_pos_attn / best_score_attn."""
+        if self.uses_fused(hidden, attn):
+            self.draft_fused(tokens, lens, hidden, attn, ngram, agg, threshold, stream=stream)
+            self.verify(logits, stream=stream)
+            return
         self.find(tokens, lens, *ngram, stream=stream)
         if attn is not None:
             self.rank_attn(attn, lens, agg=agg, threshold=threshold, into_best=hidden is None,
@@ -73,6 +128,53 @@ class DraftStep:
             self.rank_hidden(hidden, lens, threshold=threshold, stream=stream)
         self.emit(tokens, lens, stream=stream)
         self.verify(logits, stream=stream)
+
+    def plan(self, tokens, lens, logits, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
+             threshold=float("-inf"), stream=None):
+        """The step as an ordered list of (name, prepared call), one kernel per entry
+        except "find" on long contexts (two): the same work as run(), with every
+        argument marshalled once so that issuing a step costs only the launches."""
+        P = dict(stream=stream, prepare=True)
+        if self.uses_fused(hidden, attn):
+            if hidden is not None:
+                d = pld_draft_hidden(tokens, lens, ngram[0], ngram[1], hidden, self.K,
+                                     self.cand_pos, self.cand_count, self.ngram_used,
+                                     self.best_pos, self.best_score, self.draft, self.draft_len,
+                                     threshold=threshold, scores=self.scores, **P)
+            else:
+                d = pld_draft_attn(tokens, lens, ngram[0], ngram[1], attn, self.K, self.cand_pos,
+                                   self.cand_count, self.ngram_used, self.best_pos,
+                                   self.best_score, self.draft, self.draft_len, agg=agg,
+                                   threshold=threshold, scores=self.scores_attn, **P)
+            ops = [("draft", d)]
+        else:
+            ops = [("find", pld_find_candidates(tokens, lens, ngram[0], ngram[1], self.cand_pos,
+                                                self.cand_count, self.ngram_used, self.scratch,
+                                                **P))]
+            if attn is not None:
+                into = hidden is None
+                ops.append(("score_attn", pld_score_attn(attn, lens, self.cand_pos,
+                                                         self.cand_count, self.workspace, agg=agg,
+                                                         threshold=threshold,
+                                                         scores=self.scores_attn, **P)))
+                ops.append(("select_attn", pld_select_best(
+                    self.B, self.best_pos if into else self.best_pos_attn,
+                    self.best_score if into else self.best_score_attn, self.workspace, **P)))
+            if hidden is not None:
+                ops.append(("score_hidden", pld_score_hidden(hidden, lens, self.cand_pos,
+                                                             self.cand_count, self.workspace,
+                                                             threshold=threshold,
+                                                             scores=self.scores, **P)))
+                ops.append(("select", pld_select_best(self.B, self.best_pos, self.best_score,
+                                                      self.workspace, **P)))
+            ops.append(("emit", pld_emit_draft(tokens, lens, self.best_pos, self.K, self.draft,
+                                               self.draft_len, **P)))
+        ops.append(("verify_argmax", pld_verify_argmax(logits, self.draft_len, self.workspace,
+                                                       **P)))
+        ops.append(("verify_accept", pld_verify_accept(self.draft, self.draft_len,
+                                                       self.accept_len, self.out_tokens,
+                                                       self.out_count, self.workspace, **P)))
+        return ops
 
     def host(self):
         """Copies every output to host numpy arrays (synchronises)."""

@@ -21,15 +21,16 @@ from paper_2412_01447_amd.step import DraftStep
 
 pytestmark = pytest.mark.gpu
 
-CASES = [(1, True), (1, False), (2, True), (2, False), (3, True), (3, False), (4, True),
-         (5, True), (5, False)]
+CASES = [(1, True, "fused"), (1, False, "split"), (2, True, "fused"), (2, False, "fused"),
+         (2, True, "split"), (3, True, "fused"), (3, False, "split"), (3, False, "fused"),
+         (4, True, "split"), (5, True, "split"), (5, False, "split")]
 
 
-@pytest.mark.parametrize("cid,structured", CASES, ids=[f"cfg{c}_{'structured' if s else 'random'}"
-                                                       for c, s in CASES])
-def test_config_step_parity(cid, structured):
+@pytest.mark.parametrize("cid,structured,mode", CASES,
+                         ids=[f"cfg{c}_{'structured' if s else 'random'}_{m}" for c, s, m in CASES])
+def test_config_step_parity(cid, structured, mode):
     cfg = synth.CONFIGS[cid]
-    say("config", cid, cfg.name, "structured" if structured else "random")
+    say("config", cid, cfg.name, "structured" if structured else "random", mode)
     dev = torch.device("cuda:0")
     w = synth.make_workload(cfg, dev, structured=structured)
     toks, lens = w["tokens"], w["lens"]
@@ -50,7 +51,7 @@ def test_config_step_parity(cid, structured):
     say("  oracle: counts", cc.tolist()[:8], "n", sorted(set(nu.tolist())), "accept",
         rver[0].tolist()[:16])
     # ---- GPU step, as the benchmark launches it
-    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, keep_scores=True)
+    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, keep_scores=True, mode=mode)
     zd = d_bf16(z) if bf16 else d_f32(z)
     attn_d = d_f32(w["attn"]) if w["attn"] is not None else None
     td, ld = d_i32(toks), d_i32(lens)

@@ -362,3 +362,158 @@ def test_workspace_shared_across_calls_and_determinism():
     for r in runs[1:]:
         for x, y in zip(r, runs[0]):
             assert np.array_equal(x, y, equal_nan=True)
+
+
+# ------------------------------------------------------- one-launch drafting
+DRAFT_CASES = [
+    # (B, tok_stride, V, n_min, n_max, d, R, K, seed)
+    (9, 1, 3, 1, 1, 64, 0, 4, 0), (9, 50, 3, 1, 3, 64, 0, 4, 1), (12, 700, 6, 1, 4, 520, 0, 9, 2),
+    (8, 4096, 40, 1, 3, 4096, 0, 10, 3), (5, 8192, 2, 2, 5, 128, 0, 16, 4),
+    (9, 300, 4, 1, 2, 0, 7, 6, 5), (6, 8192, 20, 1, 1, 0, 40, 16, 6), (4, 5000, 1, 1, 3, 0, 3, 8, 7),
+]
+
+
+@pytest.mark.parametrize("case", DRAFT_CASES, ids=[f"B{c[0]}_S{c[1]}_V{c[2]}_n{c[3]}-{c[4]}_"
+                                                   f"{'d' + str(c[5]) if c[5] else 'R' + str(c[6])}"
+                                                   for c in DRAFT_CASES])
+def test_draft_fused_parity(case):
+    """The one-launch drafting call equals the oracle's find, rank and emit, and
+    its scores are bit-identical to the separate ranking call."""
+    B, stride, V, nmin, nmax, d, R, K, seed = case
+    say("draft fused", case)
+    rng = np.random.default_rng(100 + seed)
+    toks = rng.integers(0, V, size=(B, stride)).astype(np.int32)
+    lens = rng.integers(1, stride + 1, size=B).astype(np.int32)
+    lens[0] = stride
+    if B > 2:
+        lens[1] = 0
+        lens[2] = stride + 1
+    ref_find = oracle.find(toks, lens, nmin, nmax)
+    cp, cc, nu = ref_find
+    i32 = dict(dtype=torch.int32, device="cuda")
+    o = dict(cand_pos=torch.full((B, stride), -1, **i32), cand_count=torch.zeros(B, **i32),
+             ngram_used=torch.zeros(B, **i32), best_pos=torch.zeros(B, **i32),
+             best_score=torch.zeros(B, dtype=torch.float32, device="cuda"),
+             draft=torch.zeros((B, K), **i32), draft_len=torch.zeros(B, **i32),
+             scores=torch.full((B, stride), 777.0, dtype=torch.float32, device="cuda"))
+    for th in (-math.inf, 0.0):
+        if d:
+            bits = synth.f32_to_bf16_bits(rng.standard_normal((B, stride, d)).astype(np.float32))
+            hd = d_bf16(bits)
+            ref = oracle.rank_hidden(bits, lens, cp, cc, threshold=th)
+            pld.pld_draft_hidden(d_i32(toks), d_i32(lens), nmin, nmax, hd, K, o["cand_pos"],
+                                 o["cand_count"], o["ngram_used"], o["best_pos"], o["best_score"],
+                                 o["draft"], o["draft_len"], threshold=th, scores=o["scores"])
+            split = gpu_rank_hidden(hd, lens, cp, cc, threshold=th)
+        else:
+            A = synth.make_attn(B, R, stride, lens, seed=seed)
+            ref = oracle.rank_attn(A, lens, cp, cc, oracle.AGG_SUM, threshold=th)
+            pld.pld_draft_attn(d_i32(toks), d_i32(lens), nmin, nmax, d_f32(A), K, o["cand_pos"],
+                               o["cand_count"], o["ngram_used"], o["best_pos"], o["best_score"],
+                               o["draft"], o["draft_len"], threshold=th, scores=o["scores"])
+            split = gpu_rank_attn(d_f32(A), lens, cp, cc, pld.PLD_AGG_SUM, threshold=th)
+        torch.cuda.synchronize()
+        g = {k: v.cpu().numpy() for k, v in o.items()}
+        check_find((g["cand_pos"], g["cand_count"], g["ngram_used"]), ref_find, str(case))
+        rsc, rbp, rbs = ref
+        check_scores(g["scores"], rsc, cc, str(case))
+        flips = check_best(g["best_pos"], g["best_score"], rsc, rbp, rbs, cp, cc, str(case),
+                           threshold=th)
+        for b in range(B):          # same bits as the separate ranking call
+            n = cc[b]
+            assert np.array_equal(g["scores"][b, :n], split[0][b, :n], equal_nan=True)
+        assert np.array_equal(g["best_pos"], split[1])
+        rd, rl = oracle.emit(toks, lens, g["best_pos"] if flips else rbp, K)
+        assert np.array_equal(g["draft"], rd) and np.array_equal(g["draft_len"], rl)
+
+
+# ------------------------------------------------ halves and graph replays
+def test_halves_equal_combined_calls():
+    """score + select == rank, verify_argmax + verify_accept == verify_greedy, bit for bit."""
+    say("halves")
+    from paper_2412_01447_amd.step import DraftStep
+    cfg = synth.Config("t", 6, 12000, 300, 1.1, 0.3, (8, 32), (1, 2), 256, "both", 9, 8, "f32", 31)
+    w = synth.make_workload(cfg, "cuda", structured=False)
+    toks, lens = d_i32(w["tokens"]), d_i32(w["lens"])
+    attn = d_f32(w["attn"])
+    dr, dl = synth.intended_drafts(w["metas"], cfg.K)
+    z = d_f32(synth.logits_for(w, dr, dl))
+    a = DraftStep(cfg.B, cfg.T, cfg.K, device="cuda", keep_scores=True, mode="split")
+    b = DraftStep(cfg.B, cfg.T, cfg.K, device="cuda", keep_scores=True, mode="split")
+    a.run(toks, lens, z, hidden=w["hidden"], attn=attn, ngram=cfg.ngram)
+    b.find(toks, lens, *cfg.ngram)
+    b.score_attn(attn, lens)
+    b.select(into_best=False)
+    b.score_hidden(w["hidden"], lens)
+    b.select()
+    b.emit(toks, lens)
+    b.verify_argmax(z)
+    b.verify_accept()
+    torch.cuda.synchronize()
+    ha, hb = a.host(), b.host()
+    for k in ha:
+        assert np.array_equal(ha[k], hb[k], equal_nan=True), k
+    assert int(torch.count_nonzero(b.workspace).item()) == 0
+
+
+@pytest.mark.parametrize("mode", ["fused", "split"])
+def test_graph_replays_match_eager(mode):
+    """The step captured in a HIP graph gives the eager result on every replay,
+    with eager work and synchronisations between the replays."""
+    say("graph replay", mode)
+    from paper_2412_01447_amd.step import DraftStep
+    cfg = synth.Config("t", 5, 6000, 400, 1.1, 0.3, (8, 32), (1, 3), 512, "hidden", 0, 10, "f32", 41)
+    w = synth.make_workload(cfg, "cuda", structured=True)
+    toks, lens = d_i32(w["tokens"]), d_i32(w["lens"])
+    dr, dl = synth.intended_drafts(w["metas"], cfg.K)
+    z = d_f32(synth.logits_for(w, dr, dl))
+    eager = DraftStep(cfg.B, cfg.T, cfg.K, device="cuda", keep_scores=True, mode=mode)
+    eager.run(toks, lens, z, hidden=w["hidden"], ngram=cfg.ngram)
+    torch.cuda.synchronize()
+    want = eager.host()
+    st = DraftStep(cfg.B, cfg.T, cfg.K, device="cuda", keep_scores=True, mode=mode)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        st.run(toks, lens, z, hidden=w["hidden"], ngram=cfg.ngram)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        st.run(toks, lens, z, hidden=w["hidden"], ngram=cfg.ngram)
+    for rep in range(4):
+        for t in (st.cand_count, st.best_pos, st.draft, st.out_tokens):  # scribble, replay
+            t.fill_(-9)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = st.host()
+        for k in want:
+            assert np.array_equal(got[k], want[k], equal_nan=True), (rep, k)
+        assert int(torch.count_nonzero(st.workspace).item()) == 0
+        eager.run(toks, lens, z, hidden=w["hidden"], ngram=cfg.ngram)   # eager work between
+        torch.cuda.synchronize()
+
+
+def test_verify_aligned_rows_with_tail():
+    """16-byte aligned rows (the persistent kernel) whose width is not a whole
+    number of vectors: the last elements of each row are taken one by one."""
+    say("verify aligned rows with tail")
+    rng = np.random.default_rng(12)
+    for dt, V, pad in (("f32", 1001, 3), ("f32", 4094, 2), ("bf16", 8191, 1), ("bf16", 3001, 7)):
+        B, K = 5, 7
+        Z = rng.standard_normal((B, K + 1, V + pad)).astype(np.float32)
+        Z[:, :, V - 1] = 50.0           # the maximum sits in the tail
+        Z[1, :, V - 2] = 50.0           # a tie between the last vector's end and the tail
+        draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+        draft[0, :3] = V - 1
+        L = np.array([7, 3, 0, 7, 5], np.int32)
+        view = np.ascontiguousarray(Z[:, :, :V])
+        if dt == "f32":
+            ref = oracle.verify(view, draft, L)
+            got = gpu_verify(d_f32(Z)[:, :, :V], draft, L)
+        else:
+            bits = synth.f32_to_bf16_bits(Z)
+            ref = oracle.verify(np.ascontiguousarray(bits[:, :, :V]), draft, L, bf16=True)
+            got = gpu_verify(d_bf16(bits)[:, :, :V], draft, L)
+        check_verify(got, ref, f"{dt} V={V}")
