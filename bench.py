@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 METRIC = "draft+verify step latency (us) per batch; ranking-kernel HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 MALL_BYTES = 256 << 20         # last-level (Infinity) cache
-SEG = 64                       # smallest HBM read granule counted for gathered data
+SEG = 128                      # HBM fetch granule of gathered data (a 128-byte line)
 
 
 def parse():
@@ -56,7 +56,7 @@ def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fu
     out = {}
     out["find"] = int(lens.astype(np.int64).sum() * 4 + C.sum() * 4)
     if cfg.rank in ("attn", "both"):
-        # distinct 64-byte segments of each attention row that hold a key j-1
+        # distinct 128-byte lines of each attention row that hold a key j-1
         segs = 0
         for b in range(B):
             keys = cand_pos[b, :C[b]].astype(np.int64) - 1
@@ -74,6 +74,35 @@ def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fu
         out["draft"] = sum(out.pop(k) for k in ("find", "score_hidden", "score_attn", "select",
                                                 "select_attn", "emit") if k in out)
     return out
+
+
+# kernels behind each timed call (names as rocprofv3 reports them)
+KERNELS = {"draft": "pld::draft_kernel", "find": "pld::find_", "score_hidden": "pld::rank_hidden_kernel",
+           "score_attn": "pld::rank_attn_kernel", "select": "pld::rank_finish_kernel",
+           "select_attn": "pld::rank_finish_kernel", "emit": "pld::emit_kernel",
+           "verify_argmax": "pld::verify_argmax_kernel", "verify_accept": "pld::verify_accept_kernel"}
+
+
+def measured_traffic(workload, call):
+    """HBM bytes per launch of the call's kernel from the committed counter runs
+    (profiles/traffic.json), or None when the kernel sources changed since."""
+    import glob
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        table = json.load(f)
+    h = hashlib.sha256()
+    for fn in sorted(glob.glob(os.path.join(ROOT, "paper_2412_01447_amd", "csrc", "*"))):
+        h.update(os.path.basename(fn).encode())
+        with open(fn, "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != table.get("sources_sha256"):
+        return None
+    rows = table.get("workloads", {}).get(workload, {})
+    hits = [v for k, v in rows.items() if k.startswith(KERNELS.get(call, "?"))]
+    return sum(hits) if hits else None
 
 
 def main():
@@ -166,7 +195,8 @@ def main():
         achieved = nbytes[dominant] / (dom_ms * 1e-3) / 1e9
         roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": None, "bytes_per_launch": nbytes[dominant],
+                    "traffic": measured_traffic(cfg.name, dominant),
+                    "bytes_per_launch": nbytes[dominant],
                     "avg_us": round(dom_ms * 1e3, 2)}
         log(f"[bench] {dominant}: {dom_ms * 1e3:.2f} us avg, {achieved:.1f} GB/s")
 

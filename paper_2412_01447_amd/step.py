@@ -15,7 +15,8 @@ from . import (DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, pld_draft_attn, pld_draft_hidd
 
 class DraftStep:
     """mode: "split" runs the separate calls (find, rank, emit), "fused" the one-launch
-    drafting call (tok_stride <= 8192, one ranking), "auto" picks fused when it applies."""
+    drafting call (tok_stride <= 8192, one ranking), "auto" the one-launch call for
+    hidden-state ranking when it applies and the separate calls otherwise."""
 
     def __init__(self, B, tok_stride, K, device="cuda", cap=None, keep_scores=False, mode="auto"):
         if mode not in ("auto", "fused", "split"):
@@ -96,7 +97,10 @@ class DraftStep:
                 raise ValueError("the one-launch drafting call takes one artifact and "
                                  "tok_stride <= 8192")
             return True
-        return self.mode == "auto" and one and self.tok_stride <= DRAFT_MAX_TOK_STRIDE
+        # auto: the one-launch call for hidden-state ranking; attention gathers of a
+        # long candidate list are address-bound on one CU, so they go wide
+        return (self.mode == "auto" and hidden is not None and attn is None and
+                self.tok_stride <= DRAFT_MAX_TOK_STRIDE)
 
     def draft_fused(self, tokens, lens, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
                     threshold=float("-inf"), stream=None):
