@@ -144,9 +144,13 @@ def main():
         step.run(s["tokens"], s["lens"], s["logits"], hidden=s["hidden"], attn=s["attn"],
                  ngram=cfg.ngram)
 
-    # one step to learn the data-dependent byte counts
+    # one step to learn the data-dependent byte counts (and, for the one-call
+    # drafting, how many blocks should share a sequence)
     run(base)
     torch.cuda.synchronize()
+    if fused:
+        step.tune_split(step.cand_count.cpu().numpy(), hidden=base["hidden"] is not None)
+        log(f"[bench] drafting with {step.draft_split} block(s) per sequence")
     nbytes = algorithmic_bytes(cfg, lens, step.cand_count.cpu().numpy(),
                                step.draft_len.cpu().numpy(), step.cand_pos.cpu().numpy(), elt,
                                fused)
@@ -221,7 +225,8 @@ def main():
                    "ngram": list(cfg.ngram), "ranking": cfg.rank, "hidden_dim": cfg.d,
                    "attn_rows": cfg.R, "K": cfg.K, "logits": cfg.logits,
                    "inputs": "hidden bf16, attention f32, tokens int32",
-                   "drafting": "one launch" if fused else "separate calls",
+                   "drafting": (f"one call, {step.draft_split} block(s) per sequence" if fused
+                                else "separate calls"),
                    "input_copies": copies,
                    "step_bytes": step_bytes},
         "roofline": roofline,

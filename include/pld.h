@@ -236,28 +236,39 @@ int pld_verify_accept(const int32_t *draft, const int32_t *draft_len, int B, int
 
 /*
  * pld_draft_hidden / pld_draft_attn -- the drafting half of a step in one
- * launch: pld_find_candidates, then pld_rank_hidden (or pld_rank_attn), then
+ * call: pld_find_candidates, then pld_rank_hidden (or pld_rank_attn), then
  * pld_emit_draft, with the same definitions, outputs and device-side rules
- * (Eq. 1, Eq. 2 / Eq. 3 and Sec. 4.3).  One block owns one sequence, so
- * the scores, choices and drafts are bit-identical to the separate calls;
- * it needs tok_stride <= 8192 and its time grows with a sequence's own
- * candidate count, so it suits short candidate lists (small batches, the
- * latency regime).  `scores` may be NULL.  No workspace is used.
- * Errors: as the separate calls; tok_stride > 8192 is PLD_ERR_INVALID.
+ * (Eq. 1, Eq. 2 / Eq. 3 and Sec. 4.3); scores, choices and drafts are
+ * bit-identical to the separate calls.  Needs tok_stride <= 8192.
+ *
+ *   blocks_per_seq  S in [1, PLD_MAX_DRAFT_SPLIT]: S blocks share a sequence,
+ *                   each scoring every S-th occurrence.  S = 1 is one launch
+ *                   and uses no workspace -- the lowest latency when the
+ *                   candidate lists are short; S > 1 adds a small finishing
+ *                   launch and spreads long lists over S compute units, and
+ *                   then needs `workspace` (pld_workspace_bytes, as for the
+ *                   ranking calls; left zero).
+ *   scores          may be NULL.
+ * Errors: as the separate calls; tok_stride > 8192 or S out of range is
+ * PLD_ERR_INVALID; S > 1 without a large enough workspace is PLD_ERR_WORKSPACE.
  */
+#define PLD_MAX_DRAFT_SPLIT 256
+
 int pld_draft_hidden(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B,
                      int ngram_min, int ngram_max, const uint16_t *hidden, int64_t h_seq_stride,
                      int64_t h_row_stride, int64_t n_rows, int d, float threshold, int K,
                      int32_t *cand_pos, int64_t cap, int32_t *cand_count, int32_t *ngram_used,
                      float *scores, int32_t *best_pos, float *best_score, int32_t *draft,
-                     int32_t *draft_len, void *stream);
+                     int32_t *draft_len, int blocks_per_seq, void *workspace,
+                     size_t workspace_bytes, void *stream);
 
 int pld_draft_attn(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B,
                    int ngram_min, int ngram_max, const float *attn, int64_t a_seq_stride,
                    int64_t a_row_stride, int64_t n_keys, int R, int agg, float threshold, int K,
                    int32_t *cand_pos, int64_t cap, int32_t *cand_count, int32_t *ngram_used,
                    float *scores, int32_t *best_pos, float *best_score, int32_t *draft,
-                   int32_t *draft_len, void *stream);
+                   int32_t *draft_len, int blocks_per_seq, void *workspace,
+                   size_t workspace_bytes, void *stream);
 
 #ifdef __cplusplus
 }

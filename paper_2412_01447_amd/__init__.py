@@ -25,7 +25,7 @@ __all__ = [
 PLD_OK, PLD_ERR_INVALID, PLD_ERR_ALIGN, PLD_ERR_WORKSPACE, PLD_ERR_LAUNCH = range(5)
 PLD_F32, PLD_BF16 = 0, 1
 PLD_AGG_SUM, PLD_AGG_MAX = 0, 1
-PLD_MAX_NGRAM, PLD_MAX_HIDDEN, PLD_MAX_BATCH = 8, 16384, 4096
+PLD_MAX_NGRAM, PLD_MAX_HIDDEN, PLD_MAX_BATCH, PLD_MAX_DRAFT_SPLIT = 8, 16384, 4096, 256
 DRAFT_MAX_TOK_STRIDE = 8192     # one-launch drafting: one block per sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -57,9 +57,11 @@ _SIGNATURES = {
     "pld_verify_argmax": ([_vp, _int, _i64, _i64, _int, _int, _vp, _int, _vp, _sz, _vp], _int),
     "pld_verify_accept": ([_vp, _vp, _int, _int, _vp, _vp, _vp, _vp, _sz, _vp], _int),
     "pld_draft_hidden": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _i64, _i64, _int, _f32, _int,
-                          _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _int),
+                          _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _int, _vp, _sz, _vp],
+                         _int),
     "pld_draft_attn": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _i64, _i64, _int, _int, _f32,
-                        _int, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp], _int),
+                        _int, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _int, _vp, _sz, _vp],
+                       _int),
 }
 
 
@@ -226,8 +228,8 @@ def pld_verify_greedy(logits, draft, draft_len, accept_len, out_tokens, out_coun
 
 def pld_draft_hidden(tokens, lens, ngram_min, ngram_max, hidden, K, cand_pos, cand_count,
                      ngram_used, best_pos, best_score, draft, draft_len, threshold=float("-inf"),
-                     scores=None, stream=None, prepare=False):
-    """find + hidden-state ranking + emit in one launch (tok_stride <= 8192)."""
+                     scores=None, blocks_per_seq=1, workspace=None, stream=None, prepare=False):
+    """find + hidden-state ranking + emit in one call (tok_stride <= 8192)."""
     import torch
     _need(tokens, torch.int32, "tokens", 2)
     _need(hidden, torch.bfloat16, "hidden", 3)
@@ -235,17 +237,19 @@ def pld_draft_hidden(tokens, lens, ngram_min, ngram_max, hidden, K, cand_pos, ca
     if draft.shape[1] != K or draft.stride(0) != K:
         raise TypeError("draft must be a contiguous [B][K] tensor")
     B, n_rows, d = hidden.shape
-    return _run("pld_draft_hidden", (_ptr(tokens), tokens.stride(0), _ptr(lens), tokens.shape[0],
-          ngram_min, ngram_max, _ptr(hidden), hidden.stride(0), hidden.stride(1), n_rows, d,
-          float(threshold), K, _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count),
-          _ptr(ngram_used), _ptr(scores), _ptr(best_pos), _ptr(best_score), _ptr(draft),
-          _ptr(draft_len), _stream(stream),), prepare)
+    return _run("pld_draft_hidden", (
+        _ptr(tokens), tokens.stride(0), _ptr(lens), tokens.shape[0], ngram_min, ngram_max,
+        _ptr(hidden), hidden.stride(0), hidden.stride(1), n_rows, d, float(threshold), K,
+        _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), _ptr(ngram_used), _ptr(scores),
+        _ptr(best_pos), _ptr(best_score), _ptr(draft), _ptr(draft_len), int(blocks_per_seq),
+        _ptr(workspace), _nbytes(workspace), _stream(stream)), prepare)
 
 
 def pld_draft_attn(tokens, lens, ngram_min, ngram_max, attn, K, cand_pos, cand_count, ngram_used,
                    best_pos, best_score, draft, draft_len, agg=PLD_AGG_SUM,
-                   threshold=float("-inf"), scores=None, stream=None, prepare=False):
-    """find + attention ranking + emit in one launch (tok_stride <= 8192)."""
+                   threshold=float("-inf"), scores=None, blocks_per_seq=1, workspace=None,
+                   stream=None, prepare=False):
+    """find + attention ranking + emit in one call (tok_stride <= 8192)."""
     import torch
     _need(tokens, torch.int32, "tokens", 2)
     _need(attn, torch.float32, "attn", 3)
@@ -253,11 +257,12 @@ def pld_draft_attn(tokens, lens, ngram_min, ngram_max, attn, K, cand_pos, cand_c
     if draft.shape[1] != K or draft.stride(0) != K:
         raise TypeError("draft must be a contiguous [B][K] tensor")
     B, R, n_keys = attn.shape
-    return _run("pld_draft_attn", (_ptr(tokens), tokens.stride(0), _ptr(lens), tokens.shape[0],
-          ngram_min, ngram_max, _ptr(attn), attn.stride(0), attn.stride(1), n_keys, R, int(agg),
-          float(threshold), K, _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count),
-          _ptr(ngram_used), _ptr(scores), _ptr(best_pos), _ptr(best_score), _ptr(draft),
-          _ptr(draft_len), _stream(stream),), prepare)
+    return _run("pld_draft_attn", (
+        _ptr(tokens), tokens.stride(0), _ptr(lens), tokens.shape[0], ngram_min, ngram_max,
+        _ptr(attn), attn.stride(0), attn.stride(1), n_keys, R, int(agg), float(threshold), K,
+        _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), _ptr(ngram_used), _ptr(scores),
+        _ptr(best_pos), _ptr(best_score), _ptr(draft), _ptr(draft_len), int(blocks_per_seq),
+        _ptr(workspace), _nbytes(workspace), _stream(stream)), prepare)
 
 
 def pld_score_hidden(hidden, lens, cand_pos, cand_count, workspace, threshold=float("-inf"),

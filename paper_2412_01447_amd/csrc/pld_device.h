@@ -146,6 +146,21 @@ __device__ __forceinline__ uint4 ld_stream(const uint4 *p) {
 }
 __device__ __forceinline__ float ld_stream(const float *p) { return __builtin_nontemporal_load(p); }
 
+// Copies n 16-byte chunks from global memory straight into LDS (block-wide)
+// with global_load_lds_dwordx4: no registers are held, the copy runs while the
+// block does other work, and it is complete after the block's next
+// `s_waitcnt vmcnt(0)` + barrier.  Lane l of a wave lands at the wave's LDS
+// base + 16 l, so the chunks land in order.
+__device__ __forceinline__ void copy_to_lds(const uint4 *g, uint4 *lds, int n) {
+    const int lane = threadIdx.x & (kWave - 1);
+    for (int i0 = (int)(threadIdx.x - lane); i0 < n; i0 += (int)blockDim.x) {
+        if (i0 + lane < n)
+            __builtin_amdgcn_global_load_lds(
+                (const void *)(g + i0 + lane),
+                (__attribute__((address_space(3))) void *)(lds + i0), 16, 0, 0);
+    }
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 

@@ -1,20 +1,20 @@
-// pld_draft.hip -- the whole drafting half of a PLD+ step in one kernel
-// (arXiv 2412.01447, Sec. 4): occurrence search (Eq. 1, n-grams longest
-// first), ranking by hidden-state cosine (Eq. 2) or aggregated attention
-// (Eq. 3, Sec. 7.1), selection of the best occurrence, and the draft span
-// (Sec. 4.3).
+// pld_draft.hip -- the drafting half of a PLD+ step (arXiv 2412.01447, Sec. 4)
+// in one call: occurrence search (Eq. 1, n-grams longest first), ranking by
+// hidden-state cosine (Eq. 2) or aggregated attention (Eq. 3, Sec. 7.1),
+// selection of the best occurrence, and the draft span (Sec. 4.3).
 //
-// One 1024-thread block owns one sequence (tok_stride <= 8192), so nothing
-// crosses blocks: the tokens are staged in LDS once, the occurrence list is
-// built in LDS (and written out), the query row is staged in LDS, the
-// candidates are scored by the same per-wave row routine as the multi-block
-// ranking (bit-identical scores), the argmax is a block reduction of packed
-// keys, and the draft is copied from the staged tokens.  A step therefore
-// costs one launch and three dependent trips to memory (lengths, tokens,
-// artifact rows) instead of four kernels.  The block's work grows with its
-// own candidate count, so this path is for short candidate lists (small
-// batches, the latency regime); the separate calls balance long lists across
-// the whole GPU.
+// S blocks share one sequence (grid S x B).  Every block stages the whole
+// token row in LDS -- the load does not wait for the length -- finds the
+// occurrences itself (the search is a few microseconds of LDS work, so
+// repeating it costs less than a launch), builds the ordered occurrence list
+// in LDS, and scores the occurrences c = s, s+S, s+2S, ... with the same
+// per-row routines as the separate ranking calls (bit-identical scores).
+//   S == 1: one block owns the sequence; it selects the best occurrence and
+//           writes the draft itself -- one launch, three dependent trips to
+//           memory (length and tokens, query row, candidate rows).
+//   S  > 1: each block folds its best key into the sequence's spread key
+//           slots in the workspace, and a small finishing kernel selects and
+//           writes the draft -- long candidate lists are spread over S CUs.
 #include <math.h>
 
 #include "pld.h"
@@ -22,9 +22,6 @@
 #include "pld_match.h"
 
 namespace pld {
-
-constexpr int kDraftWaves = kFindWavesFused;
-constexpr int kDraftThreads = kDraftWaves * kWave;
 
 struct DraftArgs {
     const int32_t *tokens;
@@ -49,24 +46,26 @@ struct DraftArgs {
     int K;
     int32_t *draft;
     int32_t *draft_len;
+    uint64_t *keys;   // [B][kKeySlots] when S > 1, zero on entry
 };
 
-// Scores this wave's candidates c = w, w + 16, ... of the block's list, G
-// rows at a time (the same per-row arithmetic as the multi-block ranking).
+// Scores this wave's share of the candidates: list slots c = first, first +
+// step, ... < total, G rows at a time (the same per-row arithmetic as the
+// multi-block ranking kernel).
 template <int G>
 __device__ void draft_score_rows(const DraftArgs &a, int b, int64_t T, bool seq_ok,
                                  const uint16_t *Hb, const uint4 *q_s, float qq,
-                                 const int32_t *s_cand, int total, uint64_t &best) {
-    const int w = threadIdx.x / kWave;
+                                 const int32_t *s_cand, int first, int step, int total,
+                                 uint64_t &best) {
     const int lane = lane_id();
     const int nch = a.d / 8;
-    const int n = total > w ? (total - w + kDraftWaves - 1) / kDraftWaves : 0;
+    const int n = total > first ? (total - first + step - 1) / step : 0;
     for (int k = 0; k < n; k += G) {
         const uint4 *rows[G];
         int32_t js[G];
 #pragma unroll
         for (int g = 0; g < G; ++g) {
-            js[g] = (k + g < n) ? s_cand[w + (k + g) * kDraftWaves] : 0;
+            js[g] = (k + g < n) ? s_cand[first + (k + g) * step] : 0;
             const bool ok = (k + g < n) && seq_ok && js[g] >= 1 && (int64_t)js[g] <= T - 2;
             rows[g] = ok ? reinterpret_cast<const uint4 *>(Hb + (int64_t)(js[g] - 1) * a.hr)
                          : nullptr;
@@ -88,102 +87,120 @@ __device__ void draft_score_rows(const DraftArgs &a, int b, int64_t T, bool seq_
                     best = key > best ? key : best;
                 }
             }
-            if (a.scores && lane == 0) a.scores[(int64_t)b * a.cap + w + (k + g) * kDraftWaves] = s;
+            if (a.scores && lane == 0) a.scores[(int64_t)b * a.cap + first + (k + g) * step] = s;
         }
     }
 }
 
-template <bool kHidden>
-__global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
-    __shared__ int32_t s_x[kFindFusedMax];                       // tokens of the sequence
-    __shared__ int32_t s_cand[kFindFusedMax];                    // occurrence positions
-    __shared__ uint4 s_q[kHidden ? PLD_MAX_HIDDEN / 8 : 1];      // query row H[T-2], bf16
-    __shared__ int s_lvl[kDraftWaves][kMaxNgram];
-    __shared__ int s_wc[kDraftWaves];
-    __shared__ uint64_t s_key[kDraftWaves];
-    const int b = blockIdx.x;
+// The draft of sequence b from its best key (Sec. 4.3), written by one wave.
+__device__ void write_draft(const DraftArgs &a, int b, int64_t T, bool tok_ok, uint64_t best) {
+    const int lane = lane_id();
+    const int32_t bp = best ? (int32_t)(uint32_t)(best & 0xffffffffu) : -1;
+    if (lane == 0) {
+        a.best_pos[b] = bp;
+        a.best_score[b] = best ? unord_f32((uint32_t)(best >> 32)) : -INFINITY;
+    }
+    int64_t L = 0;
+    if (tok_ok && bp >= 0 && (int64_t)bp <= T - 2) L = min((int64_t)a.K, T - 1 - bp);
+    const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
+    for (int i = lane; i < a.K; i += kWave)
+        a.draft[(int64_t)b * a.K + i] = (i < L) ? x[bp + 1 + i] : -1;
+    if (lane == 0) a.draft_len[b] = (int32_t)L;
+}
+
+template <bool kHidden, int kWaves>
+__global__ __launch_bounds__(kWaves * kWave) void draft_kernel(DraftArgs a) {
+    constexpr int kThreads = kWaves * kWave;
+    constexpr int kSteps = kFindFusedMax / (kWaves * kWave * kLanePos);   // passes per wave
+    static_assert(kSteps * kWaves * kWave * kLanePos == kFindFusedMax, "whole passes");
+    __shared__ __align__(16) int32_t s_buf[kFindFusedMax];   // tokens, then the occurrence list
+    extern __shared__ uint4 s_q[];             // query row H[T-2], bf16 (hidden only)
+    __shared__ int s_lvl[kWaves][kMaxNgram];
+    __shared__ uint64_t s_key[kWaves];
+    const int split = blockIdx.x, S = gridDim.x, b = blockIdx.y;
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
+
+    // the query row, the token row and the length are all requested before
+    // the first wait
     const int64_t T = a.lens[b];
     const bool tok_ok = (T >= 1 && T <= a.tok_stride);   // block-uniform
-
-    // ---- occurrences (Eq. 1), longest n first
-    int n_used = -1, total = 0;
     const bool seq_ok = kHidden ? (T >= 2 && T - 2 < a.n_rows) : (T >= 2);
     const uint16_t *Hb = kHidden ? a.hidden + (int64_t)b * a.hs : nullptr;
     const int nch = kHidden ? a.d / 8 : 0;
+    if (kHidden && tok_ok && seq_ok)   // the query row, straight into LDS
+        copy_to_lds(reinterpret_cast<const uint4 *>(Hb + (T - 2) * a.hr), s_q, nch);
+    stage_tokens(x, 0, a.tok_stride, s_buf);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+
+    // ---- occurrences (Eq. 1), longest n first
+    int n_used = -1, total = 0;
     if (tok_ok) {
-        stage_tokens(x, 0, T, s_x);
-        if (kHidden && seq_ok) {
-            // the query row depends only on T: fetch it together with the tokens
-            const uint4 *qg = reinterpret_cast<const uint4 *>(Hb + (T - 2) * a.hr);
-            for (int i = threadIdx.x; i < nch; i += kDraftThreads) s_q[i] = qg[i];
-        }
-        __syncthreads();
-        Query q;
+        const Query q = load_query(s_buf, T, a.nmax);
+        // wave w covers [w, w+1) * kSteps * 512; pass st, lane l: 8 positions from base[st]
+        const int64_t base0 = ((int64_t)w * kSteps * kWave + lane) * kLanePos;
+        uint64_t hits[kSteps];
+        int cnt[kMaxNgram];
 #pragma unroll
-        for (int k = 0; k < kMaxNgram; ++k)
-            q.v[k] = (k < a.nmax && T - 1 - k >= 0) ? s_x[T - 1 - k] : 0;
-        const int64_t base = (int64_t)w * 512;
-        int m[8];
-        wave_match(s_x, 0, T, base, q, a.nmax, m);
-        int cnt[8];
-        wave_level_counts(m, a.nmax, cnt);
-        if (lane == 0) {
+        for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
 #pragma unroll
-            for (int k = 0; k < kMaxNgram; ++k) s_lvl[w][k] = cnt[k];
+        for (int st = 0; st < kSteps; ++st) {
+            hits[st] = lane_hits(s_buf, 0, T, base0 + st * kWave * kLanePos, q, a.nmax);
+            count_levels(hits[st], a.nmax, cnt);
         }
-        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < kMaxNgram; ++k) {
+            if (k < a.nmax) {   // uniform
+                const int t = wave_sum_i32(cnt[k]);
+                if (lane == 0) s_lvl[w][k] = t;
+            }
+        }
+        __syncthreads();   // also: every token read is done, s_buf becomes the list
         n_used = 0;
         for (int n = a.nmax; n >= a.nmin; --n) {
             int t = 0;
-            for (int i = 0; i < kDraftWaves; ++i) t += s_lvl[i][n - 1];
+            for (int i = 0; i < kWaves; ++i) t += s_lvl[i][n - 1];
             if (t > 0) {
                 n_used = n;
                 total = t;
                 break;
             }
         }
-        if (n_used > 0) {
-            const int wc = wave_hits(m, n_used);
-            if (lane == 0) s_wc[w] = wc;
-            __syncthreads();
-            int start = 0;
-            for (int i = 0; i < w; ++i) start += s_wc[i];
-            int32_t *out = a.cand_pos + (int64_t)b * a.cap;
-            const uint64_t lt = lanemask_lt();
+        if (n_used > 0) {   // block-uniform; the ascending list
+            int64_t run = 0;
+            for (int i = 0; i < w; ++i) run += s_lvl[i][n_used - 1];
+            int32_t *out = split == 0 ? a.cand_pos + (int64_t)b * a.cap : nullptr;
 #pragma unroll
-            for (int it = 0; it < 8; ++it) {
-                const uint64_t mk = __ballot(m[it] >= n_used);
-                if ((mk >> lane) & 1ull) {
-                    const int slot = start + __popcll(mk & lt);
-                    const int32_t p = (int32_t)(base + it * kWave + lane);
-                    out[slot] = p;
-                    s_cand[slot] = p;
-                }
-                start += __popcll(mk);
-            }
+            for (int st = 0; st < kSteps; ++st)
+                run = emit_bits(level_bits(hits[st], n_used), base0 + st * kWave * kLanePos, s_buf,
+                                out, run);
             __syncthreads();
         }
     }
+    if (split == 0 && threadIdx.x == 0) {
+        a.cand_count[b] = total;
+        a.ngram_used[b] = n_used;
+    }
 
-    // ---- ranking and selection (Eq. 2 / Eq. 3): highest score, then latest j
+    // ---- this block's share of the ranking (Eq. 2 / Eq. 3)
     uint64_t best = 0;
     if (total > 0) {   // block-uniform
         if constexpr (kHidden) {
             float qdot = 0.f, qq = 0.f;
             if (seq_ok) row_dot<false>(s_q, s_q, nch, qdot, qq);
+            const int first = split + S * w, step = S * kWaves;
             if (nch <= 4 * kWave)
-                draft_score_rows<4>(a, b, T, seq_ok, Hb, s_q, qq, s_cand, total, best);
+                draft_score_rows<4>(a, b, T, seq_ok, Hb, s_q, qq, s_buf, first, step, total, best);
             else if (nch <= 8 * kWave)
-                draft_score_rows<2>(a, b, T, seq_ok, Hb, s_q, qq, s_cand, total, best);
+                draft_score_rows<2>(a, b, T, seq_ok, Hb, s_q, qq, s_buf, first, step, total, best);
             else
-                draft_score_rows<1>(a, b, T, seq_ok, Hb, s_q, qq, s_cand, total, best);
+                draft_score_rows<1>(a, b, T, seq_ok, Hb, s_q, qq, s_buf, first, step, total, best);
         } else {
             const float *Ab = a.attn + (int64_t)b * a.as;
-            for (int c = threadIdx.x; c < total; c += kDraftThreads) {
-                const int32_t j = s_cand[c];
+            for (int c = split + S * (int)threadIdx.x; c < total; c += S * kThreads) {
+                const int32_t j = s_buf[c];
                 float s = __builtin_nanf("");
                 if (seq_ok && j >= 1 && (int64_t)j <= T - 2 && (int64_t)(j - 1) < a.n_keys) {
                     s = attn_gather(Ab + (j - 1), a.ar, a.R, a.agg == PLD_AGG_SUM);
@@ -200,35 +217,48 @@ __global__ __launch_bounds__(kDraftThreads) void draft_kernel(DraftArgs a) {
         if (lane == 0) s_key[w] = best;
         __syncthreads();
         best = 0;
-        for (int i = 0; i < kDraftWaves; ++i) best = s_key[i] > best ? s_key[i] : best;
+        for (int i = 0; i < kWaves; ++i) best = s_key[i] > best ? s_key[i] : best;
     }
 
-    // ---- outputs and the draft (Sec. 4.3)
-    const int32_t bp = best ? (int32_t)(uint32_t)(best & 0xffffffffu) : -1;
-    if (threadIdx.x == 0) {
-        a.cand_count[b] = total;
-        a.ngram_used[b] = n_used;
-        a.best_pos[b] = bp;
-        a.best_score[b] = best ? unord_f32((uint32_t)(best >> 32)) : -INFINITY;
+    // ---- selection and the draft (Sec. 4.3)
+    if (S == 1) {
+        if (w == 0) write_draft(a, b, T, tok_ok, best);
+    } else if (threadIdx.x == 0 && best) {
+        atomicMax((unsigned long long *)&a.keys[(int64_t)b * kKeySlots + (split % kKeySlots)],
+                  (unsigned long long)best);
     }
-    int64_t L = 0;
-    if (tok_ok && bp >= 0 && (int64_t)bp <= T - 2) L = min((int64_t)a.K, T - 1 - bp);
-    for (int i = threadIdx.x; i < a.K; i += kDraftThreads)
-        a.draft[(int64_t)b * a.K + i] = (i < L) ? s_x[bp + 1 + i] : -1;
-    if (threadIdx.x == 0) a.draft_len[b] = (int32_t)L;
+}
+
+// S > 1: one wave per sequence folds the key slots (returning them to zero)
+// and writes best_pos, best_score and the draft.
+__global__ __launch_bounds__(256) void draft_finish_kernel(DraftArgs a) {
+    const int b = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave);
+    if (b >= a.B) return;   // wave-uniform
+    const int lane = lane_id();
+    uint64_t k = 0;
+    if (lane < kKeySlots) {
+        k = a.keys[(int64_t)b * kKeySlots + lane];
+        a.keys[(int64_t)b * kKeySlots + lane] = 0;
+    }
+    k = wave_max_u64(k);
+    const int64_t T = a.lens[b];
+    write_draft(a, b, T, T >= 1 && T <= a.tok_stride, k);
 }
 
 static int check_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B,
                        int ngram_min, int ngram_max, float threshold, int K,
                        const int32_t *cand_pos, int64_t cap, const int32_t *cand_count,
                        const int32_t *ngram_used, const int32_t *best_pos,
-                       const float *best_score, const int32_t *draft, const int32_t *draft_len) {
+                       const float *best_score, const int32_t *draft, const int32_t *draft_len,
+                       int S, void *workspace, size_t workspace_bytes) {
     if (!tokens || !lens || !cand_pos || !cand_count || !ngram_used || !best_pos || !best_score ||
         !draft || !draft_len)
         return PLD_ERR_INVALID;
     if (B < 1 || B > 65535 || tok_stride < 1 || tok_stride > kFindFusedMax) return PLD_ERR_INVALID;
     if (ngram_min < 1 || ngram_max < ngram_min || ngram_max > PLD_MAX_NGRAM) return PLD_ERR_INVALID;
     if (cap < tok_stride || K < 1 || isnan(threshold)) return PLD_ERR_INVALID;
+    if (S < 1 || S > PLD_MAX_DRAFT_SPLIT) return PLD_ERR_INVALID;
+    if (S > 1 && (!workspace || workspace_bytes < rank_ws_bytes(B))) return PLD_ERR_WORKSPACE;
     return PLD_OK;
 }
 
@@ -236,7 +266,8 @@ static DraftArgs make_draft(const int32_t *tokens, int64_t tok_stride, const int
                             int ngram_min, int ngram_max, float threshold, int K,
                             int32_t *cand_pos, int64_t cap, int32_t *cand_count,
                             int32_t *ngram_used, float *scores, int32_t *best_pos,
-                            float *best_score, int32_t *draft, int32_t *draft_len) {
+                            float *best_score, int32_t *draft, int32_t *draft_len,
+                            void *workspace) {
     DraftArgs a{};
     a.tokens = tokens;
     a.tok_stride = tok_stride;
@@ -255,7 +286,21 @@ static DraftArgs make_draft(const int32_t *tokens, int64_t tok_stride, const int
     a.K = K;
     a.draft = draft;
     a.draft_len = draft_len;
+    a.keys = (uint64_t *)workspace;
     return a;
+}
+
+// One block of 16 waves when it owns its sequence; 4 waves when S blocks share
+// it (more blocks fit on a CU, and each scores a fraction of the list).
+template <bool kHidden>
+static void launch_draft(const DraftArgs &a, int S, hipStream_t s) {
+    const size_t lds = kHidden ? (size_t)(a.d / 8) * sizeof(uint4) : 0;
+    if (S == 1) {
+        hipLaunchKernelGGL((draft_kernel<kHidden, 16>), dim3(1, a.B), dim3(16 * kWave), lds, s, a);
+    } else {
+        hipLaunchKernelGGL((draft_kernel<kHidden, 4>), dim3(S, a.B), dim3(4 * kWave), lds, s, a);
+        hipLaunchKernelGGL(draft_finish_kernel, dim3((a.B + 3) / 4), dim3(256), 0, s, a);
+    }
 }
 
 }  // namespace pld
@@ -268,22 +313,24 @@ extern "C" int pld_draft_hidden(const int32_t *tokens, int64_t tok_stride, const
                                 float threshold, int K, int32_t *cand_pos, int64_t cap,
                                 int32_t *cand_count, int32_t *ngram_used, float *scores,
                                 int32_t *best_pos, float *best_score, int32_t *draft,
-                                int32_t *draft_len, void *stream) {
+                                int32_t *draft_len, int blocks_per_seq, void *workspace,
+                                size_t workspace_bytes, void *stream) {
     int rc = check_draft(tokens, tok_stride, lens, B, ngram_min, ngram_max, threshold, K, cand_pos,
-                         cap, cand_count, ngram_used, best_pos, best_score, draft, draft_len);
+                         cap, cand_count, ngram_used, best_pos, best_score, draft, draft_len,
+                         blocks_per_seq, workspace, workspace_bytes);
     if (rc != PLD_OK) return rc;
     if (!hidden || d < 8 || d > PLD_MAX_HIDDEN || d % 8 != 0 || n_rows < 1) return PLD_ERR_INVALID;
     if (h_row_stride < d || h_seq_stride < 0) return PLD_ERR_INVALID;
     if (((uintptr_t)hidden & 15) || (h_row_stride % 8) || (h_seq_stride % 8)) return PLD_ERR_ALIGN;
     DraftArgs a = make_draft(tokens, tok_stride, lens, B, ngram_min, ngram_max, threshold, K,
                              cand_pos, cap, cand_count, ngram_used, scores, best_pos, best_score,
-                             draft, draft_len);
+                             draft, draft_len, workspace);
     a.hidden = hidden;
     a.hs = h_seq_stride;
     a.hr = h_row_stride;
     a.n_rows = n_rows;
     a.d = d;
-    hipLaunchKernelGGL(draft_kernel<true>, dim3(B), dim3(kDraftThreads), 0, (hipStream_t)stream, a);
+    launch_draft<true>(a, blocks_per_seq, (hipStream_t)stream);
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }
 
@@ -293,9 +340,11 @@ extern "C" int pld_draft_attn(const int32_t *tokens, int64_t tok_stride, const i
                               float threshold, int K, int32_t *cand_pos, int64_t cap,
                               int32_t *cand_count, int32_t *ngram_used, float *scores,
                               int32_t *best_pos, float *best_score, int32_t *draft,
-                              int32_t *draft_len, void *stream) {
+                              int32_t *draft_len, int blocks_per_seq, void *workspace,
+                              size_t workspace_bytes, void *stream) {
     int rc = check_draft(tokens, tok_stride, lens, B, ngram_min, ngram_max, threshold, K, cand_pos,
-                         cap, cand_count, ngram_used, best_pos, best_score, draft, draft_len);
+                         cap, cand_count, ngram_used, best_pos, best_score, draft, draft_len,
+                         blocks_per_seq, workspace, workspace_bytes);
     if (rc != PLD_OK) return rc;
     if (!attn || R < 1 || n_keys < 1 || (agg != PLD_AGG_SUM && agg != PLD_AGG_MAX))
         return PLD_ERR_INVALID;
@@ -303,13 +352,13 @@ extern "C" int pld_draft_attn(const int32_t *tokens, int64_t tok_stride, const i
     if ((uintptr_t)attn & 3) return PLD_ERR_ALIGN;
     DraftArgs a = make_draft(tokens, tok_stride, lens, B, ngram_min, ngram_max, threshold, K,
                              cand_pos, cap, cand_count, ngram_used, scores, best_pos, best_score,
-                             draft, draft_len);
+                             draft, draft_len, workspace);
     a.attn = attn;
     a.as = a_seq_stride;
     a.ar = a_row_stride;
     a.n_keys = n_keys;
     a.R = R;
     a.agg = agg;
-    hipLaunchKernelGGL(draft_kernel<false>, dim3(B), dim3(kDraftThreads), 0, (hipStream_t)stream, a);
+    launch_draft<false>(a, blocks_per_seq, (hipStream_t)stream);
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }

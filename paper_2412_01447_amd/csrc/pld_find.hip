@@ -10,14 +10,16 @@
 // ascending order.
 //
 // The tokens a block needs are first copied to LDS with independent loads, so
-// the backwards comparisons never wait on a chain of global loads.
-// Compaction is a wave ballot (one bit per lane, 64 positions per ballot), a
-// popcount of the lower lanes' bits for the lane's slot, and an exclusive
-// scan of per-wave and per-block counts.  Sequences up to kFindFusedMax
-// tokens take one 1024-thread block each (count, pick n, compact, in one
-// kernel); longer ones split into kFindTile-position blocks: a count kernel
-// writes per-tile counts to the scratch buffer, and the compaction kernel
-// derives its tile's output offset from the counts of the tiles before it.
+// the backwards comparisons never wait on a chain of global loads.  Each lane
+// then takes 8 consecutive positions: it reads the 16 tokens around them with
+// four aligned 16-byte LDS loads and builds, per n, an 8-bit hit mask from
+// register compares -- no branch per comparison, 512 positions per wave
+// pass.  Compaction is an exclusive wave scan of the lanes' hit counts plus
+// the per-wave and per-block counts.  Sequences up to kFindFusedMax tokens
+// take one 1024-thread block each (count, pick n, compact, in one kernel);
+// longer ones split into kFindTile-position blocks: a count kernel writes
+// per-tile counts to the scratch buffer, and the compaction kernel derives
+// its tile's output offset from the counts of the tiles before it.
 #include "pld.h"
 #include "pld_device.h"
 #include "pld_match.h"
@@ -39,11 +41,13 @@ struct FindArgs {
 };
 
 // ---------------------------------------------------------------- fused
-// One 1024-thread block per sequence, tok_stride <= kFindFusedMax.
+// One 1024-thread block per sequence, tok_stride <= kFindFusedMax: every lane
+// takes 8 positions, so one pass covers the sequence.
+static_assert(kFindFusedMax == kFindWavesFused * kWave * kLanePos, "one pass per block");
+
 __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(FindArgs a) {
-    __shared__ int32_t s_x[kFindFusedMax];
+    __shared__ __align__(16) int32_t s_x[kFindFusedMax];
     __shared__ int s_lvl[kFindWavesFused][kMaxNgram];
-    __shared__ int s_wc[kFindWavesFused];
     const int b = blockIdx.x;
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
@@ -58,17 +62,19 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
     }
     stage_tokens(x, 0, T, s_x);
     __syncthreads();
-    Query q;
+    const Query q = load_query(s_x, T, a.nmax);
+    const int64_t base = (int64_t)threadIdx.x * kLanePos;
+    const uint64_t hits = lane_hits(s_x, 0, T, base, q, a.nmax);
+    int cnt[kMaxNgram];
 #pragma unroll
-    for (int k = 0; k < kMaxNgram; ++k) q.v[k] = (k < a.nmax && T - 1 - k >= 0) ? s_x[T - 1 - k] : 0;
-    const int64_t base = (int64_t)w * 512;
-    int m[8];
-    wave_match(s_x, 0, T, base, q, a.nmax, m);
-    int cnt[8];
-    wave_level_counts(m, a.nmax, cnt);
-    if (lane == 0) {
+    for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
+    count_levels(hits, a.nmax, cnt);
 #pragma unroll
-        for (int k = 0; k < kMaxNgram; ++k) s_lvl[w][k] = cnt[k];
+    for (int k = 0; k < kMaxNgram; ++k) {
+        if (k < a.nmax) {   // uniform
+            const int t = wave_sum_i32(cnt[k]);
+            if (lane == 0) s_lvl[w][k] = t;
+        }
     }
     __syncthreads();
     // the longest n with an occurrence (every thread, same answer)
@@ -82,13 +88,10 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
             break;
         }
     }
-    if (n_used > 0) {
-        const int wc = wave_hits(m, n_used);
-        if (lane == 0) s_wc[w] = wc;
-        __syncthreads();
-        int64_t start = 0;
-        for (int i = 0; i < w; ++i) start += s_wc[i];
-        wave_emit(m, n_used, base, a.cand_pos + (int64_t)b * a.cap, start);
+    if (n_used > 0) {   // the per-wave counts at n give each wave's offset
+        int64_t run = 0;
+        for (int i = 0; i < w; ++i) run += s_lvl[i][n_used - 1];
+        emit_bits(level_bits(hits, n_used), base, a.cand_pos + (int64_t)b * a.cap, nullptr, run);
     }
     if (threadIdx.x == 0) {
         a.cand_count[b] = total;
@@ -97,9 +100,13 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
 }
 
 // ---------------------------------------------------------------- tiled
-// A tile covers positions [tile*kFindTile, (tile+1)*kFindTile); its LDS copy
-// starts kMaxNgram-1 tokens earlier so the backwards comparisons stay inside.
-constexpr int kHalo = kMaxNgram - 1;
+// A tile covers positions [tile*kFindTile, (tile+1)*kFindTile), one pass of
+// 8 positions per lane; its LDS copy starts kHalo >= kMaxNgram-1 tokens
+// earlier so the backwards comparisons stay inside (8, not 7, keeps every
+// lane's 16-byte window loads aligned).
+constexpr int kHalo = 8;
+static_assert(kHalo >= kMaxNgram - 1 && kFindTile == kFindWavesTiled * kWave * kLanePos,
+              "one pass per tile");
 
 __device__ __forceinline__ int64_t tile_lo(int tile) {
     int64_t lo = (int64_t)tile * kFindTile - kHalo;
@@ -107,7 +114,7 @@ __device__ __forceinline__ int64_t tile_lo(int tile) {
 }
 
 __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_count_kernel(FindArgs a) {
-    __shared__ int32_t s_x[kFindTile + kHalo];
+    __shared__ __align__(16) int32_t s_x[kFindTile + kHalo];
     __shared__ int s_lvl[kFindWavesTiled][kMaxNgram];
     const int tile = blockIdx.x, b = blockIdx.y;
     const int w = threadIdx.x / kWave;
@@ -116,25 +123,22 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_count_kernel(Fin
     const int64_t T = a.lens[b];
     const int64_t t0 = (int64_t)tile * kFindTile;
     const bool live = (T >= 1 && T <= a.tok_stride && t0 <= T - 2);
-    int cnt[8];
+    int cnt[kMaxNgram];
 #pragma unroll
     for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
     if (live) {   // block-uniform
         const int64_t lo = tile_lo(tile);
         const int64_t hi = (t0 + kFindTile < T - 1) ? t0 + kFindTile : T - 1;
         stage_tokens(x, lo, hi, s_x);
-        Query q;
-#pragma unroll
-        for (int k = 0; k < kMaxNgram; ++k)
-            q.v[k] = (k < a.nmax && T - 1 - k >= 0) ? x[T - 1 - k] : 0;
+        const Query q = load_query(x, T, a.nmax);
         __syncthreads();
-        int m[8];
-        wave_match(s_x, lo, T, t0 + (int64_t)w * 512, q, a.nmax, m);
-        wave_level_counts(m, a.nmax, cnt);
+        count_levels(lane_hits(s_x, lo, T, t0 + (int64_t)threadIdx.x * kLanePos, q, a.nmax),
+                     a.nmax, cnt);
     }
-    if (lane == 0) {
 #pragma unroll
-        for (int k = 0; k < kMaxNgram; ++k) s_lvl[w][k] = cnt[k];
+    for (int k = 0; k < kMaxNgram; ++k) {
+        const int t = wave_sum_i32(cnt[k]);
+        if (lane == 0) s_lvl[w][k] = t;
     }
     __syncthreads();
     if (threadIdx.x < kMaxNgram) {
@@ -145,7 +149,7 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_count_kernel(Fin
 }
 
 __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_compact_kernel(FindArgs a) {
-    __shared__ int32_t s_x[kFindTile + kHalo];
+    __shared__ __align__(16) int32_t s_x[kFindTile + kHalo];
     __shared__ int s_tot[kMaxNgram];
     __shared__ int s_pre[kMaxNgram];
     __shared__ int s_wc[kFindWavesTiled];
@@ -169,7 +173,7 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_compact_kernel(F
     __syncthreads();
     {
         // totals over all tiles, and over the tiles before this one
-        int tot[8], pre[8];
+        int tot[kMaxNgram], pre[kMaxNgram];
 #pragma unroll
         for (int k = 0; k < kMaxNgram; ++k) tot[k] = pre[k] = 0;
         for (int t = threadIdx.x; t < a.ntiles; t += blockDim.x) {
@@ -182,12 +186,7 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_compact_kernel(F
         }
 #pragma unroll
         for (int k = 0; k < kMaxNgram; ++k) {
-            int tk = tot[k], pk = pre[k];
-#pragma unroll
-            for (int s = 32; s >= 1; s >>= 1) {
-                tk += __shfl_xor(tk, s);
-                pk += __shfl_xor(pk, s);
-            }
+            const int tk = wave_sum_i32(tot[k]), pk = wave_sum_i32(pre[k]);
             if (lane == 0 && (tk | pk)) {
                 atomicAdd(&s_tot[k], tk);
                 atomicAdd(&s_pre[k], pk);
@@ -207,20 +206,16 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_compact_kernel(F
         const int64_t lo = tile_lo(tile);
         const int64_t hi = (t0 + kFindTile < T - 1) ? t0 + kFindTile : T - 1;
         stage_tokens(x, lo, hi, s_x);
-        Query q;
-#pragma unroll
-        for (int k = 0; k < kMaxNgram; ++k)
-            q.v[k] = (k < a.nmax && T - 1 - k >= 0) ? x[T - 1 - k] : 0;
+        const Query q = load_query(x, T, a.nmax);
         __syncthreads();
-        const int64_t base = t0 + (int64_t)w * 512;
-        int m[8];
-        wave_match(s_x, lo, T, base, q, a.nmax, m);
-        const int wc = wave_hits(m, n_used);
+        const int64_t base = t0 + (int64_t)threadIdx.x * kLanePos;
+        const uint32_t bits = level_bits(lane_hits(s_x, lo, T, base, q, a.nmax), n_used);
+        const int wc = wave_sum_i32(__popc(bits));
         if (lane == 0) s_wc[w] = wc;
         __syncthreads();
-        int64_t start = s_pre[n_used - 1];
-        for (int i = 0; i < w; ++i) start += s_wc[i];
-        wave_emit(m, n_used, base, a.cand_pos + (int64_t)b * a.cap, start);
+        int64_t run = s_pre[n_used - 1];
+        for (int i = 0; i < w; ++i) run += s_wc[i];
+        emit_bits(bits, base, a.cand_pos + (int64_t)b * a.cap, nullptr, run);
     }
     if (tile == 0 && threadIdx.x == 0) {
         a.cand_count[b] = n_used > 0 ? s_tot[n_used - 1] : 0;

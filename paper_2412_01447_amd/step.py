@@ -7,7 +7,8 @@ Eq. 2 / Eq. 3, draft Sec. 4.3, greedy verification Sec. 4.4).
 """
 import torch
 
-from . import (DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, pld_draft_attn, pld_draft_hidden,
+from . import (DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, PLD_MAX_DRAFT_SPLIT, pld_draft_attn,
+               pld_draft_hidden,
                pld_emit_draft, pld_find_candidates, pld_find_scratch_bytes, pld_rank_attn,
                pld_rank_hidden, pld_score_attn, pld_score_hidden, pld_select_best,
                pld_verify_accept, pld_verify_argmax, pld_verify_greedy, pld_workspace_bytes)
@@ -18,10 +19,12 @@ class DraftStep:
     drafting call (tok_stride <= 8192, one ranking), "auto" the one-launch call for
     hidden-state ranking when it applies and the separate calls otherwise."""
 
-    def __init__(self, B, tok_stride, K, device="cuda", cap=None, keep_scores=False, mode="auto"):
+    def __init__(self, B, tok_stride, K, device="cuda", cap=None, keep_scores=False, mode="auto",
+                 draft_split=1):
         if mode not in ("auto", "fused", "split"):
             raise ValueError(mode)
         self.B, self.tok_stride, self.K, self.mode = B, tok_stride, K, mode
+        self.draft_split = int(draft_split)
         cap = tok_stride if cap is None else cap
         i32 = dict(dtype=torch.int32, device=device)
         self.cand_pos = torch.full((B, cap), -1, **i32)
@@ -97,10 +100,17 @@ class DraftStep:
                 raise ValueError("the one-launch drafting call takes one artifact and "
                                  "tok_stride <= 8192")
             return True
-        # auto: the one-launch call for hidden-state ranking; attention gathers of a
-        # long candidate list are address-bound on one CU, so they go wide
-        return (self.mode == "auto" and hidden is not None and attn is None and
-                self.tok_stride <= DRAFT_MAX_TOK_STRIDE)
+        return self.mode == "auto" and one and self.tok_stride <= DRAFT_MAX_TOK_STRIDE
+
+    def tune_split(self, cand_count, hidden=True):
+        """Blocks per sequence for the one-call drafting from observed candidate
+        counts (e.g. the previous step's): about four rows per block for hidden
+        states (one per wave), 64 candidates per block for attention gathers."""
+        import math
+        per = 4 if hidden else 64
+        mx = int(max(int(c) for c in cand_count)) if len(cand_count) else 0
+        self.draft_split = max(1, min(PLD_MAX_DRAFT_SPLIT, math.ceil(mx / per)))
+        return self.draft_split
 
     def draft_fused(self, tokens, lens, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
                     threshold=float("-inf"), stream=None):
@@ -109,12 +119,14 @@ class DraftStep:
             pld_draft_hidden(tokens, lens, ngram[0], ngram[1], hidden, self.K, self.cand_pos,
                              self.cand_count, self.ngram_used, self.best_pos, self.best_score,
                              self.draft, self.draft_len, threshold=threshold, scores=self.scores,
+                             blocks_per_seq=self.draft_split, workspace=self.workspace,
                              stream=stream)
         else:
             pld_draft_attn(tokens, lens, ngram[0], ngram[1], attn, self.K, self.cand_pos,
                            self.cand_count, self.ngram_used, self.best_pos, self.best_score,
                            self.draft, self.draft_len, agg=agg, threshold=threshold,
-                           scores=self.scores_attn, stream=stream)
+                           scores=self.scores_attn, blocks_per_seq=self.draft_split,
+                           workspace=self.workspace, stream=stream)
 
     def run(self, tokens, lens, logits, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
             threshold=float("-inf"), stream=None):
@@ -144,12 +156,16 @@ class DraftStep:
                 d = pld_draft_hidden(tokens, lens, ngram[0], ngram[1], hidden, self.K,
                                      self.cand_pos, self.cand_count, self.ngram_used,
                                      self.best_pos, self.best_score, self.draft, self.draft_len,
-                                     threshold=threshold, scores=self.scores, **P)
+                                     threshold=threshold, scores=self.scores,
+                                     blocks_per_seq=self.draft_split, workspace=self.workspace,
+                                     **P)
             else:
                 d = pld_draft_attn(tokens, lens, ngram[0], ngram[1], attn, self.K, self.cand_pos,
                                    self.cand_count, self.ngram_used, self.best_pos,
                                    self.best_score, self.draft, self.draft_len, agg=agg,
-                                   threshold=threshold, scores=self.scores_attn, **P)
+                                   threshold=threshold, scores=self.scores_attn,
+                                   blocks_per_seq=self.draft_split, workspace=self.workspace,
+                                   **P)
             ops = [("draft", d)]
         else:
             ops = [("find", pld_find_candidates(tokens, lens, ngram[0], ngram[1], self.cand_pos,

@@ -23,7 +23,7 @@ pytestmark = pytest.mark.gpu
 
 CASES = [(1, True, "fused"), (1, False, "split"), (2, True, "fused"), (2, False, "fused"),
          (2, True, "split"), (3, True, "fused"), (3, False, "split"), (3, False, "fused"),
-         (4, True, "split"), (5, True, "split"), (5, False, "split")]
+         (3, False, "fused1"), (4, True, "split"), (5, True, "split"), (5, False, "split")]
 
 
 @pytest.mark.parametrize("cid,structured,mode", CASES,
@@ -51,7 +51,10 @@ def test_config_step_parity(cid, structured, mode):
     say("  oracle: counts", cc.tolist()[:8], "n", sorted(set(nu.tolist())), "accept",
         rver[0].tolist()[:16])
     # ---- GPU step, as the benchmark launches it
-    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, keep_scores=True, mode=mode)
+    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, keep_scores=True,
+                     mode="fused" if mode.startswith("fused") else mode)
+    if mode == "fused":     # blocks per sequence from the candidate counts, as the bench does
+        say("  blocks per sequence:", step.tune_split(cc, hidden=w["hidden"] is not None))
     zd = d_bf16(z) if bf16 else d_f32(z)
     attn_d = d_f32(w["attn"]) if w["attn"] is not None else None
     td, ld = d_i32(toks), d_i32(lens)

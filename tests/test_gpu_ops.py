@@ -97,6 +97,39 @@ def test_find_parity(case):
     check_find(gpu_find(toks, lens, nmin, nmax, cap=stride + 37), ref, str(case) + " cap")
 
 
+@pytest.mark.parametrize("stride", [8192, 20000])
+def test_find_lane31_hits(stride):
+    """Sparse hits at positions 31 mod 64 (plus lane 63 once): a 64-position
+    ballot with bit 31 set and the upper half otherwise empty must not widen
+    into the upper lanes.  Both the one-block path and the tiled path, and the
+    one-call drafting."""
+    say("find lane 31", stride)
+    B = 2
+    toks = (np.arange(B * stride, dtype=np.int64).reshape(B, stride) % 1000003 + 10).astype(np.int32)
+    lens = np.array([stride, stride - 5], np.int32)
+    for b in range(B):
+        T = lens[b]
+        toks[b, T - 1] = 7
+        toks[b, 31:T - 1:64] = 7
+        toks[b, 63] = 7
+    ref = oracle.find(toks, lens, 1, 1)
+    assert ref[1][0] > 100
+    check_find(gpu_find(toks, lens, 1, 1), ref, f"lane31 {stride}")
+    if stride <= pld.DRAFT_MAX_TOK_STRIDE:
+        i32 = dict(dtype=torch.int32, device="cuda")
+        K = 4
+        A = synth.make_attn(B, 3, stride, lens, seed=5)
+        for split in (1, 5):
+            o = [torch.full((B, stride), -1, **i32), torch.zeros(B, **i32), torch.zeros(B, **i32),
+                 torch.zeros(B, **i32), torch.zeros(B, dtype=torch.float32, device="cuda"),
+                 torch.zeros((B, K), **i32), torch.zeros(B, **i32)]
+            pld.pld_draft_attn(d_i32(toks), d_i32(lens), 1, 1, d_f32(A), K, *o,
+                               blocks_per_seq=split, workspace=workspace(B, K))
+            torch.cuda.synchronize()
+            check_find((o[0].cpu().numpy(), o[1].cpu().numpy(), o[2].cpu().numpy()), ref,
+                       f"lane31 draft split {split}")
+
+
 def test_find_planted_ngrams_multi_tile():
     """Long sequences with planted n-gram repeats crossing tile borders."""
     say("find planted multi-tile")
@@ -373,14 +406,16 @@ DRAFT_CASES = [
 ]
 
 
+@pytest.mark.parametrize("split", [1, 3, 64])
 @pytest.mark.parametrize("case", DRAFT_CASES, ids=[f"B{c[0]}_S{c[1]}_V{c[2]}_n{c[3]}-{c[4]}_"
                                                    f"{'d' + str(c[5]) if c[5] else 'R' + str(c[6])}"
                                                    for c in DRAFT_CASES])
-def test_draft_fused_parity(case):
-    """The one-launch drafting call equals the oracle's find, rank and emit, and
-    its scores are bit-identical to the separate ranking call."""
+def test_draft_fused_parity(case, split):
+    """The one-call drafting equals the oracle's find, rank and emit, and its
+    scores are bit-identical to the separate ranking call, for any number of
+    blocks per sequence."""
     B, stride, V, nmin, nmax, d, R, K, seed = case
-    say("draft fused", case)
+    say("draft fused", case, "split", split)
     rng = np.random.default_rng(100 + seed)
     toks = rng.integers(0, V, size=(B, stride)).astype(np.int32)
     lens = rng.integers(1, stride + 1, size=B).astype(np.int32)
@@ -391,6 +426,7 @@ def test_draft_fused_parity(case):
     ref_find = oracle.find(toks, lens, nmin, nmax)
     cp, cc, nu = ref_find
     i32 = dict(dtype=torch.int32, device="cuda")
+    ws = workspace(B, K)
     o = dict(cand_pos=torch.full((B, stride), -1, **i32), cand_count=torch.zeros(B, **i32),
              ngram_used=torch.zeros(B, **i32), best_pos=torch.zeros(B, **i32),
              best_score=torch.zeros(B, dtype=torch.float32, device="cuda"),
@@ -403,17 +439,20 @@ def test_draft_fused_parity(case):
             ref = oracle.rank_hidden(bits, lens, cp, cc, threshold=th)
             pld.pld_draft_hidden(d_i32(toks), d_i32(lens), nmin, nmax, hd, K, o["cand_pos"],
                                  o["cand_count"], o["ngram_used"], o["best_pos"], o["best_score"],
-                                 o["draft"], o["draft_len"], threshold=th, scores=o["scores"])
-            split = gpu_rank_hidden(hd, lens, cp, cc, threshold=th)
+                                 o["draft"], o["draft_len"], threshold=th, scores=o["scores"],
+                                 blocks_per_seq=split, workspace=ws)
+            split_ref = gpu_rank_hidden(hd, lens, cp, cc, threshold=th)
         else:
             A = synth.make_attn(B, R, stride, lens, seed=seed)
             ref = oracle.rank_attn(A, lens, cp, cc, oracle.AGG_SUM, threshold=th)
             pld.pld_draft_attn(d_i32(toks), d_i32(lens), nmin, nmax, d_f32(A), K, o["cand_pos"],
                                o["cand_count"], o["ngram_used"], o["best_pos"], o["best_score"],
-                               o["draft"], o["draft_len"], threshold=th, scores=o["scores"])
-            split = gpu_rank_attn(d_f32(A), lens, cp, cc, pld.PLD_AGG_SUM, threshold=th)
+                               o["draft"], o["draft_len"], threshold=th, scores=o["scores"],
+                               blocks_per_seq=split, workspace=ws)
+            split_ref = gpu_rank_attn(d_f32(A), lens, cp, cc, pld.PLD_AGG_SUM, threshold=th)
         torch.cuda.synchronize()
         g = {k: v.cpu().numpy() for k, v in o.items()}
+        assert int(torch.count_nonzero(ws).item()) == 0
         check_find((g["cand_pos"], g["cand_count"], g["ngram_used"]), ref_find, str(case))
         rsc, rbp, rbs = ref
         check_scores(g["scores"], rsc, cc, str(case))
@@ -421,8 +460,8 @@ def test_draft_fused_parity(case):
                            threshold=th)
         for b in range(B):          # same bits as the separate ranking call
             n = cc[b]
-            assert np.array_equal(g["scores"][b, :n], split[0][b, :n], equal_nan=True)
-        assert np.array_equal(g["best_pos"], split[1])
+            assert np.array_equal(g["scores"][b, :n], split_ref[0][b, :n], equal_nan=True)
+        assert np.array_equal(g["best_pos"], split_ref[1])
         rd, rl = oracle.emit(toks, lens, g["best_pos"] if flips else rbp, K)
         assert np.array_equal(g["draft"], rd) and np.array_equal(g["draft_len"], rl)
 
