@@ -92,8 +92,10 @@ __device__ void draft_score_rows(const DraftArgs &a, int b, int64_t T, bool seq_
     }
 }
 
-// The draft of sequence b from its best key (Sec. 4.3), written by one wave.
-__device__ void write_draft(const DraftArgs &a, int b, int64_t T, bool tok_ok, uint64_t best) {
+// The draft of sequence b from its best key (Sec. 4.3), written by one wave;
+// `x` is the sequence's token row (global memory or its LDS copy).
+__device__ void write_draft(const DraftArgs &a, int b, int64_t T, bool tok_ok, uint64_t best,
+                            const int32_t *x) {
     const int lane = lane_id();
     const int32_t bp = best ? (int32_t)(uint32_t)(best & 0xffffffffu) : -1;
     if (lane == 0) {
@@ -102,7 +104,6 @@ __device__ void write_draft(const DraftArgs &a, int b, int64_t T, bool tok_ok, u
     }
     int64_t L = 0;
     if (tok_ok && bp >= 0 && (int64_t)bp <= T - 2) L = min((int64_t)a.K, T - 1 - bp);
-    const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
     for (int i = lane; i < a.K; i += kWave)
         a.draft[(int64_t)b * a.K + i] = (i < L) ? x[bp + 1 + i] : -1;
     if (lane == 0) a.draft_len[b] = (int32_t)L;
@@ -113,7 +114,13 @@ __global__ __launch_bounds__(kWaves * kWave) void draft_kernel(DraftArgs a) {
     constexpr int kThreads = kWaves * kWave;
     constexpr int kSteps = kFindFusedMax / (kWaves * kWave * kLanePos);   // passes per wave
     static_assert(kSteps * kWaves * kWave * kLanePos == kFindFusedMax, "whole passes");
-    __shared__ __align__(16) int32_t s_buf[kFindFusedMax];   // tokens, then the occurrence list
+    // One block per sequence (16 waves) keeps the tokens for the draft and puts
+    // the occurrence list in an array of its own; with several blocks per
+    // sequence the list overwrites the tokens (more blocks fit on a CU).
+    constexpr bool kKeep = kWaves == 16;
+    __shared__ __align__(16) int32_t s_buf[kFindFusedMax];   // the tokens
+    __shared__ int32_t s_own[kKeep ? kFindFusedMax : 1];
+    int32_t *s_list = kKeep ? s_own : s_buf;                 // the occurrence list
     extern __shared__ uint4 s_q[];             // query row H[T-2], bf16 (hidden only)
     __shared__ int s_lvl[kWaves][kMaxNgram];
     __shared__ uint64_t s_key[kWaves];
@@ -129,9 +136,15 @@ __global__ __launch_bounds__(kWaves * kWave) void draft_kernel(DraftArgs a) {
     const bool seq_ok = kHidden ? (T >= 2 && T - 2 < a.n_rows) : (T >= 2);
     const uint16_t *Hb = kHidden ? a.hidden + (int64_t)b * a.hs : nullptr;
     const int nch = kHidden ? a.d / 8 : 0;
-    if (kHidden && tok_ok && seq_ok)   // the query row, straight into LDS
+    // the token row straight into LDS when it is 16-byte aligned (it does not
+    // wait for the length), then the query row
+    if (((uintptr_t)x & 15) == 0 && (a.tok_stride & 3) == 0)
+        copy_to_lds(reinterpret_cast<const uint4 *>(x), reinterpret_cast<uint4 *>(s_buf),
+                    (int)(a.tok_stride / 4));
+    else
+        stage_tokens(x, 0, a.tok_stride, s_buf);
+    if (kHidden && tok_ok && seq_ok)
         copy_to_lds(reinterpret_cast<const uint4 *>(Hb + (T - 2) * a.hr), s_q, nch);
-    stage_tokens(x, 0, a.tok_stride, s_buf);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
@@ -157,7 +170,7 @@ __global__ __launch_bounds__(kWaves * kWave) void draft_kernel(DraftArgs a) {
                 if (lane == 0) s_lvl[w][k] = t;
             }
         }
-        __syncthreads();   // also: every token read is done, s_buf becomes the list
+        __syncthreads();   // every token read of the search is done
         n_used = 0;
         for (int n = a.nmax; n >= a.nmin; --n) {
             int t = 0;
@@ -174,8 +187,8 @@ __global__ __launch_bounds__(kWaves * kWave) void draft_kernel(DraftArgs a) {
             int32_t *out = split == 0 ? a.cand_pos + (int64_t)b * a.cap : nullptr;
 #pragma unroll
             for (int st = 0; st < kSteps; ++st)
-                run = emit_bits(level_bits(hits[st], n_used), base0 + st * kWave * kLanePos, s_buf,
-                                out, run);
+                run = emit_bits(level_bits(hits[st], n_used), base0 + st * kWave * kLanePos,
+                                s_list, out, run);
             __syncthreads();
         }
     }
@@ -192,15 +205,15 @@ __global__ __launch_bounds__(kWaves * kWave) void draft_kernel(DraftArgs a) {
             if (seq_ok) row_dot<false>(s_q, s_q, nch, qdot, qq);
             const int first = split + S * w, step = S * kWaves;
             if (nch <= 4 * kWave)
-                draft_score_rows<4>(a, b, T, seq_ok, Hb, s_q, qq, s_buf, first, step, total, best);
+                draft_score_rows<4>(a, b, T, seq_ok, Hb, s_q, qq, s_list, first, step, total, best);
             else if (nch <= 8 * kWave)
-                draft_score_rows<2>(a, b, T, seq_ok, Hb, s_q, qq, s_buf, first, step, total, best);
+                draft_score_rows<2>(a, b, T, seq_ok, Hb, s_q, qq, s_list, first, step, total, best);
             else
-                draft_score_rows<1>(a, b, T, seq_ok, Hb, s_q, qq, s_buf, first, step, total, best);
+                draft_score_rows<1>(a, b, T, seq_ok, Hb, s_q, qq, s_list, first, step, total, best);
         } else {
             const float *Ab = a.attn + (int64_t)b * a.as;
             for (int c = split + S * (int)threadIdx.x; c < total; c += S * kThreads) {
-                const int32_t j = s_buf[c];
+                const int32_t j = s_list[c];
                 float s = __builtin_nanf("");
                 if (seq_ok && j >= 1 && (int64_t)j <= T - 2 && (int64_t)(j - 1) < a.n_keys) {
                     s = attn_gather(Ab + (j - 1), a.ar, a.R, a.agg == PLD_AGG_SUM);
@@ -222,7 +235,7 @@ __global__ __launch_bounds__(kWaves * kWave) void draft_kernel(DraftArgs a) {
 
     // ---- selection and the draft (Sec. 4.3)
     if (S == 1) {
-        if (w == 0) write_draft(a, b, T, tok_ok, best);
+        if (w == 0) write_draft(a, b, T, tok_ok, best, kKeep ? s_buf : x);
     } else if (threadIdx.x == 0 && best) {
         atomicMax((unsigned long long *)&a.keys[(int64_t)b * kKeySlots + (split % kKeySlots)],
                   (unsigned long long)best);
@@ -242,7 +255,7 @@ __global__ __launch_bounds__(256) void draft_finish_kernel(DraftArgs a) {
     }
     k = wave_max_u64(k);
     const int64_t T = a.lens[b];
-    write_draft(a, b, T, T >= 1 && T <= a.tok_stride, k);
+    write_draft(a, b, T, T >= 1 && T <= a.tok_stride, k, a.tokens + (int64_t)b * a.tok_stride);
 }
 
 static int check_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B,

@@ -105,9 +105,9 @@ class DraftStep:
     def tune_split(self, cand_count, hidden=True):
         """Blocks per sequence for the one-call drafting from observed candidate
         counts (e.g. the previous step's): about four rows per block for hidden
-        states (one per wave), 64 candidates per block for attention gathers."""
+        states (one per wave), 32 candidates per block for attention gathers."""
         import math
-        per = 4 if hidden else 64
+        per = 4 if hidden else 32
         mx = int(max(int(c) for c in cand_count)) if len(cand_count) else 0
         self.draft_split = max(1, min(PLD_MAX_DRAFT_SPLIT, math.ceil(mx / per)))
         return self.draft_split
