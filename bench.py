@@ -77,7 +77,7 @@ def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fu
 
 
 # kernels behind each timed call (names as rocprofv3 reports them)
-KERNELS = {"draft": "pld::draft_kernel", "find": "pld::find_", "score_hidden": "pld::rank_hidden_kernel",
+KERNELS = {"draft": "pld::draft_", "find": "pld::find_", "score_hidden": "pld::rank_hidden_kernel",
            "score_attn": "pld::rank_attn_kernel", "select": "pld::rank_finish_kernel",
            "select_attn": "pld::rank_finish_kernel", "emit": "pld::emit_kernel",
            "verify_argmax": "pld::verify_argmax_kernel", "verify_accept": "pld::verify_accept_kernel"}
@@ -154,8 +154,8 @@ def measured_traffic(workload, call):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: the drafting step has no cross-GPU exchange in "
-              "this build (see the sharding notes); run it with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU (--gpus 1): the step shards by sequence with no "
+              "exchange between GPUs, so more GPUs only scale the batch.", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch

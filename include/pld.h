@@ -239,20 +239,37 @@ int pld_verify_accept(const int32_t *draft, const int32_t *draft_len, int B, int
  * call: pld_find_candidates, then pld_rank_hidden (or pld_rank_attn), then
  * pld_emit_draft, with the same definitions, outputs and device-side rules
  * (Eq. 1, Eq. 2 / Eq. 3 and Sec. 4.3); scores, choices and drafts are
- * bit-identical to the separate calls.  Needs tok_stride <= 8192.
+ * bit-identical to the separate calls.
  *
- *   blocks_per_seq  S in [1, PLD_MAX_DRAFT_SPLIT]: S blocks share a sequence,
- *                   each scoring every S-th occurrence.  S = 1 is one launch
- *                   and uses no workspace -- the lowest latency when the
- *                   candidate lists are short; S > 1 adds a small finishing
- *                   launch and spreads long lists over S compute units, and
- *                   then needs `workspace` (pld_workspace_bytes, as for the
- *                   ranking calls; left zero).
+ *   blocks_per_seq  S in [1, PLD_MAX_DRAFT_SPLIT]:
+ *                   S = 1: one block per sequence and one launch, no
+ *                     workspace; needs tok_stride <= 8192.  The lowest
+ *                     latency for short contexts and short candidate lists.
+ *                   S > 1: the positions are split into S slices of
+ *                     P = ceil(tok_stride / S) rounded up to a multiple of 8
+ *                     (P <= 8192), one block each; a block finds, scores and
+ *                     lists the occurrences in its slice, and a finishing
+ *                     launch compacts the lists and writes the selection and
+ *                     the draft (with ngram_min < ngram_max a counting launch
+ *                     comes first).  Spreads long contexts and long lists
+ *                     over S x B blocks.
+ *   workspace       S > 1: at least pld_draft_workspace_bytes(B, S) bytes of
+ *                   its own (not shared with the ranking or verification
+ *                   calls), zero before the first call.  Its first B*128
+ *                   bytes (the key slots) are left zero by every call; the
+ *                   rest is per-block counts, rewritten by each call.  Calls
+ *                   that share one workspace must not overlap in time.
+ *   cand_pos, scores  entries past cand_count are unspecified on return.
  *   scores          may be NULL.
- * Errors: as the separate calls; tok_stride > 8192 or S out of range is
- * PLD_ERR_INVALID; S > 1 without a large enough workspace is PLD_ERR_WORKSPACE.
+ * Errors: as the separate calls; S out of range, S = 1 with tok_stride > 8192
+ * or S > 1 with P > 8192 is PLD_ERR_INVALID; S > 1 without a large enough
+ * workspace is PLD_ERR_WORKSPACE.
  */
-#define PLD_MAX_DRAFT_SPLIT 256
+#define PLD_MAX_DRAFT_SPLIT 1024
+
+/* Workspace bytes of the one-call drafting for B sequences and S blocks per
+ * sequence (0 for S = 1, and for arguments out of range). */
+size_t pld_draft_workspace_bytes(int B, int blocks_per_seq);
 
 int pld_draft_hidden(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B,
                      int ngram_min, int ngram_max, const uint16_t *hidden, int64_t h_seq_stride,

@@ -18,15 +18,17 @@ __all__ = [
     "pld_version", "pld_status_string", "pld_workspace_bytes", "pld_find_scratch_bytes",
     "pld_find_candidates",
     "pld_rank_hidden", "pld_rank_attn", "pld_emit_draft", "pld_verify_greedy",
-    "pld_draft_hidden", "pld_draft_attn", "DRAFT_MAX_TOK_STRIDE", "pld_score_hidden",
+    "pld_draft_hidden", "pld_draft_attn", "pld_draft_workspace_bytes", "DRAFT_MAX_TOK_STRIDE",
+    "DRAFT_MAX_PART", "pld_score_hidden",
     "pld_score_attn", "pld_select_best", "pld_verify_argmax", "pld_verify_accept",
 ]
 
 PLD_OK, PLD_ERR_INVALID, PLD_ERR_ALIGN, PLD_ERR_WORKSPACE, PLD_ERR_LAUNCH = range(5)
 PLD_F32, PLD_BF16 = 0, 1
 PLD_AGG_SUM, PLD_AGG_MAX = 0, 1
-PLD_MAX_NGRAM, PLD_MAX_HIDDEN, PLD_MAX_BATCH, PLD_MAX_DRAFT_SPLIT = 8, 16384, 4096, 256
-DRAFT_MAX_TOK_STRIDE = 8192     # one-launch drafting: one block per sequence
+PLD_MAX_NGRAM, PLD_MAX_HIDDEN, PLD_MAX_BATCH, PLD_MAX_DRAFT_SPLIT = 8, 16384, 4096, 1024
+DRAFT_MAX_TOK_STRIDE = 8192     # one-call drafting, one block per sequence (S = 1)
+DRAFT_MAX_PART = 8192           # one-call drafting, S > 1: positions per block
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 library_path = os.path.join(_HERE, "libpld.so")
@@ -39,6 +41,7 @@ _SIGNATURES = {
     "pld_version": ([], _int),
     "pld_status_string": ([_int], ctypes.c_char_p),
     "pld_workspace_bytes": ([_int, _int], _sz),
+    "pld_draft_workspace_bytes": ([_int, _int], _sz),
     "pld_find_scratch_bytes": ([_int, _i64], _sz),
     "pld_find_candidates": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _vp, _vp, _vp, _sz, _vp],
                             _int),
@@ -150,6 +153,10 @@ def pld_workspace_bytes(B, K):
     return int(_load().pld_workspace_bytes(B, K))
 
 
+def pld_draft_workspace_bytes(B, blocks_per_seq):
+    return int(_load().pld_draft_workspace_bytes(B, blocks_per_seq))
+
+
 def pld_find_scratch_bytes(B, tok_stride):
     return int(_load().pld_find_scratch_bytes(B, tok_stride))
 
@@ -229,7 +236,8 @@ def pld_verify_greedy(logits, draft, draft_len, accept_len, out_tokens, out_coun
 def pld_draft_hidden(tokens, lens, ngram_min, ngram_max, hidden, K, cand_pos, cand_count,
                      ngram_used, best_pos, best_score, draft, draft_len, threshold=float("-inf"),
                      scores=None, blocks_per_seq=1, workspace=None, stream=None, prepare=False):
-    """find + hidden-state ranking + emit in one call (tok_stride <= 8192)."""
+    """find + hidden-state ranking + emit in one call (blocks_per_seq 1: tok_stride <= 8192;
+    more: a workspace of pld_draft_workspace_bytes(B, blocks_per_seq) bytes)."""
     import torch
     _need(tokens, torch.int32, "tokens", 2)
     _need(hidden, torch.bfloat16, "hidden", 3)
@@ -249,7 +257,8 @@ def pld_draft_attn(tokens, lens, ngram_min, ngram_max, attn, K, cand_pos, cand_c
                    best_pos, best_score, draft, draft_len, agg=PLD_AGG_SUM,
                    threshold=float("-inf"), scores=None, blocks_per_seq=1, workspace=None,
                    stream=None, prepare=False):
-    """find + attention ranking + emit in one call (tok_stride <= 8192)."""
+    """find + attention ranking + emit in one call (blocks_per_seq 1: tok_stride <= 8192;
+    more: a workspace of pld_draft_workspace_bytes(B, blocks_per_seq) bytes)."""
     import torch
     _need(tokens, torch.int32, "tokens", 2)
     _need(attn, torch.float32, "attn", 3)

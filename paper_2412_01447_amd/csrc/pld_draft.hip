@@ -3,18 +3,22 @@
 // hidden-state cosine (Eq. 2) or aggregated attention (Eq. 3, Sec. 7.1),
 // selection of the best occurrence, and the draft span (Sec. 4.3).
 //
-// S blocks share one sequence (grid S x B).  Every block stages the whole
-// token row in LDS -- the load does not wait for the length -- finds the
-// occurrences itself (the search is a few microseconds of LDS work, so
-// repeating it costs less than a launch), builds the ordered occurrence list
-// in LDS, and scores the occurrences c = s, s+S, s+2S, ... with the same
-// per-row routines as the separate ranking calls (bit-identical scores).
-//   S == 1: one block owns the sequence; it selects the best occurrence and
-//           writes the draft itself -- one launch, three dependent trips to
-//           memory (length and tokens, query row, candidate rows).
-//   S  > 1: each block folds its best key into the sequence's spread key
-//           slots in the workspace, and a small finishing kernel selects and
-//           writes the draft -- long candidate lists are spread over S CUs.
+// S == 1 (tok_stride <= 8192): one 1024-thread block owns a sequence.  It
+//   copies the token row and the query row into LDS, finds the occurrences,
+//   scores them with the same per-row routines as the separate ranking calls
+//   (bit-identical scores), selects, and writes the draft -- one launch.
+// S  > 1: the positions are partitioned.  Block s of a sequence owns the
+//   positions [s*P, (s+1)*P) (P <= 8192, a multiple of 8): it stages only
+//   those tokens, finds its own occurrences, scores them, and folds its best
+//   key into the sequence's key slots.  Its part of the occurrence list (and
+//   of the scores) goes to offset s*P of the outputs -- a block never holds
+//   more occurrences than positions, so this stays inside the row.  A
+//   finishing kernel turns the per-block counts into offsets, compacts the
+//   parts in order, and selects and writes the draft.  With a range of n-gram
+//   lengths a counting pass first writes per-block occurrence counts of every
+//   n, from which every block takes the same longest n.  Work per block is a
+//   P-position slice, so long contexts and long candidate lists spread over
+//   as many CUs as the caller asks for.
 #include <math.h>
 
 #include "pld.h"
@@ -22,6 +26,14 @@
 #include "pld_match.h"
 
 namespace pld {
+
+constexpr int kPartMax = 8192;                  // positions per block, S > 1
+constexpr int kPartWaves = 4;                   // 256 threads per block, S > 1
+constexpr int kPartPass = kPartWaves * kWave * kLanePos;   // 2048 positions per pass
+constexpr int kPartPasses = kPartMax / kPartPass;
+constexpr int kWindow = 16384;                  // list entries per compaction pass
+constexpr int kFinishThreads = 1024;
+static_assert(PLD_MAX_DRAFT_SPLIT <= kFinishThreads, "one block count per finishing thread");
 
 struct DraftArgs {
     const int32_t *tokens;
@@ -46,17 +58,36 @@ struct DraftArgs {
     int K;
     int32_t *draft;
     int32_t *draft_len;
-    uint64_t *keys;   // [B][kKeySlots] when S > 1, zero on entry
+    // S > 1 only (workspace)
+    int S;
+    int64_t P;
+    uint64_t *keys;     // [B][kKeySlots], zero on entry and on exit
+    int32_t *hcount;    // [B][S] occurrences found by each block
+    int32_t *lvl;       // [B][S][kMaxNgram] per-n counts (ngram_min < ngram_max)
 };
+
+static size_t part_ws_bytes(int B, int S) {
+    return align_up((size_t)B * kKeySlots * 8, 256) + align_up((size_t)B * S * 4, 256) +
+           align_up((size_t)B * S * kMaxNgram * 4, 256);
+}
+
+static void part_ws_layout(DraftArgs &a, void *ws) {
+    char *p = (char *)ws;
+    a.keys = (uint64_t *)p;
+    p += align_up((size_t)a.B * kKeySlots * 8, 256);
+    a.hcount = (int32_t *)p;
+    p += align_up((size_t)a.B * a.S * 4, 256);
+    a.lvl = (int32_t *)p;
+}
 
 // Scores this wave's share of the candidates: list slots c = first, first +
 // step, ... < total, G rows at a time (the same per-row arithmetic as the
-// multi-block ranking kernel).
+// multi-block ranking kernel); score c goes to scores[b][out0 + c].
 template <int G>
 __device__ void draft_score_rows(const DraftArgs &a, int b, int64_t T, bool seq_ok,
                                  const uint16_t *Hb, const uint4 *q_s, float qq,
                                  const int32_t *s_cand, int first, int step, int total,
-                                 uint64_t &best) {
+                                 int64_t out0, uint64_t &best) {
     const int lane = lane_id();
     const int nch = a.d / 8;
     const int n = total > first ? (total - first + step - 1) / step : 0;
@@ -87,9 +118,56 @@ __device__ void draft_score_rows(const DraftArgs &a, int b, int64_t T, bool seq_
                     best = key > best ? key : best;
                 }
             }
-            if (a.scores && lane == 0) a.scores[(int64_t)b * a.cap + first + (k + g) * step] = s;
+            if (a.scores && lane == 0)
+                a.scores[(int64_t)b * a.cap + out0 + first + (k + g) * step] = s;
         }
     }
+}
+
+// The block's share of the ranking (Eq. 2 / Eq. 3) over the list s_cand of
+// `total` candidates: list slots w, w + kWaves, ... per wave (hidden), or one
+// slot per thread (attention).  Returns the block's best key in every thread;
+// `s_q` holds the query row (hidden), `s_key` is kWaves words of LDS.
+template <bool kHidden, int kWaves>
+__device__ uint64_t rank_candidates(const DraftArgs &a, int b, int64_t T, bool seq_ok,
+                                    const int32_t *s_cand, int total, int64_t out0,
+                                    const uint4 *s_q, uint64_t *s_key) {
+    const int w = threadIdx.x / kWave;
+    const int lane = lane_id();
+    uint64_t best = 0;
+    if constexpr (kHidden) {
+        const uint16_t *Hb = a.hidden + (int64_t)b * a.hs;
+        const int nch = a.d / 8;
+        float qdot = 0.f, qq = 0.f;
+        if (seq_ok) row_dot<false>(s_q, s_q, nch, qdot, qq);
+        if (nch <= 4 * kWave)
+            draft_score_rows<4>(a, b, T, seq_ok, Hb, s_q, qq, s_cand, w, kWaves, total, out0, best);
+        else if (nch <= 8 * kWave)
+            draft_score_rows<2>(a, b, T, seq_ok, Hb, s_q, qq, s_cand, w, kWaves, total, out0, best);
+        else
+            draft_score_rows<1>(a, b, T, seq_ok, Hb, s_q, qq, s_cand, w, kWaves, total, out0, best);
+        // (every lane of a wave holds the wave's best)
+    } else {
+        const float *Ab = a.attn + (int64_t)b * a.as;
+        for (int c = threadIdx.x; c < total; c += kWaves * kWave) {
+            const int32_t j = s_cand[c];
+            float s = __builtin_nanf("");
+            if (seq_ok && j >= 1 && (int64_t)j <= T - 2 && (int64_t)(j - 1) < a.n_keys) {
+                s = attn_gather(Ab + (j - 1), a.ar, a.R, a.agg == PLD_AGG_SUM);
+                if (s > a.threshold) {
+                    const uint64_t k = rank_key(s, j);
+                    best = k > best ? k : best;
+                }
+            }
+            if (a.scores) a.scores[(int64_t)b * a.cap + out0 + c] = s;
+        }
+        best = wave_max_u64(best);
+    }
+    if (lane == 0) s_key[w] = best;
+    __syncthreads();
+    best = 0;
+    for (int i = 0; i < kWaves; ++i) best = s_key[i] > best ? s_key[i] : best;
+    return best;
 }
 
 // The draft of sequence b from its best key (Sec. 4.3), written by one wave;
@@ -109,60 +187,47 @@ __device__ void write_draft(const DraftArgs &a, int b, int64_t T, bool tok_ok, u
     if (lane == 0) a.draft_len[b] = (int32_t)L;
 }
 
-template <bool kHidden, int kWaves>
-__global__ __launch_bounds__(kWaves * kWave) void draft_kernel(DraftArgs a) {
-    constexpr int kThreads = kWaves * kWave;
-    constexpr int kSteps = kFindFusedMax / (kWaves * kWave * kLanePos);   // passes per wave
-    static_assert(kSteps * kWaves * kWave * kLanePos == kFindFusedMax, "whole passes");
-    // One block per sequence (16 waves) keeps the tokens for the draft and puts
-    // the occurrence list in an array of its own; with several blocks per
-    // sequence the list overwrites the tokens (more blocks fit on a CU).
-    constexpr bool kKeep = kWaves == 16;
+// ------------------------------------------------------------------- S == 1
+template <bool kHidden>
+__global__ __launch_bounds__(kFindWavesFused * kWave) void draft_kernel(DraftArgs a) {
+    constexpr int kWaves = kFindWavesFused;
+    static_assert(kFindFusedMax == kWaves * kWave * kLanePos, "one pass per block");
     __shared__ __align__(16) int32_t s_buf[kFindFusedMax];   // the tokens
-    __shared__ int32_t s_own[kKeep ? kFindFusedMax : 1];
-    int32_t *s_list = kKeep ? s_own : s_buf;                 // the occurrence list
-    extern __shared__ uint4 s_q[];             // query row H[T-2], bf16 (hidden only)
+    __shared__ int32_t s_list[kFindFusedMax];                // the occurrence list
+    extern __shared__ uint4 s_q[];                           // query row H[T-2] (hidden)
     __shared__ int s_lvl[kWaves][kMaxNgram];
     __shared__ uint64_t s_key[kWaves];
-    const int split = blockIdx.x, S = gridDim.x, b = blockIdx.y;
+    const int b = blockIdx.y;
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
 
-    // the query row, the token row and the length are all requested before
-    // the first wait
+    // the token row straight into LDS when it is 16-byte aligned (it does not
+    // wait for the length), then the query row
     const int64_t T = a.lens[b];
     const bool tok_ok = (T >= 1 && T <= a.tok_stride);   // block-uniform
     const bool seq_ok = kHidden ? (T >= 2 && T - 2 < a.n_rows) : (T >= 2);
-    const uint16_t *Hb = kHidden ? a.hidden + (int64_t)b * a.hs : nullptr;
-    const int nch = kHidden ? a.d / 8 : 0;
-    // the token row straight into LDS when it is 16-byte aligned (it does not
-    // wait for the length), then the query row
     if (((uintptr_t)x & 15) == 0 && (a.tok_stride & 3) == 0)
         copy_to_lds(reinterpret_cast<const uint4 *>(x), reinterpret_cast<uint4 *>(s_buf),
                     (int)(a.tok_stride / 4));
     else
         stage_tokens(x, 0, a.tok_stride, s_buf);
     if (kHidden && tok_ok && seq_ok)
-        copy_to_lds(reinterpret_cast<const uint4 *>(Hb + (T - 2) * a.hr), s_q, nch);
+        copy_to_lds(reinterpret_cast<const uint4 *>(a.hidden + (int64_t)b * a.hs + (T - 2) * a.hr),
+                    s_q, a.d / 8);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    // ---- occurrences (Eq. 1), longest n first
+    // ---- occurrences (Eq. 1), longest n first: one pass, 8 positions a lane
     int n_used = -1, total = 0;
     if (tok_ok) {
         const Query q = load_query(s_buf, T, a.nmax);
-        // wave w covers [w, w+1) * kSteps * 512; pass st, lane l: 8 positions from base[st]
-        const int64_t base0 = ((int64_t)w * kSteps * kWave + lane) * kLanePos;
-        uint64_t hits[kSteps];
+        const int64_t base = (int64_t)threadIdx.x * kLanePos;
+        const uint64_t hits = lane_hits(s_buf, 0, T, base, q, a.nmax);
         int cnt[kMaxNgram];
 #pragma unroll
         for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
-#pragma unroll
-        for (int st = 0; st < kSteps; ++st) {
-            hits[st] = lane_hits(s_buf, 0, T, base0 + st * kWave * kLanePos, q, a.nmax);
-            count_levels(hits[st], a.nmax, cnt);
-        }
+        count_levels(hits, a.nmax, cnt);
 #pragma unroll
         for (int k = 0; k < kMaxNgram; ++k) {
             if (k < a.nmax) {   // uniform
@@ -170,7 +235,7 @@ __global__ __launch_bounds__(kWaves * kWave) void draft_kernel(DraftArgs a) {
                 if (lane == 0) s_lvl[w][k] = t;
             }
         }
-        __syncthreads();   // every token read of the search is done
+        __syncthreads();
         n_used = 0;
         for (int n = a.nmax; n >= a.nmin; --n) {
             int t = 0;
@@ -184,78 +249,268 @@ __global__ __launch_bounds__(kWaves * kWave) void draft_kernel(DraftArgs a) {
         if (n_used > 0) {   // block-uniform; the ascending list
             int64_t run = 0;
             for (int i = 0; i < w; ++i) run += s_lvl[i][n_used - 1];
-            int32_t *out = split == 0 ? a.cand_pos + (int64_t)b * a.cap : nullptr;
-#pragma unroll
-            for (int st = 0; st < kSteps; ++st)
-                run = emit_bits(level_bits(hits[st], n_used), base0 + st * kWave * kLanePos,
-                                s_list, out, run);
+            emit_bits(level_bits(hits, n_used), base, s_list, a.cand_pos + (int64_t)b * a.cap,
+                      run);
             __syncthreads();
         }
     }
-    if (split == 0 && threadIdx.x == 0) {
+    if (threadIdx.x == 0) {
         a.cand_count[b] = total;
         a.ngram_used[b] = n_used;
     }
-
-    // ---- this block's share of the ranking (Eq. 2 / Eq. 3)
     uint64_t best = 0;
-    if (total > 0) {   // block-uniform
-        if constexpr (kHidden) {
-            float qdot = 0.f, qq = 0.f;
-            if (seq_ok) row_dot<false>(s_q, s_q, nch, qdot, qq);
-            const int first = split + S * w, step = S * kWaves;
-            if (nch <= 4 * kWave)
-                draft_score_rows<4>(a, b, T, seq_ok, Hb, s_q, qq, s_list, first, step, total, best);
-            else if (nch <= 8 * kWave)
-                draft_score_rows<2>(a, b, T, seq_ok, Hb, s_q, qq, s_list, first, step, total, best);
-            else
-                draft_score_rows<1>(a, b, T, seq_ok, Hb, s_q, qq, s_list, first, step, total, best);
-        } else {
-            const float *Ab = a.attn + (int64_t)b * a.as;
-            for (int c = split + S * (int)threadIdx.x; c < total; c += S * kThreads) {
-                const int32_t j = s_list[c];
-                float s = __builtin_nanf("");
-                if (seq_ok && j >= 1 && (int64_t)j <= T - 2 && (int64_t)(j - 1) < a.n_keys) {
-                    s = attn_gather(Ab + (j - 1), a.ar, a.R, a.agg == PLD_AGG_SUM);
-                    if (s > a.threshold) {
-                        const uint64_t k = rank_key(s, j);
-                        best = k > best ? k : best;
-                    }
-                }
-                if (a.scores) a.scores[(int64_t)b * a.cap + c] = s;
-            }
-            best = wave_max_u64(best);
-        }
-        // (hidden: every lane of a wave already holds the wave's best)
-        if (lane == 0) s_key[w] = best;
-        __syncthreads();
-        best = 0;
-        for (int i = 0; i < kWaves; ++i) best = s_key[i] > best ? s_key[i] : best;
-    }
+    if (total > 0)   // block-uniform
+        best = rank_candidates<kHidden, kWaves>(a, b, T, seq_ok, s_list, total, 0, s_q, s_key);
+    if (w == 0) write_draft(a, b, T, tok_ok, best, s_buf);
+}
 
-    // ---- selection and the draft (Sec. 4.3)
-    if (S == 1) {
-        if (w == 0) write_draft(a, b, T, tok_ok, best, kKeep ? s_buf : x);
-    } else if (threadIdx.x == 0 && best) {
-        atomicMax((unsigned long long *)&a.keys[(int64_t)b * kKeySlots + (split % kKeySlots)],
-                  (unsigned long long)best);
+// ------------------------------------------------------------------- S  > 1
+// Block s of sequence b: positions [lo, lo + P) with lo = s*P; the tokens
+// x[s0, s1) with s0 = lo - 8 (0 when lo == 0) and s1 = min(lo + P,
+// tok_stride) are staged, asynchronously when the copy is 16-byte aligned.
+__device__ __forceinline__ void stage_part(const int32_t *x, int64_t s0, int64_t s1, int32_t *s) {
+    if ((((uintptr_t)(x + s0)) & 15) == 0 && ((s1 - s0) & 3) == 0)
+        copy_to_lds(reinterpret_cast<const uint4 *>(x + s0), reinterpret_cast<uint4 *>(s),
+                    (int)((s1 - s0) / 4));
+    else
+        stage_tokens(x, s0, s1, s);
+}
+
+// Hit words of this thread, pass by pass (pass t: the 8 positions from
+// lo + t*2048 + 8*threadIdx.x); zero from lo + P on.
+__device__ __forceinline__ void part_hits(const int32_t *s_x, int64_t s0, int64_t T, int64_t lo,
+                                          int64_t P, const Query &q, int nmax,
+                                          uint64_t (&hits)[kPartPasses]) {
+#pragma unroll
+    for (int t = 0; t < kPartPasses; ++t) {
+        const int64_t base = lo + (int64_t)t * kPartPass + (int64_t)threadIdx.x * kLanePos;
+        hits[t] = (base < lo + P) ? lane_hits(s_x, s0, T, base, q, nmax) : 0ull;
     }
 }
 
-// S > 1: one wave per sequence folds the key slots (returning them to zero)
-// and writes best_pos, best_score and the draft.
-__global__ __launch_bounds__(256) void draft_finish_kernel(DraftArgs a) {
-    const int b = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave);
-    if (b >= a.B) return;   // wave-uniform
+// Counting pass (ngram_min < ngram_max): per-block occurrence counts of every n.
+__global__ __launch_bounds__(kPartWaves * kWave) void draft_count_kernel(DraftArgs a) {
+    __shared__ __align__(16) int32_t s_x[kPartMax + 8];
+    __shared__ int s_cnt[kMaxNgram];
+    const int s = blockIdx.x, b = blockIdx.y;
     const int lane = lane_id();
-    uint64_t k = 0;
-    if (lane < kKeySlots) {
-        k = a.keys[(int64_t)b * kKeySlots + lane];
-        a.keys[(int64_t)b * kKeySlots + lane] = 0;
-    }
-    k = wave_max_u64(k);
+    const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
     const int64_t T = a.lens[b];
-    write_draft(a, b, T, T >= 1 && T <= a.tok_stride, k, a.tokens + (int64_t)b * a.tok_stride);
+    const int64_t lo = (int64_t)s * a.P;
+    int32_t *out = a.lvl + ((int64_t)b * a.S + s) * kMaxNgram;
+    if (!(T >= 1 && T <= a.tok_stride) || lo > T - 2) {   // block-uniform
+        if (threadIdx.x < kMaxNgram) out[threadIdx.x] = 0;
+        return;
+    }
+    if (threadIdx.x < kMaxNgram) s_cnt[threadIdx.x] = 0;
+    const int64_t s0 = lo >= 8 ? lo - 8 : 0;
+    const int64_t s1 = (lo + a.P < a.tok_stride) ? lo + a.P : a.tok_stride;
+    stage_part(x, s0, s1, s_x);
+    const Query q = load_query(x, T, a.nmax);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    uint64_t hits[kPartPasses];
+    part_hits(s_x, s0, T, lo, a.P, q, a.nmax, hits);
+    int cnt[kMaxNgram];
+#pragma unroll
+    for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
+#pragma unroll
+    for (int t = 0; t < kPartPasses; ++t) count_levels(hits[t], a.nmax, cnt);
+#pragma unroll
+    for (int k = 0; k < kMaxNgram; ++k) {
+        if (k < a.nmax) {   // uniform
+            const int c = wave_sum_i32(cnt[k]);
+            if (lane == 0 && c) atomicAdd(&s_cnt[k], c);
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < kMaxNgram) out[threadIdx.x] = s_cnt[threadIdx.x];
+}
+
+// The n every block and the finishing kernel use: ngram_max when it is the
+// only length; otherwise the longest n whose occurrence count over all blocks
+// of the sequence is non-zero (0 when there is none).  Block-wide; s_tot is
+// kMaxNgram words of LDS.
+__device__ int part_n(const DraftArgs &a, int b, int *s_tot) {
+    if (a.nmin == a.nmax) return a.nmax;
+    if (threadIdx.x < kMaxNgram) s_tot[threadIdx.x] = 0;
+    __syncthreads();
+    int t[kMaxNgram];
+#pragma unroll
+    for (int k = 0; k < kMaxNgram; ++k) t[k] = 0;
+    for (int s = threadIdx.x; s < a.S; s += blockDim.x) {
+        const int32_t *c = a.lvl + ((int64_t)b * a.S + s) * kMaxNgram;
+#pragma unroll
+        for (int k = 0; k < kMaxNgram; ++k)
+            if (k < a.nmax) t[k] += c[k];
+    }
+#pragma unroll
+    for (int k = 0; k < kMaxNgram; ++k) {
+        if (k < a.nmax) {   // uniform
+            const int v = wave_sum_i32(t[k]);
+            if (lane_id() == 0 && v) atomicAdd(&s_tot[k], v);
+        }
+    }
+    __syncthreads();
+    for (int n = a.nmax; n >= a.nmin; --n)
+        if (s_tot[n - 1] > 0) return n;
+    return 0;
+}
+
+// Dynamic LDS of the partitioned kernel: the block's tokens (P + 8, then its
+// list), 16-byte aligned, then the query row (hidden) -- sized to the slice so
+// that small slices leave room for many blocks per CU.
+static size_t part_tok_bytes(int64_t P) { return align_up((size_t)(P + 8) * 4, 16); }
+
+template <bool kHidden>
+__global__ __launch_bounds__(kPartWaves * kWave) void draft_part_kernel(DraftArgs a) {
+    extern __shared__ uint4 s_dyn[];
+    int32_t *s_x = reinterpret_cast<int32_t *>(s_dyn);   // tokens, then the block's list
+    const uint4 *s_q = s_dyn + ((a.P + 8) * 4 + 15) / 16;   // query row H[T-2] (hidden)
+    __shared__ int s_tot[kMaxNgram];
+    __shared__ int s_wc[kPartPasses][kPartWaves];
+    __shared__ uint64_t s_key[kPartWaves];
+    const int s = blockIdx.x, b = blockIdx.y;
+    const int w = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
+    const int64_t T = a.lens[b];
+    const int64_t lo = (int64_t)s * a.P;
+    if (!(T >= 1 && T <= a.tok_stride)) return;   // the finishing kernel reports it
+    if (lo > T - 2) {                              // no position of this block can match
+        if (threadIdx.x == 0) a.hcount[(int64_t)b * a.S + s] = 0;
+        return;
+    }
+    const bool seq_ok = kHidden ? (T >= 2 && T - 2 < a.n_rows) : (T >= 2);
+    const int64_t s0 = lo >= 8 ? lo - 8 : 0;
+    const int64_t s1 = (lo + a.P < a.tok_stride) ? lo + a.P : a.tok_stride;
+    stage_part(x, s0, s1, s_x);
+    if (kHidden && seq_ok)
+        copy_to_lds(reinterpret_cast<const uint4 *>(a.hidden + (int64_t)b * a.hs + (T - 2) * a.hr),
+                    const_cast<uint4 *>(s_q), a.d / 8);
+    const Query q = load_query(x, T, a.nmax);
+    __builtin_amdgcn_s_waitcnt(0);
+    const int n = part_n(a, b, s_tot);   // block-uniform
+    __syncthreads();                     // (also: the staged tokens are in place)
+    if (n == 0) {
+        if (threadIdx.x == 0) a.hcount[(int64_t)b * a.S + s] = 0;
+        return;
+    }
+    uint64_t hits[kPartPasses];
+    part_hits(s_x, s0, T, lo, a.P, q, a.nmax, hits);
+    uint32_t bits[kPartPasses];
+#pragma unroll
+    for (int t = 0; t < kPartPasses; ++t) {
+        bits[t] = level_bits(hits[t], n);
+        const int c = wave_sum_i32(__popc(bits[t]));
+        if (lane == 0) s_wc[t][w] = c;
+    }
+    __syncthreads();   // every token read is done: s_x becomes the block's list
+    // list order is ascending position: pass, then wave, then lane
+    int total = 0;
+    int start[kPartPasses];
+#pragma unroll
+    for (int t = 0; t < kPartPasses; ++t) {
+        start[t] = total;
+        for (int i = 0; i < kPartWaves; ++i) {
+            if (i < w) start[t] += s_wc[t][i];
+            total += s_wc[t][i];
+        }
+    }
+    if (threadIdx.x == 0) a.hcount[(int64_t)b * a.S + s] = total;
+    if (total == 0) return;   // block-uniform
+    int32_t *out = a.cand_pos + (int64_t)b * a.cap + lo;
+#pragma unroll
+    for (int t = 0; t < kPartPasses; ++t)
+        emit_bits(bits[t], lo + (int64_t)t * kPartPass + (int64_t)threadIdx.x * kLanePos, s_x,
+                  out, start[t]);
+    __syncthreads();
+    const uint64_t best =
+        rank_candidates<kHidden, kPartWaves>(a, b, T, seq_ok, s_x, total, lo, s_q, s_key);
+    if (threadIdx.x == 0 && best)
+        atomicMax((unsigned long long *)&a.keys[(int64_t)b * kKeySlots + (s % kKeySlots)],
+                  (unsigned long long)best);
+}
+
+// One block per sequence: the selection from the key slots (returned to
+// zero) and the draft; the offsets of the blocks' parts, in-order compaction
+// of the list (and the scores) through an LDS window, ngram_used and the
+// count.  A part's entries only move towards the start of the row (its
+// offset is at most s*P) and never over a later part's entries, and every
+// entry of a window is read before any of the window is written.
+__global__ __launch_bounds__(kFinishThreads) void draft_finish_part_kernel(DraftArgs a) {
+    __shared__ int32_t s_off[PLD_MAX_DRAFT_SPLIT + 1];
+    __shared__ int32_t s_win[kWindow];
+    __shared__ int s_tot[kMaxNgram];
+    __shared__ int s_wsum[kFinishThreads / kWave];
+    const int b = blockIdx.x;
+    const int w = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const int64_t T = a.lens[b];
+    const bool tok_ok = (T >= 1 && T <= a.tok_stride);   // block-uniform
+    // the selection does not depend on the list: the last wave writes it and
+    // the draft first, while the others start on the offsets
+    if (w == kFinishThreads / kWave - 1) {
+        uint64_t k = 0;
+        if (lane < kKeySlots) {
+            k = a.keys[(int64_t)b * kKeySlots + lane];
+            a.keys[(int64_t)b * kKeySlots + lane] = 0;
+        }
+        k = wave_max_u64(k);
+        write_draft(a, b, T, tok_ok, k, a.tokens + (int64_t)b * a.tok_stride);
+    }
+    int n = -1, total = 0;
+    if (tok_ok) {
+        n = part_n(a, b, s_tot);
+        // exclusive scan of the per-block counts, one per thread
+        const int c = (n > 0 && (int)threadIdx.x < a.S) ? a.hcount[(int64_t)b * a.S + threadIdx.x]
+                                                        : 0;
+        int wt;
+        const int ex = wave_excl_scan(c, wt);
+        if (lane == 0) s_wsum[w] = wt;
+        __syncthreads();
+        int pre = 0;
+        for (int i = 0; i < kFinishThreads / kWave; ++i) {
+            if (i < w) pre += s_wsum[i];
+            total += s_wsum[i];
+        }
+        if ((int)threadIdx.x < a.S) s_off[threadIdx.x] = pre + ex;
+        if (threadIdx.x == 0) s_off[a.S] = total;
+        __syncthreads();
+        int32_t *rows[2] = {a.cand_pos + (int64_t)b * a.cap,
+                            a.scores ? reinterpret_cast<int32_t *>(a.scores + (int64_t)b * a.cap)
+                                     : nullptr};
+        for (int r = 0; r < 2; ++r) {
+            int32_t *v = rows[r];
+            if (!v) continue;   // uniform
+            for (int w0 = 0; w0 < total; w0 += kWindow) {
+                const int wn = min(kWindow, total - w0);
+                for (int i = threadIdx.x; i < wn; i += kFinishThreads) {
+                    const int dpos = w0 + i;
+                    // the part p with s_off[p] <= dpos < s_off[p+1]
+                    int lo = 0, hi = a.S;
+                    while (hi - lo > 1) {
+                        const int mid = (lo + hi) >> 1;
+                        if (s_off[mid] <= dpos) lo = mid; else hi = mid;
+                    }
+                    s_win[i] = v[(int64_t)lo * a.P + (dpos - s_off[lo])];
+                }
+                __syncthreads();
+                for (int i = threadIdx.x; i < wn; i += kFinishThreads) v[w0 + i] = s_win[i];
+                __syncthreads();
+            }
+        }
+    }
+    if (threadIdx.x == 0) {
+        a.cand_count[b] = total;
+        a.ngram_used[b] = tok_ok ? (total > 0 ? n : 0) : -1;
+    }
+}
+
+// ------------------------------------------------------------------- host
+static int64_t part_width(int64_t tok_stride, int S) {
+    const int64_t p = (tok_stride + S - 1) / S;
+    return (p + kLanePos - 1) / kLanePos * kLanePos;
 }
 
 static int check_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B,
@@ -267,11 +522,13 @@ static int check_draft(const int32_t *tokens, int64_t tok_stride, const int32_t 
     if (!tokens || !lens || !cand_pos || !cand_count || !ngram_used || !best_pos || !best_score ||
         !draft || !draft_len)
         return PLD_ERR_INVALID;
-    if (B < 1 || B > 65535 || tok_stride < 1 || tok_stride > kFindFusedMax) return PLD_ERR_INVALID;
+    if (B < 1 || B > 65535 || tok_stride < 1 || tok_stride > kMaxTokStride) return PLD_ERR_INVALID;
     if (ngram_min < 1 || ngram_max < ngram_min || ngram_max > PLD_MAX_NGRAM) return PLD_ERR_INVALID;
     if (cap < tok_stride || K < 1 || isnan(threshold)) return PLD_ERR_INVALID;
     if (S < 1 || S > PLD_MAX_DRAFT_SPLIT) return PLD_ERR_INVALID;
-    if (S > 1 && (!workspace || workspace_bytes < rank_ws_bytes(B))) return PLD_ERR_WORKSPACE;
+    if (S == 1 && tok_stride > kFindFusedMax) return PLD_ERR_INVALID;
+    if (S > 1 && part_width(tok_stride, S) > kPartMax) return PLD_ERR_INVALID;
+    if (S > 1 && (!workspace || workspace_bytes < part_ws_bytes(B, S))) return PLD_ERR_WORKSPACE;
     return PLD_OK;
 }
 
@@ -279,7 +536,7 @@ static DraftArgs make_draft(const int32_t *tokens, int64_t tok_stride, const int
                             int ngram_min, int ngram_max, float threshold, int K,
                             int32_t *cand_pos, int64_t cap, int32_t *cand_count,
                             int32_t *ngram_used, float *scores, int32_t *best_pos,
-                            float *best_score, int32_t *draft, int32_t *draft_len,
+                            float *best_score, int32_t *draft, int32_t *draft_len, int S,
                             void *workspace) {
     DraftArgs a{};
     a.tokens = tokens;
@@ -299,26 +556,37 @@ static DraftArgs make_draft(const int32_t *tokens, int64_t tok_stride, const int
     a.K = K;
     a.draft = draft;
     a.draft_len = draft_len;
-    a.keys = (uint64_t *)workspace;
+    a.S = S;
+    if (S > 1) {
+        a.P = part_width(tok_stride, S);
+        part_ws_layout(a, workspace);
+    }
     return a;
 }
 
-// One block of 16 waves when it owns its sequence; 4 waves when S blocks share
-// it (more blocks fit on a CU, and each scores a fraction of the list).
 template <bool kHidden>
-static void launch_draft(const DraftArgs &a, int S, hipStream_t s) {
+static void launch_draft(const DraftArgs &a, hipStream_t s) {
     const size_t lds = kHidden ? (size_t)(a.d / 8) * sizeof(uint4) : 0;
-    if (S == 1) {
-        hipLaunchKernelGGL((draft_kernel<kHidden, 16>), dim3(1, a.B), dim3(16 * kWave), lds, s, a);
-    } else {
-        hipLaunchKernelGGL((draft_kernel<kHidden, 4>), dim3(S, a.B), dim3(4 * kWave), lds, s, a);
-        hipLaunchKernelGGL(draft_finish_kernel, dim3((a.B + 3) / 4), dim3(256), 0, s, a);
+    if (a.S == 1) {
+        hipLaunchKernelGGL(draft_kernel<kHidden>, dim3(1, a.B), dim3(kFindWavesFused * kWave),
+                           lds, s, a);
+        return;
     }
+    if (a.nmin < a.nmax)
+        hipLaunchKernelGGL(draft_count_kernel, dim3(a.S, a.B), dim3(kPartWaves * kWave), 0, s, a);
+    hipLaunchKernelGGL(draft_part_kernel<kHidden>, dim3(a.S, a.B), dim3(kPartWaves * kWave),
+                       part_tok_bytes(a.P) + lds, s, a);
+    hipLaunchKernelGGL(draft_finish_part_kernel, dim3(a.B), dim3(kFinishThreads), 0, s, a);
 }
 
 }  // namespace pld
 
 using namespace pld;
+
+extern "C" size_t pld_draft_workspace_bytes(int B, int blocks_per_seq) {
+    if (B < 1 || B > 65535 || blocks_per_seq < 1 || blocks_per_seq > PLD_MAX_DRAFT_SPLIT) return 0;
+    return blocks_per_seq == 1 ? 0 : part_ws_bytes(B, blocks_per_seq);
+}
 
 extern "C" int pld_draft_hidden(const int32_t *tokens, int64_t tok_stride, const int32_t *lens,
                                 int B, int ngram_min, int ngram_max, const uint16_t *hidden,
@@ -337,13 +605,13 @@ extern "C" int pld_draft_hidden(const int32_t *tokens, int64_t tok_stride, const
     if (((uintptr_t)hidden & 15) || (h_row_stride % 8) || (h_seq_stride % 8)) return PLD_ERR_ALIGN;
     DraftArgs a = make_draft(tokens, tok_stride, lens, B, ngram_min, ngram_max, threshold, K,
                              cand_pos, cap, cand_count, ngram_used, scores, best_pos, best_score,
-                             draft, draft_len, workspace);
+                             draft, draft_len, blocks_per_seq, workspace);
     a.hidden = hidden;
     a.hs = h_seq_stride;
     a.hr = h_row_stride;
     a.n_rows = n_rows;
     a.d = d;
-    launch_draft<true>(a, blocks_per_seq, (hipStream_t)stream);
+    launch_draft<true>(a, (hipStream_t)stream);
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }
 
@@ -365,13 +633,13 @@ extern "C" int pld_draft_attn(const int32_t *tokens, int64_t tok_stride, const i
     if ((uintptr_t)attn & 3) return PLD_ERR_ALIGN;
     DraftArgs a = make_draft(tokens, tok_stride, lens, B, ngram_min, ngram_max, threshold, K,
                              cand_pos, cap, cand_count, ngram_used, scores, best_pos, best_score,
-                             draft, draft_len, workspace);
+                             draft, draft_len, blocks_per_seq, workspace);
     a.attn = attn;
     a.as = a_seq_stride;
     a.ar = a_row_stride;
     a.n_keys = n_keys;
     a.R = R;
     a.agg = agg;
-    launch_draft<false>(a, blocks_per_seq, (hipStream_t)stream);
+    launch_draft<false>(a, (hipStream_t)stream);
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }

@@ -7,25 +7,26 @@ Eq. 2 / Eq. 3, draft Sec. 4.3, greedy verification Sec. 4.4).
 """
 import torch
 
-from . import (DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, PLD_MAX_DRAFT_SPLIT, pld_draft_attn,
-               pld_draft_hidden,
+from . import (DRAFT_MAX_PART, DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, PLD_MAX_DRAFT_SPLIT,
+               pld_draft_attn, pld_draft_hidden, pld_draft_workspace_bytes,
                pld_emit_draft, pld_find_candidates, pld_find_scratch_bytes, pld_rank_attn,
                pld_rank_hidden, pld_score_attn, pld_score_hidden, pld_select_best,
                pld_verify_accept, pld_verify_argmax, pld_verify_greedy, pld_workspace_bytes)
 
 
 class DraftStep:
-    """mode: "split" runs the separate calls (find, rank, emit), "fused" the one-launch
-    drafting call (tok_stride <= 8192, one ranking), "auto" the one-launch call for
-    hidden-state ranking when it applies and the separate calls otherwise."""
+    """mode: "split" runs the separate calls (find, rank, emit), "fused" the one-call
+    drafting (one ranking artifact), "auto" the one-call drafting when there is one
+    ranking artifact and the separate calls otherwise.  draft_split is the one-call
+    drafting's blocks per sequence (1: one block owns a sequence, tok_stride <= 8192)."""
 
     def __init__(self, B, tok_stride, K, device="cuda", cap=None, keep_scores=False, mode="auto",
                  draft_split=1):
         if mode not in ("auto", "fused", "split"):
             raise ValueError(mode)
         self.B, self.tok_stride, self.K, self.mode = B, tok_stride, K, mode
-        self.draft_split = int(draft_split)
         cap = tok_stride if cap is None else cap
+        self.device = device
         i32 = dict(dtype=torch.int32, device=device)
         self.cand_pos = torch.full((B, cap), -1, **i32)
         self.cand_count = torch.zeros(B, **i32)
@@ -47,6 +48,25 @@ class DraftStep:
         nscratch = pld_find_scratch_bytes(B, tok_stride)
         self.scratch = (torch.empty(nscratch, dtype=torch.uint8, device=device)
                         if nscratch else None)
+        # the one-call drafting's own workspace (key slots left zero, counts rewritten)
+        self.draft_ws = None
+        self.set_split(max(int(draft_split), self.min_split()))
+
+    def min_split(self):
+        """The fewest blocks per sequence the one-call drafting accepts."""
+        if self.tok_stride <= DRAFT_MAX_TOK_STRIDE:
+            return 1
+        return max(2, -(-self.tok_stride // DRAFT_MAX_PART))
+
+    def set_split(self, S):
+        S = int(S)
+        if not self.min_split() <= S <= PLD_MAX_DRAFT_SPLIT:
+            raise ValueError(f"blocks per sequence {S} out of range")
+        self.draft_split = S
+        need = pld_draft_workspace_bytes(self.B, S) if S > 1 else 0
+        if need and (self.draft_ws is None or self.draft_ws.numel() < need):
+            self.draft_ws = torch.zeros(need, dtype=torch.uint8, device=self.device)
+        return S
 
     def find(self, tokens, lens, ngram_min=1, ngram_max=1, stream=None):
         pld_find_candidates(tokens, lens, ngram_min, ngram_max, self.cand_pos, self.cand_count,
@@ -96,21 +116,24 @@ class DraftStep:
     def uses_fused(self, hidden, attn):
         one = (hidden is None) != (attn is None)
         if self.mode == "fused":
-            if not one or self.tok_stride > DRAFT_MAX_TOK_STRIDE:
-                raise ValueError("the one-launch drafting call takes one artifact and "
-                                 "tok_stride <= 8192")
+            if not one:
+                raise ValueError("the one-call drafting takes one ranking artifact")
             return True
-        return self.mode == "auto" and one and self.tok_stride <= DRAFT_MAX_TOK_STRIDE
+        return self.mode == "auto" and one
 
     def tune_split(self, cand_count, hidden=True):
         """Blocks per sequence for the one-call drafting from observed candidate
-        counts (e.g. the previous step's): about four rows per block for hidden
-        states (one per wave), 32 candidates per block for attention gathers."""
+        counts (e.g. the previous step's).  Short contexts with short lists keep
+        one block per sequence (one launch); otherwise the positions are split so
+        that a block holds about 16 hidden-state rows or 32 attention gathers."""
         import math
-        per = 4 if hidden else 32
         mx = int(max(int(c) for c in cand_count)) if len(cand_count) else 0
-        self.draft_split = max(1, min(PLD_MAX_DRAFT_SPLIT, math.ceil(mx / per)))
-        return self.draft_split
+        small = 64 if hidden else 256
+        if self.tok_stride <= DRAFT_MAX_TOK_STRIDE and mx <= small:
+            return self.set_split(1)
+        per = 16 if hidden else 32
+        S = max(2, self.min_split(), math.ceil(mx / per))
+        return self.set_split(min(PLD_MAX_DRAFT_SPLIT, S))
 
     def draft_fused(self, tokens, lens, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
                     threshold=float("-inf"), stream=None):
@@ -119,14 +142,14 @@ class DraftStep:
             pld_draft_hidden(tokens, lens, ngram[0], ngram[1], hidden, self.K, self.cand_pos,
                              self.cand_count, self.ngram_used, self.best_pos, self.best_score,
                              self.draft, self.draft_len, threshold=threshold, scores=self.scores,
-                             blocks_per_seq=self.draft_split, workspace=self.workspace,
+                             blocks_per_seq=self.draft_split, workspace=self.draft_ws,
                              stream=stream)
         else:
             pld_draft_attn(tokens, lens, ngram[0], ngram[1], attn, self.K, self.cand_pos,
                            self.cand_count, self.ngram_used, self.best_pos, self.best_score,
                            self.draft, self.draft_len, agg=agg, threshold=threshold,
                            scores=self.scores_attn, blocks_per_seq=self.draft_split,
-                           workspace=self.workspace, stream=stream)
+                           workspace=self.draft_ws, stream=stream)
 
     def run(self, tokens, lens, logits, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
             threshold=float("-inf"), stream=None):
@@ -157,14 +180,14 @@ class DraftStep:
                                      self.cand_pos, self.cand_count, self.ngram_used,
                                      self.best_pos, self.best_score, self.draft, self.draft_len,
                                      threshold=threshold, scores=self.scores,
-                                     blocks_per_seq=self.draft_split, workspace=self.workspace,
+                                     blocks_per_seq=self.draft_split, workspace=self.draft_ws,
                                      **P)
             else:
                 d = pld_draft_attn(tokens, lens, ngram[0], ngram[1], attn, self.K, self.cand_pos,
                                    self.cand_count, self.ngram_used, self.best_pos,
                                    self.best_score, self.draft, self.draft_len, agg=agg,
                                    threshold=threshold, scores=self.scores_attn,
-                                   blocks_per_seq=self.draft_split, workspace=self.workspace,
+                                   blocks_per_seq=self.draft_split, workspace=self.draft_ws,
                                    **P)
             ops = [("draft", d)]
         else:

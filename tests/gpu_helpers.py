@@ -54,6 +54,17 @@ def workspace(B, K):
     return torch.zeros(pld.pld_workspace_bytes(B, K), dtype=torch.uint8, device=dev())
 
 
+def draft_workspace(B, S):
+    """The one-call drafting's workspace (None for one block per sequence)."""
+    n = pld.pld_draft_workspace_bytes(B, S)
+    return torch.zeros(n, dtype=torch.uint8, device=dev()) if n else None
+
+
+def draft_keys_zero(ws, B):
+    """The key slots (the first B*128 bytes) are left zero by every call."""
+    return ws is None or int(torch.count_nonzero(ws[:B * 128]).item()) == 0
+
+
 def scratch(B, tok_stride, fill=0x5A):
     """Find scratch, deliberately filled with garbage: its contents must not matter."""
     n = pld.pld_find_scratch_bytes(B, tok_stride)

@@ -3,7 +3,7 @@ arguments on the host (CPU only; no kernel is ever launched here).
 
 Every error-path call below carries at least one argument the host check
 rejects, so it returns before any HIP call.  Those calls use placeholder
-pointers, so they run only where no GPU is visible; on a GPU machine the same
+pointers, so they run only where no GPU is visible; on a machine with a GPU the same
 paths are exercised with real device buffers by the GPU tests.
 """
 import ctypes
@@ -71,6 +71,13 @@ def test_workspace_and_scratch_bytes():
     assert pld.pld_find_scratch_bytes(8, 8193) >= 8 * 5 * 8 * 4
     assert pld.pld_find_scratch_bytes(4, 131072) >= 4 * 64 * 8 * 4
     assert pld.pld_find_scratch_bytes(0, 9000) == 0
+    # one-call drafting: none for one block per sequence; key slots, per-block
+    # counts and per-block per-n counts for split positions
+    assert pld.pld_draft_workspace_bytes(8, 1) == 0
+    assert pld.pld_draft_workspace_bytes(8, 37) >= 8 * 16 * 8 + 8 * 37 * 4 + 8 * 37 * 8 * 4
+    assert pld.pld_draft_workspace_bytes(8, 1024) > pld.pld_draft_workspace_bytes(8, 37)
+    assert pld.pld_draft_workspace_bytes(8, 1025) == 0
+    assert pld.pld_draft_workspace_bytes(0, 4) == 0
 
 
 P = ctypes.c_void_p
@@ -133,3 +140,27 @@ def test_host_validation_error_codes():
     assert v(MIS, 0, 40, 10, 10, 3, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_AL  # fp32 alignment
     assert v(F, 0, 40, 10, 10, 3, F, F, 1, F, F, F, F, 8, NULL) == E_WS
     assert v(F, 0, 40, 10, 10, 3, F, F, 1, F, F, F, NULL, 1 << 20, NULL) == E_WS
+
+
+@pytest.mark.skipif(not _no_gpu(), reason="placeholder pointers are only used where no GPU is visible")
+def test_draft_host_validation():
+    """The one-call drafting's own checks: blocks per sequence, the slice
+    width for split positions, the context limit of one block per sequence,
+    and the workspace of split positions."""
+    lib = pld._load()
+    E_INV, E_WS = pld.PLD_ERR_INVALID, pld.PLD_ERR_WORKSPACE
+    d = lib.pld_draft_attn
+
+    def call(tok_stride, S, ws=F, ws_bytes=1 << 24, K=4, cap=None):
+        cap = tok_stride if cap is None else cap
+        return d(F, tok_stride, F, 2, 1, 1, F, 8 * tok_stride, tok_stride, tok_stride, 8, 0, INF,
+                 K, F, cap, F, F, NULL, F, F, F, F, S, ws, ws_bytes, NULL)
+
+    assert call(8193, 1) == E_INV                  # one block per sequence: <= 8192 tokens
+    assert call(20000, 2) == E_INV                 # slices of 10000 positions > 8192
+    assert call(100, 0) == E_INV
+    assert call(100, 1025) == E_INV
+    assert call(100, 3, ws=NULL, ws_bytes=0) == E_WS
+    assert call(20000, 3, ws_bytes=pld.pld_draft_workspace_bytes(2, 3) - 1) == E_WS
+    assert call(100, 3, K=0) == E_INV
+    assert call(100, 3, cap=99) == E_INV

@@ -16,14 +16,18 @@ import torch
 import oracle
 import synth
 from gpu_helpers import (check_best, check_find, check_scores, check_verify, d_bf16, d_f32,
-                         d_i32, gpu_emit, gpu_verify, say, sparse_hidden_rows)
+                         d_i32, draft_keys_zero, gpu_emit, gpu_verify, say, sparse_hidden_rows)
 from paper_2412_01447_amd.step import DraftStep
 
 pytestmark = pytest.mark.gpu
 
+# mode: "split" separate calls; "fused" the one-call drafting with blocks per sequence
+# from the candidate counts, as the benchmark tunes it; "fused1" one block per
+# sequence; "fused8" positions split over 8 blocks per sequence
 CASES = [(1, True, "fused"), (1, False, "split"), (2, True, "fused"), (2, False, "fused"),
-         (2, True, "split"), (3, True, "fused"), (3, False, "split"), (3, False, "fused"),
-         (3, False, "fused1"), (4, True, "split"), (5, True, "split"), (5, False, "split")]
+         (2, True, "split"), (2, True, "fused8"), (3, True, "fused"), (3, False, "split"),
+         (3, False, "fused"), (3, False, "fused1"), (4, True, "split"), (5, True, "split"),
+         (5, False, "split"), (5, True, "fused"), (5, False, "fused")]
 
 
 @pytest.mark.parametrize("cid,structured,mode", CASES,
@@ -55,6 +59,8 @@ def test_config_step_parity(cid, structured, mode):
                      mode="fused" if mode.startswith("fused") else mode)
     if mode == "fused":     # blocks per sequence from the candidate counts, as the bench does
         say("  blocks per sequence:", step.tune_split(cc, hidden=w["hidden"] is not None))
+    elif mode == "fused8":
+        step.set_split(8)
     zd = d_bf16(z) if bf16 else d_f32(z)
     attn_d = d_f32(w["attn"]) if w["attn"] is not None else None
     td, ld = d_i32(toks), d_i32(lens)
@@ -62,6 +68,7 @@ def test_config_step_parity(cid, structured, mode):
     torch.cuda.synchronize()
     g = step.host()
     assert int(torch.count_nonzero(step.workspace).item()) == 0
+    assert draft_keys_zero(step.draft_ws, cfg.B)
     check_find((g["cand_pos"], g["cand_count"], g["ngram_used"]), (cp, cc, nu), cfg.name)
     flips = 0
     if "h" in ref:

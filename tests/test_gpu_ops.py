@@ -15,6 +15,7 @@ import oracle
 import paper_2412_01447_amd as pld
 import synth
 from gpu_helpers import (check_best, check_find, check_scores, check_verify, d_bf16, d_f32,
+                         draft_keys_zero, draft_workspace,
                          d_i32, gpu_emit, gpu_find, gpu_rank_attn, gpu_rank_hidden, gpu_verify,
                          say, workspace)
 
@@ -102,7 +103,7 @@ def test_find_lane31_hits(stride):
     """Sparse hits at positions 31 mod 64 (plus lane 63 once): a 64-position
     ballot with bit 31 set and the upper half otherwise empty must not widen
     into the upper lanes.  Both the one-block path and the tiled path, and the
-    one-call drafting."""
+    one-call drafting with one block and with split positions."""
     say("find lane 31", stride)
     B = 2
     toks = (np.arange(B * stride, dtype=np.int64).reshape(B, stride) % 1000003 + 10).astype(np.int32)
@@ -115,16 +116,16 @@ def test_find_lane31_hits(stride):
     ref = oracle.find(toks, lens, 1, 1)
     assert ref[1][0] > 100
     check_find(gpu_find(toks, lens, 1, 1), ref, f"lane31 {stride}")
-    if stride <= pld.DRAFT_MAX_TOK_STRIDE:
+    if True:
         i32 = dict(dtype=torch.int32, device="cuda")
         K = 4
         A = synth.make_attn(B, 3, stride, lens, seed=5)
-        for split in (1, 5):
+        for split in ((1, 5) if stride <= pld.DRAFT_MAX_TOK_STRIDE else (3, 40)):
             o = [torch.full((B, stride), -1, **i32), torch.zeros(B, **i32), torch.zeros(B, **i32),
                  torch.zeros(B, **i32), torch.zeros(B, dtype=torch.float32, device="cuda"),
                  torch.zeros((B, K), **i32), torch.zeros(B, **i32)]
             pld.pld_draft_attn(d_i32(toks), d_i32(lens), 1, 1, d_f32(A), K, *o,
-                               blocks_per_seq=split, workspace=workspace(B, K))
+                               blocks_per_seq=split, workspace=draft_workspace(B, split))
             torch.cuda.synchronize()
             check_find((o[0].cpu().numpy(), o[1].cpu().numpy(), o[2].cpu().numpy()), ref,
                        f"lane31 draft split {split}")
@@ -397,23 +398,27 @@ def test_workspace_shared_across_calls_and_determinism():
             assert np.array_equal(x, y, equal_nan=True)
 
 
-# ------------------------------------------------------- one-launch drafting
+# ------------------------------------------------------- one-call drafting
 DRAFT_CASES = [
     # (B, tok_stride, V, n_min, n_max, d, R, K, seed)
     (9, 1, 3, 1, 1, 64, 0, 4, 0), (9, 50, 3, 1, 3, 64, 0, 4, 1), (12, 700, 6, 1, 4, 520, 0, 9, 2),
     (8, 4096, 40, 1, 3, 4096, 0, 10, 3), (5, 8192, 2, 2, 5, 128, 0, 16, 4),
     (9, 300, 4, 1, 2, 0, 7, 6, 5), (6, 8192, 20, 1, 1, 0, 40, 16, 6), (4, 5000, 1, 1, 3, 0, 3, 8, 7),
+    # long contexts (split positions only) and a stride that is not a multiple of 4
+    (3, 20000, 30, 1, 3, 256, 0, 8, 8), (3, 40000, 5, 1, 1, 0, 5, 8, 9),
+    (4, 20001, 3, 2, 4, 64, 0, 5, 10),
 ]
+DRAFT_SPLITS = [1, 3, 64, 1000]
 
 
-@pytest.mark.parametrize("split", [1, 3, 64])
+@pytest.mark.parametrize("split", DRAFT_SPLITS)
 @pytest.mark.parametrize("case", DRAFT_CASES, ids=[f"B{c[0]}_S{c[1]}_V{c[2]}_n{c[3]}-{c[4]}_"
                                                    f"{'d' + str(c[5]) if c[5] else 'R' + str(c[6])}"
                                                    for c in DRAFT_CASES])
 def test_draft_fused_parity(case, split):
     """The one-call drafting equals the oracle's find, rank and emit, and its
     scores are bit-identical to the separate ranking call, for any number of
-    blocks per sequence."""
+    blocks per sequence the call accepts (and an error for those it rejects)."""
     B, stride, V, nmin, nmax, d, R, K, seed = case
     say("draft fused", case, "split", split)
     rng = np.random.default_rng(100 + seed)
@@ -423,10 +428,12 @@ def test_draft_fused_parity(case, split):
     if B > 2:
         lens[1] = 0
         lens[2] = stride + 1
+    part = -(-(-(-stride // split)) // 8) * 8           # positions per block, split > 1
+    accepted = (stride <= pld.DRAFT_MAX_TOK_STRIDE) if split == 1 else part <= pld.DRAFT_MAX_PART
     ref_find = oracle.find(toks, lens, nmin, nmax)
     cp, cc, nu = ref_find
     i32 = dict(dtype=torch.int32, device="cuda")
-    ws = workspace(B, K)
+    ws = draft_workspace(B, split)
     o = dict(cand_pos=torch.full((B, stride), -1, **i32), cand_count=torch.zeros(B, **i32),
              ngram_used=torch.zeros(B, **i32), best_pos=torch.zeros(B, **i32),
              best_score=torch.zeros(B, dtype=torch.float32, device="cuda"),
@@ -436,23 +443,33 @@ def test_draft_fused_parity(case, split):
         if d:
             bits = synth.f32_to_bf16_bits(rng.standard_normal((B, stride, d)).astype(np.float32))
             hd = d_bf16(bits)
+            call = lambda: pld.pld_draft_hidden(
+                d_i32(toks), d_i32(lens), nmin, nmax, hd, K, o["cand_pos"], o["cand_count"],
+                o["ngram_used"], o["best_pos"], o["best_score"], o["draft"], o["draft_len"],
+                threshold=th, scores=o["scores"], blocks_per_seq=split, workspace=ws)
+            if not accepted:
+                with pytest.raises(pld.PLDError):
+                    call()
+                return
             ref = oracle.rank_hidden(bits, lens, cp, cc, threshold=th)
-            pld.pld_draft_hidden(d_i32(toks), d_i32(lens), nmin, nmax, hd, K, o["cand_pos"],
-                                 o["cand_count"], o["ngram_used"], o["best_pos"], o["best_score"],
-                                 o["draft"], o["draft_len"], threshold=th, scores=o["scores"],
-                                 blocks_per_seq=split, workspace=ws)
+            call()
             split_ref = gpu_rank_hidden(hd, lens, cp, cc, threshold=th)
         else:
             A = synth.make_attn(B, R, stride, lens, seed=seed)
+            call = lambda: pld.pld_draft_attn(
+                d_i32(toks), d_i32(lens), nmin, nmax, d_f32(A), K, o["cand_pos"], o["cand_count"],
+                o["ngram_used"], o["best_pos"], o["best_score"], o["draft"], o["draft_len"],
+                threshold=th, scores=o["scores"], blocks_per_seq=split, workspace=ws)
+            if not accepted:
+                with pytest.raises(pld.PLDError):
+                    call()
+                return
             ref = oracle.rank_attn(A, lens, cp, cc, oracle.AGG_SUM, threshold=th)
-            pld.pld_draft_attn(d_i32(toks), d_i32(lens), nmin, nmax, d_f32(A), K, o["cand_pos"],
-                               o["cand_count"], o["ngram_used"], o["best_pos"], o["best_score"],
-                               o["draft"], o["draft_len"], threshold=th, scores=o["scores"],
-                               blocks_per_seq=split, workspace=ws)
+            call()
             split_ref = gpu_rank_attn(d_f32(A), lens, cp, cc, pld.PLD_AGG_SUM, threshold=th)
         torch.cuda.synchronize()
         g = {k: v.cpu().numpy() for k, v in o.items()}
-        assert int(torch.count_nonzero(ws).item()) == 0
+        assert draft_keys_zero(ws, B)
         check_find((g["cand_pos"], g["cand_count"], g["ngram_used"]), ref_find, str(case))
         rsc, rbp, rbs = ref
         check_scores(g["scores"], rsc, cc, str(case))
