@@ -107,28 +107,75 @@ __device__ __forceinline__ uint32_t argmax_key_index(uint64_t k) {
 // ------------------------------------------------------- wave reductions
 __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-    lo = (uint32_t)__shfl_xor((int)lo, m);
-    hi = (uint32_t)__shfl_xor((int)hi, m);
-    return ((uint64_t)hi << 32) | lo;
+// Wave reductions use DPP lane moves -- quad permutes, the half-row and row
+// mirrors, and the row broadcasts of lanes 15 and 31 -- a few cycles each,
+// where a shuffle goes through the LDS crossbar.  The total lands in lane 63
+// and is read back as a scalar, so every lane gets the same bits, and the
+// association depends only on the lane layout, never on the data.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int dpp_move(int v) {   // lanes the move does not reach get 0
+    return __builtin_amdgcn_update_dpp(0, v, kCtrl, kRowMask, 0xf, false);
+}
+constexpr int kDppQuadSwap1 = 0xb1;   // quad_perm [1,0,3,2]
+constexpr int kDppQuadSwap2 = 0x4e;   // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+constexpr int kDppBcast15 = 0x142;    // lane 15 of a row into the next row (rows 1, 3)
+constexpr int kDppBcast31 = 0x143;    // lane 31 into rows 2 and 3
+constexpr int kDppShr1 = 0x111;       // row_shr:1 (+1, +3, +7 likewise)
+
+__device__ __forceinline__ int wave_sum_i32(int v) {
+    v += dpp_move<kDppQuadSwap1, 0xf>(v);
+    v += dpp_move<kDppQuadSwap2, 0xf>(v);
+    v += dpp_move<kDppHalfMirror, 0xf>(v);
+    v += dpp_move<kDppMirror, 0xf>(v);
+    v += dpp_move<kDppBcast15, 0xa>(v);
+    v += dpp_move<kDppBcast31, 0xc>(v);
+    return __builtin_amdgcn_readlane(v, 63);
+}
+
+__device__ __forceinline__ float wave_sum_f32(float v) {
+    v += __int_as_float(dpp_move<kDppQuadSwap1, 0xf>(__float_as_int(v)));
+    v += __int_as_float(dpp_move<kDppQuadSwap2, 0xf>(__float_as_int(v)));
+    v += __int_as_float(dpp_move<kDppHalfMirror, 0xf>(__float_as_int(v)));
+    v += __int_as_float(dpp_move<kDppMirror, 0xf>(__float_as_int(v)));
+    v += __int_as_float(dpp_move<kDppBcast15, 0xa>(__float_as_int(v)));
+    v += __int_as_float(dpp_move<kDppBcast31, 0xc>(__float_as_int(v)));
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint64_t dpp_max_step(uint64_t v) {
+    const uint32_t lo = (uint32_t)dpp_move<kCtrl, kRowMask>((int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)dpp_move<kCtrl, kRowMask>((int)(uint32_t)(v >> 32));
+    const uint64_t o = ((uint64_t)hi << 32) | lo;
+    return o > v ? o : v;
 }
 
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-        uint64_t o = shfl_xor_u64(v, m);
-        v = o > v ? o : v;
-    }
-    return v;
+    v = dpp_max_step<kDppQuadSwap1, 0xf>(v);
+    v = dpp_max_step<kDppQuadSwap2, 0xf>(v);
+    v = dpp_max_step<kDppHalfMirror, 0xf>(v);
+    v = dpp_max_step<kDppMirror, 0xf>(v);
+    v = dpp_max_step<kDppBcast15, 0xa>(v);
+    v = dpp_max_step<kDppBcast31, 0xc>(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+    return ((uint64_t)hi << 32) | lo;
 }
 
-// Butterfly sum: every lane ends with the same, bit-identical total, and the
-// association depends only on the lane layout, never on the data.
-__device__ __forceinline__ float wave_sum_f32(float v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-    return v;
+// Exclusive prefix sum over the lanes (shifts by 1, 2, 4, 8 within each row
+// of 16, then the row broadcasts); `total` gets the wave's sum.
+__device__ __forceinline__ int wave_excl_scan(int v, int &total) {
+    int x = v;
+    x += dpp_move<kDppShr1, 0xf>(x);
+    x += dpp_move<kDppShr1 + 1, 0xf>(x);
+    x += dpp_move<kDppShr1 + 3, 0xf>(x);
+    x += dpp_move<kDppShr1 + 7, 0xf>(x);
+    x += dpp_move<kDppBcast15, 0xa>(x);
+    x += dpp_move<kDppBcast31, 0xc>(x);
+    total = __builtin_amdgcn_readlane(x, 63);
+    return x - v;
 }
 
 __device__ __forceinline__ uint64_t lanemask_lt() {

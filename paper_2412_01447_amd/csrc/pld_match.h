@@ -112,25 +112,6 @@ __device__ __forceinline__ void count_levels(uint64_t hits, int nmax, int (&cnt)
         if (k < nmax) cnt[k] += __popc((uint32_t)(hits >> (8 * k)) & 0xffu);
 }
 
-__device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-    return v;
-}
-
-// Exclusive prefix sum over the lanes of the wave; `total` gets the sum.
-__device__ __forceinline__ int wave_excl_scan(int v, int &total) {
-    const int lane = lane_id();
-    int x = v;
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const int y = __shfl_up(x, d);
-        x += lane >= d ? y : 0;
-    }
-    total = __shfl(x, kWave - 1);
-    return x - v;
-}
-
 // Writes the positions base + j of the set bits j of `bits` to out[run ...]
 // (and out2[run ...] when given) in ascending order across the wave's lanes;
 // returns run plus the wave's number of bits.

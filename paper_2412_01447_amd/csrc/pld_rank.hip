@@ -88,14 +88,10 @@ __device__ void candidate_prefix(const RankCommon &c, uint32_t *pre) {
     const int b1 = min(b0 + per, c.B);
     uint32_t sum = 0;
     for (int b = b0; b < b1; ++b) sum += clamped_count(c, b);
-    // inclusive scan across the wave
-    uint32_t inc = sum;
+    // inclusive scan across the wave (two's-complement sums: same bits as unsigned)
+    int wt;
+    const uint32_t inc = (uint32_t)wave_excl_scan((int)sum, wt) + sum;
     const int lane = lane_id();
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const uint32_t v = (uint32_t)__shfl_up((int)inc, off);
-        if (lane >= off) inc += v;
-    }
     const int w = threadIdx.x / kWave;
     if (lane == kWave - 1) s_wave[w] = inc;
     __syncthreads();
