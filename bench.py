@@ -11,7 +11,7 @@ inputs exist in several copies at distinct addresses and consecutive steps
 rotate through them, so every step reads from HBM rather than from the 256 MB
 last-level cache.  W untimed steps run first, then exactly K steps are timed
 between two device synchronisations; HIP events on the launch stream time the
-dominant kernel inside that region.  One JSON line goes to stdout.
+dominant kernel inside that region, on every eighth step (--event-every).  One JSON line goes to stdout.
 
 The CPU oracle (test infrastructure) is timed on the host on the same inputs
 as a reported baseline, unless --no-cpu-baseline.
@@ -43,6 +43,8 @@ def parse():
                    help="CPU work the oracle baseline is given (whole steps, at least one)")
     p.add_argument("--copy-probe", action="store_true",
                    help="after the timed region, copy 1 GiB three times (counter calibration)")
+    p.add_argument("--event-every", type=int, default=8,
+                   help="bracket the dominant call with timing events on every N-th timed step")
     p.add_argument("--mode", choices=["auto", "fused", "split"], default="auto",
                    help="drafting: one-launch call (fused), separate calls (split), or auto")
     return p.parse_args()
@@ -218,7 +220,11 @@ def main():
                        attn=s_["attn"], ngram=cfg.ngram, stream=stream) for s_ in sets]
     names = [n for n, _ in plans[0]]
     assert set(names) == set(nbytes), (names, list(nbytes))
-    ev = TimingEvents(args.steps)
+    # the dominant call is bracketed by events on every `event_every`-th timed
+    # step: an event pair adds its own dispatches to the step, so sampling keeps
+    # the step time close to the unbracketed one
+    timed = [k for k in range(args.steps) if k % args.event_every == 0]
+    ev = TimingEvents(len(timed))
 
     for k in range(args.warmup):
         for _, call in plans[k % copies]:
@@ -226,17 +232,18 @@ def main():
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for k in range(args.steps):
+        e = k // args.event_every if k % args.event_every == 0 else -1
         for name, call in plans[k % copies]:
-            if name == dominant:
-                ev.record(2 * k, stream)
+            if name == dominant and e >= 0:
+                ev.record(2 * e, stream)
                 call()
-                ev.record(2 * k + 1, stream)
+                ev.record(2 * e + 1, stream)
             else:
                 call()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ms_per_step = elapsed * 1e3 / args.steps
-    dom_ms = sum(ev.elapsed_ms(2 * k, 2 * k + 1) for k in range(args.steps)) / args.steps
+    dom_ms = sum(ev.elapsed_ms(2 * e, 2 * e + 1) for e in range(len(timed))) / len(timed)
     ev.close()
 
     roofline = None
@@ -246,7 +253,7 @@ def main():
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                     "traffic": measured_traffic(cfg.name, dominant),
                     "bytes_per_launch": nbytes[dominant],
-                    "avg_us": round(dom_ms * 1e3, 2)}
+                    "avg_us": round(dom_ms * 1e3, 2), "launches_timed": len(timed)}
         log(f"[bench] {dominant}: {dom_ms * 1e3:.2f} us avg, {achieved:.1f} GB/s")
 
     if args.copy_probe:
