@@ -75,6 +75,9 @@ __device__ __forceinline__ uint32_t clamp8(int64_t v) {
 // p - i >= 0 with p <= T-2 implies T-1-i >= 1, so q.v[i] is a real token.
 __device__ __forceinline__ uint64_t lane_hits(const int32_t *s, int64_t s0, int64_t T,
                                               int64_t base, const Query &q, int nmax) {
+    // a wave whose first position is past T-2 has nothing to compare (the
+    // lanes' bases grow with the lane, so this is the same test for all)
+    if (base - (int64_t)kLanePos * lane_id() > T - 2) return 0ull;
     const int i0 = (int)(base - s0) - 8;
     int32_t w[16];
 #pragma unroll
@@ -117,6 +120,7 @@ __device__ __forceinline__ void count_levels(uint64_t hits, int nmax, int (&cnt)
 // returns run plus the wave's number of bits.
 __device__ __forceinline__ int64_t emit_bits(uint32_t bits, int64_t base, int32_t *out,
                                              int32_t *out2, int64_t run) {
+    if (__ballot(bits != 0u) == 0ull) return run;   // nothing in this wave
     int total;
     int64_t o = run + wave_excl_scan(__popc(bits), total);
     while (bits) {

@@ -182,36 +182,29 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArg
 
 // One wave per sequence, one lane per row: y_i from the row keys, the first
 // mismatch by a ballot, the emitted tokens; the keys are returned to zero.
+// The length, the keys and the draft are requested together (every slot and
+// draft entry exists whatever the length; the argmax never writes a slot past
+// the draft, so those are zero already and zeroing all K+1 is the same).
 __global__ __launch_bounds__(256) void verify_accept_kernel(VerifyArgs a) {
     const int b = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave);
     const int lane = lane_id();
     if (b >= a.B) return;   // wave-uniform
     const int K = a.K;
-    const int L = a.draft_len[b];
-    int32_t *out = a.out_tokens + (int64_t)b * (K + 1);
-    if (L < 0 || L > K) {
-        for (int r = lane; r <= K; r += kWave) out[r] = -1;
-        if (lane == 0) {
-            a.accept_len[b] = -1;
-            a.out_count[b] = 0;
-        }
-        return;
-    }
     uint64_t *slot = a.keys + (int64_t)b * (K + 1);
     const int32_t *dr = a.draft + (int64_t)b * K;
-    int acc = L;           // accepted length: first mismatch, else L
-    int32_t y_acc = -1;    // the model's token at position acc
-    bool found = false;
-    for (int base = 0; base <= L; base += kWave) {
+    int32_t *out = a.out_tokens + (int64_t)b * (K + 1);
+    const int L = a.draft_len[b];
+    const bool ok = (L >= 0 && L <= K);   // wave-uniform
+    int acc = ok ? L : -1;  // accepted length: first mismatch, else L
+    int32_t y_acc = -1;     // the model's token at position acc
+    bool found = !ok;
+    for (int base = 0; base <= K; base += kWave) {
         const int r = base + lane;
-        int32_t y = -1;
-        bool mism = false;
-        if (r <= L) {
-            const uint64_t k = slot[r];
-            slot[r] = 0;
-            y = (int32_t)argmax_key_index(k);
-            mism = (r < L) && (y != dr[r]);
-        }
+        const uint64_t k = (r <= K) ? slot[r] : 0ull;
+        const int32_t d = (r < K) ? dr[r] : -1;
+        if (r <= K) slot[r] = 0;
+        const int32_t y = (int32_t)argmax_key_index(k);
+        const bool mism = !found && (r < L) && (y != d);
         const uint64_t mk = __ballot(mism);
         if (!found && mk) {
             const int f = __ffsll((unsigned long long)mk) - 1;
@@ -221,10 +214,11 @@ __global__ __launch_bounds__(256) void verify_accept_kernel(VerifyArgs a) {
         }
         if (!found && L >= base && L < base + kWave) y_acc = __shfl(y, L - base);
     }
-    for (int r = lane; r <= K; r += kWave) out[r] = r < acc ? dr[r] : (r == acc ? y_acc : -1);
+    for (int r = lane; r <= K; r += kWave)
+        out[r] = !ok ? -1 : (r < acc ? dr[r] : (r == acc ? y_acc : -1));
     if (lane == 0) {
         a.accept_len[b] = acc;
-        a.out_count[b] = acc + 1;
+        a.out_count[b] = ok ? acc + 1 : 0;
     }
 }
 
