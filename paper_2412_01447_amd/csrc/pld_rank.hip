@@ -74,20 +74,24 @@ struct RankAttnArgs {
 
 // pre[b] = number of candidates before sequence b; pre[B] = total.  Counts
 // outside [0, cap] count as 0.  Block-wide: each thread sums a contiguous run
-// of sequences; the thread sums are scanned with wave shuffles and one LDS
-// exchange of the wave totals.
+// of sequences; the thread sums are scanned across the wave (DPP) and with one
+// LDS exchange of the wave totals.  With s_lens, the lengths are copied to
+// LDS in the same pass.
 __device__ __forceinline__ uint32_t clamped_count(const RankCommon &c, int b) {
     const int32_t n = c.cand_count[b];
     return (n >= 0 && (int64_t)n <= c.cap) ? (uint32_t)n : 0u;
 }
 
-__device__ void candidate_prefix(const RankCommon &c, uint32_t *pre) {
+__device__ void candidate_prefix(const RankCommon &c, uint32_t *pre, int32_t *s_lens = nullptr) {
     __shared__ uint32_t s_wave[kRankWaves];
     const int per = (c.B + kRankThreads - 1) / kRankThreads;
     const int b0 = threadIdx.x * per;
     const int b1 = min(b0 + per, c.B);
     uint32_t sum = 0;
-    for (int b = b0; b < b1; ++b) sum += clamped_count(c, b);
+    for (int b = b0; b < b1; ++b) {
+        sum += clamped_count(c, b);
+        if (s_lens) s_lens[b] = c.lens[b];   // (requested with the count)
+    }
     // inclusive scan across the wave (two's-complement sums: same bits as unsigned)
     int wt;
     const uint32_t inc = (uint32_t)wave_excl_scan((int)sum, wt) + sum;
@@ -152,12 +156,13 @@ __global__ __launch_bounds__(256) void rank_finish_kernel(RankCommon c) {
 // ---------------------------------------------------------------- hidden
 // Scores the rows i = first, first + kRankWaves, ... < end of sequence b (one
 // wave's share of a segment).  The wave fetches the candidate positions of up
-// to 64 rows with one load, then scores G rows at a time with all their loads
-// in flight.  `best` collects the wave's best key.
+// to 64 rows with one load (the first batch, jv0, comes in prefetched), then
+// scores G rows at a time with all their loads in flight.  `best` collects the
+// wave's best key.
 template <int G>
 __device__ void score_rows(const RankHiddenArgs &a, int b, int64_t T, bool seq_ok,
                            const uint16_t *Hb, const uint4 *q_s, float qq, uint32_t first,
-                           uint32_t end, uint32_t seq_start, uint64_t &best) {
+                           uint32_t end, uint32_t seq_start, int32_t jv0, uint64_t &best) {
     const RankCommon &c = a.c;
     const int lane = lane_id();
     const int nch = a.d / 8;
@@ -165,8 +170,8 @@ __device__ void score_rows(const RankHiddenArgs &a, int b, int64_t T, bool seq_o
     for (uint32_t base = 0; base < n; base += kWave) {
         const uint32_t nb = min((uint32_t)kWave, n - base);
         const uint32_t mine = base + lane;
-        int32_t jv = 0;
-        if (mine < n)
+        int32_t jv = jv0;   // the first batch was requested with the query row
+        if (base > 0 && mine < n)
             jv = c.cand_pos[(int64_t)b * c.cap + (first + mine * kRankWaves - seq_start)];
         for (uint32_t r = 0; r < nb; r += G) {
             const uint4 *rows[G];
@@ -210,7 +215,8 @@ __global__ __launch_bounds__(kRankThreads) void rank_hidden_kernel(RankHiddenArg
     const int nch = a.d / 8;
     uint4 *q_s = smem;                                         // nch chunks of 8 bf16
     uint32_t *pre = reinterpret_cast<uint32_t *>(smem + nch);  // B + 1
-    candidate_prefix(c, pre);
+    int32_t *lens = reinterpret_cast<int32_t *>(pre + c.B + 1); // B
+    candidate_prefix(c, pre, lens);
     uint32_t lo0, hi;
     block_share(pre[c.B], lo0, hi);
     const int w = threadIdx.x / kWave;
@@ -221,23 +227,26 @@ __global__ __launch_bounds__(kRankThreads) void rank_hidden_kernel(RankHiddenArg
     while (lo < hi) {
         while (pre[b + 1] <= lo) ++b;                          // skip empty sequences
         const uint32_t seg_hi = min(hi, pre[b + 1]);
-        const int64_t T = c.lens[b];
+        const int64_t T = lens[b];
         const bool seq_ok = (T >= 2 && T - 2 < a.n_rows);
         const uint16_t *Hb = a.hidden + (int64_t)b * a.hs;
-        if (seq_ok) {
-            const uint4 *qg = reinterpret_cast<const uint4 *>(Hb + (T - 2) * a.hr);
-            for (int i = threadIdx.x; i < nch; i += kRankThreads) q_s[i] = qg[i];
-        }
+        // the wave's first 64 candidate positions and the query row travel together
+        const uint32_t first = lo + w;
+        const uint32_t nw = seg_hi > first ? (seg_hi - first + kRankWaves - 1) / kRankWaves : 0;
+        const int32_t jv0 = (uint32_t)lane < nw
+            ? c.cand_pos[(int64_t)b * c.cap + (first + (uint32_t)lane * kRankWaves - pre[b])] : 0;
+        if (seq_ok) copy_to_lds(reinterpret_cast<const uint4 *>(Hb + (T - 2) * a.hr), q_s, nch);
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         float qdot = 0.f, qq = 0.f;
         if (seq_ok) row_dot<false>(q_s, q_s, nch, qdot, qq);
         uint64_t best = 0;
         if (nch <= 4 * kWave)
-            score_rows<4>(a, b, T, seq_ok, Hb, q_s, qq, lo + w, seg_hi, pre[b], best);
+            score_rows<4>(a, b, T, seq_ok, Hb, q_s, qq, first, seg_hi, pre[b], jv0, best);
         else if (nch <= 8 * kWave)
-            score_rows<2>(a, b, T, seq_ok, Hb, q_s, qq, lo + w, seg_hi, pre[b], best);
+            score_rows<2>(a, b, T, seq_ok, Hb, q_s, qq, first, seg_hi, pre[b], jv0, best);
         else
-            score_rows<1>(a, b, T, seq_ok, Hb, q_s, qq, lo + w, seg_hi, pre[b], best);
+            score_rows<1>(a, b, T, seq_ok, Hb, q_s, qq, first, seg_hi, pre[b], jv0, best);
         if (lane == 0) s_best[w] = best;
         __syncthreads();                                       // also: q_s is restaged next
         if (threadIdx.x == 0) {
@@ -356,7 +365,7 @@ static int prep_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stri
 // The ranking grids are persistent: as many blocks as fit on the device at
 // once, each taking an equal contiguous share of the flattened candidates.
 static void launch_hidden(const RankHiddenArgs &a, hipStream_t s) {
-    const size_t lds = (size_t)(a.d / 8) * sizeof(uint4) + (size_t)(a.c.B + 1) * sizeof(uint32_t);
+    const size_t lds = (size_t)(a.d / 8) * sizeof(uint4) + (size_t)(2 * a.c.B + 1) * sizeof(uint32_t);
     const int grid = resident_blocks(reinterpret_cast<const void *>(&rank_hidden_kernel),
                                      kRankThreads, lds) * PLD_RANK_OVERSUB;
     hipLaunchKernelGGL(rank_hidden_kernel, dim3(grid), dim3(kRankThreads), lds, s, a);
