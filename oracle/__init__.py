@@ -60,8 +60,10 @@ def load_library(path):
     lib.pld_ref_emit.argtypes = [_vp, _i64, _vp, _vp, _int, _int, _vp, _vp]
     lib.pld_ref_verify.argtypes = [_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int, _vp, _vp,
                                    _vp, _vp]
+    lib.pld_ref_verify_sample.argtypes = [_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int,
+                                          ctypes.c_double, _vp, _i64, _vp, _vp, _vp, _vp]
     for f in (lib.pld_ref_find, lib.pld_ref_rank_hidden, lib.pld_ref_rank_attn,
-              lib.pld_ref_emit, lib.pld_ref_verify):
+              lib.pld_ref_emit, lib.pld_ref_verify, lib.pld_ref_verify_sample):
         f.restype = _int
     return lib
 
@@ -176,6 +178,34 @@ def verify(logits, draft, draft_len, bf16=False):
                                 _p(draft_len), B, _p(acc), _p(out), _p(cnt), _p(rowarg))
     _check(rc, "verify")
     return acc, out, cnt, rowarg
+
+
+def verify_sample(logits, draft, draft_len, temperature, uniforms, bf16=False):
+    """Sampling verification (Sec. 4.4 with a temperature; Sec. 5 samples at T = 1).
+
+    Row i's token is the inverse CDF of softmax(Z[b][i] / temperature) at the
+    caller's uniform draw uniforms[b][i] in [0, 1); acceptance keeps the draft
+    up to the first mismatch with these samples.
+    logits: float32 [B, K+1, V], or uint16 bf16 bits when ``bf16``; uniforms:
+    float32 [B, K+1].  Returns (accept_len [B], out_tokens [B, K+1],
+    out_count [B], row_sample [B, K+1]).
+    """
+    z = _c(logits, np.uint16 if bf16 else np.float32)
+    B, K1, V = z.shape
+    K = K1 - 1
+    draft = _c(draft, np.int32)
+    draft_len = _c(draft_len, np.int32)
+    u = _c(uniforms, np.float32)
+    assert draft.shape == (B, K) and u.shape == (B, K1)
+    acc = np.zeros(B, np.int32)
+    out = np.zeros((B, K1), np.int32)
+    cnt = np.zeros(B, np.int32)
+    rows = np.zeros((B, K1), np.int32)
+    rc = _load().pld_ref_verify_sample(_p(z), DT_BF16 if bf16 else DT_F32, K1 * V, V, V, K,
+                                       _p(draft), _p(draft_len), B, float(temperature), _p(u), K1,
+                                       _p(acc), _p(out), _p(cnt), _p(rows))
+    _check(rc, "verify_sample")
+    return acc, out, cnt, rows
 
 
 def step_hidden(tokens, lens, hidden_bits, logits, K, ngram_min=1, ngram_max=1,

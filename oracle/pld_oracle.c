@@ -36,6 +36,7 @@
  * force on tiny inputs, library reductions, closed forms and invariants).
  */
 #include <math.h>
+#include <stdlib.h>
 #include <stddef.h>
 #include <stdint.h>
 #include <string.h>
@@ -264,6 +265,24 @@ int pld_ref_emit(const int32_t *tokens, int64_t tok_stride, const int32_t *lens,
 }
 
 /* --------------------------------------------------------------- verify */
+/* The acceptance rule shared by both verifications (Sec. 4.4): a = the first
+ * i < L whose model token y[i] differs from draft[i], else L; the step emits
+ * draft[0..a-1] followed by y[a] (count a + 1). */
+static void accept_prefix(const int *y, const int32_t *draft, int L, int32_t *out,
+                          int32_t *accept_len, int32_t *out_count) {
+    int a = L;
+    for (int i = 0; i < L; ++i) {
+        if (y[i] != draft[i]) {
+            a = i;
+            break;
+        }
+    }
+    for (int i = 0; i < a; ++i) out[i] = draft[i];
+    out[a] = y[a];
+    *accept_len = a;
+    *out_count = a + 1;
+}
+
 /*
  * Greedy verification (Sec. 3 "greedy acceptance"; Sec. 4.4): one forward
  * pass gives K+1 distributions; at temperature 0 the model's token at
@@ -313,17 +332,83 @@ int pld_ref_verify(const void *logits, int dtype, int64_t l_seq_stride, int64_t 
             y[i] = arg;
             if (row_argmax) row_argmax[(int64_t)b * (K + 1) + i] = arg;
         }
-        int a = L;
-        for (int i = 0; i < L; ++i) {
-            if (y[i] != draft[(int64_t)b * K + i]) {
-                a = i;
-                break;
-            }
-        }
-        for (int i = 0; i < a; ++i) out[i] = draft[(int64_t)b * K + i];
-        out[a] = y[a];
-        accept_len[b] = a;
-        out_count[b] = a + 1;
+        accept_prefix(y, draft + (int64_t)b * K, L, out, &accept_len[b], &out_count[b]);
     }
+    return REF_OK;
+}
+
+/* Sampling verification (Sec. 4.4: sample a token at every draft position
+ * from the target model's distribution and keep the draft up to the first
+ * mismatch; Sec. 5 runs it at temperature 1).  For the rows i = 0..L of
+ * sequence b, with z = Z[b][i] and tau = temperature:
+ *     p_v = exp((z_v - max_w z_w) / tau),  S = sum_v p_v,  t = u[b][i] * S,
+ *     y_i = the smallest v with p_0 + ... + p_v > t
+ * (the inverse CDF of softmax(z / tau) at the caller's uniform draw u; if
+ * rounding leaves no such v, the last v with p_v > 0).  A row whose entries
+ * are all -inf has no mass: y_i = 0.  u outside [0, 1) is clamped to it.
+ * Acceptance is the greedy rule on these samples: a = the first i < L with
+ * y_i != draft[i], else L; the step emits draft[0..a-1] followed by y_a.  */
+int pld_ref_verify_sample(const void *logits, int dtype, int64_t l_seq_stride,
+                          int64_t l_row_stride, int V, int K, const int32_t *draft,
+                          const int32_t *draft_len, int B, double temperature,
+                          const float *uniforms, int64_t u_stride, int32_t *accept_len,
+                          int32_t *out_tokens, int32_t *out_count, int32_t *row_sample) {
+    if (!logits || !draft || !draft_len || !uniforms || !accept_len || !out_tokens || !out_count)
+        return REF_ERR;
+    if (B < 0 || K < 1 || V < 1 || (dtype != 0 && dtype != 1)) return REF_ERR;
+    if (!(temperature > 0.0) || isinf(temperature) || u_stride < K + 1) return REF_ERR;
+    double *p = (double *)malloc(sizeof(double) * (size_t)V);
+    if (!p) return REF_ERR;
+    for (int b = 0; b < B; ++b) {
+        int L = draft_len[b];
+        int32_t *out = out_tokens + (int64_t)b * (K + 1);
+        for (int i = 0; i <= K; ++i) {
+            out[i] = -1;
+            if (row_sample) row_sample[(int64_t)b * (K + 1) + i] = -1;
+        }
+        if (L < 0 || L > K) {
+            accept_len[b] = -1;
+            out_count[b] = 0;
+            continue;
+        }
+        int y[K + 1];
+        for (int i = 0; i <= L; ++i) {
+            int64_t base = (int64_t)b * l_seq_stride + (int64_t)i * l_row_stride;
+            double m = -INFINITY;
+            for (int v = 0; v < V; ++v) {
+                double z = (dtype == 0) ? (double)((const float *)logits)[base + v]
+                                        : bf16_to_double(((const uint16_t *)logits)[base + v]);
+                p[v] = z;
+                if (z > m) m = z;
+            }
+            int pick = 0;
+            if (m > -INFINITY) {
+                double S = 0.0;
+                for (int v = 0; v < V; ++v) {
+                    p[v] = exp((p[v] - m) / temperature);
+                    S += p[v];
+                }
+                double u = (double)uniforms[(int64_t)b * u_stride + i];
+                if (!(u >= 0.0)) u = 0.0;
+                if (u >= 1.0) u = nextafter(1.0, 0.0);
+                double t = u * S, c = 0.0;
+                int last = 0, found = 0;
+                for (int v = 0; v < V; ++v) {
+                    if (p[v] > 0.0) last = v;
+                    c += p[v];
+                    if (c > t) {
+                        pick = v;
+                        found = 1;
+                        break;
+                    }
+                }
+                if (!found) pick = last;
+            }
+            y[i] = pick;
+            if (row_sample) row_sample[(int64_t)b * (K + 1) + i] = pick;
+        }
+        accept_prefix(y, draft + (int64_t)b * K, L, out, &accept_len[b], &out_count[b]);
+    }
+    free(p);
     return REF_OK;
 }

@@ -63,3 +63,30 @@ def verify(Z, draft):
     while a < L and y[a] == draft[a]:
         a += 1
     return a, list(draft[:a]) + [y[a]], y
+
+
+def sample_row(z, temperature, u):
+    """Inverse CDF of softmax(z / temperature) at u, with numpy's cumsum and
+    searchsorted (the first index whose cumulative mass exceeds u * total)."""
+    z = np.asarray(z, np.float64)
+    m = z.max()
+    if m == -np.inf:
+        return 0
+    p = np.exp((z - m) / temperature)
+    c = np.cumsum(p)
+    u = min(max(float(u), 0.0), float(np.nextafter(1.0, 0.0)))
+    v = int(np.searchsorted(c, u * c[-1], side="right"))
+    if v >= len(z):
+        v = int(np.flatnonzero(p > 0)[-1])
+    return v
+
+
+def verify_sample(Z, draft, temperature, u):
+    """Sampling verification: the sampled token of every row, then the prefix
+    of the draft that agrees with them."""
+    L = len(draft)
+    y = [sample_row(Z[i], temperature, u[i]) for i in range(L + 1)]
+    a = 0
+    while a < L and y[a] == draft[a]:
+        a += 1
+    return a, list(draft[:a]) + [y[a]], y

@@ -9,6 +9,8 @@ pass on the unmodified source.  CPU only; the mistakes live in the oracle.
 import os
 import subprocess
 
+import math
+
 import numpy as np
 import pytest
 
@@ -33,8 +35,14 @@ MUTANTS = {
     "draft truncation off by one": ("L = T - 1 - j;", "L = T - j;"),
     "attention key j instead of j-1": ("a_row_stride + (j - 1)];", "a_row_stride + j];"),
     "norm without the square": ("hh += hv * hv;", "hh += hv;"),
-    "accept counts one past the mismatch": ("a = i;\n                break;", "a = i + 1;\n                break;"),
+    "accept counts one past the mismatch": ("a = i;\n            break;", "a = i + 1;\n            break;"),
     "threshold taken as >=": ("!(v > threshold)", "!(v >= threshold)"),
+    "sample boundary taken as >=": ("if (c > t) {", "if (c >= t) {"),
+    "sampling temperature ignored": ("p[v] = exp((p[v] - m) / temperature);",
+                                     "p[v] = exp(p[v] - m);"),
+    "sampling uses the previous row's uniform": (
+        "double u = (double)uniforms[(int64_t)b * u_stride + i];",
+        "double u = (double)uniforms[(int64_t)b * u_stride + (i > 0 ? i - 1 : 0)];"),
 }
 
 
@@ -93,6 +101,32 @@ def _pins_pass():
                                         threshold=float(bs[0]))
         if bp[0] != -1:
             return False
+        # sampling verification: closed forms, the strict boundary, brute force
+        for a_, b_, tau in ((3.0, 1.0, 1.0), (3.0, 1.0, 0.5)):
+            z = np.array([[[math.log(a_), math.log(b_)], [0.0, 0.0]]], np.float32)
+            p0 = a_ ** (1 / tau) / (a_ ** (1 / tau) + b_ ** (1 / tau))
+            for u, want in ((p0 * 0.999, 0), (p0 * 1.001, 1)):
+                _, _, _, rows = oracle.verify_sample(z, np.full((1, 1), -1, np.int32),
+                                                     np.array([0], np.int32), tau,
+                                                     np.array([[u, 0.0]], np.float32))
+                if rows[0, 0] != want:
+                    return False
+        _, _, _, rows = oracle.verify_sample(np.zeros((1, 2, 2), np.float32),
+                                             np.full((1, 1), -1, np.int32),
+                                             np.array([0], np.int32), 1.0,
+                                             np.array([[0.5, 0.0]], np.float32))
+        if rows[0, 0] != 1:
+            return False
+        for _ in range(40):
+            K, V = 3, 5
+            Zs = rng.standard_normal((K + 1, V)).astype(np.float32)
+            us = rng.random(K + 1).astype(np.float32)
+            dr = rng.integers(0, V, K).astype(np.int32)
+            acc, out, cnt, rows = oracle.verify_sample(Zs[None], dr[None],
+                                                       np.array([K], np.int32), 1.0, us[None])
+            a_, toks, y = brute.verify_sample(Zs, list(dr), 1.0, us)
+            if list(rows[0]) != y or acc[0] != a_:
+                return False
         return True
     except Exception:
         return False

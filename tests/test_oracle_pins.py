@@ -343,3 +343,104 @@ def test_structured_step_finds_planted_source():
     dr, dl = oracle.emit(toks, lens, bp, cfg.K)
     want, wn = synth.intended_drafts(metas, cfg.K)
     assert np.array_equal(dr, want) and np.array_equal(dl, wn)
+
+
+# ------------------------------------------------------- sampling verification
+def _sample1(z, tau, u):
+    """One row through a K = 1 call with an empty draft (L = 0): row 0 is sampled."""
+    Z = np.stack([np.asarray(z, np.float32), np.zeros(len(z), np.float32)])[None]
+    acc, out, cnt, rows = oracle.verify_sample(Z, np.full((1, 1), -1, np.int32),
+                                               np.array([0], np.int32), tau,
+                                               np.array([[u, 0.0]], np.float32))
+    assert acc[0] == 0 and cnt[0] == 1 and out[0, 0] == rows[0, 0]
+    return int(rows[0, 0])
+
+
+def test_sample_two_tokens_closed_form():
+    """softmax of [log a, log b] / tau puts a^(1/tau) / (a^(1/tau) + b^(1/tau)) on token 0."""
+    for a, b, tau in ((3.0, 1.0, 1.0), (1.0, 4.0, 1.0), (3.0, 1.0, 0.5), (2.0, 5.0, 2.0)):
+        z = [math.log(a), math.log(b)]
+        p0 = a ** (1 / tau) / (a ** (1 / tau) + b ** (1 / tau))
+        assert _sample1(z, tau, p0 * 0.999) == 0
+        assert _sample1(z, tau, min(p0 * 1.001, 0.9999)) == 1
+
+
+def test_sample_exact_boundary_and_zero_mass():
+    """The cumulative mass must exceed u * S strictly; tokens without mass are
+    never drawn; u is clamped to [0, 1); a row with no mass gives token 0."""
+    assert _sample1([0.0, 0.0], 1.0, 0.5) == 1               # t lands exactly on the boundary
+    assert _sample1([0.0, 0.0, 0.0, 0.0], 1.0, 0.25) == 1
+    z = [-math.inf, 0.0, -math.inf, 0.0, -math.inf]
+    assert _sample1(z, 1.0, 0.0) == 1
+    assert _sample1(z, 1.0, 0.4999) == 1
+    assert _sample1(z, 1.0, 0.5) == 3
+    assert _sample1(z, 1.0, 0.9999) == 3
+    assert _sample1(z, 1.0, 1.5) == 3                        # clamped below 1
+    assert _sample1(z, 1.0, -0.3) == 1                       # clamped to 0
+    assert _sample1([-math.inf] * 4, 1.0, 0.7) == 0
+
+
+def test_sample_small_temperature_is_argmax():
+    """As tau -> 0 the distribution concentrates on the first maximum."""
+    z = [0.3, 1.7, -0.4, 1.6, 1.7]
+    for u in (0.0, 0.3, 0.49, 0.999):
+        assert _sample1(z, 1e-3, u) in (1, 4)
+    assert _sample1(z, 1e-3, 0.0) == 1 and _sample1(z, 1e-3, 0.3) == 1
+    assert _sample1(z, 1e-3, 0.999) == 4                     # the two maxima share the mass
+
+
+def test_sample_distribution_matches_softmax():
+    """The inverse CDF maps uniform draws to softmax(z / tau): token frequencies
+    over a regular grid of u equal the probabilities to within the grid step."""
+    z = np.array([0.2, -1.0, 1.5, 0.0, 0.7, -3.0], np.float32)
+    for tau in (1.0, 0.6):
+        p = np.exp((z.astype(np.float64) - z.max()) / tau)
+        p /= p.sum()
+        n = 4000
+        grid = (np.arange(n) + 0.5) / n
+        Z = np.broadcast_to(z, (n, 2, 6)).copy()
+        U = np.stack([grid, np.zeros(n)], axis=1).astype(np.float32)
+        acc, out, cnt, rows = oracle.verify_sample(Z, np.full((n, 1), -1, np.int32),
+                                                   np.zeros(n, np.int32), tau, U)
+        freq = np.bincount(rows[:, 0], minlength=6) / n
+        assert np.allclose(freq, p, atol=1.5 / n)
+
+
+@settings(max_examples=300, deadline=None)
+@given(st.integers(1, 6), st.integers(1, 9), st.sampled_from([0.5, 1.0, 2.0]), st.data())
+def test_verify_sample_matches_brute(K, V, tau, data):
+    """Random small logits (ties, -inf entries) and uniforms: the oracle's samples
+    and acceptance equal numpy's cumsum / searchsorted reading."""
+    vals = data.draw(st.lists(st.lists(st.sampled_from([-2.0, -1.0, 0.0, 0.5, 1.0, 3.0, -math.inf]),
+                                       min_size=V, max_size=V), min_size=K + 1, max_size=K + 1))
+    Z = np.array(vals, np.float32)
+    u = np.array(data.draw(st.lists(st.sampled_from([0.0, 0.1, 0.25, 0.5, 0.73, 0.999, 1.0]),
+                                    min_size=K + 1, max_size=K + 1)), np.float32)
+    L = data.draw(st.integers(0, K))
+    draft = np.full(K, -1, np.int32)
+    draft[:L] = data.draw(st.lists(st.integers(0, V - 1), min_size=L, max_size=L))
+    acc, out, cnt, rows = oracle.verify_sample(Z[None], draft[None], np.array([L], np.int32),
+                                               tau, u[None])
+    a, toks, y = brute.verify_sample(Z, list(draft[:L]), tau, u)
+    assert acc[0] == a and cnt[0] == a + 1
+    assert list(out[0, :a + 1]) == toks and np.all(out[0, a + 1:] == -1)
+    assert list(rows[0, :L + 1]) == y and np.all(rows[0, L + 1:] == -1)
+    assert np.array_equal(out[0, :a], draft[:a])
+
+
+def test_verify_sample_acceptance_and_bad_lengths():
+    """Drafts equal to the samples are accepted whole (K+1 tokens out); a draft
+    differing at i keeps i tokens; bad lengths give -1 / 0 as in greedy."""
+    rng = np.random.default_rng(5)
+    B, K, V = 3, 4, 7
+    Z = rng.standard_normal((B, K + 1, V)).astype(np.float32)
+    U = rng.random((B, K + 1)).astype(np.float32)
+    _, _, _, rows = oracle.verify_sample(Z, np.zeros((B, K), np.int32), np.full(B, K, np.int32),
+                                         1.0, U)
+    draft = rows[:, :K].copy()
+    draft[1, 2] = (draft[1, 2] + 1) % V
+    lens = np.array([K, K, 9], np.int32)
+    acc, out, cnt, r2 = oracle.verify_sample(Z, draft, lens, 1.0, U)
+    assert acc[0] == K and cnt[0] == K + 1 and list(out[0]) == list(rows[0])
+    assert acc[1] == 2 and list(out[1, :3]) == [draft[1, 0], draft[1, 1], rows[1, 2]]
+    assert acc[2] == -1 and cnt[2] == 0 and np.all(out[2] == -1)
