@@ -47,10 +47,14 @@ def parse():
                    help="bracket the dominant call with timing events on every N-th timed step")
     p.add_argument("--mode", choices=["auto", "fused", "split"], default="auto",
                    help="drafting: one-launch call (fused), separate calls (split), or auto")
+    p.add_argument("--verify", choices=["greedy", "sample"], default="greedy",
+                   help="verification: argmax (greedy) or sampling at --temperature")
+    p.add_argument("--temperature", type=float, default=1.0)
     return p.parse_args()
 
 
-def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fused):
+def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fused,
+                      sample=False):
     """What each kernel must move per step (never the dense work it avoids)."""
     import numpy as np
     B, K = cfg.B, cfg.K
@@ -69,7 +73,10 @@ def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fu
         out["score_hidden"] = int(((C + (C > 0)) * cfg.d * 2).sum() + C.sum() * 4)
         out["select"] = B * 8 * 2 + B * 8
     out["emit"] = int(B * K * 4 * 2)
-    out["verify_argmax"] = int(((draft_len.astype(np.int64) + 1) * cfg.V * elt_logits).sum())
+    rows = draft_len.astype(np.int64) + 1
+    # the logits rows i <= L once, plus (sampling) the draws those rows use
+    out["verify_sample" if sample else "verify_argmax"] = int(
+        (rows * cfg.V * elt_logits).sum() + (rows.sum() * 4 if sample else 0))
     out["verify_accept"] = int(((draft_len.astype(np.int64) + 1) * 8 * 2).sum() + B * K * 4 +
                                B * (K + 1) * 4)
     if fused:   # one launch does find, rank, select and emit
@@ -82,7 +89,8 @@ def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fu
 KERNELS = {"draft": "pld::draft_", "find": "pld::find_", "score_hidden": "pld::rank_hidden_kernel",
            "score_attn": "pld::rank_attn_kernel", "select": "pld::rank_finish_kernel",
            "select_attn": "pld::rank_finish_kernel", "emit": "pld::emit_kernel",
-           "verify_argmax": "pld::verify_argmax_kernel", "verify_accept": "pld::verify_accept_kernel"}
+           "verify_argmax": "pld::verify_argmax_kernel", "verify_accept": "pld::verify_accept_kernel",
+           "verify_sample": "pld::sample_"}
 
 
 class TimingEvents:
@@ -187,6 +195,10 @@ def main():
                 attn=torch.from_numpy(w["attn"]).to(dev) if w["attn"] is not None else None)
     step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, mode=args.mode)
     fused = step.uses_fused(base["hidden"], base["attn"])
+    sample = args.verify == "sample"
+    if sample:
+        step.set_sampling(args.temperature, cfg.V, bf16,
+                          uniforms=torch.from_numpy(synth.make_uniforms(cfg.B, cfg.K, cfg.seed)).to(dev))
 
     def run(s):
         step.run(s["tokens"], s["lens"], s["logits"], hidden=s["hidden"], attn=s["attn"],
@@ -201,7 +213,7 @@ def main():
         log(f"[bench] drafting with {step.draft_split} block(s) per sequence")
     nbytes = algorithmic_bytes(cfg, lens, step.cand_count.cpu().numpy(),
                                step.draft_len.cpu().numpy(), step.cand_pos.cpu().numpy(), elt,
-                               fused)
+                               fused, sample=sample)
     step_bytes = sum(nbytes.values())
     dominant = max(nbytes, key=nbytes.get)
     # input copies at distinct addresses: the steps of one rotation touch at
@@ -266,7 +278,9 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, w, z, bf16, args.cpu_seconds, log)
+        cpu = cpu_baseline(cfg, w, z, bf16, args.cpu_seconds, log,
+                           (args.temperature, synth.make_uniforms(cfg.B, cfg.K, cfg.seed))
+                           if sample else None)
 
     line = {
         "metric": METRIC, "value": round(ms_per_step * 1e3, 2), "unit": "us", "n_gpus": 1,
@@ -279,6 +293,8 @@ def main():
                    "inputs": "hidden bf16, attention f32, tokens int32",
                    "drafting": (f"one call, {step.draft_split} block(s) per sequence" if fused
                                 else "separate calls"),
+                   "verification": (f"sampling at temperature {args.temperature}" if sample
+                                    else "greedy"),
                    "input_copies": copies,
                    "step_bytes": step_bytes},
         "roofline": roofline,
@@ -287,7 +303,7 @@ def main():
     print(json.dumps(line), flush=True)
 
 
-def cpu_baseline(cfg, w, z, bf16, seconds, log):
+def cpu_baseline(cfg, w, z, bf16, seconds, log, sampling=None):
     """The oracle's whole step on the host, single-threaded, on the same inputs."""
     import numpy as np
     import torch
@@ -316,7 +332,10 @@ def cpu_baseline(cfg, w, z, bf16, seconds, log):
             sh, bh, _ = oracle.rank_hidden(hb, lens, p, c)
             best = bh
         dr, dl = oracle.emit(toks, lens, best, cfg.K)
-        oracle.verify(z, dr, dl, bf16=bf16)
+        if sampling is not None:
+            oracle.verify_sample(z, dr, dl, sampling[0], sampling[1], bf16=bf16)
+        else:
+            oracle.verify(z, dr, dl, bf16=bf16)
 
     n = 0
     t0 = time.perf_counter()

@@ -197,6 +197,44 @@ int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride, int64
                       void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * pld_verify_sample -- sampling verification (Sec. 3 and Sec. 4.4 with a
+ * temperature; the paper's sampling experiments use tau = 1).  Instead of the
+ * argmax, y_i is drawn from softmax(Z[b][i] / tau) by inversion at the
+ * caller's uniform u = uniforms[b][i]: with p_v = exp((Z[v] - max Z) / tau)
+ * and S = sum_v p_v, y_i is the first v whose cumulative mass p_0 + ... + p_v
+ * exceeds u * S.  Acceptance and outputs are then those of pld_verify_greedy
+ * with these y_i; for a draft that puts all its mass on one token this is
+ * the usual speculative rejection sampling.
+ *
+ *   temperature  tau > 0, finite, with log2(e) / tau representable in fp32
+ *   uniforms     fp32 [B][u_stride] device memory, u_stride >= K+1, 4-byte
+ *                aligned; u < 0 or NaN counts as 0, u >= 1 as the largest
+ *                float below 1.  Only entries i <= draft_len[b] are read.
+ *   row_sample   int32 [B][K+1] or NULL: y_i for i <= L, -1 for the rows
+ *                past the draft (all -1 when draft_len is out of range)
+ *   workspace    at least pld_verify_sample_workspace_bytes(B, K, V, dtype)
+ *                bytes, zero-filled once like every workspace; its first
+ *                pld_workspace_bytes(B, K) bytes are left zero by the call and
+ *                the rest is per-call statistics, rewritten each time.
+ * Arithmetic: the masses are fp32 (2^((z - m) * log2(e)/tau)) and are summed
+ * per 512-vector segment of the row, then over the segments; a row of -inf
+ * gives y = 0, and where rounding leaves no element past the target the last
+ * element with nonzero mass is taken.  +inf and NaN logits are outside the
+ * contract.  Results are bit-identical from run to run.
+ * Errors: as pld_verify_greedy, plus PLD_ERR_INVALID for a bad temperature,
+ * NULL uniforms or u_stride < K+1 and PLD_ERR_ALIGN for misaligned uniforms.
+ */
+int pld_verify_sample(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
+                      int V, int K, const int32_t *draft, const int32_t *draft_len, int B,
+                      double temperature, const float *uniforms, int64_t u_stride,
+                      int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
+                      int32_t *row_sample, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes of pld_verify_sample (0 for arguments out of range); it is
+ * at least pld_workspace_bytes(B, K), so one buffer serves every call. */
+size_t pld_verify_sample_workspace_bytes(int B, int K, int V, int dtype);
+
+/*
  * The two halves of the ranking calls and of verification, for callers that
  * schedule (or time) the phases separately.  Run in order on one stream with
  * the same workspace, they produce exactly what the combined call produces.
@@ -209,8 +247,11 @@ int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride, int64
  *   best_score and returns the workspace to zero.
  * pld_verify_argmax -- y_i = argmax_v Z[b][i][v] for the rows i <= draft_len[b],
  *   kept in the workspace.
+ * pld_verify_sample_tokens -- the sampling half of pld_verify_sample: y_i
+ *   for the rows i <= draft_len[b] (and row_sample, may be NULL), kept in the
+ *   workspace in the same form, so that pld_verify_accept finishes it.
  * pld_verify_accept -- the accepted length and emitted tokens from those
- *   row maxima (Sec. 4.4); returns the workspace to zero.
+ *   row tokens (Sec. 4.4); returns the workspace to zero.
  * Arguments and errors as in the combined calls.
  */
 int pld_score_hidden(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
@@ -233,6 +274,50 @@ int pld_verify_argmax(const void *logits, int dtype, int64_t l_seq_stride, int64
 int pld_verify_accept(const int32_t *draft, const int32_t *draft_len, int B, int K,
                       int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
                       void *workspace, size_t workspace_bytes, void *stream);
+
+int pld_verify_sample_tokens(const void *logits, int dtype, int64_t l_seq_stride,
+                             int64_t l_row_stride, int V, int K, const int32_t *draft_len, int B,
+                             double temperature, const float *uniforms, int64_t u_stride,
+                             int32_t *row_sample, void *workspace, size_t workspace_bytes,
+                             void *stream);
+
+/*
+ * pld_verify_sample -- sampling verification (Sec. 3 and Sec. 4.4 with a
+ * temperature; the paper's sampling experiments use tau = 1).  Instead of the
+ * argmax, y_i is drawn from softmax(Z[b][i] / tau) by inversion at the
+ * caller's uniform u = uniforms[b][i]: with p_v = exp((Z[v] - max Z) / tau)
+ * and S = sum_v p_v, y_i is the first v whose cumulative mass p_0 + ... + p_v
+ * exceeds u * S.  Acceptance and outputs are then those of pld_verify_greedy
+ * with these y_i; for a draft that puts all its mass on one token this is
+ * the usual speculative rejection sampling.
+ *
+ *   temperature  tau > 0, finite, with log2(e) / tau representable in fp32
+ *   uniforms     fp32 [B][u_stride] device memory, u_stride >= K+1, 4-byte
+ *                aligned; u < 0 or NaN counts as 0, u >= 1 as the largest
+ *                float below 1.  Only entries i <= draft_len[b] are read.
+ *   row_sample   int32 [B][K+1] or NULL: y_i for i <= L, -1 for the rows
+ *                past the draft (all -1 when draft_len is out of range)
+ *   workspace    at least pld_verify_sample_workspace_bytes(B, K, V, dtype)
+ *                bytes, zero-filled once like every workspace; its first
+ *                pld_workspace_bytes(B, K) bytes are left zero by the call and
+ *                the rest is per-call statistics, rewritten each time.
+ * Arithmetic: the masses are fp32 (2^((z - m) * log2(e)/tau)) and are summed
+ * per 512-vector segment of the row, then over the segments; a row of -inf
+ * gives y = 0, and where rounding leaves no element past the target the last
+ * element with nonzero mass is taken.  +inf and NaN logits are outside the
+ * contract.  Results are bit-identical from run to run.
+ * Errors: as pld_verify_greedy, plus PLD_ERR_INVALID for a bad temperature,
+ * NULL uniforms or u_stride < K+1 and PLD_ERR_ALIGN for misaligned uniforms.
+ */
+int pld_verify_sample(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
+                      int V, int K, const int32_t *draft, const int32_t *draft_len, int B,
+                      double temperature, const float *uniforms, int64_t u_stride,
+                      int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
+                      int32_t *row_sample, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes of pld_verify_sample (0 for arguments out of range); it is
+ * at least pld_workspace_bytes(B, K), so one buffer serves every call. */
+size_t pld_verify_sample_workspace_bytes(int B, int K, int V, int dtype);
 
 /*
  * pld_draft_hidden / pld_draft_attn -- the drafting half of a step in one

@@ -390,7 +390,7 @@ int pld_ref_verify_sample(const void *logits, int dtype, int64_t l_seq_stride,
                 }
                 double u = (double)uniforms[(int64_t)b * u_stride + i];
                 if (!(u >= 0.0)) u = 0.0;
-                if (u >= 1.0) u = nextafter(1.0, 0.0);
+                if (u >= 1.0) u = (double)nextafterf(1.0f, 0.0f);   /* the draws are fp32 */
                 double t = u * S, c = 0.0;
                 int last = 0, found = 0;
                 for (int v = 0; v < V; ++v) {

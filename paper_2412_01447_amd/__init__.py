@@ -21,6 +21,7 @@ __all__ = [
     "pld_draft_hidden", "pld_draft_attn", "pld_draft_workspace_bytes", "DRAFT_MAX_TOK_STRIDE",
     "DRAFT_MAX_PART", "pld_score_hidden",
     "pld_score_attn", "pld_select_best", "pld_verify_argmax", "pld_verify_accept",
+    "pld_verify_sample", "pld_verify_sample_workspace_bytes", "pld_verify_sample_tokens",
 ]
 
 PLD_OK, PLD_ERR_INVALID, PLD_ERR_ALIGN, PLD_ERR_WORKSPACE, PLD_ERR_LAUNCH = range(5)
@@ -42,6 +43,7 @@ _SIGNATURES = {
     "pld_status_string": ([_int], ctypes.c_char_p),
     "pld_workspace_bytes": ([_int, _int], _sz),
     "pld_draft_workspace_bytes": ([_int, _int], _sz),
+    "pld_verify_sample_workspace_bytes": ([_int, _int, _int, _int], _sz),
     "pld_find_scratch_bytes": ([_int, _i64], _sz),
     "pld_find_candidates": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _vp, _vp, _vp, _sz, _vp],
                             _int),
@@ -59,6 +61,10 @@ _SIGNATURES = {
     "pld_select_best": ([_int, _vp, _vp, _vp, _sz, _vp], _int),
     "pld_verify_argmax": ([_vp, _int, _i64, _i64, _int, _int, _vp, _int, _vp, _sz, _vp], _int),
     "pld_verify_accept": ([_vp, _vp, _int, _int, _vp, _vp, _vp, _vp, _sz, _vp], _int),
+    "pld_verify_sample": ([_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int, ctypes.c_double, _vp,
+                           _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp], _int),
+    "pld_verify_sample_tokens": ([_vp, _int, _i64, _i64, _int, _int, _vp, _int, ctypes.c_double,
+                                  _vp, _i64, _vp, _vp, _sz, _vp], _int),
     "pld_draft_hidden": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _i64, _i64, _int, _f32, _int,
                           _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _int, _vp, _sz, _vp],
                          _int),
@@ -157,6 +163,10 @@ def pld_draft_workspace_bytes(B, blocks_per_seq):
     return int(_load().pld_draft_workspace_bytes(B, blocks_per_seq))
 
 
+def pld_verify_sample_workspace_bytes(B, K, V, dtype):
+    return int(_load().pld_verify_sample_workspace_bytes(B, K, V, dtype))
+
+
 def pld_find_scratch_bytes(B, tok_stride):
     return int(_load().pld_find_scratch_bytes(B, tok_stride))
 
@@ -231,6 +241,32 @@ def pld_verify_greedy(logits, draft, draft_len, accept_len, out_tokens, out_coun
     return _run("pld_verify_greedy", (_ptr(logits), dtype, logits.stride(0), logits.stride(1), V, K,
           _ptr(draft), _ptr(draft_len), B, _ptr(accept_len), _ptr(out_tokens), _ptr(out_count),
           _ptr(workspace), _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_verify_sample(logits, draft, draft_len, temperature, uniforms, accept_len, out_tokens,
+                      out_count, workspace, row_sample=None, stream=None, prepare=False):
+    """Sampling verification: y_i drawn from softmax(logits / temperature) at uniforms [B][>=K+1]
+    (fp32); outputs as pld_verify_greedy, plus the per-row samples when row_sample is given."""
+    import torch
+    if logits.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("logits must be float32 or bfloat16")
+    _need(logits, logits.dtype, "logits", 3)
+    _need(uniforms, torch.float32, "uniforms", 2)
+    B, K1, V = logits.shape
+    K = K1 - 1
+    if draft.shape != (B, K) or draft.stride(0) != K:
+        raise TypeError("draft must be a contiguous [B][K] tensor")
+    if out_tokens.shape != (B, K1) or out_tokens.stride(0) != K1:
+        raise TypeError("out_tokens must be a contiguous [B][K+1] tensor")
+    if uniforms.shape[0] != B or uniforms.shape[1] < K1:
+        raise TypeError("uniforms must be [B][>=K+1]")
+    if row_sample is not None and (row_sample.shape != (B, K1) or row_sample.stride(0) != K1):
+        raise TypeError("row_sample must be a contiguous [B][K+1] tensor")
+    dtype = PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
+    return _run("pld_verify_sample", (_ptr(logits), dtype, logits.stride(0), logits.stride(1), V, K,
+          _ptr(draft), _ptr(draft_len), B, float(temperature), _ptr(uniforms), uniforms.stride(0),
+          _ptr(accept_len), _ptr(out_tokens), _ptr(out_count), _ptr(row_sample), _ptr(workspace),
+          _nbytes(workspace), _stream(stream),), prepare)
 
 
 def pld_draft_hidden(tokens, lens, ngram_min, ngram_max, hidden, K, cand_pos, cand_count,
@@ -314,6 +350,26 @@ def pld_verify_argmax(logits, draft_len, workspace, stream=None, prepare=False):
     dtype = PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
     return _run("pld_verify_argmax", (_ptr(logits), dtype, logits.stride(0), logits.stride(1), V, K1 - 1,
           _ptr(draft_len), B, _ptr(workspace), _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_verify_sample_tokens(logits, draft_len, temperature, uniforms, workspace, row_sample=None,
+                             stream=None, prepare=False):
+    """Sampled tokens of the K+1 rows (rows past each draft skipped) into the workspace."""
+    import torch
+    if logits.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("logits must be float32 or bfloat16")
+    _need(logits, logits.dtype, "logits", 3)
+    _need(uniforms, torch.float32, "uniforms", 2)
+    B, K1, V = logits.shape
+    if uniforms.shape[0] != B or uniforms.shape[1] < K1:
+        raise TypeError("uniforms must be [B][>=K+1]")
+    if row_sample is not None and (row_sample.shape != (B, K1) or row_sample.stride(0) != K1):
+        raise TypeError("row_sample must be a contiguous [B][K+1] tensor")
+    dtype = PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
+    return _run("pld_verify_sample_tokens", (_ptr(logits), dtype, logits.stride(0),
+          logits.stride(1), V, K1 - 1, _ptr(draft_len), B, float(temperature), _ptr(uniforms),
+          uniforms.stride(0), _ptr(row_sample), _ptr(workspace), _nbytes(workspace),
+          _stream(stream),), prepare)
 
 
 def pld_verify_accept(draft, draft_len, accept_len, out_tokens, out_count, workspace,

@@ -164,6 +164,35 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
     return ((uint64_t)hi << 32) | lo;
 }
 
+// A DPP move whose unreached lanes get `fill` (the identity of the caller's
+// operation) instead of 0.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float dpp_move_f(float v, float fill) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(fill), __float_as_int(v),
+                                                      kCtrl, kRowMask, 0xf, false));
+}
+
+__device__ __forceinline__ float wave_max_f32(float v) {
+    v = fmaxf(v, dpp_move_f<kDppQuadSwap1, 0xf>(v, -INFINITY));
+    v = fmaxf(v, dpp_move_f<kDppQuadSwap2, 0xf>(v, -INFINITY));
+    v = fmaxf(v, dpp_move_f<kDppHalfMirror, 0xf>(v, -INFINITY));
+    v = fmaxf(v, dpp_move_f<kDppMirror, 0xf>(v, -INFINITY));
+    v = fmaxf(v, dpp_move_f<kDppBcast15, 0xa>(v, -INFINITY));
+    v = fmaxf(v, dpp_move_f<kDppBcast31, 0xc>(v, -INFINITY));
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+// Inclusive prefix sum of floats over the lanes, in a fixed association.
+__device__ __forceinline__ float wave_incl_scan_f32(float x) {
+    x += dpp_move_f<kDppShr1, 0xf>(x, 0.f);
+    x += dpp_move_f<kDppShr1 + 1, 0xf>(x, 0.f);
+    x += dpp_move_f<kDppShr1 + 3, 0xf>(x, 0.f);
+    x += dpp_move_f<kDppShr1 + 7, 0xf>(x, 0.f);
+    x += dpp_move_f<kDppBcast15, 0xa>(x, 0.f);
+    x += dpp_move_f<kDppBcast31, 0xc>(x, 0.f);
+    return x;
+}
+
 // Exclusive prefix sum over the lanes (shifts by 1, 2, 4, 8 within each row
 // of 16, then the row broadcasts); `total` gets the wave's sum.
 __device__ __forceinline__ int wave_excl_scan(int v, int &total) {

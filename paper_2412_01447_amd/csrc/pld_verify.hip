@@ -17,6 +17,17 @@
 // kernel boundary orders the two), reads the row keys back with one thread
 // per sequence, computes the accepted length, writes the outputs and returns
 // the slots to zero.  Rows i > L are never read.
+//
+// Sampling verification (Sec. 3 and Sec. 4.4 with a temperature tau): y_i is
+// drawn from softmax(Z[b][i] / tau) by inversion at a caller-supplied uniform
+// u: the first v whose cumulative mass exceeds u times the row's total.  One
+// streaming pass writes, per 512-vector segment of a row, the segment maximum
+// and the segment's mass relative to it; a pick kernel per row combines the
+// segment masses, finds the segment the target falls in and re-reads only that
+// segment (1/nseg of the row) to find the token; the greedy acceptance kernel
+// then runs on the picked tokens, which the pick kernel stores in the key
+// slots in the argmax keys' format.
+#include <float.h>
 #include <math.h>
 
 #include "pld.h"
@@ -83,6 +94,31 @@ struct Elem<1> {
     }
 };
 
+// A logits row as [head | 16-byte vectors | tail]: the head takes the
+// elements before the first 16-byte boundary, the tail those after the last
+// whole vector; both are read one element at a time.
+template <typename T, int P>
+struct RowView {
+    const T *row;
+    const uint4 *vec;   // the body's vectors
+    int head;           // elements before the body
+    int nvec;           // vectors in the body
+    int64_t body_end;   // first element of the tail
+};
+template <typename T, int P>
+__device__ __forceinline__ RowView<T, P> row_view(const void *logits, int64_t ls, int64_t lr,
+                                                  int b, int i, int V) {
+    RowView<T, P> r;
+    r.row = reinterpret_cast<const T *>(logits) + (int64_t)b * ls + (int64_t)i * lr;
+    const int mis = (int)(((uintptr_t)r.row & 15) / sizeof(T));
+    r.head = mis ? (P - mis) : 0;
+    if (r.head > V) r.head = V;
+    r.nvec = (V - r.head) / P;
+    r.body_end = r.head + (int64_t)r.nvec * P;
+    r.vec = reinterpret_cast<const uint4 *>(r.row + r.head);
+    return r;
+}
+
 template <int kBf16>
 __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArgs a) {
     using E = Elem<kBf16>;
@@ -91,16 +127,13 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArg
     __shared__ uint64_t s_key[kVerifyWaves];
     const int split = blockIdx.x, i = blockIdx.y, b = blockIdx.z;
 
-    const T *row = reinterpret_cast<const T *>(a.logits) + (int64_t)b * a.ls + (int64_t)i * a.lr;
-    // The row as [head | 16-byte vectors | tail]; head and tail are scalar.
-    const int mis = (int)(((uintptr_t)row & 15) / sizeof(T));
-    int head = mis ? (P - mis) : 0;
-    if (head > a.V) head = a.V;
-    const int nvec = (a.V - head) / P;
-    const int64_t body_end = head + (int64_t)nvec * P;
+    const RowView<T, P> rv = row_view<T, P>(a.logits, a.ls, a.lr, b, i, a.V);
+    const T *row = rv.row;
+    const int head = rv.head, nvec = rv.nvec;
+    const int64_t body_end = rv.body_end;
     const int v0 = min(split * a.chunk, nvec);
     const int v1 = (split == a.S - 1) ? nvec : min(v0 + a.chunk, nvec);
-    const uint4 *vec = reinterpret_cast<const uint4 *>(row + head);
+    const uint4 *vec = rv.vec;
     const int64_t my_v = v0 + threadIdx.x;
 
     // The first batch of this thread's vectors is requested together with the
@@ -222,6 +255,244 @@ __global__ __launch_bounds__(256) void verify_accept_kernel(VerifyArgs a) {
     }
 }
 
+// -------------------------------------------------------------- sampling
+// Mass of one element relative to a maximum m: 2^((z - m) * k) with
+// k = log2(e) / tau, i.e. exp((z - m) / tau).  The subtraction comes first so
+// that the exponent's rounding error scales with z - m, not with m.  The pick
+// kernel recomputes the masses of one segment with the segment's own maximum,
+// so it gets bit-for-bit the values the statistics pass summed.
+__device__ __forceinline__ float rel_mass(float z, float m, float k) {
+    return __builtin_amdgcn_exp2f((z - m) * k);
+}
+
+constexpr int kSegVecs = kWave * kVerifyUnroll;   // 16-byte vectors per segment
+
+struct SampleArgs {
+    const void *logits;
+    int64_t ls, lr;
+    int V, K, B;
+    int S;          // statistics blocks per row
+    int nseg_max;   // segment slots per row in `stats`
+    float k;        // log2(e) / tau
+    const float *uniforms;
+    int64_t u_stride;
+    const int32_t *draft_len;
+    uint64_t *keys;        // [B][K+1]: the picked tokens, in the argmax keys' format
+    int32_t *row_sample;   // [B][K+1] or null
+    float2 *stats;         // [B][K+1][nseg_max]: (segment maximum, mass relative to it)
+};
+
+__host__ __device__ __forceinline__ int seg_count(int nvec) {
+    return nvec > 0 ? (nvec + kSegVecs - 1) / kSegVecs : 1;
+}
+
+// One wave per segment: lane l takes vectors l, l+64, ..., l+448 of it (each
+// load instruction reads 1 KB contiguous), plus one head element (segment 0)
+// and one tail element (last segment).  Rows past the draft are not read.
+template <int kBf16>
+__global__ __launch_bounds__(kVerifyThreads) void sample_stats_kernel(SampleArgs a) {
+    using E = Elem<kBf16>;
+    using T = typename E::T;
+    constexpr int P = E::kPerVec;
+    constexpr uint32_t kNegInf2 = kBf16 ? 0xff80ff80u : 0xff800000u;   // -inf in every element
+    const int i = blockIdx.y, b = blockIdx.z;
+    const int L = a.draft_len[b];
+    if (L < 0 || L > a.K || i > L) return;
+    const RowView<T, P> rv = row_view<T, P>(a.logits, a.ls, a.lr, b, i, a.V);
+    const int nseg = seg_count(rv.nvec);
+    const int lane = lane_id();
+    float2 *st = a.stats + ((int64_t)b * (a.K + 1) + i) * a.nseg_max;
+    const int step = a.S * kVerifyWaves;
+    for (int g = blockIdx.x * kVerifyWaves + (int)threadIdx.x / kWave; g < nseg; g += step) {
+        const int64_t v_base = (int64_t)g * kSegVecs + lane;
+        uint4 r[kVerifyUnroll];
+#pragma unroll
+        for (int u = 0; u < kVerifyUnroll; ++u) {
+            const int64_t vi = v_base + (int64_t)u * kWave;
+            r[u] = make_uint4(kNegInf2, kNegInf2, kNegInf2, kNegInf2);
+            if (vi < rv.nvec) r[u] = ld_stream(rv.vec + vi);
+        }
+        const float zh = (g == 0 && lane < rv.head) ? E::get(rv.row, lane) : -INFINITY;
+        const float zt =
+            (g == nseg - 1 && rv.body_end + lane < a.V) ? E::get(rv.row, rv.body_end + lane)
+                                                        : -INFINITY;
+        float z[kVerifyUnroll][P];
+        float m = fmaxf(zh, zt);
+#pragma unroll
+        for (int u = 0; u < kVerifyUnroll; ++u) {
+            E::unpack(r[u], z[u]);
+#pragma unroll
+            for (int e = 0; e < P; ++e) m = fmaxf(m, z[u][e]);
+        }
+        const float M = wave_max_f32(m);
+        float mass = 0.f;
+        if (M > -INFINITY) {   // wave-uniform; an all -inf segment has no mass
+            mass = rel_mass(zh, M, a.k) + rel_mass(zt, M, a.k);
+#pragma unroll
+            for (int u = 0; u < kVerifyUnroll; ++u)
+#pragma unroll
+                for (int e = 0; e < P; ++e) mass += rel_mass(z[u][e], M, a.k);
+            mass = wave_sum_f32(mass);
+        }
+        if (lane == 0) st[g] = make_float2(M, mass);
+    }
+}
+
+// The segment masses of one row, rescaled to the row maximum M, as one wave's
+// lanes (64 segments per round); lanes past the last segment get 0.
+__device__ __forceinline__ float seg_weight(const float2 *st, int g, int nseg, float M,
+                                            float k, float &seg_max) {
+    seg_max = -INFINITY;
+    if (g >= nseg) return 0.f;
+    const float2 v = st[g];
+    seg_max = v.x;
+    return v.x > -INFINITY ? v.y * rel_mass(v.x, M, k) : 0.f;
+}
+
+// One block per row i <= L: the segment the target u * (total mass) falls in,
+// then that segment's elements, split into contiguous runs of at most kPer
+// per thread, scanned in index order.  Every wave computes the segment search
+// (a few rounds of DPP work) itself, so no barrier is needed before the
+// re-read.  The result is the first element whose cumulative mass exceeds the
+// target; where rounding leaves no such element the last element with mass
+// is taken, so the token always has nonzero probability.
+template <int kBf16>
+__global__ __launch_bounds__(kVerifyThreads) void sample_pick_kernel(SampleArgs a) {
+    using E = Elem<kBf16>;
+    using T = typename E::T;
+    constexpr int P = E::kPerVec;
+    constexpr int kPer = (kSegVecs * P + 2 * P + kVerifyThreads - 1) / kVerifyThreads;
+    __shared__ float s_tot[kVerifyWaves];
+    __shared__ int s_first[kVerifyWaves];
+    __shared__ int s_last[kVerifyWaves];
+    __shared__ int s_pick;
+    const int i = blockIdx.x, b = blockIdx.y;
+    const int L = a.draft_len[b];
+    const int64_t slot = (int64_t)b * (a.K + 1) + i;
+    if (L < 0 || L > a.K || i > L) {   // block-uniform
+        if (a.row_sample && threadIdx.x == 0) a.row_sample[slot] = -1;
+        return;
+    }
+    const RowView<T, P> rv = row_view<T, P>(a.logits, a.ls, a.lr, b, i, a.V);
+    const int nseg = seg_count(rv.nvec);
+    const float2 *st = a.stats + slot * a.nseg_max;
+    const int lane = lane_id(), w = (int)threadIdx.x / kWave;
+    const float k = a.k;
+
+    float M = -INFINITY;
+    for (int g0 = 0; g0 < nseg; g0 += kWave) {
+        const int g = g0 + lane;
+        M = fmaxf(M, wave_max_f32(g < nseg ? st[g].x : -INFINITY));
+    }
+    int y = 0;   // a row of -inf only: token 0
+    if (M > -INFINITY) {
+        // Total mass: the rounds' inclusive scans chained through `carry`,
+        // the same operations the search below repeats, so the search's last
+        // cumulative value is bit-identical to the total.
+        float tot = 0.f, mg;
+        for (int g0 = 0; g0 < nseg; g0 += kWave) {
+            const float wg = seg_weight(st, g0 + lane, nseg, M, k, mg);
+            const float W = tot + wave_incl_scan_f32(wg);
+            tot = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(W), kWave - 1));
+        }
+        float u = a.uniforms[(int64_t)b * a.u_stride + i];
+        if (!(u >= 0.f)) u = 0.f;                   // also NaN
+        if (u >= 1.f) u = 0x1.fffffep-1f;           // the largest float below 1
+        const float t = u * tot;   // < tot: u <= 1 - 2^-24 rounds below any positive total
+
+        int gc = -1, glast = 0;
+        float r_loc = INFINITY, mc = M;
+        float carry = 0.f;
+        for (int g0 = 0; g0 < nseg && gc < 0; g0 += kWave) {
+            const float wg = seg_weight(st, g0 + lane, nseg, M, k, mg);
+            const float W = carry + wave_incl_scan_f32(wg);
+            const uint64_t cross = __ballot(W > t && wg > 0.f);
+            const uint64_t pos = __ballot(wg > 0.f);
+            if (pos) glast = g0 + 63 - __clzll((long long)pos);
+            if (cross) {
+                const int f = __ffsll((unsigned long long)cross) - 1;
+                // Mass before the segment: the previous lane's cumulative value.
+                const float before =
+                    f > 0 ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(W), f - 1))
+                          : carry;
+                gc = g0 + f;
+                mc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mg), f));
+                // Target inside the segment, in units of its own maximum.
+                r_loc = fmaxf(t - before, 0.f) / rel_mass(mc, M, k);
+            }
+            carry = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(W), kWave - 1));
+        }
+        if (gc < 0) {   // rounding left no crossing: the last segment with mass, its last element
+            gc = glast;
+            mc = st[gc].x;
+            r_loc = INFINITY;
+        }
+
+        const int64_t e0 = gc == 0 ? 0 : rv.head + (int64_t)gc * kSegVecs * P;
+        const int64_t e1 = gc == nseg - 1 ? a.V : rv.head + (int64_t)(gc + 1) * kSegVecs * P;
+        const int per = (int)((e1 - e0 + kVerifyThreads - 1) / kVerifyThreads);
+        const int64_t my0 = e0 + (int64_t)threadIdx.x * per;
+        float p[kPer];
+        float sum = 0.f;
+        int last = -1;
+#pragma unroll
+        for (int e = 0; e < kPer; ++e) {
+            const int64_t idx = my0 + e;
+            const bool in = e < per && idx < e1;
+            p[e] = in ? rel_mass(E::get(rv.row, in ? idx : 0), mc, k) : 0.f;
+            sum += p[e];
+            if (p[e] > 0.f) last = (int)idx;
+        }
+        // Block inclusive scan of the per-thread sums.
+        float incl = wave_incl_scan_f32(sum);
+        if (lane == kWave - 1) s_tot[w] = incl;
+        const uint64_t has = __ballot(last >= 0);
+        const int wave_last = has ? __builtin_amdgcn_readlane(last, 63 - __clzll((long long)has)) : -1;
+        if (lane == 0) s_last[w] = wave_last;
+        __syncthreads();
+        float before = 0.f;
+        for (int q = 0; q < w; ++q) before += s_tot[q];
+        const float prev_lane = __shfl(incl, lane > 0 ? lane - 1 : 0);
+        incl += before;
+        const float excl = lane > 0 ? prev_lane + before : before;
+        const uint64_t cross = __ballot(incl > r_loc && sum > 0.f);
+        if (lane == 0) s_first[w] = cross ? __ffsll((unsigned long long)cross) - 1 : kWave;
+        __syncthreads();
+        int tw = -1;
+        for (int q = 0; q < kVerifyWaves; ++q)
+            if (s_first[q] < kWave) {
+                tw = q;
+                break;
+            }
+        if (tw < 0) {   // no crossing (rounding, or the fallback): the last element with mass
+            y = (int)e0;
+            for (int q = kVerifyWaves - 1; q >= 0; --q)
+                if (s_last[q] >= 0) {
+                    y = s_last[q];
+                    break;
+                }
+        } else {
+            if ((int)threadIdx.x == tw * kWave + s_first[tw]) {
+                const float rr = fmaxf(r_loc - excl, 0.f);
+                int pick = -1;
+                float c = 0.f;   // the partial sums `sum` went through
+#pragma unroll
+                for (int e = 0; e < kPer; ++e) {
+                    c += p[e];
+                    if (pick < 0 && c > rr) pick = (int)(my0 + e);
+                }
+                s_pick = pick >= 0 ? pick : last;   // sum > 0, so `last` exists
+            }
+            __syncthreads();
+            y = s_pick;
+        }
+    }
+    if (threadIdx.x == 0) {
+        a.keys[slot] = argmax_key(0.f, (uint32_t)y);
+        if (a.row_sample) a.row_sample[slot] = y;
+    }
+}
+
 // ------------------------------------------------------------------ emit
 // draft[b][i] = x[j*+1+i] for i < L = min(K, T-1-j*), -1 after (Sec. 4.3).
 __global__ __launch_bounds__(256) void emit_kernel(const int32_t *tokens, int64_t tok_stride,
@@ -283,6 +554,59 @@ static void launch_accept(const VerifyArgs &a, hipStream_t s) {
     hipLaunchKernelGGL(verify_accept_kernel, dim3((a.B + 3) / 4), dim3(256), 0, s, a);
 }
 
+// The ranking and verification calls share the leading, zero-invariant part
+// of a workspace; the sampling statistics come after it.
+static size_t common_ws_bytes(int B, int K) {
+    const size_t r = rank_ws_bytes(B);
+    const size_t v = verify_ws_bytes(B, K);
+    return r > v ? r : v;
+}
+static int sample_nseg_max(int V, int dtype) {
+    return seg_count(V / (dtype == PLD_F32 ? 4 : 8));   // a row has at most V / P whole vectors
+}
+static size_t sample_ws_bytes(int B, int K, int V, int dtype) {
+    return common_ws_bytes(B, K) +
+           align_up((size_t)B * (size_t)(K + 1) * (size_t)sample_nseg_max(V, dtype) * sizeof(float2),
+                    256);
+}
+
+static void launch_sample(const VerifyArgs &va, int dtype, float k, const float *uniforms,
+                         int64_t u_stride, int32_t *row_sample, void *workspace, hipStream_t s) {
+    SampleArgs a{};
+    a.logits = va.logits;
+    a.ls = va.ls;
+    a.lr = va.lr;
+    a.V = va.V;
+    a.K = va.K;
+    a.B = va.B;
+    a.nseg_max = sample_nseg_max(va.V, dtype);
+    a.k = k;
+    a.uniforms = uniforms;
+    a.u_stride = u_stride;
+    a.draft_len = va.draft_len;
+    a.keys = va.keys;
+    a.row_sample = row_sample;
+    a.stats = reinterpret_cast<float2 *>(static_cast<char *>(workspace) +
+                                         common_ws_bytes(va.B, va.K));
+    // Statistics blocks per row: about PLD_VERIFY_TARGET_BLOCKS in all, and
+    // no more waves per row than the row has segments.
+    const int64_t rows = (int64_t)va.B * (va.K + 1);
+    int64_t S = (PLD_VERIFY_TARGET_BLOCKS + rows - 1) / rows;
+    const int64_t smax = (a.nseg_max + kVerifyWaves - 1) / kVerifyWaves;
+    if (S > smax) S = smax;
+    if (S < 1) S = 1;
+    a.S = (int)S;
+    const dim3 g_stats((unsigned)S, (unsigned)(va.K + 1), (unsigned)va.B);
+    const dim3 g_pick((unsigned)(va.K + 1), (unsigned)va.B);
+    if (dtype == PLD_F32) {
+        hipLaunchKernelGGL(sample_stats_kernel<0>, g_stats, dim3(kVerifyThreads), 0, s, a);
+        hipLaunchKernelGGL(sample_pick_kernel<0>, g_pick, dim3(kVerifyThreads), 0, s, a);
+    } else {
+        hipLaunchKernelGGL(sample_stats_kernel<1>, g_stats, dim3(kVerifyThreads), 0, s, a);
+        hipLaunchKernelGGL(sample_pick_kernel<1>, g_pick, dim3(kVerifyThreads), 0, s, a);
+    }
+}
+
 }  // namespace pld
 
 using namespace pld;
@@ -336,6 +660,65 @@ extern "C" int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_st
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }
 
+// Host checks of the sampling calls beyond those of prep_verify; k = log2(e)/tau.
+static int prep_sample(int dtype, int V, int K, int B, double temperature, const float *uniforms,
+                       int64_t u_stride, size_t workspace_bytes, float &k) {
+    if (!uniforms) return PLD_ERR_INVALID;
+    if (!(temperature > 0.0) || !(temperature <= DBL_MAX)) return PLD_ERR_INVALID;
+    const double kd = 1.4426950408889634 / temperature;
+    if (!(kd <= FLT_MAX)) return PLD_ERR_INVALID;
+    if (u_stride < (int64_t)K + 1) return PLD_ERR_INVALID;
+    if ((uintptr_t)uniforms % sizeof(float)) return PLD_ERR_ALIGN;
+    if (workspace_bytes < sample_ws_bytes(B, K, V, dtype)) return PLD_ERR_WORKSPACE;
+    k = (float)kd;
+    return PLD_OK;
+}
+
+extern "C" int pld_verify_sample_tokens(const void *logits, int dtype, int64_t l_seq_stride,
+                                        int64_t l_row_stride, int V, int K,
+                                        const int32_t *draft_len, int B, double temperature,
+                                        const float *uniforms, int64_t u_stride,
+                                        int32_t *row_sample, void *workspace,
+                                        size_t workspace_bytes, void *stream) {
+    VerifyArgs a;
+    int rc = prep_verify(logits, dtype, l_seq_stride, l_row_stride, V, K, draft_len, B, workspace,
+                         workspace_bytes, a);
+    if (rc != PLD_OK) return rc;
+    float k;
+    rc = prep_sample(dtype, V, K, B, temperature, uniforms, u_stride, workspace_bytes, k);
+    if (rc != PLD_OK) return rc;
+    launch_sample(a, dtype, k, uniforms, u_stride, row_sample, workspace, (hipStream_t)stream);
+    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+}
+
+extern "C" int pld_verify_sample(const void *logits, int dtype, int64_t l_seq_stride,
+                                 int64_t l_row_stride, int V, int K, const int32_t *draft,
+                                 const int32_t *draft_len, int B, double temperature,
+                                 const float *uniforms, int64_t u_stride, int32_t *accept_len,
+                                 int32_t *out_tokens, int32_t *out_count, int32_t *row_sample,
+                                 void *workspace, size_t workspace_bytes, void *stream) {
+    if (!draft || !accept_len || !out_tokens || !out_count) return PLD_ERR_INVALID;
+    VerifyArgs a;
+    int rc = prep_verify(logits, dtype, l_seq_stride, l_row_stride, V, K, draft_len, B, workspace,
+                         workspace_bytes, a);
+    if (rc != PLD_OK) return rc;
+    float k;
+    rc = prep_sample(dtype, V, K, B, temperature, uniforms, u_stride, workspace_bytes, k);
+    if (rc != PLD_OK) return rc;
+    a.draft = draft;
+    a.accept_len = accept_len;
+    a.out_tokens = out_tokens;
+    a.out_count = out_count;
+    launch_sample(a, dtype, k, uniforms, u_stride, row_sample, workspace, (hipStream_t)stream);
+    launch_accept(a, (hipStream_t)stream);
+    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+}
+
+extern "C" size_t pld_verify_sample_workspace_bytes(int B, int K, int V, int dtype) {
+    if (B < 1 || K < 1 || V < 1 || (dtype != PLD_F32 && dtype != PLD_BF16)) return 0;
+    return sample_ws_bytes(B, K, V, dtype);
+}
+
 extern "C" int pld_emit_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *lens,
                               const int32_t *best_pos, int B, int K, int32_t *draft,
                               int32_t *draft_len, void *stream) {
@@ -364,7 +747,5 @@ extern "C" const char *pld_status_string(int status) {
 
 extern "C" size_t pld_workspace_bytes(int B, int K) {
     if (B < 1 || K < 1) return 0;
-    const size_t r = rank_ws_bytes(B);
-    const size_t v = verify_ws_bytes(B, K);
-    return r > v ? r : v;
+    return common_ws_bytes(B, K);
 }

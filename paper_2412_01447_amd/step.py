@@ -3,15 +3,17 @@
 A convenience over the five calls of the binding: it owns the output and
 workspace tensors for a batch shape and enqueues the calls on one stream with
 no host synchronisation (arXiv 2412.01447, Sec. 4: retrieval Eq. 1, ranking
-Eq. 2 / Eq. 3, draft Sec. 4.3, greedy verification Sec. 4.4).
+Eq. 2 / Eq. 3, draft Sec. 4.3, greedy verification Sec. 4.4, or sampling
+verification at a temperature once set_sampling() is called).
 """
 import torch
 
-from . import (DRAFT_MAX_PART, DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, PLD_MAX_DRAFT_SPLIT,
-               pld_draft_attn, pld_draft_hidden, pld_draft_workspace_bytes,
+from . import (DRAFT_MAX_PART, DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, PLD_BF16, PLD_F32,
+               PLD_MAX_DRAFT_SPLIT, pld_draft_attn, pld_draft_hidden, pld_draft_workspace_bytes,
                pld_emit_draft, pld_find_candidates, pld_find_scratch_bytes, pld_rank_attn,
                pld_rank_hidden, pld_score_attn, pld_score_hidden, pld_select_best,
-               pld_verify_accept, pld_verify_argmax, pld_verify_greedy, pld_workspace_bytes)
+               pld_verify_accept, pld_verify_argmax, pld_verify_greedy, pld_verify_sample,
+               pld_verify_sample_tokens, pld_verify_sample_workspace_bytes, pld_workspace_bytes)
 
 
 class DraftStep:
@@ -51,6 +53,28 @@ class DraftStep:
         # the one-call drafting's own workspace (key slots left zero, counts rewritten)
         self.draft_ws = None
         self.set_split(max(int(draft_split), self.min_split()))
+        # sampling verification (set_sampling): temperature, the draws, the per-row tokens
+        self.temperature = None
+        self.uniforms = None
+        self.row_sample = None
+
+    def set_sampling(self, temperature, V, bf16, uniforms=None):
+        """Verify by sampling at `temperature` (None: greedy again).  `uniforms` is a
+        device fp32 [B][K+1] tensor of draws the caller refreshes before each step
+        (default: a buffer of zeros, self.uniforms, to be filled in place); the
+        workspace grows to what the sampling calls need for vocabulary V."""
+        if temperature is None:
+            self.temperature = None
+            return
+        need = pld_verify_sample_workspace_bytes(self.B, self.K, V, PLD_BF16 if bf16 else PLD_F32)
+        if self.workspace.numel() < need:
+            self.workspace = torch.zeros(need, dtype=torch.uint8, device=self.device)
+        if uniforms is None:
+            uniforms = torch.zeros((self.B, self.K + 1), dtype=torch.float32, device=self.device)
+        self.uniforms = uniforms
+        self.row_sample = torch.full((self.B, self.K + 1), -1, dtype=torch.int32,
+                                     device=self.device)
+        self.temperature = float(temperature)
 
     def min_split(self):
         """The fewest blocks per sequence the one-call drafting accepts."""
@@ -89,6 +113,11 @@ class DraftStep:
                        stream=stream)
 
     def verify(self, logits, stream=None):
+        if self.temperature is not None:
+            pld_verify_sample(logits, self.draft, self.draft_len, self.temperature, self.uniforms,
+                              self.accept_len, self.out_tokens, self.out_count, self.workspace,
+                              row_sample=self.row_sample, stream=stream)
+            return
         pld_verify_greedy(logits, self.draft, self.draft_len, self.accept_len, self.out_tokens,
                           self.out_count, self.workspace, stream=stream)
 
@@ -212,8 +241,13 @@ class DraftStep:
                                                       self.workspace, **P)))
             ops.append(("emit", pld_emit_draft(tokens, lens, self.best_pos, self.K, self.draft,
                                                self.draft_len, **P)))
-        ops.append(("verify_argmax", pld_verify_argmax(logits, self.draft_len, self.workspace,
-                                                       **P)))
+        if self.temperature is not None:
+            ops.append(("verify_sample", pld_verify_sample_tokens(
+                logits, self.draft_len, self.temperature, self.uniforms, self.workspace,
+                row_sample=self.row_sample, **P)))
+        else:
+            ops.append(("verify_argmax", pld_verify_argmax(logits, self.draft_len,
+                                                           self.workspace, **P)))
         ops.append(("verify_accept", pld_verify_accept(self.draft, self.draft_len,
                                                        self.accept_len, self.out_tokens,
                                                        self.out_count, self.workspace, **P)))

@@ -36,6 +36,7 @@ STREAM_PLANT = 2
 STREAM_ATTN = 3
 STREAM_LOGITS = 4
 STREAM_HIDDEN = 5
+STREAM_UNIFORMS = 6
 
 
 @dataclasses.dataclass(frozen=True)
@@ -268,6 +269,12 @@ def make_logits(B: int, K: int, V: int, seed: int, draft, draft_len, boost: floa
     if bf16:
         return f32_to_bf16_bits(z), p
     return z, p
+
+
+def make_uniforms(B: int, K: int, seed: int) -> np.ndarray:
+    """The draws of sampling verification: fp32 [B][K+1], uniform on [0, 1)."""
+    return np.stack([rng_for(seed, b, STREAM_UNIFORMS).random(K + 1, dtype=np.float32)
+                     for b in range(B)])
 
 
 def intended_drafts(metas, K):

@@ -74,7 +74,7 @@ def sample_row(z, temperature, u):
         return 0
     p = np.exp((z - m) / temperature)
     c = np.cumsum(p)
-    u = min(max(float(u), 0.0), float(np.nextafter(1.0, 0.0)))
+    u = min(max(float(u), 0.0), float(np.nextafter(np.float32(1), np.float32(0))))
     v = int(np.searchsorted(c, u * c[-1], side="right"))
     if v >= len(z):
         v = int(np.flatnonzero(p > 0)[-1])

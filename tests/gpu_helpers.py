@@ -186,6 +186,91 @@ def gpu_verify(logits_dev, draft, draft_len, ws=None):
     return acc.cpu().numpy(), out.cpu().numpy(), cnt.cpu().numpy()
 
 
+def sample_workspace(B, K, V, bf16):
+    n = pld.pld_verify_sample_workspace_bytes(B, K, V, pld.PLD_BF16 if bf16 else pld.PLD_F32)
+    return torch.zeros(n, dtype=torch.uint8, device=dev())
+
+
+def gpu_verify_sample(logits_dev, draft, draft_len, temperature, uniforms, ws=None):
+    """pld_verify_sample; returns (accept_len, out_tokens, out_count, row_sample) and checks
+    that the shared leading part of the workspace is zero again."""
+    B, K1, V = logits_dev.shape
+    bf16 = logits_dev.dtype == torch.bfloat16
+    acc = torch.full((B,), -7, dtype=torch.int32, device=dev())
+    out = torch.full((B, K1), -7, dtype=torch.int32, device=dev())
+    cnt = torch.full((B,), -7, dtype=torch.int32, device=dev())
+    rows = torch.full((B, K1), -7, dtype=torch.int32, device=dev())
+    ws = sample_workspace(B, K1 - 1, V, bf16) if ws is None else ws
+    u = uniforms if torch.is_tensor(uniforms) else d_f32(uniforms)
+    pld.pld_verify_sample(logits_dev, d_i32(draft), d_i32(draft_len), temperature, u, acc, out,
+                          cnt, ws, row_sample=rows)
+    torch.cuda.synchronize()
+    assert_ws_zero(ws[:pld.pld_workspace_bytes(B, K1 - 1)])
+    return acc.cpu().numpy(), out.cpu().numpy(), cnt.cpu().numpy(), rows.cpu().numpy()
+
+
+SAMPLE_EPS = 1e-5   # fp32 mass sums vs the fp64 oracle: tolerance on the target, relative to S
+
+
+def sample_window_ok(z, temperature, u, y, eps=SAMPLE_EPS):
+    """Is y the inverse-CDF sample of softmax(z / temperature) at u for a target
+    within eps * S of u * S (fp64 masses)?  z: one row as float64."""
+    m = z.max()
+    if m == -np.inf:
+        return y == 0
+    if not 0 <= y < len(z):
+        return False
+    p = np.exp((z - m) / temperature)
+    c = np.cumsum(p)
+    S = c[-1]
+    u = min(max(float(u), 0.0), float(np.nextafter(np.float32(1), np.float32(0))))
+    if u != u:
+        u = 0.0
+    t = u * S
+    before = c[y - 1] if y > 0 else 0.0
+    return bool(p[y] > 0 and c[y] > t - eps * S and before <= t + eps * S)
+
+
+def check_sample(z_rows, temperature, uniforms, draft, draft_len, g, r, what="",
+                 max_flip_frac=0.15):
+    """GPU sampling verification against the oracle's.  Rows past the draft and
+    invalid lengths must match exactly; each sampled row must equal the oracle's
+    token or be one that a target within SAMPLE_EPS * S would give (a flip, from
+    fp32 vs fp64 mass sums, counted); acceptance and outputs must follow exactly
+    from the GPU's own samples.  z_rows(b, i) -> float64 row.  Returns flips."""
+    ga, go, gc, gy = g
+    ra, ro, rc, ry = r
+    B, K1 = gy.shape
+    K = K1 - 1
+    flips = rows = 0
+    for b in range(B):
+        L = int(draft_len[b])
+        if L < 0 or L > K:
+            assert (ga[b], gc[b]) == (-1, 0) and (go[b] == -1).all() and (gy[b] == -1).all(), \
+                f"{what} b={b}: invalid length"
+            continue
+        assert (gy[b, L + 1:] == -1).all(), f"{what} b={b}: rows past the draft"
+        for i in range(L + 1):
+            rows += 1
+            if gy[b, i] != ry[b, i]:
+                flips += 1
+                assert sample_window_ok(z_rows(b, i), temperature, uniforms[b, i], int(gy[b, i])), \
+                    f"{what} b={b} i={i}: GPU {gy[b, i]} vs oracle {ry[b, i]} is no rounding flip"
+        a = 0
+        while a < L and gy[b, a] == draft[b, a]:
+            a += 1
+        want = np.full(K1, -1, np.int32)
+        want[:a] = draft[b, :a]
+        want[a] = gy[b, a]
+        assert ga[b] == a and gc[b] == a + 1, f"{what} b={b}: accept {ga[b]} vs {a}"
+        assert np.array_equal(go[b], want), f"{what} b={b}: out_tokens"
+    assert flips <= max(3, max_flip_frac * rows), f"{what}: {flips} of {rows} rows flipped"
+    if flips:
+        print(f"  {what}: {flips} of {rows} sampled rows differ from the oracle within the "
+              f"rounding window", flush=True)
+    return flips
+
+
 def check_verify(g, r, what=""):
     ga, go, gc = g
     ra, ro, rc = r[:3]

@@ -78,6 +78,16 @@ def test_workspace_and_scratch_bytes():
     assert pld.pld_draft_workspace_bytes(8, 1024) > pld.pld_draft_workspace_bytes(8, 37)
     assert pld.pld_draft_workspace_bytes(8, 1025) == 0
     assert pld.pld_draft_workspace_bytes(0, 4) == 0
+    # sampling verification: the shared part, then (max, mass) per 512-vector
+    # segment of each of the B*(K+1) rows
+    f32, bf16 = pld.PLD_F32, pld.PLD_BF16
+    assert pld.pld_verify_sample_workspace_bytes(8, 10, 32000, f32) >= \
+        pld.pld_workspace_bytes(8, 10) + 8 * 11 * 16 * 8
+    assert pld.pld_verify_sample_workspace_bytes(64, 16, 128256, bf16) >= \
+        pld.pld_workspace_bytes(64, 16) + 64 * 17 * 32 * 8
+    assert pld.pld_verify_sample_workspace_bytes(1, 1, 1, f32) > pld.pld_workspace_bytes(1, 1)
+    assert pld.pld_verify_sample_workspace_bytes(0, 1, 5, f32) == 0
+    assert pld.pld_verify_sample_workspace_bytes(1, 1, 5, 7) == 0
 
 
 P = ctypes.c_void_p
@@ -164,3 +174,27 @@ def test_draft_host_validation():
     assert call(20000, 3, ws_bytes=pld.pld_draft_workspace_bytes(2, 3) - 1) == E_WS
     assert call(100, 3, K=0) == E_INV
     assert call(100, 3, cap=99) == E_INV
+
+
+def test_verify_sample_host_validation():
+    """Checks made before any launch: temperature, uniforms and their stride,
+    workspace size, and the checks shared with pld_verify_greedy."""
+    lib = pld._load()
+    E_INV, E_AL, E_WS = pld.PLD_ERR_INVALID, pld.PLD_ERR_ALIGN, pld.PLD_ERR_WORKSPACE
+    B, K, V = 2, 3, 1000
+    need = pld.pld_verify_sample_workspace_bytes(B, K, V, pld.PLD_F32)
+
+    def call(tau=1.0, u=F, u_stride=K + 1, ws_bytes=need, V=V, dtype=pld.PLD_F32, K=K):
+        return lib.pld_verify_sample(F, dtype, (K + 1) * V, V, V, K, F, F, B, tau, u, u_stride,
+                                     F, F, F, NULL, F, ws_bytes, NULL)
+
+    for tau in (0.0, -2.0, math.inf, -math.inf, math.nan, 1e-45):
+        assert call(tau=tau) == E_INV, tau
+    assert call(u=NULL) == E_INV
+    assert call(u_stride=K) == E_INV
+    assert call(u=MIS) == E_AL
+    assert call(ws_bytes=need - 1) == E_WS
+    assert call(ws_bytes=pld.pld_workspace_bytes(B, K)) == E_WS
+    assert call(V=0) == E_INV
+    assert call(dtype=5) == E_INV
+    assert call(K=0) == E_INV

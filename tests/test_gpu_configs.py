@@ -14,6 +14,7 @@ import pytest
 import torch
 
 import oracle
+import paper_2412_01447_amd as pld
 import synth
 from gpu_helpers import (check_best, check_find, check_scores, check_verify, d_bf16, d_f32,
                          d_i32, draft_keys_zero, gpu_emit, gpu_verify, say, sparse_hidden_rows)
@@ -97,4 +98,44 @@ def test_config_step_parity(cid, structured, mode):
     # accepted lengths cover a range (the planted prefixes work)
     say("  accept lengths:", np.bincount(rver[0], minlength=cfg.K + 1).tolist())
     del step, w, zd
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+def test_config_verify_sample(cid):
+    """Sampling verification at temperature 1 (the paper's sampling setting) at
+    each workload's full logits shape, issued as the benchmark issues it (the
+    prepared sampling half, then the acceptance), against the oracle on every
+    row: rounding flips counted and window-checked, acceptance exact."""
+    from gpu_helpers import check_sample
+    cfg = synth.CONFIGS[cid]
+    say("config sample", cid, cfg.name)
+    dev = torch.device("cuda:0")
+    toks, lens, metas = synth.make_tokens(cfg)
+    draft, dlen = synth.intended_drafts(metas, cfg.K)
+    bf16 = cfg.logits == "bf16"
+    z, _ = synth.make_logits(cfg.B, cfg.K, cfg.V, cfg.seed, draft, dlen, bf16=bf16)
+    U = synth.make_uniforms(cfg.B, cfg.K, cfg.seed)
+    ref = oracle.verify_sample(z, draft, dlen, 1.0, U, bf16=bf16)
+    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev)
+    step.set_sampling(1.0, cfg.V, bf16, uniforms=d_f32(U))
+    step.draft.copy_(d_i32(draft))
+    step.draft_len.copy_(d_i32(dlen))
+    zd = d_bf16(z) if bf16 else d_f32(z)
+    ops = dict(step.plan(d_i32(toks), d_i32(lens), zd, hidden=None, attn=None))
+    ops["verify_sample"]()
+    ops["verify_accept"]()
+    torch.cuda.synchronize()
+    assert int(torch.count_nonzero(step.workspace[:pld.pld_workspace_bytes(cfg.B, cfg.K)])) == 0
+    got = (step.accept_len.cpu().numpy(), step.out_tokens.cpu().numpy(),
+           step.out_count.cpu().numpy(), step.row_sample.cpu().numpy())
+
+    def z_rows(b, i):
+        r = synth.bf16_bits_to_f32(z[b, i]) if bf16 else z[b, i]
+        return np.asarray(r, np.float64)
+
+    flips = check_sample(z_rows, 1.0, U, draft, dlen, got, ref, cfg.name, max_flip_frac=0.25)
+    say("  sampled-row flips:", flips, " accept lengths:",
+        np.bincount(got[0][got[0] >= 0], minlength=cfg.K + 1).tolist())
+    del step, zd
     torch.cuda.empty_cache()

@@ -1,0 +1,207 @@
+"""GPU parity of sampling verification (pld_verify_sample) against the oracle.
+
+The kernels sum fp32 masses where the oracle sums fp64 ones, so a row's token
+may differ from the oracle's when the target lands within rounding of a
+boundary between two tokens: such rows are counted and each must pass the
+window check of gpu_helpers.sample_window_ok.  Rows with exactly representable
+masses (equal or -inf logits) and u = 0 must match exactly; the acceptance
+and emitted tokens must follow exactly from the GPU's own samples.  Stratified
+uniforms pin the sampled distribution itself: token counts follow softmax.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2412_01447_amd as pld
+import synth
+from gpu_helpers import (check_sample, d_bf16, d_f32, d_i32, gpu_verify, gpu_verify_sample,
+                         sample_workspace, say, workspace)
+
+pytestmark = pytest.mark.gpu
+
+SAMPLE_CASES = [
+    # (B, K, V, bf16, integer_valued, temperature, seed)
+    (3, 4, 1, False, False, 1.0, 0),
+    (5, 6, 7, False, True, 1.0, 1),
+    (5, 6, 7, True, True, 0.5, 2),
+    (4, 10, 1001, False, False, 1.0, 3),
+    (4, 10, 1001, True, False, 2.0, 4),
+    (2, 3, 1000003, False, False, 1.0, 5),     # 489 segments: the segment search loops
+    (8, 10, 32000, False, False, 1.0, 6),
+    (6, 16, 128256, True, False, 0.7, 7),
+    (3, 32, 128256, False, True, 1.0, 8),
+    (4, 8, 50000, False, False, 0.05, 9),      # nearly greedy
+    (4, 8, 50000, True, False, 50.0, 10),      # nearly uniform
+]
+
+
+def _rows_fn(zbits, bf16):
+    def z_rows(b, i):
+        r = synth.bf16_bits_to_f32(zbits[b, i]) if bf16 else zbits[b, i]
+        return np.asarray(r, np.float64)
+    return z_rows
+
+
+def _case_inputs(B, K, V, integer, seed):
+    rng = np.random.default_rng(seed)
+    if integer:
+        Z = rng.integers(-3, 4, size=(B, K + 1, V)).astype(np.float32)
+    else:
+        Z = rng.standard_normal((B, K + 1, V)).astype(np.float32)
+    L = rng.integers(0, K + 1, size=B).astype(np.int32)
+    draft = np.full((B, K), -1, np.int32)
+    for b in range(B):
+        draft[b, :L[b]] = rng.integers(0, V, size=L[b])
+        for i in range(rng.integers(0, L[b] + 1)):
+            Z[b, i, draft[b, i]] = 10.0            # likely accepted prefix
+    U = rng.random((B, K + 1), dtype=np.float32)
+    U[0, 0] = 0.0
+    U[0, 1] = np.nan
+    U[1 % B, 0] = 1.0
+    U[1 % B, 1] = -0.25
+    if B > 2:
+        L[2] = K + 1                                # invalid draft length
+    return Z, L, draft, U
+
+
+@pytest.mark.parametrize("case", SAMPLE_CASES,
+                         ids=[f"B{c[0]}_K{c[1]}_V{c[2]}_{'bf16' if c[3] else 'f32'}_t{c[5]}"
+                              for c in SAMPLE_CASES])
+def test_verify_sample_parity(case):
+    B, K, V, bf16, integer, tau, seed = case
+    say("verify_sample", case)
+    Z, L, draft, U = _case_inputs(B, K, V, integer, seed)
+    zbits = synth.f32_to_bf16_bits(Z) if bf16 else Z
+    ref = oracle.verify_sample(zbits, draft, L, tau, U, bf16=bf16)
+    zd = d_bf16(zbits) if bf16 else d_f32(Z)
+    got = gpu_verify_sample(zd, draft, L, tau, U)
+    check_sample(_rows_fn(zbits, bf16), tau, U, draft, L, got, ref, str(case))
+    # u = 0 takes the first token with mass: exact on both sides while no mass
+    # underflows fp32 (small temperatures send far tokens below 2^-126)
+    if tau >= 0.5:
+        assert got[3][0, 0] == ref[3][0, 0]
+
+
+def test_verify_sample_exact_rows():
+    """Rows whose masses are exact in fp32: every token must equal the oracle's and
+    the value the definition gives by hand."""
+    say("verify_sample exact rows")
+    B, K, V = 2, 7, 1024
+    Z = np.zeros((B, K + 1, V), np.float32)
+    U = np.zeros((B, K + 1), np.float32)
+    want = np.zeros((B, K + 1), np.int64)
+    Z[0, 0] = -np.inf                                   # no mass at all: token 0
+    U[0, 0], want[0, 0] = 0.7, 0
+    Z[0, 1] = -np.inf
+    Z[0, 1, 123] = 3.0                                  # one finite logit
+    U[0, 1], want[0, 1] = 1.0, 123
+    Z[0, 2] = -np.inf
+    Z[0, 2, [5, 700]] = 2.5                             # two equal logits: halves
+    U[0, 2], want[0, 2] = 0.25, 5
+    Z[0, 3] = Z[0, 2]
+    U[0, 3], want[0, 3] = 0.5, 700                      # t = S/2 = C(5) exactly: not > t
+    Z[0, 4] = -np.inf
+    Z[0, 4, V - 1] = -1.0                               # the last element only
+    U[0, 4], want[0, 4] = np.nan, V - 1
+    for i, j in zip(range(5, 8), (0, 517, 1023)):       # uniform rows: t = j + 1/2
+        U[0, i], want[0, i] = (j + 0.5) / V, j
+    for i, j in zip(range(8), (1, 2, 99, 256, 511, 512, 1000, 1022)):
+        U[1, i], want[1, i] = (j + 0.5) / V, j
+    Z[1, 7, :512] = -np.inf                             # half the row masked: t = 255.5 of 512
+    U[1, 7], want[1, 7] = (255 + 0.5) / 512, 512 + 255
+    draft = np.zeros((B, K), np.int32)
+    L = np.array([K, K], np.int32)
+    for dt in ("f32", "bf16"):
+        bf16 = dt == "bf16"
+        zbits = synth.f32_to_bf16_bits(Z) if bf16 else Z
+        ref = oracle.verify_sample(zbits, draft, L, 1.0, U, bf16=bf16)
+        assert np.array_equal(ref[3], want), f"{dt}: oracle {ref[3]} vs {want}"
+        got = gpu_verify_sample(d_bf16(zbits) if bf16 else d_f32(Z), draft, L, 1.0, U)
+        for g, r, name in zip(got, ref, ("accept_len", "out_tokens", "out_count", "row_sample")):
+            assert np.array_equal(g, r), f"{dt} {name}: {g} vs {r}"
+
+
+@pytest.mark.parametrize("V,scale,bf16", [(37, 1.0, False), (37, 2.0, True), (3000, 3.0, False)])
+def test_verify_sample_stratified_counts(V, scale, bf16):
+    """One logits row repeated over N = 2B rows with uniforms (j + 1/2) / N: the
+    number of rows that draw tokens <= v is N * CDF(v) up to the rounding of
+    the boundaries, a property of the sampled distribution, not of the oracle."""
+    say("verify_sample stratified", V, scale, bf16)
+    B, K, tau = 4096, 1, 0.8
+    rng = np.random.default_rng(V)
+    row = (rng.standard_normal(V) * scale).astype(np.float32)
+    if bf16:
+        row = synth.bf16_bits_to_f32(synth.f32_to_bf16_bits(row))
+    Z = np.broadcast_to(row, (B, K + 1, V)).copy()
+    N = B * (K + 1)
+    U = ((np.arange(N, dtype=np.float64) + 0.5) / N).astype(np.float32).reshape(B, K + 1)
+    draft = np.zeros((B, K), np.int32)
+    L = np.full(B, K, np.int32)
+    zd = d_bf16(synth.f32_to_bf16_bits(Z)) if bf16 else d_f32(Z)
+    got = gpu_verify_sample(zd, draft, L, tau, U)
+    y = got[3].reshape(-1)
+    assert (y >= 0).all() and (y < V).all()
+    p = np.exp((row.astype(np.float64) - row.max()) / tau)
+    cdf = np.cumsum(p) / p.sum()
+    counts = np.bincount(y, minlength=V)
+    dev = np.abs(np.cumsum(counts) - N * cdf)
+    assert dev.max() <= 2.0, f"cumulative counts off by {dev.max():.2f}"
+
+
+def test_verify_sample_misaligned_row_views():
+    """Rows that start off a 16-byte boundary: the head and tail elements."""
+    say("verify_sample misaligned")
+    rng = np.random.default_rng(19)
+    B, K, V = 3, 5, 5001
+    Z = rng.standard_normal((B, K + 1, V + 7)).astype(np.float32)
+    draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+    L = np.array([5, 2, 0], np.int32)
+    U = rng.random((B, K + 1), dtype=np.float32)
+    for off in (1, 2, 3, 5):
+        view = np.ascontiguousarray(Z[:, :, off:off + V])
+        ref = oracle.verify_sample(view, draft, L, 1.0, U)
+        got = gpu_verify_sample(d_f32(Z)[:, :, off:off + V], draft, L, 1.0, U)
+        check_sample(_rows_fn(view, False), 1.0, U, draft, L, got, ref, f"f32 offset {off}")
+        zb = np.ascontiguousarray(synth.f32_to_bf16_bits(Z)[:, :, off:off + V])
+        refb = oracle.verify_sample(zb, draft, L, 1.0, U, bf16=True)
+        gotb = gpu_verify_sample(d_bf16(synth.f32_to_bf16_bits(Z))[:, :, off:off + V], draft, L,
+                                 1.0, U)
+        check_sample(_rows_fn(zb, True), 1.0, U, draft, L, gotb, refb, f"bf16 offset {off}")
+
+
+def test_verify_sample_host_errors_and_workspace_sharing():
+    """Bad temperatures, strides and workspaces raise; one workspace serves the
+    greedy and the sampling calls in turn; repeated calls are bit-identical."""
+    say("verify_sample errors and workspace")
+    rng = np.random.default_rng(23)
+    B, K, V = 4, 6, 4099
+    Z = rng.standard_normal((B, K + 1, V)).astype(np.float32)
+    draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+    L = np.array([6, 3, 0, 5], np.int32)
+    U = rng.random((B, K + 1), dtype=np.float32)
+    zd, dd, dl, du = d_f32(Z), d_i32(draft), d_i32(L), d_f32(U)
+    acc = torch.zeros(B, dtype=torch.int32, device=zd.device)
+    out = torch.zeros((B, K + 1), dtype=torch.int32, device=zd.device)
+    cnt = torch.zeros(B, dtype=torch.int32, device=zd.device)
+    small = workspace(B, K)
+    for tau in (0.0, -1.0, float("inf"), float("nan"), 1e-45):
+        with pytest.raises(pld.PLDError):
+            pld.pld_verify_sample(zd, dd, dl, tau, du, acc, out, cnt, sample_workspace(B, K, V, False))
+    with pytest.raises(pld.PLDError) as e:
+        pld.pld_verify_sample(zd, dd, dl, 1.0, du, acc, out, cnt, small)
+    assert e.value.status == 3
+    with pytest.raises(TypeError):
+        pld.pld_verify_sample(zd, dd, dl, 1.0, du[:, :K], acc, out, cnt,
+                              sample_workspace(B, K, V, False))
+    torch.cuda.synchronize()
+
+    ws = sample_workspace(B, K, V, False)
+    ref = oracle.verify_sample(Z, draft, L, 1.3, U)
+    first = gpu_verify_sample(zd, draft, L, 1.3, U, ws=ws)
+    greedy = gpu_verify(zd, draft, L, ws=ws[:pld.pld_workspace_bytes(B, K)])
+    assert np.array_equal(greedy[0], oracle.verify(Z, draft, L)[0])
+    second = gpu_verify_sample(zd, draft, L, 1.3, U, ws=ws)
+    for a, b in zip(first, second):
+        assert np.array_equal(a, b)
+    check_sample(_rows_fn(Z, False), 1.3, U, draft, L, first, ref, "shared workspace")
