@@ -74,11 +74,16 @@ def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fu
         out["select"] = B * 8 * 2 + B * 8
     out["emit"] = int(B * K * 4 * 2)
     rows = draft_len.astype(np.int64) + 1
-    # the logits rows i <= L once, plus (sampling) the draws those rows use
-    out["verify_sample" if sample else "verify_argmax"] = int(
-        (rows * cfg.V * elt_logits).sum() + (rows.sum() * 4 if sample else 0))
-    out["verify_accept"] = int(((draft_len.astype(np.int64) + 1) * 8 * 2).sum() + B * K * 4 +
-                               B * (K + 1) * 4)
+    if sample:
+        # statistics: the logits rows i <= L once, one (max, mass) pair per segment
+        # written; finish: the pairs and the draws read, the tokens written (the
+        # re-read of one segment per row is the method's choice, not counted)
+        nseg = max(1, -(-(cfg.V * elt_logits // 16) // 512))
+        out["verify_sample_stats"] = int((rows * cfg.V * elt_logits).sum() + rows.sum() * nseg * 8)
+        out["verify_sample_finish"] = int(rows.sum() * (nseg * 8 + 4) + B * K * 4 + B * (K + 1) * 4)
+    else:
+        out["verify_argmax"] = int((rows * cfg.V * elt_logits).sum())
+        out["verify_accept"] = int((rows * 8 * 2).sum() + B * K * 4 + B * (K + 1) * 4)
     if fused:   # one launch does find, rank, select and emit
         out["draft"] = sum(out.pop(k) for k in ("find", "score_hidden", "score_attn", "select",
                                                 "select_attn", "emit") if k in out)
@@ -90,7 +95,8 @@ KERNELS = {"draft": "pld::draft_", "find": "pld::find_", "score_hidden": "pld::r
            "score_attn": "pld::rank_attn_kernel", "select": "pld::rank_finish_kernel",
            "select_attn": "pld::rank_finish_kernel", "emit": "pld::emit_kernel",
            "verify_argmax": "pld::verify_argmax_kernel", "verify_accept": "pld::verify_accept_kernel",
-           "verify_sample": "pld::sample_"}
+           "verify_sample_stats": "pld::sample_stats_kernel",
+           "verify_sample_finish": "pld::sample_finish_kernel"}
 
 
 class TimingEvents:

@@ -209,7 +209,8 @@ int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride, int64
  *   temperature  tau > 0, finite, with log2(e) / tau representable in fp32
  *   uniforms     fp32 [B][u_stride] device memory, u_stride >= K+1, 4-byte
  *                aligned; u < 0 or NaN counts as 0, u >= 1 as the largest
- *                float below 1.  Only entries i <= draft_len[b] are read.
+ *                float below 1.  Entries i <= draft_len[b] are used (others
+ *                of the first K+1 may be read ahead and are ignored).
  *   row_sample   int32 [B][K+1] or NULL: y_i for i <= L, -1 for the rows
  *                past the draft (all -1 when draft_len is out of range)
  *   workspace    at least pld_verify_sample_workspace_bytes(B, K, V, dtype)
@@ -222,8 +223,10 @@ int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride, int64
  * element with nonzero mass is taken.  +inf and NaN logits are outside the
  * contract.  Results are bit-identical from run to run.
  * Errors: as pld_verify_greedy, plus PLD_ERR_INVALID for a bad temperature,
- * NULL uniforms or u_stride < K+1 and PLD_ERR_ALIGN for misaligned uniforms.
+ * K+1 > PLD_MAX_SAMPLE_ROWS, NULL uniforms or u_stride < K+1, and
+ * PLD_ERR_ALIGN for misaligned uniforms.
  */
+#define PLD_MAX_SAMPLE_ROWS 16384
 int pld_verify_sample(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
                       int V, int K, const int32_t *draft, const int32_t *draft_len, int B,
                       double temperature, const float *uniforms, int64_t u_stride,
@@ -247,11 +250,14 @@ size_t pld_verify_sample_workspace_bytes(int B, int K, int V, int dtype);
  *   best_score and returns the workspace to zero.
  * pld_verify_argmax -- y_i = argmax_v Z[b][i][v] for the rows i <= draft_len[b],
  *   kept in the workspace.
- * pld_verify_sample_tokens -- the sampling half of pld_verify_sample: y_i
- *   for the rows i <= draft_len[b] (and row_sample, may be NULL), kept in the
- *   workspace in the same form, so that pld_verify_accept finishes it.
  * pld_verify_accept -- the accepted length and emitted tokens from those
- *   row tokens (Sec. 4.4); returns the workspace to zero.
+ *   row maxima (Sec. 4.4); returns the workspace to zero.
+ * pld_verify_sample_stats -- the streaming pass of pld_verify_sample: per
+ *   512-vector segment of each row i <= draft_len[b], the segment maximum and
+ *   the mass relative to it, into the workspace's statistics region.
+ * pld_verify_sample_finish -- the rest of pld_verify_sample from those
+ *   statistics: the segment each target falls in, re-read to find y_i, then
+ *   the acceptance and outputs; the same temperature as the statistics.
  * Arguments and errors as in the combined calls.
  */
 int pld_score_hidden(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
@@ -275,11 +281,17 @@ int pld_verify_accept(const int32_t *draft, const int32_t *draft_len, int B, int
                       int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
                       void *workspace, size_t workspace_bytes, void *stream);
 
-int pld_verify_sample_tokens(const void *logits, int dtype, int64_t l_seq_stride,
-                             int64_t l_row_stride, int V, int K, const int32_t *draft_len, int B,
-                             double temperature, const float *uniforms, int64_t u_stride,
-                             int32_t *row_sample, void *workspace, size_t workspace_bytes,
-                             void *stream);
+int pld_verify_sample_stats(const void *logits, int dtype, int64_t l_seq_stride,
+                            int64_t l_row_stride, int V, int K, const int32_t *draft_len, int B,
+                            double temperature, void *workspace, size_t workspace_bytes,
+                            void *stream);
+
+int pld_verify_sample_finish(const void *logits, int dtype, int64_t l_seq_stride,
+                             int64_t l_row_stride, int V, int K, const int32_t *draft,
+                             const int32_t *draft_len, int B, double temperature,
+                             const float *uniforms, int64_t u_stride, int32_t *accept_len,
+                             int32_t *out_tokens, int32_t *out_count, int32_t *row_sample,
+                             void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * pld_verify_sample -- sampling verification (Sec. 3 and Sec. 4.4 with a
@@ -294,7 +306,8 @@ int pld_verify_sample_tokens(const void *logits, int dtype, int64_t l_seq_stride
  *   temperature  tau > 0, finite, with log2(e) / tau representable in fp32
  *   uniforms     fp32 [B][u_stride] device memory, u_stride >= K+1, 4-byte
  *                aligned; u < 0 or NaN counts as 0, u >= 1 as the largest
- *                float below 1.  Only entries i <= draft_len[b] are read.
+ *                float below 1.  Entries i <= draft_len[b] are used (others
+ *                of the first K+1 may be read ahead and are ignored).
  *   row_sample   int32 [B][K+1] or NULL: y_i for i <= L, -1 for the rows
  *                past the draft (all -1 when draft_len is out of range)
  *   workspace    at least pld_verify_sample_workspace_bytes(B, K, V, dtype)
@@ -307,8 +320,10 @@ int pld_verify_sample_tokens(const void *logits, int dtype, int64_t l_seq_stride
  * element with nonzero mass is taken.  +inf and NaN logits are outside the
  * contract.  Results are bit-identical from run to run.
  * Errors: as pld_verify_greedy, plus PLD_ERR_INVALID for a bad temperature,
- * NULL uniforms or u_stride < K+1 and PLD_ERR_ALIGN for misaligned uniforms.
+ * K+1 > PLD_MAX_SAMPLE_ROWS, NULL uniforms or u_stride < K+1, and
+ * PLD_ERR_ALIGN for misaligned uniforms.
  */
+#define PLD_MAX_SAMPLE_ROWS 16384
 int pld_verify_sample(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
                       int V, int K, const int32_t *draft, const int32_t *draft_len, int B,
                       double temperature, const float *uniforms, int64_t u_stride,

@@ -21,13 +21,15 @@ __all__ = [
     "pld_draft_hidden", "pld_draft_attn", "pld_draft_workspace_bytes", "DRAFT_MAX_TOK_STRIDE",
     "DRAFT_MAX_PART", "pld_score_hidden",
     "pld_score_attn", "pld_select_best", "pld_verify_argmax", "pld_verify_accept",
-    "pld_verify_sample", "pld_verify_sample_workspace_bytes", "pld_verify_sample_tokens",
+    "pld_verify_sample", "pld_verify_sample_workspace_bytes", "pld_verify_sample_stats",
+    "pld_verify_sample_finish", "PLD_MAX_SAMPLE_ROWS",
 ]
 
 PLD_OK, PLD_ERR_INVALID, PLD_ERR_ALIGN, PLD_ERR_WORKSPACE, PLD_ERR_LAUNCH = range(5)
 PLD_F32, PLD_BF16 = 0, 1
 PLD_AGG_SUM, PLD_AGG_MAX = 0, 1
 PLD_MAX_NGRAM, PLD_MAX_HIDDEN, PLD_MAX_BATCH, PLD_MAX_DRAFT_SPLIT = 8, 16384, 4096, 1024
+PLD_MAX_SAMPLE_ROWS = 16384
 DRAFT_MAX_TOK_STRIDE = 8192     # one-call drafting, one block per sequence (S = 1)
 DRAFT_MAX_PART = 8192           # one-call drafting, S > 1: positions per block
 
@@ -63,8 +65,11 @@ _SIGNATURES = {
     "pld_verify_accept": ([_vp, _vp, _int, _int, _vp, _vp, _vp, _vp, _sz, _vp], _int),
     "pld_verify_sample": ([_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int, ctypes.c_double, _vp,
                            _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp], _int),
-    "pld_verify_sample_tokens": ([_vp, _int, _i64, _i64, _int, _int, _vp, _int, ctypes.c_double,
-                                  _vp, _i64, _vp, _vp, _sz, _vp], _int),
+    "pld_verify_sample_stats": ([_vp, _int, _i64, _i64, _int, _int, _vp, _int, ctypes.c_double,
+                                 _vp, _sz, _vp], _int),
+    "pld_verify_sample_finish": ([_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int,
+                                  ctypes.c_double, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
+                                 _int),
     "pld_draft_hidden": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _i64, _i64, _int, _f32, _int,
                           _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _int, _vp, _sz, _vp],
                          _int),
@@ -247,22 +252,7 @@ def pld_verify_sample(logits, draft, draft_len, temperature, uniforms, accept_le
                       out_count, workspace, row_sample=None, stream=None, prepare=False):
     """Sampling verification: y_i drawn from softmax(logits / temperature) at uniforms [B][>=K+1]
     (fp32); outputs as pld_verify_greedy, plus the per-row samples when row_sample is given."""
-    import torch
-    if logits.dtype not in (torch.float32, torch.bfloat16):
-        raise TypeError("logits must be float32 or bfloat16")
-    _need(logits, logits.dtype, "logits", 3)
-    _need(uniforms, torch.float32, "uniforms", 2)
-    B, K1, V = logits.shape
-    K = K1 - 1
-    if draft.shape != (B, K) or draft.stride(0) != K:
-        raise TypeError("draft must be a contiguous [B][K] tensor")
-    if out_tokens.shape != (B, K1) or out_tokens.stride(0) != K1:
-        raise TypeError("out_tokens must be a contiguous [B][K+1] tensor")
-    if uniforms.shape[0] != B or uniforms.shape[1] < K1:
-        raise TypeError("uniforms must be [B][>=K+1]")
-    if row_sample is not None and (row_sample.shape != (B, K1) or row_sample.stride(0) != K1):
-        raise TypeError("row_sample must be a contiguous [B][K+1] tensor")
-    dtype = PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
+    B, K, V, dtype = _sample_shapes(logits, draft, uniforms, out_tokens, row_sample)
     return _run("pld_verify_sample", (_ptr(logits), dtype, logits.stride(0), logits.stride(1), V, K,
           _ptr(draft), _ptr(draft_len), B, float(temperature), _ptr(uniforms), uniforms.stride(0),
           _ptr(accept_len), _ptr(out_tokens), _ptr(out_count), _ptr(row_sample), _ptr(workspace),
@@ -352,24 +342,44 @@ def pld_verify_argmax(logits, draft_len, workspace, stream=None, prepare=False):
           _ptr(draft_len), B, _ptr(workspace), _nbytes(workspace), _stream(stream),), prepare)
 
 
-def pld_verify_sample_tokens(logits, draft_len, temperature, uniforms, workspace, row_sample=None,
-                             stream=None, prepare=False):
-    """Sampled tokens of the K+1 rows (rows past each draft skipped) into the workspace."""
+def _sample_shapes(logits, draft, uniforms, out_tokens, row_sample):
     import torch
     if logits.dtype not in (torch.float32, torch.bfloat16):
         raise TypeError("logits must be float32 or bfloat16")
     _need(logits, logits.dtype, "logits", 3)
-    _need(uniforms, torch.float32, "uniforms", 2)
     B, K1, V = logits.shape
-    if uniforms.shape[0] != B or uniforms.shape[1] < K1:
-        raise TypeError("uniforms must be [B][>=K+1]")
+    if draft is not None and (draft.shape != (B, K1 - 1) or draft.stride(0) != K1 - 1):
+        raise TypeError("draft must be a contiguous [B][K] tensor")
+    if uniforms is not None:
+        _need(uniforms, torch.float32, "uniforms", 2)
+        if uniforms.shape[0] != B or uniforms.shape[1] < K1:
+            raise TypeError("uniforms must be [B][>=K+1]")
+    if out_tokens is not None and (out_tokens.shape != (B, K1) or out_tokens.stride(0) != K1):
+        raise TypeError("out_tokens must be a contiguous [B][K+1] tensor")
     if row_sample is not None and (row_sample.shape != (B, K1) or row_sample.stride(0) != K1):
         raise TypeError("row_sample must be a contiguous [B][K+1] tensor")
-    dtype = PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
-    return _run("pld_verify_sample_tokens", (_ptr(logits), dtype, logits.stride(0),
-          logits.stride(1), V, K1 - 1, _ptr(draft_len), B, float(temperature), _ptr(uniforms),
-          uniforms.stride(0), _ptr(row_sample), _ptr(workspace), _nbytes(workspace),
-          _stream(stream),), prepare)
+    return B, K1 - 1, V, PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
+
+
+def pld_verify_sample_stats(logits, draft_len, temperature, workspace, stream=None,
+                            prepare=False):
+    """Streaming half of sampling verification: per-segment (max, mass) of the rows
+    i <= draft_len into the workspace."""
+    B, K, V, dtype = _sample_shapes(logits, None, None, None, None)
+    return _run("pld_verify_sample_stats", (_ptr(logits), dtype, logits.stride(0),
+          logits.stride(1), V, K, _ptr(draft_len), B, float(temperature), _ptr(workspace),
+          _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_verify_sample_finish(logits, draft, draft_len, temperature, uniforms, accept_len,
+                             out_tokens, out_count, workspace, row_sample=None, stream=None,
+                             prepare=False):
+    """Second half: the sampled tokens from the statistics, then the acceptance."""
+    B, K, V, dtype = _sample_shapes(logits, draft, uniforms, out_tokens, row_sample)
+    return _run("pld_verify_sample_finish", (_ptr(logits), dtype, logits.stride(0),
+          logits.stride(1), V, K, _ptr(draft), _ptr(draft_len), B, float(temperature),
+          _ptr(uniforms), uniforms.stride(0), _ptr(accept_len), _ptr(out_tokens), _ptr(out_count),
+          _ptr(row_sample), _ptr(workspace), _nbytes(workspace), _stream(stream),), prepare)
 
 
 def pld_verify_accept(draft, draft_len, accept_len, out_tokens, out_count, workspace,

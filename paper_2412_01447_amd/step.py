@@ -13,7 +13,8 @@ from . import (DRAFT_MAX_PART, DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, PLD_BF16, PLD_
                pld_emit_draft, pld_find_candidates, pld_find_scratch_bytes, pld_rank_attn,
                pld_rank_hidden, pld_score_attn, pld_score_hidden, pld_select_best,
                pld_verify_accept, pld_verify_argmax, pld_verify_greedy, pld_verify_sample,
-               pld_verify_sample_tokens, pld_verify_sample_workspace_bytes, pld_workspace_bytes)
+               pld_verify_sample_finish, pld_verify_sample_stats, pld_verify_sample_workspace_bytes,
+               pld_workspace_bytes)
 
 
 class DraftStep:
@@ -242,12 +243,15 @@ class DraftStep:
             ops.append(("emit", pld_emit_draft(tokens, lens, self.best_pos, self.K, self.draft,
                                                self.draft_len, **P)))
         if self.temperature is not None:
-            ops.append(("verify_sample", pld_verify_sample_tokens(
-                logits, self.draft_len, self.temperature, self.uniforms, self.workspace,
+            ops.append(("verify_sample_stats", pld_verify_sample_stats(
+                logits, self.draft_len, self.temperature, self.workspace, **P)))
+            ops.append(("verify_sample_finish", pld_verify_sample_finish(
+                logits, self.draft, self.draft_len, self.temperature, self.uniforms,
+                self.accept_len, self.out_tokens, self.out_count, self.workspace,
                 row_sample=self.row_sample, **P)))
-        else:
-            ops.append(("verify_argmax", pld_verify_argmax(logits, self.draft_len,
-                                                           self.workspace, **P)))
+            return ops
+        ops.append(("verify_argmax", pld_verify_argmax(logits, self.draft_len, self.workspace,
+                                                       **P)))
         ops.append(("verify_accept", pld_verify_accept(self.draft, self.draft_len,
                                                        self.accept_len, self.out_tokens,
                                                        self.out_count, self.workspace, **P)))

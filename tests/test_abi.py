@@ -198,3 +198,14 @@ def test_verify_sample_host_validation():
     assert call(V=0) == E_INV
     assert call(dtype=5) == E_INV
     assert call(K=0) == E_INV
+    assert call(K=pld.PLD_MAX_SAMPLE_ROWS, u_stride=pld.PLD_MAX_SAMPLE_ROWS + 1,
+                ws_bytes=1 << 40) == E_INV
+    # the two halves check the same things
+    st = lib.pld_verify_sample_stats
+    assert st(F, pld.PLD_F32, (K + 1) * V, V, V, K, F, B, 0.0, F, need, NULL) == E_INV
+    assert st(F, pld.PLD_F32, (K + 1) * V, V, V, K, F, B, 1.0, F, need - 1, NULL) == E_WS
+    fin = lib.pld_verify_sample_finish
+    assert fin(F, pld.PLD_F32, (K + 1) * V, V, V, K, F, F, B, 1.0, F, K, F, F, F, NULL, F, need,
+               NULL) == E_INV
+    assert fin(F, pld.PLD_F32, (K + 1) * V, V, V, K, F, F, B, 1.0, MIS, K + 1, F, F, F, NULL, F,
+               need, NULL) == E_AL

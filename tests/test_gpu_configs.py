@@ -105,7 +105,7 @@ def test_config_step_parity(cid, structured, mode):
 def test_config_verify_sample(cid):
     """Sampling verification at temperature 1 (the paper's sampling setting) at
     each workload's full logits shape, issued as the benchmark issues it (the
-    prepared sampling half, then the acceptance), against the oracle on every
+    prepared statistics and finishing calls), against the oracle on every
     row: rounding flips counted and window-checked, acceptance exact."""
     from gpu_helpers import check_sample
     cfg = synth.CONFIGS[cid]
@@ -123,8 +123,8 @@ def test_config_verify_sample(cid):
     step.draft_len.copy_(d_i32(dlen))
     zd = d_bf16(z) if bf16 else d_f32(z)
     ops = dict(step.plan(d_i32(toks), d_i32(lens), zd, hidden=None, attn=None))
-    ops["verify_sample"]()
-    ops["verify_accept"]()
+    ops["verify_sample_stats"]()
+    ops["verify_sample_finish"]()
     torch.cuda.synchronize()
     assert int(torch.count_nonzero(step.workspace[:pld.pld_workspace_bytes(cfg.B, cfg.K)])) == 0
     got = (step.accept_len.cpu().numpy(), step.out_tokens.cpu().numpy(),

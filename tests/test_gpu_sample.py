@@ -205,3 +205,11 @@ def test_verify_sample_host_errors_and_workspace_sharing():
     for a, b in zip(first, second):
         assert np.array_equal(a, b)
     check_sample(_rows_fn(Z, False), 1.3, U, draft, L, first, ref, "shared workspace")
+    # the statistics and finishing halves give what the combined call gives
+    rows = torch.full((B, K + 1), -7, dtype=torch.int32, device=zd.device)
+    pld.pld_verify_sample_stats(zd, dl, 1.3, ws)
+    pld.pld_verify_sample_finish(zd, dd, dl, 1.3, du, acc, out, cnt, ws, row_sample=rows)
+    torch.cuda.synchronize()
+    halves = (acc.cpu().numpy(), out.cpu().numpy(), cnt.cpu().numpy(), rows.cpu().numpy())
+    for a, b in zip(first, halves):
+        assert np.array_equal(a, b)
