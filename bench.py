@@ -1,12 +1,16 @@
 #!/usr/bin/env python3
 """Benchmark of the PLD+ drafting step (find -> rank -> emit -> verify) on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--config C] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--config C] [--verify greedy|sample]
+                    [--temperature T] [--no-cpu-baseline]
 
 A step is one pass of the whole hot path over one batch of synthetic input
 already resident in HBM.  The default workload is config 2 (batch 8, context
 4096, n-grams 3..1 longest first, hidden 4096 bf16, K = 10, fp32 logits over
-32000 ids); --config picks another of the five.  To keep the caches honest the
+32000 ids); --config picks another (1-5 scale the workload up, 6 and 7 are the
+paper's attention-MAX and thresholded hidden-state settings at its input
+sizes); --verify sample verifies by sampling at --temperature (default 1)
+instead of the argmax.  To keep the caches honest the
 inputs exist in several copies at distinct addresses and consecutive steps
 rotate through them, so every step reads from HBM rather than from the 256 MB
 last-level cache.  W untimed steps run first, then exactly K steps are timed
@@ -37,7 +41,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="CPU work the oracle baseline is given (whole steps, at least one)")
@@ -206,9 +210,13 @@ def main():
         step.set_sampling(args.temperature, cfg.V, bf16,
                           uniforms=torch.from_numpy(synth.make_uniforms(cfg.B, cfg.K, cfg.seed)).to(dev))
 
+    from paper_2412_01447_amd import PLD_AGG_MAX, PLD_AGG_SUM
+    rank_args = dict(ngram=cfg.ngram, agg=PLD_AGG_MAX if cfg.agg == "max" else PLD_AGG_SUM,
+                     threshold=cfg.theta)
+
     def run(s):
         step.run(s["tokens"], s["lens"], s["logits"], hidden=s["hidden"], attn=s["attn"],
-                 ngram=cfg.ngram)
+                 **rank_args)
 
     # one step to learn the data-dependent byte counts (and, for the one-call
     # drafting, how many blocks should share a sequence)
@@ -235,7 +243,7 @@ def main():
     # every step as prepared calls (arguments marshalled once, one kernel each)
     stream = torch.cuda.current_stream()
     plans = [step.plan(s_["tokens"], s_["lens"], s_["logits"], hidden=s_["hidden"],
-                       attn=s_["attn"], ngram=cfg.ngram, stream=stream) for s_ in sets]
+                       attn=s_["attn"], stream=stream, **rank_args) for s_ in sets]
     names = [n for n, _ in plans[0]]
     assert set(names) == set(nbytes), (names, list(nbytes))
     # the dominant call is bracketed by events on every `event_every`-th timed
@@ -295,7 +303,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": cfg.name, "batch": cfg.B, "context": cfg.T, "vocab": cfg.V,
                    "ngram": list(cfg.ngram), "ranking": cfg.rank, "hidden_dim": cfg.d,
-                   "attn_rows": cfg.R, "K": cfg.K, "logits": cfg.logits,
+                   "attn_rows": cfg.R, "attn_aggregation": cfg.agg, "threshold": cfg.theta,
+                   "K": cfg.K, "logits": cfg.logits,
                    "inputs": "hidden bf16, attention f32, tokens int32",
                    "drafting": (f"one call, {step.draft_split} block(s) per sequence" if fused
                                 else "separate calls"),
@@ -332,10 +341,12 @@ def cpu_baseline(cfg, w, z, bf16, seconds, log, sampling=None):
     def one():
         p, c, n = oracle.find(toks, lens, *cfg.ngram)
         if attn is not None:
-            sa, ba, _ = oracle.rank_attn(attn, lens, p, c, oracle.AGG_SUM)
+            sa, ba, _ = oracle.rank_attn(attn, lens, p, c,
+                                         oracle.AGG_MAX if cfg.agg == "max" else oracle.AGG_SUM,
+                                         cfg.theta)
             best = ba
         if hb is not None:
-            sh, bh, _ = oracle.rank_hidden(hb, lens, p, c)
+            sh, bh, _ = oracle.rank_hidden(hb, lens, p, c, cfg.theta)
             best = bh
         dr, dl = oracle.emit(toks, lens, best, cfg.K)
         if sampling is not None:

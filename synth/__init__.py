@@ -21,6 +21,7 @@ workloads (arXiv 2412.01447, Sec. 5.1: outputs that copy spans of their input):
 * logits  -- N(0,1) verification logits [B][K+1][V]; for a random prefix of
   length p ~ U{0..K} the caller-given draft tokens get +boost (the draft is an
   input here; the generator never computes one).
+* uniforms -- the draws of sampling verification, U[0, 1) fp32 [B][K+1].
 
 Seeds are numpy SeedSequence([seed, b, stream]) per sequence and stream, so a
 sequence can be regenerated alone.
@@ -57,9 +58,11 @@ class Config:
     logits: str           # "f32" or "bf16"
     seed: int
     query_count_max: int = 0   # >0: choose a query token with at most this many hits
+    agg: str = "sum"           # attention aggregation over the R rows: "sum" or "max"
+    theta: float = float("-inf")   # ranking threshold: only scores > theta are eligible
 
 
-# The five workloads the drafting step is measured on.  Config 1 matches the
+# The workloads the drafting step is measured on.  Config 1 matches the
 # paper's input sizes (a few hundred words, Table of input lengths in App. B);
 # the others scale batch, context, vocabulary and hidden width up.
 CONFIGS = {
@@ -73,6 +76,15 @@ CONFIGS = {
               (16, 128), (1, 1), 8192, "both", 64, 16, "bf16", 3),
     5: Config("b4_t131072_v128256_d4096_hidden_k32", 4, 131072, 128256, 1.05, 0.15, (16, 128),
               (1, 1), 4096, "hidden", 0, 32, "f32", 4, query_count_max=4000),
+    # The paper's own two settings at its input sizes: PLD+(a) takes the MAX over
+    # the top-50 induction heads across layers with K = 70 (Eq. 3, Sec. 5.5 and the
+    # head-count table of Sec. 7), PLD+(h) the cosine ranking with theta = 0, the
+    # best threshold of App. B.  The last token is a frequent one (up to 64
+    # occurrences), so that ranking and threshold have candidates to act on.
+    6: Config("b1_t1024_v32000_attn_max_r50_k70", 1, 1024, 32000, 1.1, 0.40, (8, 32), (1, 1),
+              0, "attn", 50, 70, "f32", 5, query_count_max=64, agg="max"),
+    7: Config("b1_t1024_v32000_d4096_hidden_theta0_k10", 1, 1024, 32000, 1.1, 0.40, (8, 32),
+              (1, 1), 4096, "hidden", 0, 10, "f32", 6, query_count_max=64, theta=0.0),
 }
 
 

@@ -28,7 +28,9 @@ pytestmark = pytest.mark.gpu
 CASES = [(1, True, "fused"), (1, False, "split"), (2, True, "fused"), (2, False, "fused"),
          (2, True, "split"), (2, True, "fused8"), (3, True, "fused"), (3, False, "split"),
          (3, False, "fused"), (3, False, "fused1"), (4, True, "split"), (5, True, "split"),
-         (5, False, "split"), (5, True, "fused"), (5, False, "fused")]
+         (5, False, "split"), (5, True, "fused"), (5, False, "fused"),
+         (6, True, "fused"), (6, False, "fused"), (6, False, "split"), (6, True, "fused8"),
+         (7, True, "fused"), (7, False, "fused"), (7, False, "split"), (7, False, "fused8")]
 
 
 @pytest.mark.parametrize("cid,structured,mode", CASES,
@@ -42,12 +44,13 @@ def test_config_step_parity(cid, structured, mode):
     # ---- oracle, stage by stage
     cp, cc, nu = oracle.find(toks, lens, *cfg.ngram)
     ref = {}
+    agg = oracle.AGG_MAX if cfg.agg == "max" else oracle.AGG_SUM
     if w["hidden"] is not None:
         hb = sparse_hidden_rows(w["hidden"], lens, cp, cc)
-        ref["h"] = oracle.rank_hidden(hb, lens, cp, cc)
+        ref["h"] = oracle.rank_hidden(hb, lens, cp, cc, cfg.theta)
         del hb
     if w["attn"] is not None:
-        ref["a"] = oracle.rank_attn(w["attn"], lens, cp, cc, oracle.AGG_SUM)
+        ref["a"] = oracle.rank_attn(w["attn"], lens, cp, cc, agg, cfg.theta)
     drafter = ref["h"] if "h" in ref else ref["a"]
     rdraft, rdl = oracle.emit(toks, lens, drafter[1], cfg.K)
     z = synth.logits_for(w, rdraft, rdl)
@@ -65,7 +68,8 @@ def test_config_step_parity(cid, structured, mode):
     zd = d_bf16(z) if bf16 else d_f32(z)
     attn_d = d_f32(w["attn"]) if w["attn"] is not None else None
     td, ld = d_i32(toks), d_i32(lens)
-    step.run(td, ld, zd, hidden=w["hidden"], attn=attn_d, ngram=cfg.ngram)
+    step.run(td, ld, zd, hidden=w["hidden"], attn=attn_d, ngram=cfg.ngram,
+             agg=pld.PLD_AGG_MAX if cfg.agg == "max" else pld.PLD_AGG_SUM, threshold=cfg.theta)
     torch.cuda.synchronize()
     g = step.host()
     assert int(torch.count_nonzero(step.workspace).item()) == 0
@@ -75,13 +79,15 @@ def test_config_step_parity(cid, structured, mode):
     if "h" in ref:
         rsc, rbp, rbs = ref["h"]
         check_scores(g["scores"], rsc, cc, cfg.name + " hidden")
-        flips += check_best(g["best_pos"], g["best_score"], rsc, rbp, rbs, cp, cc, cfg.name)
+        flips += check_best(g["best_pos"], g["best_score"], rsc, rbp, rbs, cp, cc, cfg.name,
+                            threshold=cfg.theta)
     if "a" in ref:
         rsc, rbp, rbs = ref["a"]
         check_scores(g["scores_attn"], rsc, cc, cfg.name + " attn")
         gbp = g["best_pos_attn"] if "h" in ref else g["best_pos"]
         gbs = g["best_score_attn"] if "h" in ref else g["best_score"]
-        flips += check_best(gbp, gbs, rsc, rbp, rbs, cp, cc, cfg.name + " attn")
+        flips += check_best(gbp, gbs, rsc, rbp, rbs, cp, cc, cfg.name + " attn",
+                            threshold=cfg.theta)
     say("  near-tie flips:", flips)
     if structured and "h" in ref:
         srcs = np.array([m.query_src_end for m in w["metas"]])
@@ -101,7 +107,7 @@ def test_config_step_parity(cid, structured, mode):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5, 6])
 def test_config_verify_sample(cid):
     """Sampling verification at temperature 1 (the paper's sampling setting) at
     each workload's full logits shape, issued as the benchmark issues it (the
