@@ -14,6 +14,10 @@ out:
 * :func:`rank_attn`    -- aggregated attention ranking, Eq. 3 (Sec. 4.2.1, Sec. 7.1)
 * :func:`emit`         -- draft span x[j*+1 .. j*+K], Sec. 4.3
 * :func:`verify`       -- greedy acceptance of the longest matching prefix, Sec. 3, 4.4
+* :func:`verify_sample` -- the same acceptance on tokens drawn from softmax(Z / tau)
+* :func:`select_prefix` -- prompt lookup's selection: longest matching prefix, earliest
+  (Sec. 2, Fig. 3 caption), the baseline PLD+ replaces
+* :func:`commit`       -- the emitted tokens appended to the sequences (the generation loop)
 
 All inputs are host numpy arrays; bf16 data is passed as its uint16 bit pattern.
 """
@@ -62,8 +66,12 @@ def load_library(path):
                                    _vp, _vp]
     lib.pld_ref_verify_sample.argtypes = [_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int,
                                           ctypes.c_double, _vp, _i64, _vp, _vp, _vp, _vp]
+    lib.pld_ref_select_prefix.argtypes = [_vp, _i64, _vp, _vp, _i64, _vp, _int, _int, _vp, _vp,
+                                          _vp]
+    lib.pld_ref_commit.argtypes = [_vp, _i64, _vp, _vp, _vp, _vp, _int, _int, _vp]
     for f in (lib.pld_ref_find, lib.pld_ref_rank_hidden, lib.pld_ref_rank_attn,
-              lib.pld_ref_emit, lib.pld_ref_verify, lib.pld_ref_verify_sample):
+              lib.pld_ref_emit, lib.pld_ref_verify, lib.pld_ref_verify_sample,
+              lib.pld_ref_select_prefix, lib.pld_ref_commit):
         f.restype = _int
     return lib
 
@@ -178,6 +186,46 @@ def verify(logits, draft, draft_len, bf16=False):
                                 _p(draft_len), B, _p(acc), _p(out), _p(cnt), _p(rowarg))
     _check(rc, "verify")
     return acc, out, cnt, rowarg
+
+
+def select_prefix(tokens, lens, cand_pos, cand_count, max_match):
+    """Prompt lookup's selection (Sec. 2, Fig. 3 caption): the candidate whose
+    preceding tokens match the query's for the longest run (up to max_match),
+    the earliest among equals.  Returns (scores [B, cap] float64 match lengths,
+    NaN for out-of-range candidates; best_pos [B]; best_score [B])."""
+    tokens = _c(tokens, np.int32)
+    lens = _c(lens, np.int32)
+    cand_pos = _c(cand_pos, np.int32)
+    cand_count = _c(cand_count, np.int32)
+    B, stride = tokens.shape
+    cap = cand_pos.shape[1]
+    scores = np.zeros((B, cap), np.float64)
+    bp = np.zeros(B, np.int32)
+    bs = np.zeros(B, np.float64)
+    rc = _load().pld_ref_select_prefix(_p(tokens), stride, _p(lens), _p(cand_pos), cap,
+                                       _p(cand_count), B, int(max_match), _p(scores), _p(bp),
+                                       _p(bs))
+    _check(rc, "select_prefix")
+    return scores, bp, bs
+
+
+def commit(tokens, lens, out_tokens, out_count, limit=None, stats=None):
+    """The generation loop's append: out_tokens[b][:out_count[b]] joins sequence b
+    (capped at limit[b] and the row's capacity), lens advance, stats [B, 2] int64
+    (emitted tokens, steps) accumulate.  Works in place on copies and returns
+    (tokens, lens, stats)."""
+    tokens = np.array(tokens, np.int32, order="C")
+    lens = np.array(lens, np.int32)
+    out_tokens = _c(out_tokens, np.int32)
+    out_count = _c(out_count, np.int32)
+    B, stride = tokens.shape
+    K = out_tokens.shape[1] - 1
+    lim = None if limit is None else _c(limit, np.int32)
+    st = np.zeros((B, 2), np.int64) if stats is None else np.array(stats, np.int64)
+    rc = _load().pld_ref_commit(_p(tokens), stride, _p(lens), _p(lim), _p(out_tokens),
+                                _p(out_count), B, K, _p(st))
+    _check(rc, "commit")
+    return tokens, lens, st
 
 
 def verify_sample(logits, draft, draft_len, temperature, uniforms, bf16=False):

@@ -412,3 +412,86 @@ int pld_ref_verify_sample(const void *logits, int dtype, int64_t l_seq_stride,
     free(p);
     return REF_OK;
 }
+
+/* ------------------------------------------------------- prefix selection */
+/*
+ * Prompt lookup decoding's selection, the baseline PLD+ improves on (Sec. 2;
+ * the Fig. 3 caption: PLD proposes the candidate span with the longest
+ * matching prefix).  For a candidate j, 0 <= j <= T-2, its match length is
+ *   m_j = the largest m <= max_match with x[j-k] = x[T-1-k] for every k < m
+ *         (only indices j-k >= 0 exist),
+ * and j* = the candidate with the largest m_j, the earliest among equal
+ * lengths (prompt lookup scans the context from the start and keeps the first
+ * match).  best_score = m_j.  Out-of-range candidates get score NaN and are
+ * never chosen; a sequence with T < 2 or T > tok_stride gets best_pos = -1,
+ * best_score = -inf.  `scores` (may be NULL) has layout [B][cap].
+ */
+int pld_ref_select_prefix(const int32_t *tokens, int64_t tok_stride, const int32_t *lens,
+                          const int32_t *cand_pos, int64_t cap, const int32_t *cand_count, int B,
+                          int max_match, double *scores, int32_t *best_pos, double *best_score) {
+    if (!tokens || !lens || !cand_pos || !cand_count || !best_pos || !best_score) return REF_ERR;
+    if (B < 0 || cap < 0 || max_match < 1) return REF_ERR;
+    for (int b = 0; b < B; ++b) {
+        const int32_t *x = tokens + (int64_t)b * tok_stride;
+        const int32_t *pos = cand_pos + (int64_t)b * cap;
+        int64_t T = lens[b];
+        int64_t C = cand_count[b];
+        if (C < 0 || C > cap) C = 0;
+        int seq_ok = (T >= 2 && T <= tok_stride);
+        int32_t bj = -1;
+        double bs = -INFINITY;
+        for (int64_t c = 0; c < C; ++c) {
+            int64_t j = pos[c];
+            double s = NAN;
+            if (seq_ok && j >= 0 && j <= T - 2) {
+                int64_t m = 0;
+                while (m < max_match && j - m >= 0 && x[j - m] == x[T - 1 - m]) ++m;
+                s = (double)m;
+                if (bj < 0 || s > bs || (s == bs && j < bj)) {
+                    bs = s;
+                    bj = (int32_t)j;
+                }
+            }
+            if (scores) scores[(int64_t)b * cap + c] = s;
+        }
+        best_pos[b] = seq_ok ? bj : -1;
+        best_score[b] = seq_ok ? bs : -INFINITY;
+    }
+    return REF_OK;
+}
+
+/* ----------------------------------------------------------------- commit */
+/*
+ * The step after verification in the generation loop (Sec. 3, Sec. 4.4: the
+ * accepted draft tokens and the model's own token join the sequence):
+ *   cap_b = min(limit[b], tok_stride)   (tok_stride when limit is NULL)
+ *   m     = min(out_count[b], cap_b - T)
+ *   x[T + i] = out_tokens[b][i] for i < m;  lens[b] = T + m
+ *   stats[b] += (m, 1 if m > 0)          (emitted tokens, steps; may be NULL)
+ * A sequence with T outside [0, cap_b] or out_count outside [0, K+1] is left
+ * as it is.  The paper's average acceptance length (tokens per generation
+ * step, Sec. 5.3) is stats[b][0] / stats[b][1].
+ */
+int pld_ref_commit(int32_t *tokens, int64_t tok_stride, int32_t *lens, const int32_t *limit,
+                   const int32_t *out_tokens, const int32_t *out_count, int B, int K,
+                   int64_t *stats) {
+    if (!tokens || !lens || !out_tokens || !out_count) return REF_ERR;
+    if (B < 0 || K < 1 || tok_stride < 1) return REF_ERR;
+    for (int b = 0; b < B; ++b) {
+        int64_t cap_b = tok_stride;
+        if (limit && limit[b] < cap_b) cap_b = limit[b];
+        int64_t T = lens[b];
+        int64_t n = out_count[b];
+        if (T < 0 || T > cap_b || n < 0 || n > K + 1) continue;
+        int64_t m = n;
+        if (m > cap_b - T) m = cap_b - T;
+        for (int64_t i = 0; i < m; ++i)
+            tokens[(int64_t)b * tok_stride + T + i] = out_tokens[(int64_t)b * (K + 1) + i];
+        lens[b] = (int32_t)(T + m);
+        if (stats) {
+            stats[2 * b] += m;
+            stats[2 * b + 1] += (m > 0) ? 1 : 0;
+        }
+    }
+    return REF_OK;
+}

@@ -90,3 +90,33 @@ def verify_sample(Z, draft, temperature, u):
     while a < L and y[a] == draft[a]:
         a += 1
     return a, list(draft[:a]) + [y[a]], y
+
+
+def select_prefix(x, T, pos, max_match):
+    """Prompt lookup's selection: the match length of a candidate is the common
+    prefix of the reversed context ending at j and the reversed context ending at
+    T-1 (os.path.commonprefix on lists), capped; the best is the longest, the
+    earliest among equals (min over (-length, j))."""
+    import os.path
+    back_q = list(x[:T])[::-1]
+    lens_ = []
+    for j in pos:
+        if not 0 <= j <= T - 2:
+            lens_.append(None)
+            continue
+        m = len(os.path.commonprefix([list(x[:j + 1])[::-1], back_q]))
+        lens_.append(min(m, max_match))
+    ok = [(-m, j) for m, j in zip(lens_, pos) if m is not None]
+    if not ok:
+        return lens_, -1, -math.inf
+    m, j = min(ok)
+    return lens_, j, float(-m)
+
+
+def commit(x, T, out, n, cap):
+    """Append with Python lists: the first min(n, cap - T) of out join x[:T]."""
+    if T < 0 or T > cap or n < 0 or n > len(out):
+        return list(x), T, 0
+    keep = list(x[:T]) + list(out[:n])[:cap - T]
+    m = len(keep) - T
+    return keep + list(x[len(keep):]), len(keep), m

@@ -69,3 +69,13 @@ def test_fig3_newline_oracle():
             if "draft_K4" in e:
                 assert list(dr[0, :4]) == e["draft_K4"], key
     assert math.isclose(ex["n1"]["hidden_scores"][2], 6 / math.sqrt(42), rel_tol=1e-16)
+    # prompt lookup's selection on the same occurrences: the span of f
+    e = ex["pld_prefix"]
+    cp, cc, _ = oracle.find(toks, lens, 1, 1)
+    assert list(cp[0, :cc[0]]) == e["cand_pos"]
+    for cap_m in (8, 3, 1):
+        sc, bp, bs = oracle.select_prefix(toks, lens, cp, cc, cap_m)
+        assert list(sc[0, :cc[0]]) == e[f"match_len_max{cap_m}"], cap_m
+        assert bp[0] == e[f"best_pos_max{cap_m}"] and bs[0] == max(e[f"match_len_max{cap_m}"])
+    dr, dl = oracle.emit(toks, lens, oracle.select_prefix(toks, lens, cp, cc, 8)[1], 4)
+    assert list(dr[0]) == e["draft_K4_max8"]

@@ -43,6 +43,12 @@ MUTANTS = {
     "sampling uses the previous row's uniform": (
         "double u = (double)uniforms[(int64_t)b * u_stride + i];",
         "double u = (double)uniforms[(int64_t)b * u_stride + (i > 0 ? i - 1 : 0)];"),
+    "prefix tie goes to the latest position": ("(s == bs && j < bj)", "(s == bs && j > bj)"),
+    "prefix match compared one token early": ("x[j - m] == x[T - 1 - m]", "x[j - m] == x[T - 2 - m]"),
+    "commit ignores the limit": ("if (limit && limit[b] < cap_b) cap_b = limit[b];",
+                                 "if (limit && limit[b] < 0) cap_b = limit[b];"),
+    "commit counts a step with nothing appended": ("stats[2 * b + 1] += (m > 0) ? 1 : 0;",
+                                                   "stats[2 * b + 1] += 1;"),
 }
 
 
@@ -127,6 +133,35 @@ def _pins_pass():
             a_, toks, y = brute.verify_sample(Zs, list(dr), 1.0, us)
             if list(rows[0]) != y or acc[0] != a_:
                 return False
+        # prompt lookup's selection: the Fig. 3 fixture, brute force
+        fx, toks, lens, _, _ = golden_cases.load("fig3_newline.json")
+        e = fx["expected"]["pld_prefix"]
+        cp, cc, _ = oracle.find(toks, lens, 1, 1)
+        for cap_m in (8, 3):
+            sc, bp, _ = oracle.select_prefix(toks, lens, cp, cc, cap_m)
+            if list(sc[0, :cc[0]]) != e[f"match_len_max{cap_m}"] or bp[0] != e[f"best_pos_max{cap_m}"]:
+                return False
+        for _ in range(40):
+            T = int(rng.integers(2, 40))
+            x = rng.integers(0, 2, size=(1, T)).astype(np.int32)
+            cp, cc, _ = oracle.find(x, np.array([T], np.int32), 1, 1)
+            sc, bp, bs = oracle.select_prefix(x, np.array([T], np.int32), cp, cc, 6)
+            want, wj, ws = brute.select_prefix(x[0], T, list(cp[0, :cc[0]]), 6)
+            if [int(v) for v in sc[0, :cc[0]]] != want or bp[0] != wj:
+                return False
+        # commit: list appends under a limit, the counters
+        for _ in range(40):
+            stride, K = 12, 3
+            x = rng.integers(0, 5, size=(2, stride)).astype(np.int32)
+            T0 = rng.integers(0, stride + 1, size=2).astype(np.int32)
+            out = rng.integers(5, 9, size=(2, K + 1)).astype(np.int32)
+            n = rng.integers(0, K + 2, size=2).astype(np.int32)
+            lim = rng.integers(0, stride + 1, size=2).astype(np.int32)
+            t2, l2, s2 = oracle.commit(x, T0, out, n, limit=lim)
+            for b in range(2):
+                wx, wT, m = brute.commit(x[b], int(T0[b]), out[b], int(n[b]), int(lim[b]))
+                if list(t2[b]) != wx[:stride] or l2[b] != wT or list(s2[b]) != [m, int(m > 0)]:
+                    return False
         return True
     except Exception:
         return False

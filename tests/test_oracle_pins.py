@@ -444,3 +444,86 @@ def test_verify_sample_acceptance_and_bad_lengths():
     assert acc[0] == K and cnt[0] == K + 1 and list(out[0]) == list(rows[0])
     assert acc[1] == 2 and list(out[1, :3]) == [draft[1, 0], draft[1, 1], rows[1, 2]]
     assert acc[2] == -1 and cnt[2] == 0 and np.all(out[2] == -1)
+
+
+# ------------------------------------------------------- prefix selection
+@settings(max_examples=300, deadline=None)
+@given(token_batches(), st.integers(1, 9), st.data())
+def test_select_prefix_matches_brute(batch, max_match, data):
+    """Prompt lookup's selection (Sec. 2, Fig. 3 caption) on random small token
+    rows, over the oracle's own occurrence lists and over arbitrary (also
+    out-of-range) candidate positions: match lengths, the longest-then-earliest
+    choice and its score equal the commonprefix reading."""
+    toks, lens, n_min, n_max = batch
+    B, stride = toks.shape
+    cp, cc, _ = oracle.find(toks, lens, n_min, n_max)
+    extra = data.draw(st.lists(st.integers(-2, stride + 1), min_size=1, max_size=6))
+    for pos_lists in ([list(cp[b, :cc[b]]) for b in range(B)], [extra] * B):
+        cap = max(1, max(len(p) for p in pos_lists))
+        pos = np.full((B, cap), -1, np.int32)
+        cnt = np.zeros(B, np.int32)
+        for b, p in enumerate(pos_lists):
+            pos[b, :len(p)] = p
+            cnt[b] = len(p)
+        sc, bp, bs = oracle.select_prefix(toks, lens, pos, cnt, max_match)
+        for b in range(B):
+            T = int(lens[b])
+            if not 2 <= T <= stride:
+                assert bp[b] == -1 and bs[b] == -math.inf
+                continue
+            want, wj, ws = brute.select_prefix(toks[b], T, pos_lists[b], max_match)
+            got = [None if math.isnan(v) else int(v) for v in sc[b, :cnt[b]]]
+            assert got == want and bp[b] == wj and bs[b] == ws
+
+
+def test_select_prefix_invariants():
+    """Every n-gram occurrence matches at least n tokens back; capping at the n
+    used makes every candidate tie, so the earliest (cand_pos[0]) wins, which is
+    prompt lookup's first match."""
+    rng = np.random.default_rng(3)
+    toks = rng.integers(0, 4, size=(6, 200)).astype(np.int32)
+    lens = np.array([200, 150, 2, 1, 77, 199], np.int32)
+    cp, cc, nu = oracle.find(toks, lens, 1, 4)
+    sc, bp, bs = oracle.select_prefix(toks, lens, cp, cc, 64)
+    for b in range(6):
+        if cc[b] == 0:
+            assert bp[b] == -1
+            continue
+        assert (sc[b, :cc[b]] >= nu[b]).all()
+        assert bs[b] == sc[b, :cc[b]].max()
+        first_best = cp[b, int(np.argmax(sc[b, :cc[b]]))]   # argmax: the first, i.e. earliest
+        assert bp[b] == first_best
+    _, bp_n, bs_n = oracle.select_prefix(toks, lens, cp, cc, 1)
+    for b in range(6):
+        assert bp_n[b] == (cp[b, 0] if cc[b] else -1)
+
+
+# ------------------------------------------------------------------ commit
+@settings(max_examples=300, deadline=None)
+@given(st.data())
+def test_commit_matches_brute(data):
+    """The append of the generation loop: list concatenation, capped by the
+    limit and the row, lengths and the (emitted, steps) counters."""
+    B = data.draw(st.integers(1, 4))
+    stride = data.draw(st.integers(1, 20))
+    K = data.draw(st.integers(1, 5))
+    toks = np.array(data.draw(st.lists(st.lists(st.integers(0, 9), min_size=stride,
+                                                max_size=stride), min_size=B, max_size=B)),
+                    np.int32)
+    lens = np.array(data.draw(st.lists(st.integers(-1, stride + 1), min_size=B, max_size=B)),
+                    np.int32)
+    out = np.array(data.draw(st.lists(st.lists(st.integers(10, 19), min_size=K + 1,
+                                               max_size=K + 1), min_size=B, max_size=B)),
+                   np.int32)
+    cnt = np.array(data.draw(st.lists(st.integers(-1, K + 2), min_size=B, max_size=B)), np.int32)
+    limit = np.array(data.draw(st.lists(st.integers(0, stride + 3), min_size=B, max_size=B)),
+                     np.int32) if data.draw(st.booleans()) else None
+    stats0 = np.array(data.draw(st.lists(st.lists(st.integers(0, 50), min_size=2, max_size=2),
+                                         min_size=B, max_size=B)), np.int64)
+    t2, l2, s2 = oracle.commit(toks, lens, out, cnt, limit=limit, stats=stats0)
+    for b in range(B):
+        cap = stride if limit is None else min(int(limit[b]), stride)
+        n = int(cnt[b]) if 0 <= cnt[b] <= K + 1 else -1
+        want_x, want_T, m = brute.commit(toks[b], int(lens[b]), out[b], n, cap)
+        assert list(t2[b]) == want_x[:stride] and l2[b] == want_T
+        assert list(s2[b]) == [stats0[b, 0] + m, stats0[b, 1] + (m > 0)]
