@@ -294,45 +294,54 @@ int pld_verify_sample_finish(const void *logits, int dtype, int64_t l_seq_stride
                              void *workspace, size_t workspace_bytes, void *stream);
 
 /*
- * pld_verify_sample -- sampling verification (Sec. 3 and Sec. 4.4 with a
- * temperature; the paper's sampling experiments use tau = 1).  Instead of the
- * argmax, y_i is drawn from softmax(Z[b][i] / tau) by inversion at the
- * caller's uniform u = uniforms[b][i]: with p_v = exp((Z[v] - max Z) / tau)
- * and S = sum_v p_v, y_i is the first v whose cumulative mass p_0 + ... + p_v
- * exceeds u * S.  Acceptance and outputs are then those of pld_verify_greedy
- * with these y_i; for a draft that puts all its mass on one token this is
- * the usual speculative rejection sampling.
+ * pld_select_prefix -- prompt lookup's selection, the baseline PLD+ replaces
+ * (Sec. 2; the Fig. 3 caption: the candidate span with the longest matching
+ * prefix), for comparisons on the same occurrence lists.  For a candidate j,
+ * 0 <= j <= T-2:
+ *   m_j = the largest m <= max_match with x[j-k] = x[T-1-k] for all k < m
+ *         (indices j-k >= 0 only);
+ * j* = the largest m_j, the earliest j among equal lengths (prompt lookup
+ * keeps the first match of a left-to-right scan).  best_score = m_j.  With
+ * max_match equal to the n-gram length used by pld_find_candidates every
+ * candidate ties, and j* is the first occurrence.
  *
- *   temperature  tau > 0, finite, with log2(e) / tau representable in fp32
- *   uniforms     fp32 [B][u_stride] device memory, u_stride >= K+1, 4-byte
- *                aligned; u < 0 or NaN counts as 0, u >= 1 as the largest
- *                float below 1.  Entries i <= draft_len[b] are used (others
- *                of the first K+1 may be read ahead and are ignored).
- *   row_sample   int32 [B][K+1] or NULL: y_i for i <= L, -1 for the rows
- *                past the draft (all -1 when draft_len is out of range)
- *   workspace    at least pld_verify_sample_workspace_bytes(B, K, V, dtype)
- *                bytes, zero-filled once like every workspace; its first
- *                pld_workspace_bytes(B, K) bytes are left zero by the call and
- *                the rest is per-call statistics, rewritten each time.
- * Arithmetic: the masses are fp32 (2^((z - m) * log2(e)/tau)) and are summed
- * per 512-vector segment of the row, then over the segments; a row of -inf
- * gives y = 0, and where rounding leaves no element past the target the last
- * element with nonzero mass is taken.  +inf and NaN logits are outside the
- * contract.  Results are bit-identical from run to run.
- * Errors: as pld_verify_greedy, plus PLD_ERR_INVALID for a bad temperature,
- * K+1 > PLD_MAX_SAMPLE_ROWS, NULL uniforms or u_stride < K+1, and
- * PLD_ERR_ALIGN for misaligned uniforms.
+ *   tokens, lens  as pld_find_candidates;  cand_pos [B][cap], cand_count [B]
+ *   max_match     in [1, PLD_MAX_MATCH]
+ *   scores        float [B][cap] or NULL: m_j, NaN for candidates outside
+ *                 [0, T-2]; entries past cand_count are not written
+ * Device-side rules: a count outside [0, cap] counts as 0; a sequence with
+ * T < 2 or T > tok_stride gets best_pos = -1, best_score = -inf.
+ * Errors: PLD_ERR_INVALID (NULL, B outside [1, 65535], tok_stride or cap out
+ * of range, bad max_match), PLD_ERR_LAUNCH.
  */
-#define PLD_MAX_SAMPLE_ROWS 16384
-int pld_verify_sample(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
-                      int V, int K, const int32_t *draft, const int32_t *draft_len, int B,
-                      double temperature, const float *uniforms, int64_t u_stride,
-                      int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
-                      int32_t *row_sample, void *workspace, size_t workspace_bytes, void *stream);
+#define PLD_MAX_MATCH 1024
+int pld_select_prefix(const int32_t *tokens, int64_t tok_stride, const int32_t *lens,
+                      const int32_t *cand_pos, int64_t cap, const int32_t *cand_count, int B,
+                      int max_match, float *scores, int32_t *best_pos, float *best_score,
+                      void *stream);
 
-/* Workspace bytes of pld_verify_sample (0 for arguments out of range); it is
- * at least pld_workspace_bytes(B, K), so one buffer serves every call. */
-size_t pld_verify_sample_workspace_bytes(int B, int K, int V, int dtype);
+/*
+ * pld_commit -- the step after verification in the generation loop: the
+ * accepted draft tokens and the model's own token join the sequence (Sec. 3,
+ * Sec. 4.4).  Per sequence, with cap = min(limit[b], tok_stride) (tok_stride
+ * when limit is NULL) and T = lens[b]:
+ *   m = min(out_count[b], cap - T);  tokens[b][T + i] = out_tokens[b][i], i < m;
+ *   lens[b] = T + m;  stats[b] += (m, 1 if m > 0)   (stats may be NULL)
+ * stats[b] = (emitted tokens, steps) gives the paper's average acceptance
+ * length, tokens per generation step (Sec. 5.3), as their ratio.
+ *
+ *   tokens     int32 [B][tok_stride], lens int32 [B] (both updated in place)
+ *   limit      int32 [B] or NULL: a per-sequence length limit
+ *   out_tokens int32 [B][K+1], out_count int32 [B] (from a verification call)
+ *   stats      int64 [B][2] or NULL, accumulated
+ * Device-side rule: a sequence with T outside [0, cap] or out_count outside
+ * [0, K+1] is left unchanged.
+ * Errors: PLD_ERR_INVALID (NULL, B < 1, K < 1, tok_stride out of range),
+ * PLD_ERR_LAUNCH.
+ */
+int pld_commit(int32_t *tokens, int64_t tok_stride, int32_t *lens, const int32_t *limit,
+               const int32_t *out_tokens, const int32_t *out_count, int B, int K,
+               int64_t *stats, void *stream);
 
 /*
  * pld_draft_hidden / pld_draft_attn -- the drafting half of a step in one

@@ -22,7 +22,8 @@ __all__ = [
     "DRAFT_MAX_PART", "pld_score_hidden",
     "pld_score_attn", "pld_select_best", "pld_verify_argmax", "pld_verify_accept",
     "pld_verify_sample", "pld_verify_sample_workspace_bytes", "pld_verify_sample_stats",
-    "pld_verify_sample_finish", "PLD_MAX_SAMPLE_ROWS",
+    "pld_verify_sample_finish", "PLD_MAX_SAMPLE_ROWS", "pld_select_prefix", "pld_commit",
+    "PLD_MAX_MATCH",
 ]
 
 PLD_OK, PLD_ERR_INVALID, PLD_ERR_ALIGN, PLD_ERR_WORKSPACE, PLD_ERR_LAUNCH = range(5)
@@ -30,6 +31,7 @@ PLD_F32, PLD_BF16 = 0, 1
 PLD_AGG_SUM, PLD_AGG_MAX = 0, 1
 PLD_MAX_NGRAM, PLD_MAX_HIDDEN, PLD_MAX_BATCH, PLD_MAX_DRAFT_SPLIT = 8, 16384, 4096, 1024
 PLD_MAX_SAMPLE_ROWS = 16384
+PLD_MAX_MATCH = 1024
 DRAFT_MAX_TOK_STRIDE = 8192     # one-call drafting, one block per sequence (S = 1)
 DRAFT_MAX_PART = 8192           # one-call drafting, S > 1: positions per block
 
@@ -70,6 +72,8 @@ _SIGNATURES = {
     "pld_verify_sample_finish": ([_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int,
                                   ctypes.c_double, _vp, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp],
                                  _int),
+    "pld_select_prefix": ([_vp, _i64, _vp, _vp, _i64, _vp, _int, _int, _vp, _vp, _vp, _vp], _int),
+    "pld_commit": ([_vp, _i64, _vp, _vp, _vp, _vp, _int, _int, _vp, _vp], _int),
     "pld_draft_hidden": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _i64, _i64, _int, _f32, _int,
                           _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _int, _vp, _sz, _vp],
                          _int),
@@ -257,6 +261,34 @@ def pld_verify_sample(logits, draft, draft_len, temperature, uniforms, accept_le
           _ptr(draft), _ptr(draft_len), B, float(temperature), _ptr(uniforms), uniforms.stride(0),
           _ptr(accept_len), _ptr(out_tokens), _ptr(out_count), _ptr(row_sample), _ptr(workspace),
           _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_select_prefix(tokens, lens, cand_pos, cand_count, best_pos, best_score, max_match,
+                      scores=None, stream=None, prepare=False):
+    """Prompt lookup's selection over the occurrence lists: longest matching prefix (up to
+    max_match tokens), earliest among equals; writes best_pos [B], best_score [B]."""
+    import torch
+    _need(tokens, torch.int32, "tokens", 2)
+    _need(cand_pos, torch.int32, "cand_pos", 2)
+    return _run("pld_select_prefix", (_ptr(tokens), tokens.stride(0), _ptr(lens), _ptr(cand_pos),
+          cand_pos.stride(0), _ptr(cand_count), tokens.shape[0], int(max_match), _ptr(scores),
+          _ptr(best_pos), _ptr(best_score), _stream(stream),), prepare)
+
+
+def pld_commit(tokens, lens, out_tokens, out_count, limit=None, stats=None, stream=None,
+               prepare=False):
+    """Appends out_tokens[b][:out_count[b]] to tokens[b] (up to limit[b]), advances lens and
+    adds (emitted, steps) to stats [B][2] int64 when given."""
+    import torch
+    _need(tokens, torch.int32, "tokens", 2)
+    B, K1 = out_tokens.shape
+    if out_tokens.stride(0) != K1:
+        raise TypeError("out_tokens must be a contiguous [B][K+1] tensor")
+    if stats is not None and (stats.dtype != torch.int64 or tuple(stats.shape) != (B, 2)
+                              or not stats.is_contiguous()):
+        raise TypeError("stats must be a contiguous int64 [B][2] tensor")
+    return _run("pld_commit", (_ptr(tokens), tokens.stride(0), _ptr(lens), _ptr(limit),
+          _ptr(out_tokens), _ptr(out_count), B, K1 - 1, _ptr(stats), _stream(stream),), prepare)
 
 
 def pld_draft_hidden(tokens, lens, ngram_min, ngram_max, hidden, K, cand_pos, cand_count,

@@ -613,6 +613,35 @@ __global__ __launch_bounds__(256) void emit_kernel(const int32_t *tokens, int64_
     if (i == 0) draft_len[b] = (int32_t)L;
 }
 
+// ---------------------------------------------------------------- commit
+// The step after verification: the emitted tokens join the sequence.  One
+// wave per sequence: m = min(out_count, cap - T) tokens appended at x[T..],
+// lens advanced, the (emitted, steps) counters added to.
+__global__ __launch_bounds__(256) void commit_kernel(int32_t *tokens, int64_t tok_stride,
+                                                     int32_t *lens, const int32_t *limit,
+                                                     const int32_t *out_tokens,
+                                                     const int32_t *out_count, int B, int K,
+                                                     int64_t *stats) {
+    const int b = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave);
+    const int lane = lane_id();
+    if (b >= B) return;   // wave-uniform
+    int64_t cap = tok_stride;
+    if (limit && limit[b] < cap) cap = limit[b];
+    const int64_t T = lens[b];
+    const int64_t n = out_count[b];
+    if (T < 0 || T > cap || n < 0 || n > K + 1) return;
+    const int64_t m = min(n, cap - T);
+    for (int64_t i = lane; i < m; i += kWave)
+        tokens[(int64_t)b * tok_stride + T + i] = out_tokens[(int64_t)b * (K + 1) + i];
+    if (lane == 0) {
+        lens[b] = (int32_t)(T + m);
+        if (stats) {
+            stats[2 * b] += m;
+            stats[2 * b + 1] += m > 0 ? 1 : 0;
+        }
+    }
+}
+
 static int prep_verify(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
                        int V, int K, const int32_t *draft_len, int B, void *workspace,
                        size_t workspace_bytes, VerifyArgs &a) {
@@ -856,6 +885,17 @@ extern "C" int pld_emit_draft(const int32_t *tokens, int64_t tok_stride, const i
     if (blocks > 0x7fffffff) return PLD_ERR_INVALID;
     hipLaunchKernelGGL(emit_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
                        tokens, tok_stride, lens, best_pos, B, K, draft, draft_len);
+    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+}
+
+extern "C" int pld_commit(int32_t *tokens, int64_t tok_stride, int32_t *lens,
+                          const int32_t *limit, const int32_t *out_tokens,
+                          const int32_t *out_count, int B, int K, int64_t *stats, void *stream) {
+    if (!tokens || !lens || !out_tokens || !out_count) return PLD_ERR_INVALID;
+    if (B < 1 || K < 1 || tok_stride < 1 || tok_stride > kMaxTokStride) return PLD_ERR_INVALID;
+    hipLaunchKernelGGL(commit_kernel, dim3((unsigned)((B + 3) / 4)), dim3(256), 0,
+                       (hipStream_t)stream, tokens, tok_stride, lens, limit, out_tokens,
+                       out_count, B, K, stats);
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }
 

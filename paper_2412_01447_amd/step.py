@@ -9,12 +9,12 @@ verification at a temperature once set_sampling() is called).
 import torch
 
 from . import (DRAFT_MAX_PART, DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, PLD_BF16, PLD_F32,
-               PLD_MAX_DRAFT_SPLIT, pld_draft_attn, pld_draft_hidden, pld_draft_workspace_bytes,
-               pld_emit_draft, pld_find_candidates, pld_find_scratch_bytes, pld_rank_attn,
-               pld_rank_hidden, pld_score_attn, pld_score_hidden, pld_select_best,
-               pld_verify_accept, pld_verify_argmax, pld_verify_greedy, pld_verify_sample,
-               pld_verify_sample_finish, pld_verify_sample_stats, pld_verify_sample_workspace_bytes,
-               pld_workspace_bytes)
+               PLD_MAX_DRAFT_SPLIT, pld_commit, pld_draft_attn, pld_draft_hidden,
+               pld_draft_workspace_bytes, pld_emit_draft, pld_find_candidates,
+               pld_find_scratch_bytes, pld_rank_attn, pld_rank_hidden, pld_score_attn,
+               pld_score_hidden, pld_select_best, pld_select_prefix, pld_verify_accept,
+               pld_verify_argmax, pld_verify_greedy, pld_verify_sample, pld_verify_sample_finish,
+               pld_verify_sample_stats, pld_verify_sample_workspace_bytes, pld_workspace_bytes)
 
 
 class DraftStep:
@@ -109,6 +109,16 @@ class DraftStep:
         pld_rank_attn(attn, lens, self.cand_pos, self.cand_count, bp, bs, self.workspace, agg=agg,
                       threshold=threshold, scores=self.scores_attn, stream=stream)
 
+    def select_prefix(self, tokens, lens, max_match, stream=None):
+        """Prompt lookup's choice among the occurrences (the PLD baseline)."""
+        pld_select_prefix(tokens, lens, self.cand_pos, self.cand_count, self.best_pos,
+                          self.best_score, max_match, scores=self.scores, stream=stream)
+
+    def commit(self, tokens, lens, limit=None, stats=None, stream=None):
+        """Appends the verified tokens to the sequences and advances lens (in place)."""
+        pld_commit(tokens, lens, self.out_tokens, self.out_count, limit=limit, stats=stats,
+                   stream=stream)
+
     def emit(self, tokens, lens, stream=None):
         pld_emit_draft(tokens, lens, self.best_pos, self.K, self.draft, self.draft_len,
                        stream=stream)
@@ -181,13 +191,19 @@ class DraftStep:
                            scores=self.scores_attn, blocks_per_seq=self.draft_split,
                            workspace=self.draft_ws, stream=stream)
 
-    def run(self, tokens, lens, logits, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
-            threshold=float("-inf"), stream=None):
-        """The whole step.  With both artifacts, the hidden-state ranking drafts and the
-        attention ranking is written to best_pos_attn / best_score_attn."""
+    def make_draft(self, tokens, lens, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
+                   threshold=float("-inf"), prefix_match=None, stream=None):
+        """The drafting half of a step.  With prefix_match set, prompt lookup's selection
+        (longest matching prefix up to that many tokens) replaces the artifact ranking.
+        With both artifacts, the hidden-state ranking drafts and the attention ranking
+        is written to best_pos_attn / best_score_attn."""
+        if prefix_match is not None:
+            self.find(tokens, lens, *ngram, stream=stream)
+            self.select_prefix(tokens, lens, prefix_match, stream=stream)
+            self.emit(tokens, lens, stream=stream)
+            return
         if self.uses_fused(hidden, attn):
             self.draft_fused(tokens, lens, hidden, attn, ngram, agg, threshold, stream=stream)
-            self.verify(logits, stream=stream)
             return
         self.find(tokens, lens, *ngram, stream=stream)
         if attn is not None:
@@ -196,6 +212,12 @@ class DraftStep:
         if hidden is not None:
             self.rank_hidden(hidden, lens, threshold=threshold, stream=stream)
         self.emit(tokens, lens, stream=stream)
+
+    def run(self, tokens, lens, logits, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
+            threshold=float("-inf"), prefix_match=None, stream=None):
+        """The whole step: drafting, then verification of the drafts against `logits`."""
+        self.make_draft(tokens, lens, hidden, attn, ngram, agg, threshold, prefix_match,
+                        stream=stream)
         self.verify(logits, stream=stream)
 
     def plan(self, tokens, lens, logits, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
@@ -267,3 +289,26 @@ class DraftStep:
             out["scores"] = self.scores.cpu().numpy()
             out["scores_attn"] = self.scores_attn.cpu().numpy()
         return out
+
+
+def decode_loop(step, tokens, lens, limit, model, hidden=None, attn=None, ngram=(1, 1),
+                agg=PLD_AGG_SUM, threshold=float("-inf"), prefix_match=None, stats=None,
+                max_steps=1 << 20, check_every=4, stream=None, on_step=None):
+    """The generation loop around the drafting step, on the device: draft, verify
+    against `model(step, lens)` (the target model's logits over context + draft),
+    commit the emitted tokens; until every sequence has reached `limit` (checked
+    on the host every `check_every` steps) or `max_steps`.  `tokens` [B][stride]
+    and `lens` [B] are updated in place; `stats` (int64 [B][2], optional)
+    accumulates (emitted tokens, steps) per sequence, whose ratio is the paper's
+    average acceptance length.  `on_step(i)` runs after each commit (tests use it
+    to compare every step).  Returns the number of steps run."""
+    for i in range(max_steps):
+        if i % check_every == 0 and bool((lens >= limit).all()):
+            return i
+        step.make_draft(tokens, lens, hidden, attn, ngram, agg, threshold, prefix_match,
+                        stream=stream)
+        step.verify(model(step, lens), stream=stream)
+        step.commit(tokens, lens, limit=limit, stats=stats, stream=stream)
+        if on_step is not None:
+            on_step(i)
+    return max_steps

@@ -22,6 +22,11 @@ workloads (arXiv 2412.01447, Sec. 5.1: outputs that copy spans of their input):
   length p ~ U{0..K} the caller-given draft tokens get +boost (the draft is an
   input here; the generator never computes one).
 * uniforms -- the draws of sampling verification, U[0, 1) fp32 [B][K+1].
+* decoding tasks (DECODE_TASKS) -- for the multi-step loop: target sequences
+  (the token generator's output, whose last quarter is the continuation to
+  generate), hidden states that embed each position's last few tokens, and a
+  stand-in target model whose greedy choice at every position is the target
+  token, so that greedy decoding reproduces the target whatever the drafts.
 
 Seeds are numpy SeedSequence([seed, b, stream]) per sequence and stream, so a
 sequence can be regenerated alone.
@@ -38,6 +43,8 @@ STREAM_ATTN = 3
 STREAM_LOGITS = 4
 STREAM_HIDDEN = 5
 STREAM_UNIFORMS = 6
+STREAM_CONTEXT = 7
+STREAM_MODEL = 8
 
 
 @dataclasses.dataclass(frozen=True)
@@ -332,3 +339,104 @@ def logits_for(w, draft, draft_len):
     c = w["cfg"]
     z, _ = make_logits(c.B, c.K, c.V, c.seed, draft, draft_len, bf16=(c.logits == "bf16"))
     return z
+
+
+# ------------------------------------------------------------ decoding tasks
+@dataclasses.dataclass(frozen=True)
+class DecodeTask:
+    """A multi-step decoding run: B target sequences of length T whose last
+    quarter is generated step by step, starting from the first three quarters
+    (the prompt); a stated fraction of the generated part copies spans of the
+    prompt (input-guided generation, Sec. 5.1)."""
+    name: str
+    B: int
+    T: int
+    V: int
+    zipf_s: float
+    plant_frac: float
+    span: tuple
+    d: int
+    K: int
+    seed: int
+    window: int = 4       # hidden state of position p: decaying sum over x[p-window+1 .. p]
+    decay: float = 0.5
+    noise: float = 0.25
+
+
+DECODE_TASKS = {
+    # the paper's input sizes (App. B) with a highly overlapping output, K = 10
+    "b1_t1024_copy60_k10": DecodeTask("b1_t1024_copy60_k10", 1, 1024, 32000, 1.1, 0.6, (8, 64),
+                                      4096, 10, 21),
+    # a batch of eight, longer contexts, K = 16
+    "b8_t4096_copy50_k16": DecodeTask("b8_t4096_copy50_k16", 8, 4096, 32000, 1.1, 0.5, (8, 64),
+                                      4096, 16, 22),
+}
+
+
+def make_context_hidden(tokens: np.ndarray, d: int, seed: int, window: int = 4,
+                        decay: float = 0.5, noise: float = 0.25, device="cpu"):
+    """Hidden states [B][T][d] bf16 for the loop: H[p] = sum_k decay^k E[x[p-k]]
+    (k < window, p-k >= 0) plus N(0, noise^2), E a Gaussian table over token ids
+    (hashed to 4096 rows).  Positions whose last few tokens agree get similar
+    rows, the property the paper's hidden-state ranking relies on (Sec. 4.2.2)."""
+    import torch
+    B, T = tokens.shape
+    g = torch.Generator(device=device)
+    g.manual_seed(int(np.random.SeedSequence([seed, 0, STREAM_CONTEXT]).generate_state(1)[0]))
+    E = torch.randn((4096, d), generator=g, device=device)
+    ids = torch.from_numpy(np.where(tokens >= 0, tokens, 0) % 4096).to(device).long()
+    out = torch.empty((B, T, d), dtype=torch.bfloat16, device=device)
+    for b in range(B):
+        h = torch.zeros((T, d), device=device)
+        for k in range(window):
+            h[k:] += (decay ** k) * E[ids[b, :T - k]]
+        h += noise * torch.randn((T, d), generator=g, device=device)
+        out[b] = h.to(torch.bfloat16)
+    return out
+
+
+def make_decode_task(task: DecodeTask, device="cpu"):
+    """Targets (host int32 [B][T]), the prompt length per sequence (host int32),
+    and the loop's hidden states (device bf16 [B][T][d])."""
+    toks, lens, metas = make_tokens(task.B, task.T, task.V, task.zipf_s, task.plant_frac,
+                                    task.span, task.seed)
+    start = np.full(task.B, task.T - task.T // 4, np.int32)
+    hidden = make_context_hidden(toks, task.d, task.seed, task.window, task.decay, task.noise,
+                                 device)
+    return dict(task=task, target=toks, start=start, hidden=hidden, metas=metas)
+
+
+class TargetModel:
+    """Stand-in for the target model's forward pass over context + draft (the
+    forward pass itself is outside the drafting step).  Row i of its logits is
+    the distribution at position lens[b] + i: N(0, 1) noise, fixed per run,
+    with +boost at the target token of that position, so that its greedy
+    continuation of any prefix of the target is the target.  The logits buffer
+    is patched in place between calls rather than rebuilt."""
+
+    def __init__(self, target, K: int, V: int, seed: int, device="cpu", boost: float = 10.0):
+        import torch
+        self.device = device
+        self.target = torch.as_tensor(target, device=device).long()
+        B, self.T = self.target.shape
+        g = torch.Generator(device=device)
+        g.manual_seed(int(np.random.SeedSequence([seed, 0, STREAM_MODEL]).generate_state(1)[0]))
+        self.base = torch.randn((B, K + 1, V), generator=g, device=device)
+        self.buf = self.base.clone()
+        self.boost = float(boost)
+        self.prev = None
+        self.offs = torch.arange(K + 1, device=device)
+
+    def target_tokens(self, lens):
+        import torch
+        pos = (torch.as_tensor(lens, device=self.device).long()[:, None] + self.offs)
+        return self.target.gather(1, pos.clamp(max=self.T - 1))
+
+    def logits(self, lens):
+        """The logits for the drafts of sequences at lengths `lens` (device)."""
+        if self.prev is not None:
+            self.buf.scatter_(2, self.prev, self.base.gather(2, self.prev))
+        tok = self.target_tokens(lens)[:, :, None]
+        self.buf.scatter_(2, tok, self.base.gather(2, tok) + self.boost)
+        self.prev = tok
+        return self.buf

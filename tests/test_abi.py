@@ -209,3 +209,20 @@ def test_verify_sample_host_validation():
                NULL) == E_INV
     assert fin(F, pld.PLD_F32, (K + 1) * V, V, V, K, F, F, B, 1.0, MIS, K + 1, F, F, F, NULL, F,
                need, NULL) == E_AL
+
+
+def test_prefix_and_commit_host_validation():
+    """Host-side checks of prompt lookup's selection and the commit."""
+    lib = pld._load()
+    E_INV = pld.PLD_ERR_INVALID
+    sp = lib.pld_select_prefix
+    assert sp(NULL, 100, F, F, 100, F, 2, 4, NULL, F, F, NULL) == E_INV
+    assert sp(F, 100, F, F, 100, F, 0, 4, NULL, F, F, NULL) == E_INV
+    assert sp(F, 100, F, F, 0, F, 2, 4, NULL, F, F, NULL) == E_INV
+    assert sp(F, 100, F, F, 100, F, 2, 0, NULL, F, F, NULL) == E_INV
+    assert sp(F, 100, F, F, 100, F, 2, pld.PLD_MAX_MATCH + 1, NULL, F, F, NULL) == E_INV
+    cm = lib.pld_commit
+    assert cm(NULL, 100, F, NULL, F, F, 2, 4, NULL, NULL) == E_INV
+    assert cm(F, 100, F, NULL, F, F, 0, 4, NULL, NULL) == E_INV
+    assert cm(F, 100, F, NULL, F, F, 2, 0, NULL, NULL) == E_INV
+    assert cm(F, 0, F, NULL, F, F, 2, 4, NULL, NULL) == E_INV
