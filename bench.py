@@ -54,6 +54,10 @@ def parse():
     p.add_argument("--verify", choices=["greedy", "sample"], default="greedy",
                    help="verification: argmax (greedy) or sampling at --temperature")
     p.add_argument("--temperature", type=float, default=1.0)
+    p.add_argument("--loop", default=None,
+                   help="instead of the step benchmark, run the generation loop on a decoding "
+                        "task (synth.DECODE_TASKS) with each ranking and report the loop step "
+                        "latency and the average acceptance length")
     return p.parse_args()
 
 
@@ -183,6 +187,8 @@ def main():
     import synth
     from paper_2412_01447_amd.step import DraftStep
 
+    if args.loop:
+        return run_loop(args)
     cfg = synth.CONFIGS[args.config]
     dev = torch.device("cuda:0")
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
@@ -315,6 +321,81 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    print(json.dumps(line), flush=True)
+
+
+LOOP_METRIC = "draft+verify+commit loop step latency (us); average acceptance length"
+
+
+def run_loop(args):
+    """The generation loop (draft -> verify -> commit) on a synthetic decoding task,
+    once per ranking: PLD+ with hidden states (Eq. 2), prompt lookup's first match of
+    the longest n-gram up to 3, and prompt lookup's longest matching prefix up to 64.
+    The stand-in model's logits depend only on the lengths, so they are produced
+    before each step and the events bracket the library's calls alone."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2412_01447_amd.step import DraftStep
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    task = synth.DECODE_TASKS[args.loop]
+    dev = torch.device("cuda:0")
+    w = synth.make_decode_task(task, device=dev)
+    target, start = w["target"], w["start"]
+    B, T = target.shape
+    rankings = [("pld_plus_hidden", dict(hidden=w["hidden"], ngram=(1, 1))),
+                ("pld_first_ngram3", dict(prefix_match=3, ngram=(1, 3))),
+                ("pld_longest_prefix64", dict(prefix_match=64, ngram=(1, 1)))]
+    results = {}
+    for name, kw in rankings:
+        for rep in range(2):        # the first pass warms up
+            toks = np.where(np.arange(T)[None, :] < start[:, None], target, -1).astype(np.int32)
+            td = torch.from_numpy(toks).to(dev)
+            ld = torch.from_numpy(start.copy()).to(dev)
+            limit = torch.full((B,), T, dtype=torch.int32, device=dev)
+            stats = torch.zeros((B, 2), dtype=torch.int64, device=dev)
+            step = DraftStep(B, T, task.K, device=dev)
+            model = synth.TargetModel(target, task.K, task.V, task.seed, device=dev)
+            stream = torch.cuda.current_stream()
+            z = model.logits(ld)       # the one logits buffer, patched in place per step
+            if "hidden" in kw:         # blocks per sequence from the prompt's candidate counts
+                step.make_draft(td, ld, **kw)
+                step.tune_split(step.cand_count.cpu().numpy(), hidden=True)
+            ops = [c for _, c in step.plan(td, ld, z, commit=(limit, stats), stream=stream, **kw)]
+            ev = TimingEvents(4 * (T - int(start.min())) + 8)
+            n = 0
+            while True:
+                if n % 4 == 0 and bool((ld >= limit).all()):
+                    break
+                model.logits(ld)
+                ev.record(2 * n, stream)
+                for call in ops:
+                    call()
+                ev.record(2 * n + 1, stream)
+                n += 1
+            torch.cuda.synchronize()
+            us = [ev.elapsed_ms(2 * i, 2 * i + 1) * 1e3 for i in range(n)]
+            ev.close()
+            s = stats.cpu().numpy()
+            assert np.array_equal(td.cpu().numpy(), target), "the loop must end on the targets"
+        steps = int(s[:, 1].sum())
+        results[name] = {"avg_accept_len": round(float(s[:, 0].sum()) / max(steps, 1), 4),
+                         "loop_steps": n, "drafting": [c for c, _ in step.plan(
+                             td, ld, z, stream=stream, **kw)][:-2],
+                         "blocks_per_seq": step.draft_split,
+                         "us_per_step": round(float(np.mean(us)), 2),
+                         "us_per_step_p50": round(float(np.median(us)), 2),
+                         "tokens_generated": int(s[:, 0].sum())}
+        log(f"[loop] {name}: {n} steps, {results[name]['avg_accept_len']} tokens per step, "
+            f"{results[name]['us_per_step']} us per step")
+    first = results["pld_plus_hidden"]
+    line = {"metric": LOOP_METRIC, "value": first["us_per_step"], "unit": "us", "n_gpus": 1,
+            "higher_is_better": False, "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+            "config": {"workload": task.name, "batch": B, "context": T,
+                       "generated": int(T - start.min()), "vocab": task.V, "K": task.K,
+                       "hidden_dim": task.d, "model": "stand-in: greedy output = target"},
+            "rankings": results}
     print(json.dumps(line), flush=True)
 
 

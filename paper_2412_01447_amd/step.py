@@ -221,12 +221,23 @@ class DraftStep:
         self.verify(logits, stream=stream)
 
     def plan(self, tokens, lens, logits, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
-             threshold=float("-inf"), stream=None):
+             threshold=float("-inf"), prefix_match=None, commit=None, stream=None):
         """The step as an ordered list of (name, prepared call), one kernel per entry
         except "find" on long contexts (two): the same work as run(), with every
-        argument marshalled once so that issuing a step costs only the launches."""
+        argument marshalled once so that issuing a step costs only the launches.
+        commit=(limit, stats) appends the commit of the generation loop."""
         P = dict(stream=stream, prepare=True)
-        if self.uses_fused(hidden, attn):
+        if prefix_match is not None:
+            ops = [("find", pld_find_candidates(tokens, lens, ngram[0], ngram[1], self.cand_pos,
+                                                self.cand_count, self.ngram_used, self.scratch,
+                                                **P)),
+                   ("select_prefix", pld_select_prefix(tokens, lens, self.cand_pos,
+                                                       self.cand_count, self.best_pos,
+                                                       self.best_score, prefix_match,
+                                                       scores=self.scores, **P)),
+                   ("emit", pld_emit_draft(tokens, lens, self.best_pos, self.K, self.draft,
+                                           self.draft_len, **P))]
+        elif self.uses_fused(hidden, attn):
             if hidden is not None:
                 d = pld_draft_hidden(tokens, lens, ngram[0], ngram[1], hidden, self.K,
                                      self.cand_pos, self.cand_count, self.ngram_used,
@@ -271,12 +282,16 @@ class DraftStep:
                 logits, self.draft, self.draft_len, self.temperature, self.uniforms,
                 self.accept_len, self.out_tokens, self.out_count, self.workspace,
                 row_sample=self.row_sample, **P)))
-            return ops
-        ops.append(("verify_argmax", pld_verify_argmax(logits, self.draft_len, self.workspace,
-                                                       **P)))
-        ops.append(("verify_accept", pld_verify_accept(self.draft, self.draft_len,
-                                                       self.accept_len, self.out_tokens,
-                                                       self.out_count, self.workspace, **P)))
+        else:
+            ops.append(("verify_argmax", pld_verify_argmax(logits, self.draft_len,
+                                                           self.workspace, **P)))
+            ops.append(("verify_accept", pld_verify_accept(self.draft, self.draft_len,
+                                                           self.accept_len, self.out_tokens,
+                                                           self.out_count, self.workspace, **P)))
+        if commit is not None:
+            limit, stats = commit
+            ops.append(("commit", pld_commit(tokens, lens, self.out_tokens, self.out_count,
+                                             limit=limit, stats=stats, **P)))
         return ops
 
     def host(self):

@@ -85,7 +85,7 @@ CONFIGS = {
               (1, 1), 4096, "hidden", 0, 32, "f32", 4, query_count_max=4000),
     # The paper's own two settings at its input sizes: PLD+(a) takes the MAX over
     # the top-50 induction heads across layers with K = 70 (Eq. 3, Sec. 5.5 and the
-    # head-count table of Sec. 7), PLD+(h) the cosine ranking with theta = 0, the
+    # head-count table of App. B), PLD+(h) the cosine ranking with theta = 0, the
     # best threshold of App. B.  The last token is a frequent one (up to 64
     # occurrences), so that ranking and threshold have candidates to act on.
     6: Config("b1_t1024_v32000_attn_max_r50_k70", 1, 1024, 32000, 1.1, 0.40, (8, 32), (1, 1),
