@@ -54,6 +54,9 @@ def parse():
     p.add_argument("--verify", choices=["greedy", "sample"], default="greedy",
                    help="verification: argmax (greedy) or sampling at --temperature")
     p.add_argument("--temperature", type=float, default=1.0)
+    p.add_argument("--probe", action="store_true",
+                   help="instead of the step benchmark, run bench_probe (the read-bandwidth "
+                        "ceilings of the kernels' access patterns, from HBM) and print its lines")
     p.add_argument("--loop", default=None,
                    help="instead of the step benchmark, run the generation loop on a decoding "
                         "task (synth.DECODE_TASKS) with each ranking and report the loop step "
@@ -187,6 +190,13 @@ def main():
     import synth
     from paper_2412_01447_amd.step import DraftStep
 
+    if args.probe:
+        import subprocess
+        exe = os.path.join(ROOT, "bench_probe")
+        if not os.path.exists(exe):
+            sys.exit(f"{exe} is missing: build it with `python -c 'import __graft_entry__ as g; "
+                     "g.build()'`")
+        sys.exit(subprocess.run([exe]).returncode)
     if args.loop:
         return run_loop(args)
     cfg = synth.CONFIGS[args.config]
