@@ -551,6 +551,60 @@ def test_graph_replays_match_eager(mode):
         torch.cuda.synchronize()
 
 
+def test_graph_replays_sampling_and_loop_steps():
+    """Sampling verification, and a whole loop step (draft, verify, commit, which
+    moves the state forward), captured in HIP graphs: every replay matches the
+    same calls made eagerly, with eager work between the replays."""
+    say("graph replay: sampling and loop steps")
+    from paper_2412_01447_amd.step import DraftStep
+    cfg = synth.Config("t", 4, 3000, 300, 1.1, 0.4, (8, 32), (1, 2), 256, "hidden", 0, 8, "f32", 43)
+    w = synth.make_workload(cfg, "cuda", structured=True)
+    dr, dl = synth.intended_drafts(w["metas"], cfg.K)
+    z = d_f32(synth.logits_for(w, dr, dl))
+    U = d_f32(synth.make_uniforms(cfg.B, cfg.K, 43))
+
+    def fresh():
+        st = DraftStep(cfg.B, cfg.T + 64, cfg.K, device="cuda", keep_scores=True)
+        st.set_sampling(0.7, 300, False, uniforms=U)
+        toks = torch.full((cfg.B, cfg.T + 64), -1, dtype=torch.int32, device="cuda")
+        toks[:, :cfg.T] = d_i32(w["tokens"])
+        hid = torch.zeros((cfg.B, cfg.T + 64, 256), dtype=torch.bfloat16, device="cuda")
+        hid[:, :cfg.T] = w["hidden"]
+        return st, toks, d_i32(w["lens"]), hid, torch.zeros((cfg.B, 2), dtype=torch.int64,
+                                                           device="cuda")
+
+    def one_step(st, toks, lens, hid, stats):
+        st.run(toks, lens, z, hidden=hid, ngram=cfg.ngram)
+        st.commit(toks, lens, stats=stats)
+
+    eager = fresh()
+    cap = fresh()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):          # warm-up outside the capture, then restore the state
+        one_step(*cap)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    cap = fresh()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        one_step(*cap)
+    for rep in range(4):
+        one_step(*eager)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        a, b = eager[0].host(), cap[0].host()
+        for k in a:
+            assert np.array_equal(a[k], b[k], equal_nan=True), (rep, k)
+        for i in (1, 2, 4):
+            assert torch.equal(eager[i], cap[i]), (rep, i)
+        assert torch.equal(eager[0].row_sample, cap[0].row_sample), rep
+        ws = cap[0].workspace[:pld.pld_workspace_bytes(cfg.B, cfg.K)]
+        assert int(torch.count_nonzero(ws).item()) == 0
+    assert int(cap[2].sum()) > int(d_i32(w["lens"]).sum())   # the replays moved forward
+
+
 def test_verify_aligned_rows_with_tail():
     """16-byte aligned rows (the persistent kernel) whose width is not a whole
     number of vectors: the last elements of each row are taken one by one."""
