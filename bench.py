@@ -45,6 +45,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="CPU work the oracle baseline is given (whole steps, at least one)")
+    p.add_argument("--warm", action="store_true",
+                   help="one copy of the inputs, so steps re-read what the last-level cache holds "
+                        "(labelled warm in the output); the default rotates cold copies")
     p.add_argument("--copy-probe", action="store_true",
                    help="after the timed region, copy 1 GiB three times (counter calibration)")
     p.add_argument("--event-every", type=int, default=8,
@@ -248,7 +251,7 @@ def main():
     dominant = max(nbytes, key=nbytes.get)
     # input copies at distinct addresses: the steps of one rotation touch at
     # least twice the last-level cache
-    copies = int(min(64, max(2, math.ceil(2 * MALL_BYTES / max(step_bytes, 1)))))
+    copies = 1 if args.warm else int(min(64, max(2, math.ceil(2 * MALL_BYTES / max(step_bytes, 1)))))
     sets = [base]
     for _ in range(copies - 1):
         sets.append({k: (v.clone() if v is not None else None) for k, v in base.items()})
@@ -285,8 +288,11 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ms_per_step = elapsed * 1e3 / args.steps
-    dom_ms = sum(ev.elapsed_ms(2 * e, 2 * e + 1) for e in range(len(timed))) / len(timed)
+    dom_each = [ev.elapsed_ms(2 * e, 2 * e + 1) for e in range(len(timed))]
+    dom_ms = sum(dom_each) / len(dom_each)
     ev.close()
+    import numpy as np
+    pct = {f"p{q}_us": round(float(np.percentile(dom_each, q)) * 1e3, 2) for q in (10, 50, 90)}
 
     roofline = None
     if dom_ms:
@@ -295,7 +301,7 @@ def main():
                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                     "traffic": measured_traffic(cfg.name, dominant),
                     "bytes_per_launch": nbytes[dominant],
-                    "avg_us": round(dom_ms * 1e3, 2), "launches_timed": len(timed)}
+                    "avg_us": round(dom_ms * 1e3, 2), **pct, "launches_timed": len(timed)}
         log(f"[bench] {dominant}: {dom_ms * 1e3:.2f} us avg, {achieved:.1f} GB/s")
 
     if args.copy_probe:
@@ -327,6 +333,10 @@ def main():
                    "verification": (f"sampling at temperature {args.temperature}" if sample
                                     else "greedy"),
                    "input_copies": copies,
+                   "cache": "warm: one copy of the inputs" if args.warm else
+                            "cold: copies rotated past the last-level cache",
+                   **({"attn_bytes_dense": int(cfg.B) * cfg.R * cfg.T * 4}
+                      if cfg.rank in ("attn", "both") else {}),
                    "step_bytes": step_bytes},
         "roofline": roofline,
         "cpu_baseline": cpu,
@@ -409,10 +419,26 @@ def run_loop(args):
     print(json.dumps(line), flush=True)
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg, w, z, bf16, seconds, log, sampling=None):
-    """The oracle's whole step on the host, single-threaded, on the same inputs."""
+    """The oracle's whole step on the host, on the same inputs: single-threaded
+    (the reported value, with a per-operation breakdown), then the same oracle
+    calls spread over sequences on a pool of threads (the C oracle releases the
+    interpreter lock, so sequences run in parallel; the oracle itself is
+    unchanged)."""
     import numpy as np
     import torch
+    from concurrent.futures import ThreadPoolExecutor
 
     import oracle
     toks, lens = w["tokens"], w["lens"]
@@ -428,35 +454,61 @@ def cpu_baseline(cfg, w, z, bf16, seconds, log, sampling=None):
             hb[b, rows] = w["hidden"][b].index_select(0, idx).view(torch.int16).cpu().numpy() \
                 .view(np.uint16)
     attn = w["attn"]
+    agg = oracle.AGG_MAX if cfg.agg == "max" else oracle.AGG_SUM
+    ops = {"find": 0.0, "rank": 0.0, "emit": 0.0, "verify": 0.0}
 
-    def one():
-        p, c, n = oracle.find(toks, lens, *cfg.ngram)
+    def one(sl=slice(None), timing=None):
+        t = time.perf_counter
+        t0 = t()
+        p, c, n = oracle.find(toks[sl], lens[sl], *cfg.ngram)
+        t1 = t()
         if attn is not None:
-            sa, ba, _ = oracle.rank_attn(attn, lens, p, c,
-                                         oracle.AGG_MAX if cfg.agg == "max" else oracle.AGG_SUM,
-                                         cfg.theta)
-            best = ba
+            _, best, _ = oracle.rank_attn(attn[sl], lens[sl], p, c, agg, cfg.theta)
         if hb is not None:
-            sh, bh, _ = oracle.rank_hidden(hb, lens, p, c, cfg.theta)
-            best = bh
-        dr, dl = oracle.emit(toks, lens, best, cfg.K)
+            _, best, _ = oracle.rank_hidden(hb[sl], lens[sl], p, c, cfg.theta)
+        t2 = t()
+        dr, dl = oracle.emit(toks[sl], lens[sl], best, cfg.K)
+        t3 = t()
         if sampling is not None:
-            oracle.verify_sample(z, dr, dl, sampling[0], sampling[1], bf16=bf16)
+            oracle.verify_sample(z[sl], dr, dl, sampling[0], sampling[1][sl], bf16=bf16)
         else:
-            oracle.verify(z, dr, dl, bf16=bf16)
+            oracle.verify(z[sl], dr, dl, bf16=bf16)
+        t4 = t()
+        if timing is not None:
+            for k, a_, b_ in (("find", t0, t1), ("rank", t1, t2), ("emit", t2, t3),
+                              ("verify", t3, t4)):
+                timing[k] += b_ - a_
 
     n = 0
     t0 = time.perf_counter()
     while True:
-        one()
+        one(timing=ops)
         n += 1
         if time.perf_counter() - t0 >= seconds:
             break
     dt = (time.perf_counter() - t0) / n
     log(f"[bench] cpu oracle: {n} whole steps, {dt * 1e3:.2f} ms per step")
-    return {"value": round(dt * 1e6, 1), "unit": "us", "cores": 1, "kind": "oracle",
-            "sample": f"{n} whole steps of the same workload (all {cfg.B} sequences), "
-                      f"single-threaded C oracle in fp64"}
+    out = {"value": round(dt * 1e6, 1), "unit": "us", "cores": 1, "kind": "oracle",
+           "sample": f"{n} whole steps of the same workload (all {cfg.B} sequences), "
+                     f"single-threaded C oracle in fp64",
+           "per_op_us": {k: round(v / n * 1e6, 1) for k, v in ops.items()},
+           "cpu_model": cpu_model()}
+    threads = min(cfg.B, 16, os.cpu_count() or 1)
+    if threads > 1:
+        parts = [slice(i, i + 1) for i in range(cfg.B)]
+        with ThreadPoolExecutor(threads) as pool:
+            m = 0
+            t0 = time.perf_counter()
+            while True:
+                list(pool.map(lambda sl: one(sl), parts))
+                m += 1
+                if time.perf_counter() - t0 >= seconds / 2:
+                    break
+            dtp = (time.perf_counter() - t0) / m
+        out["parallel"] = {"value": round(dtp * 1e6, 1), "unit": "us", "threads": threads,
+                           "sample": f"{m} whole steps, one sequence per task"}
+        log(f"[bench] cpu oracle on {threads} threads: {dtp * 1e3:.2f} ms per step")
+    return out
 
 
 if __name__ == "__main__":

@@ -12,6 +12,9 @@
 //   columns  one 4-byte value from each of 64 rows 64 KB apart per lane, for
 //            285 random columns of each of 64 sequences (the attention gathers
 //            of the b64 workload); bytes counted as distinct 128-byte lines
+//   strideS  4M 4-byte reads S bytes apart (S = 32 .. 512), consecutive lanes
+//            on consecutive addresses: the time per read shows the granule the
+//            memory system fetches for scattered 4-byte loads
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -80,6 +83,18 @@ __global__ __launch_bounds__(256) void columns_kernel(const float *buf, int R, i
 #pragma unroll
         for (int u = 0; u < 32; ++u) acc += v[u];
     }
+    if (acc == 12345.f) sink[i] = acc;
+}
+
+__global__ __launch_bounds__(256) void strided_kernel(const float *p, size_t stride, float *sink) {
+    const size_t n = (size_t)gridDim.x * blockDim.x;
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(p + ((size_t)u * n + i) * stride);
+    float acc = 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
     if (acc == 12345.f) sink[i] = acc;
 }
 
@@ -177,6 +192,24 @@ int main() {
                                reinterpret_cast<float *>(sink));
         }, nsets);
         report("columns", (double)lines * R * 128, us);
+    }
+    for (int stride : {32, 64, 128, 256, 512}) {   // 4M reads, spans of 128 MB to 2 GB
+        const size_t reads = (size_t)1 << 22, threads = reads / 8;
+        const size_t span = reads * stride;
+        const int variants = (int)std::min<size_t>(4, buf_bytes / span);
+        const float *fb = reinterpret_cast<const float *>(buf);
+        const double us = time_us([&](int r) {
+            hipLaunchKernelGGL(strided_kernel, dim3((unsigned)(threads / 256)), dim3(256), 0, 0,
+                               fb + (size_t)r * (span / 4), (size_t)stride / 4,
+                               reinterpret_cast<float *>(sink));
+        }, variants);
+        char name[32];
+        std::snprintf(name, sizeof(name), "stride%d", stride);
+        std::printf("{\"pattern\": \"%s\", \"reads\": %zu, \"us\": %.2f, \"ns_per_read\": %.4f, "
+                    "\"GBps_if_64B\": %.1f, \"GBps_if_128B\": %.1f}\n",
+                    name, reads, us, us * 1e3 / reads, reads * 64.0 / (us * 1e-6) / 1e9,
+                    reads * 128.0 / (us * 1e-6) / 1e9);
+        std::fflush(stdout);
     }
     CK(hipFree(didx));
     CK(hipFree(sink));
