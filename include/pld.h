@@ -145,7 +145,9 @@ int pld_rank_hidden(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_
  * aggregation of the ablation (Sec. 7.1).  The caller passes, per sequence,
  * R rows: the attention of query position T-2 over keys 0..n_keys-1 for each
  * selected (layer, head).
- *   agg = PLD_AGG_SUM:  s_j = sum_{r<R} A[r][j-1], added in fp32 in r order
+ *   agg = PLD_AGG_SUM:  s_j = sum_{r<R} A[r][j-1], added in fp32 in a fixed
+ *                       order: eight partial sums (rows t, t+8, ... in order,
+ *                       t = 0..7), then combined pairwise (t^1, t^2, t^7)
  *   agg = PLD_AGG_MAX:  s_j = max_{r<R} A[r][j-1]
  * Selection, threshold and outputs as in pld_rank_hidden.
  *

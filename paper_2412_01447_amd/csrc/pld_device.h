@@ -329,21 +329,37 @@ __device__ __forceinline__ void rows_dot(const uint4 *const (&rows)[G], const ui
     }
 }
 
-// Aggregated attention of one candidate (Eq. 3 / Sec. 7.1): the R weights
-// A[r][j-1] (col = &A[0][j-1], rows ar apart) summed in r order in fp32, or
-// their maximum.  Up to 32 weights are requested at once.
-__device__ __forceinline__ float attn_gather(const float *col, int64_t ar, int R, bool sum) {
-    float acc = sum ? 0.f : -INFINITY;
-    for (int r0 = 0; r0 < R; r0 += 32) {
-        float v[32];
+// Aggregated attention of one candidate (Eq. 3 / Sec. 7.1), gathered by a
+// group of kGatherLanes consecutive lanes: lane t of the group reads the
+// weights A[r][j-1] of rows r = t, t+8, t+16, ... (col = &A[0][j-1], rows ar
+// apart), up to 8 of them requested at once, and sums them in that order in
+// fp32 (or takes their maximum); the group's eight partials are then combined
+// by DPP moves inside the group (lane xor 1, xor 2, then the half-row mirror),
+// which leaves the same bits in every lane of the group.  A candidate's R loads
+// are thus one trip to memory for R <= 64.  Call with the whole wave
+// converged; `active` masks the loads of lanes without a candidate.
+constexpr int kGatherLanes = 8;
+__device__ __forceinline__ float attn_gather_group(const float *col, int64_t ar, int R, bool sum,
+                                                   bool active) {
+    const int t = lane_id() & (kGatherLanes - 1);
+    const float none = sum ? 0.f : -INFINITY;
+    float acc = none;
+    for (int r0 = 0; r0 < R; r0 += 8 * kGatherLanes) {
+        float v[8];
 #pragma unroll
-        for (int u = 0; u < 32; ++u)
-            if (r0 + u < R) v[u] = ld_stream(col + (int64_t)(r0 + u) * ar);
+        for (int u = 0; u < 8; ++u) {
+            const int r = r0 + u * kGatherLanes + t;
+            v[u] = (active && r < R) ? ld_stream(col + (int64_t)r * ar) : none;
+        }
 #pragma unroll
-        for (int u = 0; u < 32; ++u)
-            if (r0 + u < R) acc = sum ? acc + v[u] : fmaxf(acc, v[u]);
+        for (int u = 0; u < 8; ++u) acc = sum ? acc + v[u] : fmaxf(acc, v[u]);
     }
-    return acc;
+    const float x1 = dpp_move_f<kDppQuadSwap1, 0xf>(acc, none);
+    acc = sum ? acc + x1 : fmaxf(acc, x1);
+    const float x2 = dpp_move_f<kDppQuadSwap2, 0xf>(acc, none);
+    acc = sum ? acc + x2 : fmaxf(acc, x2);
+    const float x4 = dpp_move_f<kDppHalfMirror, 0xf>(acc, none);
+    return sum ? acc + x4 : fmaxf(acc, x4);
 }
 
 // Eq. 2's cosine from the dot product and the two squared norms; the clamp

@@ -126,7 +126,7 @@ __device__ void draft_score_rows(const DraftArgs &a, int b, int64_t T, bool seq_
 
 // The block's share of the ranking (Eq. 2 / Eq. 3) over the list s_cand of
 // `total` candidates: list slots w, w + kWaves, ... per wave (hidden), or one
-// slot per thread (attention).  Returns the block's best key in every thread;
+// slot per group of kGatherLanes lanes (attention).  Returns the block's best key in every thread;
 // `s_q` holds the query row (hidden), `s_key` is kWaves words of LDS.
 template <bool kHidden, int kWaves>
 __device__ uint64_t rank_candidates(const DraftArgs &a, int b, int64_t T, bool seq_ok,
@@ -149,17 +149,21 @@ __device__ uint64_t rank_candidates(const DraftArgs &a, int b, int64_t T, bool s
         // (every lane of a wave holds the wave's best)
     } else {
         const float *Ab = a.attn + (int64_t)b * a.as;
-        for (int c = threadIdx.x; c < total; c += kWaves * kWave) {
-            const int32_t j = s_cand[c];
-            float s = __builtin_nanf("");
-            if (seq_ok && j >= 1 && (int64_t)j <= T - 2 && (int64_t)(j - 1) < a.n_keys) {
-                s = attn_gather(Ab + (j - 1), a.ar, a.R, a.agg == PLD_AGG_SUM);
-                if (s > a.threshold) {
-                    const uint64_t k = rank_key(s, j);
-                    best = k > best ? k : best;
-                }
+        constexpr int kPerPass = kWaves * kWave / kGatherLanes;   // a lane group per candidate
+        for (int c0 = 0; c0 < total; c0 += kPerPass) {
+            const int c = c0 + (int)threadIdx.x / kGatherLanes;
+            const int32_t j = c < total ? s_cand[c] : 0;
+            const bool ok = c < total && seq_ok && j >= 1 && (int64_t)j <= T - 2 &&
+                            (int64_t)(j - 1) < a.n_keys;
+            const float g = attn_gather_group(Ab + (ok ? j - 1 : 0), a.ar, a.R,
+                                              a.agg == PLD_AGG_SUM, ok);
+            const float s = ok ? g : __builtin_nanf("");
+            if (ok && s > a.threshold) {
+                const uint64_t k = rank_key(s, j);
+                best = k > best ? k : best;
             }
-            if (a.scores) a.scores[(int64_t)b * a.cap + out0 + c] = s;
+            if (c < total && a.scores && (threadIdx.x & (kGatherLanes - 1)) == 0)
+                a.scores[(int64_t)b * a.cap + out0 + c] = s;
         }
         best = wave_max_u64(best);
     }

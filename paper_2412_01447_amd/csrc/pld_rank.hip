@@ -268,23 +268,24 @@ __global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a)
     candidate_prefix(c, pre);
     uint32_t lo, hi;
     block_share(pre[c.B], lo, hi);
-    for (uint32_t base = lo; base < hi; base += kRankThreads) {
-        const uint32_t i = base + threadIdx.x;
+    // a group of kGatherLanes lanes per candidate
+    constexpr uint32_t kPerPass = kRankThreads / kGatherLanes;
+    for (uint32_t base = lo; base < hi; base += kPerPass) {
+        const uint32_t i = base + threadIdx.x / kGatherLanes;
         const bool active = i < hi;
         int b = active ? seq_of(pre, c.B, i) : 0;
         uint64_t key = 0;
-        if (active) {
-            const int64_t slot = (int64_t)(i - pre[b]);
-            const int32_t j = c.cand_pos[(int64_t)b * c.cap + slot];
-            const int64_t T = c.lens[b];
-            float s = __builtin_nanf("");
-            if (T >= 2 && j >= 1 && (int64_t)j <= T - 2 && (int64_t)(j - 1) < a.n_keys) {
-                const float *col = a.attn + (int64_t)b * a.as + (j - 1);
-                s = attn_gather(col, a.ar, a.R, a.agg == PLD_AGG_SUM);
-                if (s > c.threshold) key = rank_key(s, j);
-            }
-            if (c.scores) c.scores[(int64_t)b * c.cap + slot] = s;
-        }
+        const int64_t cs = active ? (int64_t)(i - pre[b]) : 0;   // the candidate's list slot
+        const int32_t j = active ? c.cand_pos[(int64_t)b * c.cap + cs] : 0;
+        const int64_t T = active ? c.lens[b] : 0;
+        const bool ok = active && T >= 2 && j >= 1 && (int64_t)j <= T - 2 &&
+                        (int64_t)(j - 1) < a.n_keys;
+        const float g = attn_gather_group(a.attn + (int64_t)b * a.as + (ok ? j - 1 : 0), a.ar,
+                                          a.R, a.agg == PLD_AGG_SUM, ok);
+        const float s = ok ? g : __builtin_nanf("");
+        if (ok && s > c.threshold) key = rank_key(s, j);
+        if (active && c.scores && (threadIdx.x & (kGatherLanes - 1)) == 0)
+            c.scores[(int64_t)b * c.cap + cs] = s;
         // one atomic per wave when all its lanes share a sequence
         const int b0 = __shfl(b, 0);
         const bool same = __ballot(active && b != b0) == 0ull;
