@@ -134,6 +134,18 @@ __device__ __forceinline__ int wave_sum_i32(int v) {
     return __builtin_amdgcn_readlane(v, 63);
 }
 
+// Maximum over the lanes of non-negative values (a move's unreached lanes
+// read 0, which no lane's value is below).
+__device__ __forceinline__ int wave_max_nonneg_i32(int v) {
+    v = max(v, dpp_move<kDppQuadSwap1, 0xf>(v));
+    v = max(v, dpp_move<kDppQuadSwap2, 0xf>(v));
+    v = max(v, dpp_move<kDppHalfMirror, 0xf>(v));
+    v = max(v, dpp_move<kDppMirror, 0xf>(v));
+    v = max(v, dpp_move<kDppBcast15, 0xa>(v));
+    v = max(v, dpp_move<kDppBcast31, 0xc>(v));
+    return __builtin_amdgcn_readlane(v, 63);
+}
+
 __device__ __forceinline__ float wave_sum_f32(float v) {
     v += __int_as_float(dpp_move<kDppQuadSwap1, 0xf>(__float_as_int(v)));
     v += __int_as_float(dpp_move<kDppQuadSwap2, 0xf>(__float_as_int(v)));

@@ -33,6 +33,9 @@ constexpr int kPartPass = kPartWaves * kWave * kLanePos;   // 2048 positions per
 constexpr int kPartPasses = kPartMax / kPartPass;
 constexpr int kWindow = 16384;                  // list entries per compaction pass
 constexpr int kFinishThreads = 1024;
+constexpr int kWindowPer = kWindow / kFinishThreads;   // entries per thread and pass
+constexpr int kSpecPer = 16;     // parts per wave read ahead by the finishing kernel
+constexpr int kSpecParts = kFinishThreads / kWave * kSpecPer;   // S it covers (256)
 static_assert(PLD_MAX_DRAFT_SPLIT <= kFinishThreads, "one block count per finishing thread");
 
 struct DraftArgs {
@@ -438,70 +441,167 @@ __global__ __launch_bounds__(kPartWaves * kWave) void draft_part_kernel(DraftArg
 
 // One block per sequence: the selection from the key slots (returned to
 // zero) and the draft; the offsets of the blocks' parts, in-order compaction
-// of the list (and the scores) through an LDS window, ngram_used and the
-// count.  A part's entries only move towards the start of the row (its
-// offset is at most s*P) and never over a later part's entries, and every
-// entry of a window is read before any of the window is written.
+// of the list (and the scores), ngram_used and the count.
+//
+// Read ahead: with S <= kSpecParts, wave w reads the first 64 entries of
+// parts w, w + 16, ... while the per-part counts are on their way; when no
+// part holds more than 64 entries these are all of them, and they are written
+// to their offsets once every thread's reads have returned -- one trip to
+// memory for the whole list.  Otherwise the list is compacted in windows of
+// kWindow entries: entry e of part p moves from p*P + e to off[p] + e; with
+// D[p] = p*P - off[p], which never decreases with p, the entry at list
+// position x comes from x + D of its part.  Per window, each non-empty part
+// marks D at its first position in the window, and a running maximum gives
+// every position its D.  Entries only move towards the start of the row, so
+// a window's sources lie at or after the window and the writes of a window
+// never reach a later window's sources; within a window every thread holds
+// its entries in registers and every read of the window has completed before
+// any of it is written.
 __global__ __launch_bounds__(kFinishThreads) void draft_finish_part_kernel(DraftArgs a) {
     __shared__ int32_t s_off[PLD_MAX_DRAFT_SPLIT + 1];
-    __shared__ int32_t s_win[kWindow];
+    __shared__ __align__(16) int32_t s_d[kWindow];   // D of each window position
+    __shared__ int s_wmax[kFinishThreads / kWave];
     __shared__ int s_tot[kMaxNgram];
     __shared__ int s_wsum[kFinishThreads / kWave];
+    __shared__ int s_wcmax[kFinishThreads / kWave];
     const int b = blockIdx.x;
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
+    // every load that does not wait for another goes out first: the key slots
+    // (last wave), the per-block counts, the read-ahead, then the length
+    const bool last = (w == kFinishThreads / kWave - 1);
+    uint64_t key = 0;
+    if (last && lane < kKeySlots) key = a.keys[(int64_t)b * kKeySlots + lane];
+    const int cnt = ((int)threadIdx.x < a.S) ? a.hcount[(int64_t)b * a.S + threadIdx.x] : 0;
+    int32_t *pos = a.cand_pos + (int64_t)b * a.cap;
+    float *sc = a.scores ? a.scores + (int64_t)b * a.cap : nullptr;
+    // read ahead: entry `lane` of parts w + 16 j (in the row whatever the counts)
+    const bool spec = a.S <= kSpecParts;   // uniform
+    int32_t spv[kSpecPer];
+    float ssv[kSpecPer];
+    if (spec) {
+#pragma unroll
+        for (int j = 0; j < kSpecPer; ++j) {
+            const int q = w + j * (kFinishThreads / kWave);
+            const int64_t src = (int64_t)q * a.P + lane;
+            if (q < a.S && lane < a.P && src < a.tok_stride) {
+                spv[j] = pos[src];
+                if (sc) ssv[j] = sc[src];
+            }
+        }
+    }
     const int64_t T = a.lens[b];
     const bool tok_ok = (T >= 1 && T <= a.tok_stride);   // block-uniform
     // the selection does not depend on the list: the last wave writes it and
     // the draft first, while the others start on the offsets
-    if (w == kFinishThreads / kWave - 1) {
-        uint64_t k = 0;
-        if (lane < kKeySlots) {
-            k = a.keys[(int64_t)b * kKeySlots + lane];
-            a.keys[(int64_t)b * kKeySlots + lane] = 0;
-        }
-        k = wave_max_u64(k);
-        write_draft(a, b, T, tok_ok, k, a.tokens + (int64_t)b * a.tok_stride);
+    if (last) {
+        if (lane < kKeySlots) a.keys[(int64_t)b * kKeySlots + lane] = 0;
+        key = wave_max_u64(key);
+        write_draft(a, b, T, tok_ok, key, a.tokens + (int64_t)b * a.tok_stride);
     }
     int n = -1, total = 0;
     if (tok_ok) {
         n = part_n(a, b, s_tot);
         // exclusive scan of the per-block counts, one per thread
-        const int c = (n > 0 && (int)threadIdx.x < a.S) ? a.hcount[(int64_t)b * a.S + threadIdx.x]
-                                                        : 0;
+        const int c = n > 0 ? cnt : 0;
         int wt;
         const int ex = wave_excl_scan(c, wt);
-        if (lane == 0) s_wsum[w] = wt;
+        const int cmax = wave_max_nonneg_i32(c);
+        if (lane == 0) {
+            s_wsum[w] = wt;
+            s_wcmax[w] = cmax;
+        }
         __syncthreads();
-        int pre = 0;
+        int pre = 0, most = 0;
         for (int i = 0; i < kFinishThreads / kWave; ++i) {
             if (i < w) pre += s_wsum[i];
             total += s_wsum[i];
+            most = max(most, s_wcmax[i]);
         }
         if ((int)threadIdx.x < a.S) s_off[threadIdx.x] = pre + ex;
         if (threadIdx.x == 0) s_off[a.S] = total;
-        __syncthreads();
-        int32_t *rows[2] = {a.cand_pos + (int64_t)b * a.cap,
-                            a.scores ? reinterpret_cast<int32_t *>(a.scores + (int64_t)b * a.cap)
-                                     : nullptr};
-        for (int r = 0; r < 2; ++r) {
-            int32_t *v = rows[r];
-            if (!v) continue;   // uniform
-            for (int w0 = 0; w0 < total; w0 += kWindow) {
-                const int wn = min(kWindow, total - w0);
-                for (int i = threadIdx.x; i < wn; i += kFinishThreads) {
-                    const int dpos = w0 + i;
-                    // the part p with s_off[p] <= dpos < s_off[p+1]
-                    int lo = 0, hi = a.S;
-                    while (hi - lo > 1) {
-                        const int mid = (lo + hi) >> 1;
-                        if (s_off[mid] <= dpos) lo = mid; else hi = mid;
-                    }
-                    s_win[i] = v[(int64_t)lo * a.P + (dpos - s_off[lo])];
+        __builtin_amdgcn_s_waitcnt(0);   // the read-ahead has returned ...
+        __syncthreads();                 // ... in every thread (and s_off is complete)
+        if (spec && most <= kWave) {     // block-uniform: the read-ahead holds the list
+#pragma unroll
+            for (int j = 0; j < kSpecPer; ++j) {
+                const int q = w + j * (kFinishThreads / kWave);
+                if (q < a.S && lane < s_off[q + 1] - s_off[q]) {
+                    pos[s_off[q] + lane] = spv[j];
+                    if (sc) sc[s_off[q] + lane] = ssv[j];
                 }
+            }
+        }
+        for (int w0 = 0; !(spec && most <= kWave) && w0 < total; w0 += kWindow) {
+            const int wn = min(kWindow, total - w0);
+            const int nk = (wn + kFinishThreads - 1) / kFinishThreads;   // block-uniform
+            for (int i = threadIdx.x; i < wn; i += kFinishThreads) s_d[i] = 0;
+            __syncthreads();
+            for (int q = threadIdx.x; q < a.S; q += kFinishThreads) {
+                const int o = s_off[q], e = s_off[q + 1];
+                if (e > o && e > w0 && o < w0 + wn)
+                    s_d[o > w0 ? o - w0 : 0] = (int)((int64_t)q * a.P - o);
+            }
+            __syncthreads();
+            // running maximum: kWindowPer consecutive positions per thread,
+            // then across the lanes (DPP) and the waves
+            {
+                const int base = (int)threadIdx.x * kWindowPer;
+                int v[kWindowPer];
+#pragma unroll
+                for (int c = 0; c < kWindowPer / 4; ++c) {
+                    const int4 t = reinterpret_cast<const int4 *>(s_d + base)[c];
+                    v[4 * c] = t.x;
+                    v[4 * c + 1] = t.y;
+                    v[4 * c + 2] = t.z;
+                    v[4 * c + 3] = t.w;
+                }
+#pragma unroll
+                for (int c = 0; c < kWindowPer; ++c) {
+                    if (base + c >= wn) v[c] = 0;
+                    if (c > 0) v[c] = max(v[c], v[c - 1]);
+                }
+                int inc = v[kWindowPer - 1];
+                inc = max(inc, dpp_move<kDppShr1, 0xf>(inc));
+                inc = max(inc, dpp_move<kDppShr1 + 1, 0xf>(inc));
+                inc = max(inc, dpp_move<kDppShr1 + 3, 0xf>(inc));
+                inc = max(inc, dpp_move<kDppShr1 + 7, 0xf>(inc));
+                inc = max(inc, dpp_move<kDppBcast15, 0xa>(inc));
+                inc = max(inc, dpp_move<kDppBcast31, 0xc>(inc));
+                if (lane == kWave - 1) s_wmax[w] = inc;
+                int carry = __shfl_up(inc, 1);
+                if (lane == 0) carry = 0;
                 __syncthreads();
-                for (int i = threadIdx.x; i < wn; i += kFinishThreads) v[w0 + i] = s_win[i];
+                for (int i = 0; i < w; ++i) carry = max(carry, s_wmax[i]);
+#pragma unroll
+                for (int c = 0; c < kWindowPer / 4; ++c)
+                    reinterpret_cast<int4 *>(s_d + base)[c] =
+                        make_int4(max(v[4 * c], carry), max(v[4 * c + 1], carry),
+                                  max(v[4 * c + 2], carry), max(v[4 * c + 3], carry));
                 __syncthreads();
+            }
+            int32_t pv[kWindowPer];
+            float sv[kWindowPer];
+            // all of this thread's reads of the window are issued before any
+            // is waited for: one trip to memory per window
+#pragma unroll
+            for (int k = 0; k < kWindowPer; ++k) {
+                const int i = (int)threadIdx.x + k * kFinishThreads;
+                if (k < nk && i < wn) {
+                    const int64_t src = (int64_t)s_d[i] + w0 + i;
+                    pv[k] = pos[src];
+                    if (sc) sv[k] = sc[src];
+                }
+            }
+            __builtin_amdgcn_s_waitcnt(0);   // the reads have returned ...
+            __syncthreads();                 // ... in every thread of the block
+#pragma unroll
+            for (int k = 0; k < kWindowPer; ++k) {
+                const int i = (int)threadIdx.x + k * kFinishThreads;
+                if (k < nk && i < wn) {
+                    pos[w0 + i] = pv[k];
+                    if (sc) sc[w0 + i] = sv[k];
+                }
             }
         }
     }

@@ -407,6 +407,8 @@ DRAFT_CASES = [
     # long contexts (split positions only) and a stride that is not a multiple of 4
     (3, 20000, 30, 1, 3, 256, 0, 8, 8), (3, 40000, 5, 1, 1, 0, 5, 8, 9),
     (4, 20001, 3, 2, 4, 64, 0, 5, 10),
+    # more occurrences in one sequence than one compaction window (16384) holds
+    (2, 40000, 1, 1, 1, 0, 3, 5, 11), (2, 36000, 2, 1, 1, 64, 0, 5, 12),
 ]
 DRAFT_SPLITS = [1, 3, 64, 1000]
 
@@ -481,6 +483,15 @@ def test_draft_fused_parity(case, split):
         assert np.array_equal(g["best_pos"], split_ref[1])
         rd, rl = oracle.emit(toks, lens, g["best_pos"] if flips else rbp, K)
         assert np.array_equal(g["draft"], rd) and np.array_equal(g["draft_len"], rl)
+
+
+@pytest.mark.parametrize("split", [64, 57, 1000])
+def test_draft_finish_read_ahead_limits(split):
+    """All-equal tokens make every position an occurrence.  4096 positions in
+    64 parts of 64 entries fill the finishing kernel's read-ahead exactly; 57
+    parts of 72 hold more than it reads per part, and 512 parts of 8 are more
+    parts than it covers: both take the windowed compaction."""
+    test_draft_fused_parity((2, 4096, 1, 1, 1, 64, 0, 6, 13), split)
 
 
 # ------------------------------------------------ halves and graph replays
