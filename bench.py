@@ -52,6 +52,9 @@ def parse():
                    help="after the timed region, copy 1 GiB three times (counter calibration)")
     p.add_argument("--event-every", type=int, default=8,
                    help="bracket the dominant call with timing events on every N-th timed step")
+    p.add_argument("--split", type=int, default=0,
+                   help="blocks per sequence of the one-call drafting (default: from the "
+                        "first step's candidate counts)")
     p.add_argument("--mode", choices=["auto", "fused", "split"], default="auto",
                    help="drafting: one-launch call (fused), separate calls (split), or auto")
     p.add_argument("--verify", choices=["greedy", "sample"], default="greedy",
@@ -241,9 +244,6 @@ def main():
     # drafting, how many blocks should share a sequence)
     run(base)
     torch.cuda.synchronize()
-    if fused:
-        step.tune_split(step.cand_count.cpu().numpy(), hidden=base["hidden"] is not None)
-        log(f"[bench] drafting with {step.draft_split} block(s) per sequence")
     nbytes = algorithmic_bytes(cfg, lens, step.cand_count.cpu().numpy(),
                                step.draft_len.cpu().numpy(), step.cand_pos.cpu().numpy(), elt,
                                fused, sample=sample)
@@ -258,11 +258,22 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] step bytes {step_bytes / 1e6:.2f} MB {json.dumps(nbytes)}; "
         f"dominant {dominant}; {copies} input copies")
-
     # every step as prepared calls (arguments marshalled once, one kernel each)
     stream = torch.cuda.current_stream()
-    plans = [step.plan(s_["tokens"], s_["lens"], s_["logits"], hidden=s_["hidden"],
-                       attn=s_["attn"], stream=stream, **rank_args) for s_ in sets]
+
+    def make_plans():
+        return [step.plan(s_["tokens"], s_["lens"], s_["logits"], hidden=s_["hidden"],
+                          attn=s_["attn"], stream=stream, **rank_args) for s_ in sets]
+
+    if fused:
+        # blocks per sequence for the one-call drafting, from the first step's
+        # candidate counts (or as given)
+        if args.split:
+            step.set_split(args.split)
+        else:
+            step.tune_split(step.cand_count.cpu().numpy(), hidden=base["hidden"] is not None)
+        log(f"[bench] drafting with {step.draft_split} block(s) per sequence")
+    plans = make_plans()
     names = [n for n, _ in plans[0]]
     assert set(names) == set(nbytes), (names, list(nbytes))
     # the dominant call is bracketed by events on every `event_every`-th timed
@@ -381,7 +392,10 @@ def run_loop(args):
             z = model.logits(ld)       # the one logits buffer, patched in place per step
             if "hidden" in kw:         # blocks per sequence from the prompt's candidate counts
                 step.make_draft(td, ld, **kw)
-                step.tune_split(step.cand_count.cpu().numpy(), hidden=True)
+                if args.split:
+                    step.set_split(args.split)
+                else:
+                    step.tune_split(step.cand_count.cpu().numpy(), hidden=True)
             ops = [c for _, c in step.plan(td, ld, z, commit=(limit, stats), stream=stream, **kw)]
             ev = TimingEvents(4 * (T - int(start.min())) + 8)
             n = 0

@@ -28,14 +28,21 @@
 namespace pld {
 
 constexpr int kPartMax = 8192;                  // positions per block, S > 1
-constexpr int kPartWaves = 4;                   // 256 threads per block, S > 1
-constexpr int kPartPass = kPartWaves * kWave * kLanePos;   // 2048 positions per pass
-constexpr int kPartPasses = kPartMax / kPartPass;
+constexpr int kPartWaves = 4;                   // counting pass; ranking blocks of many
+constexpr int kPartWavesFew = 8;                // ranking blocks when the grid is small
+constexpr int kFewBlocks = 512;                 // B*S up to which the blocks get 8 waves
+// Positions searched per pass and passes per block for a block of kWaves waves.
+template <int kWaves>
+struct PartShape {
+    static constexpr int kPass = kWaves * kWave * kLanePos;
+    static constexpr int kPasses = kPartMax / kPass;
+};
 constexpr int kWindow = 16384;                  // list entries per compaction pass
 constexpr int kFinishThreads = 1024;
 constexpr int kWindowPer = kWindow / kFinishThreads;   // entries per thread and pass
 constexpr int kSpecPer = 16;     // parts per wave read ahead by the finishing kernel
-constexpr int kSpecParts = kFinishThreads / kWave * kSpecPer;   // S it covers (256)
+constexpr int kSpecWaves = kFinishThreads / kWave - 1;   // all but the draft's wave
+constexpr int kSpecParts = kSpecWaves * kSpecPer;        // S it covers (240)
 static_assert(PLD_MAX_DRAFT_SPLIT <= kFinishThreads, "one block count per finishing thread");
 
 struct DraftArgs {
@@ -285,12 +292,14 @@ __device__ __forceinline__ void stage_part(const int32_t *x, int64_t s0, int64_t
 
 // Hit words of this thread, pass by pass (pass t: the 8 positions from
 // lo + t*2048 + 8*threadIdx.x); zero from lo + P on.
+template <int kWaves>
 __device__ __forceinline__ void part_hits(const int32_t *s_x, int64_t s0, int64_t T, int64_t lo,
                                           int64_t P, const Query &q, int nmax,
-                                          uint64_t (&hits)[kPartPasses]) {
+                                          uint64_t (&hits)[PartShape<kWaves>::kPasses]) {
+    constexpr int kPasses = PartShape<kWaves>::kPasses, kPass = PartShape<kWaves>::kPass;
 #pragma unroll
-    for (int t = 0; t < kPartPasses; ++t) {
-        const int64_t base = lo + (int64_t)t * kPartPass + (int64_t)threadIdx.x * kLanePos;
+    for (int t = 0; t < kPasses; ++t) {
+        const int64_t base = lo + (int64_t)t * kPass + (int64_t)threadIdx.x * kLanePos;
         hits[t] = (base < lo + P) ? lane_hits(s_x, s0, T, base, q, nmax) : 0ull;
     }
 }
@@ -316,13 +325,13 @@ __global__ __launch_bounds__(kPartWaves * kWave) void draft_count_kernel(DraftAr
     const Query q = load_query(x, T, a.nmax);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    uint64_t hits[kPartPasses];
-    part_hits(s_x, s0, T, lo, a.P, q, a.nmax, hits);
+    uint64_t hits[PartShape<kPartWaves>::kPasses];
+    part_hits<kPartWaves>(s_x, s0, T, lo, a.P, q, a.nmax, hits);
     int cnt[kMaxNgram];
 #pragma unroll
     for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
 #pragma unroll
-    for (int t = 0; t < kPartPasses; ++t) count_levels(hits[t], a.nmax, cnt);
+    for (int t = 0; t < PartShape<kPartWaves>::kPasses; ++t) count_levels(hits[t], a.nmax, cnt);
 #pragma unroll
     for (int k = 0; k < kMaxNgram; ++k) {
         if (k < a.nmax) {   // uniform
@@ -369,14 +378,15 @@ __device__ int part_n(const DraftArgs &a, int b, int *s_tot) {
 // that small slices leave room for many blocks per CU.
 static size_t part_tok_bytes(int64_t P) { return align_up((size_t)(P + 8) * 4, 16); }
 
-template <bool kHidden>
-__global__ __launch_bounds__(kPartWaves * kWave) void draft_part_kernel(DraftArgs a) {
+template <bool kHidden, int kWaves>
+__global__ __launch_bounds__(kWaves * kWave) void draft_part_kernel(DraftArgs a) {
+    constexpr int kPasses = PartShape<kWaves>::kPasses, kPass = PartShape<kWaves>::kPass;
     extern __shared__ uint4 s_dyn[];
     int32_t *s_x = reinterpret_cast<int32_t *>(s_dyn);   // tokens, then the block's list
     const uint4 *s_q = s_dyn + ((a.P + 8) * 4 + 15) / 16;   // query row H[T-2] (hidden)
     __shared__ int s_tot[kMaxNgram];
-    __shared__ int s_wc[kPartPasses][kPartWaves];
-    __shared__ uint64_t s_key[kPartWaves];
+    __shared__ int s_wc[kPasses][kWaves];
+    __shared__ uint64_t s_key[kWaves];
     const int s = blockIdx.x, b = blockIdx.y;
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
@@ -403,11 +413,11 @@ __global__ __launch_bounds__(kPartWaves * kWave) void draft_part_kernel(DraftArg
         if (threadIdx.x == 0) a.hcount[(int64_t)b * a.S + s] = 0;
         return;
     }
-    uint64_t hits[kPartPasses];
-    part_hits(s_x, s0, T, lo, a.P, q, a.nmax, hits);
-    uint32_t bits[kPartPasses];
+    uint64_t hits[kPasses];
+    part_hits<kWaves>(s_x, s0, T, lo, a.P, q, a.nmax, hits);
+    uint32_t bits[kPasses];
 #pragma unroll
-    for (int t = 0; t < kPartPasses; ++t) {
+    for (int t = 0; t < kPasses; ++t) {
         bits[t] = level_bits(hits[t], n);
         const int c = wave_sum_i32(__popc(bits[t]));
         if (lane == 0) s_wc[t][w] = c;
@@ -415,11 +425,11 @@ __global__ __launch_bounds__(kPartWaves * kWave) void draft_part_kernel(DraftArg
     __syncthreads();   // every token read is done: s_x becomes the block's list
     // list order is ascending position: pass, then wave, then lane
     int total = 0;
-    int start[kPartPasses];
+    int start[kPasses];
 #pragma unroll
-    for (int t = 0; t < kPartPasses; ++t) {
+    for (int t = 0; t < kPasses; ++t) {
         start[t] = total;
-        for (int i = 0; i < kPartWaves; ++i) {
+        for (int i = 0; i < kWaves; ++i) {
             if (i < w) start[t] += s_wc[t][i];
             total += s_wc[t][i];
         }
@@ -428,12 +438,12 @@ __global__ __launch_bounds__(kPartWaves * kWave) void draft_part_kernel(DraftArg
     if (total == 0) return;   // block-uniform
     int32_t *out = a.cand_pos + (int64_t)b * a.cap + lo;
 #pragma unroll
-    for (int t = 0; t < kPartPasses; ++t)
-        emit_bits(bits[t], lo + (int64_t)t * kPartPass + (int64_t)threadIdx.x * kLanePos, s_x,
+    for (int t = 0; t < kPasses; ++t)
+        emit_bits(bits[t], lo + (int64_t)t * kPass + (int64_t)threadIdx.x * kLanePos, s_x,
                   out, start[t]);
     __syncthreads();
     const uint64_t best =
-        rank_candidates<kHidden, kPartWaves>(a, b, T, seq_ok, s_x, total, lo, s_q, s_key);
+        rank_candidates<kHidden, kWaves>(a, b, T, seq_ok, s_x, total, lo, s_q, s_key);
     if (threadIdx.x == 0 && best)
         atomicMax((unsigned long long *)&a.keys[(int64_t)b * kKeySlots + (s % kKeySlots)],
                   (unsigned long long)best);
@@ -443,8 +453,9 @@ __global__ __launch_bounds__(kPartWaves * kWave) void draft_part_kernel(DraftArg
 // zero) and the draft; the offsets of the blocks' parts, in-order compaction
 // of the list (and the scores), ngram_used and the count.
 //
-// Read ahead: with S <= kSpecParts, wave w reads the first 64 entries of
-// parts w, w + 16, ... while the per-part counts are on their way; when no
+// Read ahead: with S <= kSpecParts, wave w < 15 reads the first 64 entries
+// of parts w, w + 15, ... while the per-part counts are on their way (the
+// last wave, which writes the draft, keeps its memory queue to itself); when no
 // part holds more than 64 entries these are all of them, and they are written
 // to their offsets once every thread's reads have returned -- one trip to
 // memory for the whole list.  Otherwise the list is compacted in windows of
@@ -475,14 +486,14 @@ __global__ __launch_bounds__(kFinishThreads) void draft_finish_part_kernel(Draft
     const int cnt = ((int)threadIdx.x < a.S) ? a.hcount[(int64_t)b * a.S + threadIdx.x] : 0;
     int32_t *pos = a.cand_pos + (int64_t)b * a.cap;
     float *sc = a.scores ? a.scores + (int64_t)b * a.cap : nullptr;
-    // read ahead: entry `lane` of parts w + 16 j (in the row whatever the counts)
+    // read ahead: entry `lane` of parts w + 15 j (in the row whatever the counts)
     const bool spec = a.S <= kSpecParts;   // uniform
     int32_t spv[kSpecPer];
     float ssv[kSpecPer];
-    if (spec) {
+    if (spec && !last) {
 #pragma unroll
         for (int j = 0; j < kSpecPer; ++j) {
-            const int q = w + j * (kFinishThreads / kWave);
+            const int q = w + j * kSpecWaves;
             const int64_t src = (int64_t)q * a.P + lane;
             if (q < a.S && lane < a.P && src < a.tok_stride) {
                 spv[j] = pos[src];
@@ -525,7 +536,7 @@ __global__ __launch_bounds__(kFinishThreads) void draft_finish_part_kernel(Draft
         if (spec && most <= kWave) {     // block-uniform: the read-ahead holds the list
 #pragma unroll
             for (int j = 0; j < kSpecPer; ++j) {
-                const int q = w + j * (kFinishThreads / kWave);
+                const int q = last ? a.S : w + j * kSpecWaves;
                 if (q < a.S && lane < s_off[q + 1] - s_off[q]) {
                     pos[s_off[q] + lane] = spv[j];
                     if (sc) sc[s_off[q] + lane] = ssv[j];
@@ -678,8 +689,14 @@ static void launch_draft(const DraftArgs &a, hipStream_t s) {
     }
     if (a.nmin < a.nmax)
         hipLaunchKernelGGL(draft_count_kernel, dim3(a.S, a.B), dim3(kPartWaves * kWave), 0, s, a);
-    hipLaunchKernelGGL(draft_part_kernel<kHidden>, dim3(a.S, a.B), dim3(kPartWaves * kWave),
-                       part_tok_bytes(a.P) + lds, s, a);
+    // blocks of 8 waves when the grid is small (more rows in flight per block),
+    // of 4 otherwise (more blocks resident per CU); the results are the same
+    if ((int64_t)a.B * a.S <= kFewBlocks)
+        hipLaunchKernelGGL((draft_part_kernel<kHidden, kPartWavesFew>), dim3(a.S, a.B),
+                           dim3(kPartWavesFew * kWave), part_tok_bytes(a.P) + lds, s, a);
+    else
+        hipLaunchKernelGGL((draft_part_kernel<kHidden, kPartWaves>), dim3(a.S, a.B),
+                           dim3(kPartWaves * kWave), part_tok_bytes(a.P) + lds, s, a);
     hipLaunchKernelGGL(draft_finish_part_kernel, dim3(a.B), dim3(kFinishThreads), 0, s, a);
 }
 

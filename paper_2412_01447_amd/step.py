@@ -164,16 +164,58 @@ class DraftStep:
     def tune_split(self, cand_count, hidden=True):
         """Blocks per sequence for the one-call drafting from observed candidate
         counts (e.g. the previous step's).  Short contexts with short lists keep
-        one block per sequence (one launch); otherwise the positions are split so
-        that a block holds about 16 hidden-state rows or 32 attention gathers."""
+        one block per sequence (one launch).  Otherwise, for hidden-state ranking,
+        about 32 rows per block of the longest list and at least 512 blocks in
+        all (the library gives grids of up to 512 blocks 8 waves each, two per
+        CU); for attention ranking, about 32 gathers per block."""
         import math
         mx = int(max(int(c) for c in cand_count)) if len(cand_count) else 0
         small = 64 if hidden else 256
         if self.tok_stride <= DRAFT_MAX_TOK_STRIDE and mx <= small:
             return self.set_split(1)
-        per = 16 if hidden else 32
-        S = max(2, self.min_split(), math.ceil(mx / per))
+        if hidden:
+            S = max(math.ceil(mx / 32), 512 // self.B)
+        else:
+            S = math.ceil(mx / 32)
+        S = max(2, self.min_split(), S)
         return self.set_split(min(PLD_MAX_DRAFT_SPLIT, S))
+
+    def autotune_split(self, call, cand_count, hidden=True, factors=(0.5, 1.0, 2.0), reps=16,
+                       trials=2):
+        """Blocks per sequence for the one-call drafting, measured.  The candidates
+        are tune_split's choice for these counts (its split form when that is one
+        block) scaled by `factors`, plus one block per sequence where the stride
+        allows it.  `call(i)` issues the i-th call to time -- the drafting call, or
+        a whole step around it (a caller can rotate inputs through i); each
+        candidate gets one warm-up call and `trials` runs of `reps` calls between
+        two events, and the one with the lowest mean of its best run stays set.
+        The outputs of the drafting do not depend on the choice, only its time."""
+        import math
+        mx = int(max(int(c) for c in cand_count)) if len(cand_count) else 0
+        base = self.tune_split(cand_count, hidden)
+        if base == 1:
+            base = max(2, math.ceil(mx / 32))
+        cands = {min(PLD_MAX_DRAFT_SPLIT, max(2, self.min_split(), round(base * f)))
+                 for f in factors}
+        if self.min_split() == 1:
+            cands.add(1)
+        best = None
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        for S in sorted(cands):
+            self.set_split(S)
+            call(0)
+            t = float("inf")
+            for _ in range(trials):
+                e0.record()
+                for i in range(reps):
+                    call(i)
+                e1.record()
+                e1.synchronize()
+                t = min(t, e0.elapsed_time(e1) / reps)
+            if best is None or t < best[0]:
+                best = (t, S)
+        return self.set_split(best[1])
 
     def draft_fused(self, tokens, lens, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
                     threshold=float("-inf"), stream=None):

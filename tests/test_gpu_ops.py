@@ -485,13 +485,60 @@ def test_draft_fused_parity(case, split):
         assert np.array_equal(g["draft"], rd) and np.array_equal(g["draft_len"], rl)
 
 
-@pytest.mark.parametrize("split", [64, 57, 1000])
+@pytest.mark.parametrize("split", [64, 57, 240, 241, 1000])
 def test_draft_finish_read_ahead_limits(split):
     """All-equal tokens make every position an occurrence.  4096 positions in
-    64 parts of 64 entries fill the finishing kernel's read-ahead exactly; 57
-    parts of 72 hold more than it reads per part, and 512 parts of 8 are more
-    parts than it covers: both take the windowed compaction."""
+    64 parts of 64 entries fill the finishing kernel's read-ahead exactly, as
+    do 240 parts (of 24; the most it covers); 57 parts of 72 hold more than it
+    reads per part, and 241 or 1000 parts are more than it covers: these take
+    the windowed compaction."""
     test_draft_fused_parity((2, 4096, 1, 1, 1, 64, 0, 6, 13), split)
+
+
+def test_autotune_split_keeps_the_results():
+    """DraftStep.autotune_split times a few blocks-per-sequence choices (8-wave
+    blocks for small grids, 4-wave blocks for large ones) and keeps one; the
+    drafting outputs are the same bits under every choice and equal the
+    oracle's."""
+    from paper_2412_01447_amd.step import DraftStep
+    say("autotune split")
+    B, stride, V, d, K = 3, 20000, 40, 64, 8
+    rng = np.random.default_rng(77)
+    toks = rng.integers(0, V, size=(B, stride)).astype(np.int32)
+    lens = np.array([stride, stride - 3, 777], np.int32)
+    bits = synth.f32_to_bf16_bits(rng.standard_normal((B, stride, d)).astype(np.float32))
+    td, ld, hd = d_i32(toks), d_i32(lens), d_bf16(bits)
+    step = DraftStep(B, stride, K, device="cuda", mode="fused")
+    step.set_split(step.min_split())
+    outs = []
+    for S in (step.min_split(), 64, 200, 1000):   # 4-wave blocks where B*S > 512
+        step.set_split(S)
+        step.draft_fused(td, ld, hidden=hd)
+        torch.cuda.synchronize()
+        outs.append([t.clone() for t in (step.cand_pos, step.cand_count, step.best_pos,
+                                         step.best_score, step.draft, step.draft_len)])
+    chosen = step.autotune_split(lambda i: step.draft_fused(td, ld, hidden=hd),
+                                 step.cand_count.cpu().numpy(), hidden=True, reps=2, trials=1)
+    assert step.min_split() <= chosen <= pld.PLD_MAX_DRAFT_SPLIT and step.draft_split == chosen
+    step.draft_fused(td, ld, hidden=hd)
+    torch.cuda.synchronize()
+    outs.append([t.clone() for t in (step.cand_pos, step.cand_count, step.best_pos,
+                                     step.best_score, step.draft, step.draft_len)])
+    cc = outs[0][1].cpu().numpy()
+    for o in outs[1:]:
+        assert np.array_equal(o[1].cpu().numpy(), cc)
+        for b in range(B):
+            assert torch.equal(o[0][b, :cc[b]], outs[0][0][b, :cc[b]])
+        for x, y in zip(o[2:], outs[0][2:]):
+            assert torch.equal(x, y)
+    cp, rc, _ = oracle.find(toks, lens, 1, 1)
+    assert np.array_equal(cc, rc)
+    rsc, rbp, rbs = oracle.rank_hidden(bits, lens, cp, rc)
+    flips = check_best(outs[0][2].cpu().numpy(), outs[0][3].cpu().numpy(), rsc, rbp, rbs, cp, rc,
+                       "autotune")
+    rd, rl = oracle.emit(toks, lens, outs[0][2].cpu().numpy() if flips else rbp, K)
+    assert np.array_equal(outs[0][4].cpu().numpy(), rd)
+    assert np.array_equal(outs[0][5].cpu().numpy(), rl)
 
 
 # ------------------------------------------------ halves and graph replays
