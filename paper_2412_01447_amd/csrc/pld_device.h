@@ -225,14 +225,14 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 }
 
 // Loads of data read exactly once per call (logits rows, candidate hidden
-// rows, gathered attention weights): the nontemporal hint streams them past
-// the caches, which measurably raises the HBM read rate on gfx950.
+// rows): the nontemporal hint streams them past the caches, which measurably
+// raises the HBM read rate on gfx950.  (The attention gathers are not in this
+// class: nearby candidates share 128-byte lines of weights.)
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 ld_stream(const uint4 *p) {
     const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
     return make_uint4(v.x, v.y, v.z, v.w);
 }
-__device__ __forceinline__ float ld_stream(const float *p) { return __builtin_nontemporal_load(p); }
 
 // Copies n 16-byte chunks from global memory straight into LDS (block-wide)
 // with global_load_lds_dwordx4: no registers are held, the copy runs while the
@@ -348,8 +348,10 @@ __device__ __forceinline__ void rows_dot(const uint4 *const (&rows)[G], const ui
 // fp32 (or takes their maximum); the group's eight partials are then combined
 // by DPP moves inside the group (lane xor 1, xor 2, then the half-row mirror),
 // which leaves the same bits in every lane of the group.  A candidate's R loads
-// are thus one trip to memory for R <= 64.  Call with the whole wave
-// converged; `active` masks the loads of lanes without a candidate.
+// are thus one trip to memory for R <= 64.  Plain (cached) loads: candidates
+// a few positions apart read the same 128-byte lines, and a line kept in L2
+// serves the second one.  Call with the whole wave converged; `active` masks
+// the loads of lanes without a candidate.
 constexpr int kGatherLanes = 8;
 __device__ __forceinline__ float attn_gather_group(const float *col, int64_t ar, int R, bool sum,
                                                    bool active) {
@@ -361,7 +363,7 @@ __device__ __forceinline__ float attn_gather_group(const float *col, int64_t ar,
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
             const int r = r0 + u * kGatherLanes + t;
-            v[u] = (active && r < R) ? ld_stream(col + (int64_t)r * ar) : none;
+            v[u] = (active && r < R) ? col[(int64_t)r * ar] : none;
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u) acc = sum ? acc + v[u] : fmaxf(acc, v[u]);

@@ -114,11 +114,28 @@ __device__ void candidate_prefix(const RankCommon &c, uint32_t *pre, int32_t *s_
 }
 
 // Block k's share [lo, hi) of n items split evenly over the grid (32-bit).
-__device__ __forceinline__ void block_share(uint32_t n, uint32_t &lo, uint32_t &hi) {
-    const uint32_t g = gridDim.x, k = blockIdx.x;
+__device__ __forceinline__ void block_share(uint32_t n, uint32_t k, uint32_t &lo, uint32_t &hi) {
+    const uint32_t g = gridDim.x;
     const uint32_t q = n / g, r = n % g;
     lo = k * q + min(k, r);
     hi = lo + q + (k < r ? 1u : 0u);
+}
+
+// Consecutive blocks go to the eight XCDs in turn, and each XCD has its own
+// L2.  For the attention gathers, whose neighbouring shares read some of the
+// same 128-byte lines, block k takes share index
+//   (i / m) * 8m + x * m + i % m,   x = k % 8, i = k / 8, m = kXcdRun,
+// so that each XCD works through runs of m consecutive shares (most shared
+// lines stay in one L2) while the runs of all XCDs interleave along the list
+// (every XCD sees the same mix of cheap and costly candidates; one contiguous
+// eighth per XCD was measured slower).  Blocks past the last whole group of
+// 8m keep their own index.  A permutation: the results do not depend on it.
+constexpr uint32_t kXcds = 8, kXcdRun = 16;
+__device__ __forceinline__ uint32_t xcd_run_index(uint32_t k) {
+    const uint32_t group = kXcds * kXcdRun;
+    if (k >= gridDim.x / group * group) return k;
+    const uint32_t x = k % kXcds, i = k / kXcds;
+    return (i / kXcdRun) * group + x * kXcdRun + i % kXcdRun;
 }
 
 // Largest b with pre[b] <= i (i < pre[B]); lands on a non-empty sequence.
@@ -218,7 +235,7 @@ __global__ __launch_bounds__(kRankThreads) void rank_hidden_kernel(RankHiddenArg
     int32_t *lens = reinterpret_cast<int32_t *>(pre + c.B + 1); // B
     candidate_prefix(c, pre, lens);
     uint32_t lo0, hi;
-    block_share(pre[c.B], lo0, hi);
+    block_share(pre[c.B], blockIdx.x, lo0, hi);
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     if (lo0 >= hi) return;   // block-uniform: nothing to score
@@ -267,7 +284,7 @@ __global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a)
     const RankCommon &c = a.c;
     candidate_prefix(c, pre);
     uint32_t lo, hi;
-    block_share(pre[c.B], lo, hi);
+    block_share(pre[c.B], xcd_run_index(blockIdx.x), lo, hi);
     // a group of kGatherLanes lanes per candidate
     constexpr uint32_t kPerPass = kRankThreads / kGatherLanes;
     for (uint32_t base = lo; base < hi; base += kPerPass) {
