@@ -167,7 +167,8 @@ class DraftStep:
         one block per sequence (one launch).  Otherwise, for hidden-state ranking,
         about 32 rows per block of the longest list and at least 512 blocks in
         all (the library gives grids of up to 512 blocks 8 waves each, two per
-        CU); for attention ranking, about 32 gathers per block."""
+        CU); for attention ranking, about 32 gathers per block; and at least 64
+        positions per block."""
         import math
         mx = int(max(int(c) for c in cand_count)) if len(cand_count) else 0
         small = 64 if hidden else 256
@@ -177,6 +178,7 @@ class DraftStep:
             S = max(math.ceil(mx / 32), 512 // self.B)
         else:
             S = math.ceil(mx / 32)
+        S = min(S, math.ceil(self.tok_stride / 64))
         S = max(2, self.min_split(), S)
         return self.set_split(min(PLD_MAX_DRAFT_SPLIT, S))
 
