@@ -68,10 +68,16 @@ def _pins_pass():
         sc, bp, bs = oracle.rank_attn(A, lens, cp, cc, oracle.AGG_SUM)
         if bp[0] != ex["attn_sum_best_pos"]:
             return False
+        # the token row padded with a sentinel past T, so that a slip that reads
+        # beyond the sequence sees a defined value; the length is compared too
+        padded = np.full((toks.shape[0], toks.shape[1] + 16), 424242, np.int32)
+        padded[:, :toks.shape[1]] = toks
         for K in (3, 12):
-            dr, dl = oracle.emit(toks, lens, np.array([10], np.int32), K)
-            if list(dr[0]) != ex[f"draft_K{K}"]:
-                return False
+            for tk in (toks, padded):
+                dr, dl = oracle.emit(tk, lens, np.array([10], np.int32), K)
+                want = ex[f"draft_K{K}"]
+                if list(dr[0]) != want or dl[0] != sum(1 for t in want if t != -1):
+                    return False
         for vc in fx["verify_cases"]:
             Z, dr, dl = golden_cases.verify_case(vc)
             acc, out, cnt, ra = oracle.verify(Z, dr, dl)
