@@ -346,6 +346,25 @@ int pld_commit(int32_t *tokens, int64_t tok_stride, int32_t *lens, const int32_t
                int64_t *stats, void *stream);
 
 /*
+ * pld_accept_commit -- pld_verify_accept followed by pld_commit in one launch,
+ * for the generation loop after pld_verify_argmax (Sec. 3, Sec. 4.4): the
+ * accepted length and emitted tokens from the row maxima in the workspace
+ * (which is returned to zero), then those tokens appended to the sequence,
+ * the length advanced and the counters added to.  Every output (accept_len,
+ * out_tokens, out_count, tokens, lens, stats) is the same as the two calls
+ * give; one dependent launch fewer per step.
+ *
+ *   draft ... workspace   as pld_verify_accept
+ *   tokens ... stats      as pld_commit (K is the same)
+ * Device-side rules: those of the two calls.
+ * Errors: the union of the two calls' errors.
+ */
+int pld_accept_commit(const int32_t *draft, const int32_t *draft_len, int B, int K,
+                      int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
+                      int32_t *tokens, int64_t tok_stride, int32_t *lens, const int32_t *limit,
+                      int64_t *stats, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * pld_draft_hidden / pld_draft_attn -- the drafting half of a step in one
  * call: pld_find_candidates, then pld_rank_hidden (or pld_rank_attn), then
  * pld_emit_draft, with the same definitions, outputs and device-side rules

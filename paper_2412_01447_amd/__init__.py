@@ -22,7 +22,7 @@ __all__ = [
     "DRAFT_MAX_PART", "pld_score_hidden",
     "pld_score_attn", "pld_select_best", "pld_verify_argmax", "pld_verify_accept",
     "pld_verify_sample", "pld_verify_sample_workspace_bytes", "pld_verify_sample_stats",
-    "pld_verify_sample_finish", "PLD_MAX_SAMPLE_ROWS", "pld_select_prefix", "pld_commit",
+    "pld_verify_sample_finish", "PLD_MAX_SAMPLE_ROWS", "pld_select_prefix", "pld_commit", "pld_accept_commit",
     "PLD_MAX_MATCH",
 ]
 
@@ -74,6 +74,8 @@ _SIGNATURES = {
                                  _int),
     "pld_select_prefix": ([_vp, _i64, _vp, _vp, _i64, _vp, _int, _int, _vp, _vp, _vp, _vp], _int),
     "pld_commit": ([_vp, _i64, _vp, _vp, _vp, _vp, _int, _int, _vp, _vp], _int),
+    "pld_accept_commit": ([_vp, _vp, _int, _int, _vp, _vp, _vp, _vp, _i64, _vp, _vp, _vp, _vp,
+                           _sz, _vp], _int),
     "pld_draft_hidden": ([_vp, _i64, _vp, _int, _int, _int, _vp, _i64, _i64, _i64, _int, _f32, _int,
                           _vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _int, _vp, _sz, _vp],
                          _int),
@@ -289,6 +291,25 @@ def pld_commit(tokens, lens, out_tokens, out_count, limit=None, stats=None, stre
         raise TypeError("stats must be a contiguous int64 [B][2] tensor")
     return _run("pld_commit", (_ptr(tokens), tokens.stride(0), _ptr(lens), _ptr(limit),
           _ptr(out_tokens), _ptr(out_count), B, K1 - 1, _ptr(stats), _stream(stream),), prepare)
+
+
+def pld_accept_commit(draft, draft_len, accept_len, out_tokens, out_count, tokens, lens, workspace,
+                      limit=None, stats=None, stream=None, prepare=False):
+    """pld_verify_accept then pld_commit in one launch: the accepted length and emitted
+    tokens from the row maxima in the workspace, appended to tokens[b] (up to limit[b]),
+    lens advanced, (emitted, steps) added to stats [B][2] int64 when given."""
+    import torch
+    _need(tokens, torch.int32, "tokens", 2)
+    B, K = draft.shape
+    if draft.stride(0) != K or out_tokens.shape != (B, K + 1) or out_tokens.stride(0) != K + 1:
+        raise TypeError("draft [B][K] and out_tokens [B][K+1] must be contiguous")
+    if stats is not None and (stats.dtype != torch.int64 or tuple(stats.shape) != (B, 2)
+                              or not stats.is_contiguous()):
+        raise TypeError("stats must be a contiguous int64 [B][2] tensor")
+    return _run("pld_accept_commit", (
+        _ptr(draft), _ptr(draft_len), B, K, _ptr(accept_len), _ptr(out_tokens), _ptr(out_count),
+        _ptr(tokens), tokens.stride(0), _ptr(lens), _ptr(limit), _ptr(stats), _ptr(workspace),
+        _nbytes(workspace), _stream(stream),), prepare)
 
 
 def pld_draft_hidden(tokens, lens, ngram_min, ngram_max, hidden, K, cand_pos, cand_count,

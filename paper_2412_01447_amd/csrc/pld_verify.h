@@ -96,15 +96,22 @@ __device__ __forceinline__ RowView<T, P> row_view(const void *logits, int64_t ls
     return r;
 }
 
+// The accepted length a (-1 for an invalid draft length) and the model's
+// token y_a, the same in every lane of the wave.
+struct Accepted {
+    int acc;
+    int32_t y;
+};
+
 // Acceptance of one sequence by one wave, one lane per row: the first
 // mismatch by a ballot, then the emitted tokens (Sec. 4.4).  `row_token(r)`
 // gives y_r for r <= K (its value past L is not used); it is called for every
 // r <= K of a round before the draft entries are compared.  `draft_token(r)`
 // gives draft[r] for r < K and -1 for r = K; lane l asks for r = l, l+64, ...
 template <class RowToken, class DraftToken>
-__device__ __forceinline__ void accept_wave(int K, int L, RowToken row_token,
-                                            DraftToken draft_token, int32_t *out,
-                                            int32_t *accept_len, int32_t *out_count) {
+__device__ __forceinline__ Accepted accept_wave(int K, int L, RowToken row_token,
+                                                DraftToken draft_token, int32_t *out,
+                                                int32_t *accept_len, int32_t *out_count) {
     const int lane = lane_id();
     const bool ok = (L >= 0 && L <= K);   // wave-uniform
     int acc = ok ? L : -1;  // accepted length: first mismatch, else L
@@ -130,6 +137,7 @@ __device__ __forceinline__ void accept_wave(int K, int L, RowToken row_token,
         *accept_len = acc;
         *out_count = ok ? acc + 1 : 0;
     }
+    return Accepted{acc, y_acc};
 }
 
 // The ranking and verification calls share the leading, zero-invariant part

@@ -123,12 +123,11 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArg
     }
 }
 
-// One wave per sequence: y_i from the row keys, which are returned to zero.
-// Every slot exists whatever the length, and the argmax never writes a slot
-// past the draft, so those are zero already and zeroing all K+1 is the same.
-__global__ __launch_bounds__(256) void verify_accept_kernel(VerifyArgs a) {
-    const int b = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave);
-    if (b >= a.B) return;   // wave-uniform
+// The acceptance of sequence b by one wave: y_i from the row keys, which are
+// returned to zero.  Every slot exists whatever the length, and the argmax
+// never writes a slot past the draft, so those are zero already and zeroing
+// all K+1 is the same.
+__device__ __forceinline__ Accepted accept_from_keys(const VerifyArgs &a, int b) {
     const int K = a.K;
     uint64_t *slot = a.keys + (int64_t)b * (K + 1);
     const int L = a.draft_len[b];
@@ -139,8 +138,15 @@ __global__ __launch_bounds__(256) void verify_accept_kernel(VerifyArgs a) {
     };
     const int32_t *dr = a.draft + (int64_t)b * K;
     auto draft_token = [&](int r) { return r < K ? dr[r] : -1; };
-    accept_wave(K, L, key_token, draft_token, a.out_tokens + (int64_t)b * (K + 1), a.accept_len + b,
-                a.out_count + b);
+    return accept_wave(K, L, key_token, draft_token, a.out_tokens + (int64_t)b * (K + 1),
+                       a.accept_len + b, a.out_count + b);
+}
+
+// One wave per sequence: the acceptance after the argmax launch.
+__global__ __launch_bounds__(256) void verify_accept_kernel(VerifyArgs a) {
+    const int b = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave);
+    if (b >= a.B) return;   // wave-uniform
+    accept_from_keys(a, b);
 }
 
 // ------------------------------------------------------------------ emit
@@ -185,6 +191,41 @@ __global__ __launch_bounds__(256) void commit_kernel(int32_t *tokens, int64_t to
         if (stats) {
             stats[2 * b] += m;
             stats[2 * b + 1] += m > 0 ? 1 : 0;
+        }
+    }
+}
+
+struct CommitArgs {
+    int32_t *tokens;
+    int64_t tok_stride;
+    int32_t *lens;
+    const int32_t *limit;
+    int64_t *stats;
+};
+
+// The acceptance and then the commit of sequence b by the same wave
+// (pld_accept_commit): the outputs of verify_accept_kernel followed by
+// commit_kernel, with the committed tokens taken from the draft and y_a
+// directly instead of being read back from out_tokens.
+__global__ __launch_bounds__(256) void accept_commit_kernel(VerifyArgs a, CommitArgs c) {
+    const int b = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave);
+    const int lane = lane_id();
+    if (b >= a.B) return;   // wave-uniform
+    const Accepted r = accept_from_keys(a, b);
+    int64_t cap = c.tok_stride;
+    if (c.limit && c.limit[b] < cap) cap = c.limit[b];
+    const int64_t T = c.lens[b];
+    const int64_t n = r.acc >= 0 ? r.acc + 1 : 0;   // out_count
+    if (T < 0 || T > cap) return;
+    const int64_t m = min(n, cap - T);
+    const int32_t *dr = a.draft + (int64_t)b * a.K;
+    for (int64_t i = lane; i < m; i += kWave)
+        c.tokens[(int64_t)b * c.tok_stride + T + i] = i < r.acc ? dr[i] : r.y;
+    if (lane == 0) {
+        c.lens[b] = (int32_t)(T + m);
+        if (c.stats) {
+            c.stats[2 * b] += m;
+            c.stats[2 * b + 1] += m > 0 ? 1 : 0;
         }
     }
 }
@@ -296,6 +337,31 @@ extern "C" int pld_emit_draft(const int32_t *tokens, int64_t tok_stride, const i
     if (blocks > 0x7fffffff) return PLD_ERR_INVALID;
     hipLaunchKernelGGL(emit_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream,
                        tokens, tok_stride, lens, best_pos, B, K, draft, draft_len);
+    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+}
+
+extern "C" int pld_accept_commit(const int32_t *draft, const int32_t *draft_len, int B, int K,
+                                 int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
+                                 int32_t *tokens, int64_t tok_stride, int32_t *lens,
+                                 const int32_t *limit, int64_t *stats, void *workspace,
+                                 size_t workspace_bytes, void *stream) {
+    if (!draft || !draft_len || !accept_len || !out_tokens || !out_count || !tokens || !lens)
+        return PLD_ERR_INVALID;
+    if (B < 1 || K < 1 || B > 65535 || K + 1 > 65535) return PLD_ERR_INVALID;
+    if (tok_stride < 1 || tok_stride > kMaxTokStride) return PLD_ERR_INVALID;
+    if (!workspace || workspace_bytes < verify_ws_bytes(B, K)) return PLD_ERR_WORKSPACE;
+    VerifyArgs a{};
+    a.K = K;
+    a.B = B;
+    a.draft = draft;
+    a.draft_len = draft_len;
+    a.accept_len = accept_len;
+    a.out_tokens = out_tokens;
+    a.out_count = out_count;
+    a.keys = (uint64_t *)workspace;
+    const CommitArgs c{tokens, tok_stride, lens, limit, stats};
+    hipLaunchKernelGGL(accept_commit_kernel, dim3((unsigned)((B + 3) / 4)), dim3(256), 0,
+                       (hipStream_t)stream, a, c);
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }
 

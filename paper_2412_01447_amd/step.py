@@ -9,7 +9,7 @@ verification at a temperature once set_sampling() is called).
 import torch
 
 from . import (DRAFT_MAX_PART, DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, PLD_BF16, PLD_F32,
-               PLD_MAX_DRAFT_SPLIT, pld_commit, pld_draft_attn, pld_draft_hidden,
+               PLD_MAX_DRAFT_SPLIT, pld_accept_commit, pld_commit, pld_draft_attn, pld_draft_hidden,
                pld_draft_workspace_bytes, pld_emit_draft, pld_find_candidates,
                pld_find_scratch_bytes, pld_rank_attn, pld_rank_hidden, pld_score_attn,
                pld_score_hidden, pld_select_best, pld_select_prefix, pld_verify_accept,
@@ -269,7 +269,8 @@ class DraftStep:
         """The step as an ordered list of (name, prepared call), one kernel per entry
         except "find" on long contexts (two): the same work as run(), with every
         argument marshalled once so that issuing a step costs only the launches.
-        commit=(limit, stats) appends the commit of the generation loop."""
+        commit=(limit, stats) adds the commit of the generation loop (with greedy
+        verification, fused into the acceptance's launch: pld_accept_commit)."""
         P = dict(stream=stream, prepare=True)
         if prefix_match is not None:
             ops = [("find", pld_find_candidates(tokens, lens, ngram[0], ngram[1], self.cand_pos,
@@ -334,8 +335,13 @@ class DraftStep:
                                                            self.out_count, self.workspace, **P)))
         if commit is not None:
             limit, stats = commit
-            ops.append(("commit", pld_commit(tokens, lens, self.out_tokens, self.out_count,
-                                             limit=limit, stats=stats, **P)))
+            if ops[-1][0] == "verify_accept":   # the acceptance and the commit in one launch
+                ops[-1] = ("verify_accept_commit", pld_accept_commit(
+                    self.draft, self.draft_len, self.accept_len, self.out_tokens, self.out_count,
+                    tokens, lens, self.workspace, limit=limit, stats=stats, **P))
+            else:
+                ops.append(("commit", pld_commit(tokens, lens, self.out_tokens, self.out_count,
+                                                 limit=limit, stats=stats, **P)))
         return ops
 
     def host(self):

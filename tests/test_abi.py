@@ -226,6 +226,19 @@ def test_prefix_and_commit_host_validation():
     assert cm(F, 100, F, NULL, F, F, 0, 4, NULL, NULL) == E_INV
     assert cm(F, 100, F, NULL, F, F, 2, 0, NULL, NULL) == E_INV
     assert cm(F, 0, F, NULL, F, F, 2, 4, NULL, NULL) == E_INV
+    # the acceptance with the commit: the union of the two calls' checks
+    ac = lib.pld_accept_commit
+    ws_n = pld.pld_workspace_bytes(2, 4)
+    ok = (F, F, 2, 4, F, F, F, F, 100, F, NULL, NULL, F, ws_n, NULL)
+    for k in (0, 1, 4, 5, 6, 7, 9):      # required pointers
+        args = list(ok)
+        args[k] = NULL
+        assert ac(*args) == E_INV, k
+    assert ac(*(ok[:2] + (0,) + ok[3:])) == E_INV                  # B
+    assert ac(*(ok[:3] + (0,) + ok[4:])) == E_INV                  # K
+    assert ac(*(ok[:8] + (0,) + ok[9:])) == E_INV                  # tok_stride
+    assert ac(*(ok[:12] + (NULL,) + ok[13:])) == pld.PLD_ERR_WORKSPACE
+    assert ac(*(ok[:13] + (ws_n - 1,) + ok[14:])) == pld.PLD_ERR_WORKSPACE
 
 
 def test_split_rule():

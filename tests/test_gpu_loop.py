@@ -17,7 +17,7 @@ import golden_cases
 import oracle
 import paper_2412_01447_amd as pld
 import synth
-from gpu_helpers import RTOL, d_i32, dev, say
+from gpu_helpers import RTOL, d_f32, d_i32, dev, say
 from paper_2412_01447_amd.step import DraftStep, decode_loop
 
 pytestmark = pytest.mark.gpu
@@ -118,6 +118,54 @@ def test_commit_parity():
     t2, l2, _ = oracle.commit(toks, lens, out, cnt)
     torch.cuda.synchronize()
     assert np.array_equal(td.cpu().numpy(), t2) and np.array_equal(ld.cpu().numpy(), l2)
+
+
+def test_accept_commit_parity():
+    """pld_accept_commit equals pld_verify_accept followed by pld_commit, and the
+    oracle's verification and commit: accepted lengths, emitted tokens, rows,
+    lengths and counters, over two steps, with invalid draft lengths, limits that
+    cut the append and invalid sequence lengths; the workspace ends at zero."""
+    say("accept + commit")
+    rng = np.random.default_rng(11)
+    B, K, V, stride = 9, 6, 50, 40
+    Z = rng.standard_normal((B, K + 1, V)).astype(np.float32)
+    draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+    agree = np.array([6, 0, 2, 6, 3, 6, 1, 6, 4])
+    for b in range(B):
+        draft[b, :agree[b]] = Z[b, :agree[b]].argmax(axis=1)
+    dlen = np.array([6, 0, 3, 6, -1, 7, 6, 2, 6], np.int32)
+    toks = rng.integers(0, 100, size=(B, stride)).astype(np.int32)
+    lens = np.array([10, 38, 40, 0, 5, 12, -1, 39, 20], np.int32)
+    limit = np.array([40, 40, 40, 3, 40, 40, 40, 40, 25], np.int32)
+    stats0 = rng.integers(0, 9, size=(B, 2)).astype(np.int64)
+    zd, dr, dl, lim = d_f32(Z), d_i32(draft), d_i32(dlen), d_i32(limit)
+    i32 = dict(dtype=torch.int32, device=dev())
+    runs = {}
+    for fused in (False, True):
+        ws = torch.zeros(pld.pld_workspace_bytes(B, K), dtype=torch.uint8, device=dev())
+        td, ld = d_i32(toks), d_i32(lens)
+        sd = torch.from_numpy(stats0.copy()).to(dev())
+        acc, out, cnt = (torch.full((B,), -7, **i32), torch.full((B, K + 1), -7, **i32),
+                         torch.full((B,), -7, **i32))
+        for _ in range(2):
+            pld.pld_verify_argmax(zd, dl, ws)
+            if fused:
+                pld.pld_accept_commit(dr, dl, acc, out, cnt, td, ld, ws, limit=lim, stats=sd)
+            else:
+                pld.pld_verify_accept(dr, dl, acc, out, cnt, ws)
+                pld.pld_commit(td, ld, out, cnt, limit=lim, stats=sd)
+            torch.cuda.synchronize()
+            assert int(torch.count_nonzero(ws).item()) == 0
+        runs[fused] = [t.cpu().numpy() for t in (acc, out, cnt, td, ld, sd)]
+    for x, y in zip(runs[False], runs[True]):
+        assert np.array_equal(x, y)
+    ra, ro, rc, _ = oracle.verify(Z, draft, dlen)
+    wt, wl, ws_ = toks, lens, stats0
+    for _ in range(2):
+        wt, wl, ws_ = oracle.commit(wt, wl, ro, rc, limit=limit, stats=ws_)
+    acc, out, cnt, t, l, s_ = runs[True]
+    assert np.array_equal(acc, ra) and np.array_equal(out, ro) and np.array_equal(cnt, rc)
+    assert np.array_equal(t, wt) and np.array_equal(l, wl) and np.array_equal(s_, ws_)
 
 
 # ------------------------------------------------------------- the loop
