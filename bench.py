@@ -2,7 +2,10 @@
 """Benchmark of the PLD+ drafting step (find -> rank -> emit -> verify) on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--config C] [--verify greedy|sample]
-                    [--temperature T] [--no-cpu-baseline]
+                    [--temperature T] [--mode auto|fused|split] [--split S] [--warm]
+                    [--no-cpu-baseline] [--copy-probe]
+    python bench.py --loop TASK        # the generation loop, once per ranking
+    python bench.py --probe            # bandwidth ceilings of the access patterns
 
 A step is one pass of the whole hot path over one batch of synthetic input
 already resident in HBM.  The default workload is config 2 (batch 8, context
