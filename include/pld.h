@@ -81,7 +81,7 @@ size_t pld_workspace_bytes(int B, int K);
 
 /*
  * Bytes of scratch pld_find_candidates needs for batch B and token stride
- * tok_stride: 0 up to tok_stride = 8192 (one block per sequence), else the
+ * tok_stride: 0 up to tok_stride = 16384 (one block per sequence), else the
  * per-tile occurrence counts.  Returns 0 when an argument is out of range.
  */
 size_t pld_find_scratch_bytes(int B, int64_t tok_stride);

@@ -22,6 +22,7 @@ constexpr int kFindTile = 2048;          // positions per block, multi-block fin
 constexpr int kFindWavesTiled = 4;       // 256 threads, 512 positions per wave
 constexpr int kFindWavesFused = 16;      // 1024 threads, one block per sequence
 constexpr int kFindFusedMax = kFindWavesFused * 512;  // tok_stride <= 8192: fused path
+constexpr int kFindFusedPasses = 2;   // the one-block search takes tok_stride <= 16384
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -62,7 +63,7 @@ inline int resident_blocks(const void *kernel, int threads, size_t dyn_lds) {
 
 // Scratch of the multi-block find: per-tile occurrence counts of every n.
 inline size_t find_scratch_bytes(int B, int64_t tok_stride) {
-    if (tok_stride <= kFindFusedMax) return 0;
+    if (tok_stride <= kFindFusedPasses * kFindFusedMax) return 0;   // the one-block search
     const int64_t ntiles = (tok_stride + kFindTile - 1) / kFindTile;
     return align_up((size_t)B * (size_t)ntiles * 8 * sizeof(int32_t), 256);
 }

@@ -15,8 +15,8 @@
 // four aligned 16-byte LDS loads and builds, per n, an 8-bit hit mask from
 // register compares -- no branch per comparison, 512 positions per wave
 // pass.  Compaction is an exclusive wave scan of the lanes' hit counts plus
-// the per-wave and per-block counts.  Sequences up to kFindFusedMax tokens
-// take one 1024-thread block each (count, pick n, compact, in one kernel);
+// the per-wave and per-block counts.  Sequences up to 16384 tokens take one
+// 1024-thread block each (count, pick n, compact, in one kernel);
 // longer ones split into kFindTile-position blocks: a count kernel writes
 // per-tile counts to the scratch buffer, and the compaction kernel derives
 // its tile's output offset from the counts of the tiles before it.
@@ -41,13 +41,15 @@ struct FindArgs {
 };
 
 // ---------------------------------------------------------------- fused
-// One 1024-thread block per sequence, tok_stride <= kFindFusedMax: every lane
-// takes 8 positions, so one pass covers the sequence.
-static_assert(kFindFusedMax == kFindWavesFused * kWave * kLanePos, "one pass per block");
+// One 1024-thread block per sequence, tok_stride <= kPasses * kFindFusedMax:
+// every lane takes 8 positions per pass, a pass covers 8192 positions, and
+// all the tokens sit in LDS (64 KB for two passes).
+static_assert(kFindFusedMax == kFindWavesFused * kWave * kLanePos, "8192 positions per pass");
 
+template <int kPasses>
 __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(FindArgs a) {
-    __shared__ __align__(16) int32_t s_x[kFindFusedMax];
-    __shared__ int s_lvl[kFindWavesFused][kMaxNgram];
+    __shared__ __align__(16) int32_t s_x[kPasses * kFindFusedMax];
+    __shared__ int s_lvl[kPasses][kFindWavesFused][kMaxNgram];
     const int b = blockIdx.x;
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
@@ -63,35 +65,48 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
     stage_tokens(x, 0, T, s_x);
     __syncthreads();
     const Query q = load_query(s_x, T, a.nmax);
-    const int64_t base = (int64_t)threadIdx.x * kLanePos;
-    const uint64_t hits = lane_hits(s_x, 0, T, base, q, a.nmax);
-    int cnt[kMaxNgram];
+    uint64_t hits[kPasses];
 #pragma unroll
-    for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
-    count_levels(hits, a.nmax, cnt);
+    for (int t = 0; t < kPasses; ++t) {
+        const int64_t base = (int64_t)t * kFindFusedMax + (int64_t)threadIdx.x * kLanePos;
+        hits[t] = lane_hits(s_x, 0, T, base, q, a.nmax);
+        int cnt[kMaxNgram];
 #pragma unroll
-    for (int k = 0; k < kMaxNgram; ++k) {
-        if (k < a.nmax) {   // uniform
-            const int t = wave_sum_i32(cnt[k]);
-            if (lane == 0) s_lvl[w][k] = t;
+        for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
+        count_levels(hits[t], a.nmax, cnt);
+#pragma unroll
+        for (int k = 0; k < kMaxNgram; ++k) {
+            if (k < a.nmax) {   // uniform
+                const int c = wave_sum_i32(cnt[k]);
+                if (lane == 0) s_lvl[t][w][k] = c;
+            }
         }
     }
     __syncthreads();
     // the longest n with an occurrence (every thread, same answer)
     int n_used = 0, total = 0;
     for (int n = a.nmax; n >= a.nmin; --n) {
-        int t = 0;
-        for (int i = 0; i < kFindWavesFused; ++i) t += s_lvl[i][n - 1];
-        if (t > 0) {
+        int c = 0;
+        for (int t = 0; t < kPasses; ++t)
+            for (int i = 0; i < kFindWavesFused; ++i) c += s_lvl[t][i][n - 1];
+        if (c > 0) {
             n_used = n;
-            total = t;
+            total = c;
             break;
         }
     }
-    if (n_used > 0) {   // the per-wave counts at n give each wave's offset
+    if (n_used > 0) {   // ascending: pass, then wave, then lane
         int64_t run = 0;
-        for (int i = 0; i < w; ++i) run += s_lvl[i][n_used - 1];
-        emit_bits(level_bits(hits, n_used), base, a.cand_pos + (int64_t)b * a.cap, nullptr, run);
+#pragma unroll
+        for (int t = 0; t < kPasses; ++t) {
+            int64_t r = run;
+            for (int i = 0; i < kFindWavesFused; ++i) {
+                if (i < w) r += s_lvl[t][i][n_used - 1];
+                run += s_lvl[t][i][n_used - 1];
+            }
+            const int64_t base = (int64_t)t * kFindFusedMax + (int64_t)threadIdx.x * kLanePos;
+            emit_bits(level_bits(hits[t], n_used), base, a.cand_pos + (int64_t)b * a.cap, nullptr, r);
+        }
     }
     if (threadIdx.x == 0) {
         a.cand_count[b] = total;
@@ -255,7 +270,10 @@ extern "C" int pld_find_candidates(const int32_t *tokens, int64_t tok_stride, co
     a.ntiles = (int)((tok_stride + kFindTile - 1) / kFindTile);
     hipStream_t s = (hipStream_t)stream;
     if (tok_stride <= kFindFusedMax) {
-        hipLaunchKernelGGL(find_fused_kernel, dim3(B), dim3(kFindWavesFused * kWave), 0, s, a);
+        hipLaunchKernelGGL(find_fused_kernel<1>, dim3(B), dim3(kFindWavesFused * kWave), 0, s, a);
+    } else if (tok_stride <= kFindFusedPasses * kFindFusedMax) {
+        hipLaunchKernelGGL(find_fused_kernel<kFindFusedPasses>, dim3(B),
+                           dim3(kFindWavesFused * kWave), 0, s, a);
     } else {
         if (!scratch || scratch_bytes < find_scratch_bytes(B, tok_stride)) return PLD_ERR_WORKSPACE;
         a.tile_counts = (int32_t *)scratch;

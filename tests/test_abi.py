@@ -66,9 +66,10 @@ def test_workspace_and_scratch_bytes():
     assert pld.pld_workspace_bytes(64, 32) >= pld.pld_workspace_bytes(64, 16)
     assert pld.pld_workspace_bytes(64, 16) >= 64 * 17 * 8      # verify keys: B*(K+1) u64
     assert pld.pld_workspace_bytes(4096, 1) >= 4096 * 8        # ranking keys: B u64
-    # find: no scratch up to 8192 tokens, per-tile counts beyond
+    # find: no scratch up to 16384 tokens (one block per sequence), per-tile counts beyond
     assert pld.pld_find_scratch_bytes(8, 8192) == 0
-    assert pld.pld_find_scratch_bytes(8, 8193) >= 8 * 5 * 8 * 4
+    assert pld.pld_find_scratch_bytes(8, 16384) == 0
+    assert pld.pld_find_scratch_bytes(8, 16385) >= 8 * 9 * 8 * 4
     assert pld.pld_find_scratch_bytes(4, 131072) >= 4 * 64 * 8 * 4
     assert pld.pld_find_scratch_bytes(0, 9000) == 0
     # one-call drafting: none for one block per sequence; key slots, per-block

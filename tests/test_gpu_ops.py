@@ -73,7 +73,9 @@ FIND_CASES = [
     # (B, tok_stride, V, n_min, n_max, seed)
     (16, 1, 2, 1, 1, 0), (16, 5, 2, 1, 2, 1), (16, 64, 3, 1, 3, 2), (16, 700, 5, 1, 4, 3),
     (12, 4096, 50, 1, 3, 4), (8, 8192, 7, 2, 5, 5), (8, 8192, 1, 1, 8, 6),
-    (6, 8193, 4, 1, 1, 7), (5, 20000, 3, 1, 3, 8), (4, 70000, 1000, 1, 2, 9),
+    (6, 8193, 4, 1, 1, 7), (5, 12000, 30, 1, 3, 12), (6, 16384, 2, 1, 4, 13),
+    (4, 16384, 1, 1, 1, 14), (4, 16385, 3, 1, 2, 15),
+    (5, 20000, 3, 1, 3, 8), (4, 70000, 1000, 1, 2, 9),
     (3, 131072, 2, 8, 8, 10), (3, 50000, 1, 1, 1, 11),
 ]
 
@@ -98,7 +100,7 @@ def test_find_parity(case):
     check_find(gpu_find(toks, lens, nmin, nmax, cap=stride + 37), ref, str(case) + " cap")
 
 
-@pytest.mark.parametrize("stride", [8192, 20000])
+@pytest.mark.parametrize("stride", [8192, 16384, 20000])
 def test_find_lane31_hits(stride):
     """Sparse hits at positions 31 mod 64 (plus lane 63 once): a 64-position
     ballot with bit 31 set and the upper half otherwise empty must not widen
