@@ -543,6 +543,65 @@ def test_autotune_split_keeps_the_results():
     assert np.array_equal(outs[0][5].cpu().numpy(), rl)
 
 
+def test_draft_random_shapes():
+    """Seeded random shapes of the one-call drafting -- hidden (bf16, d up to 4096) and
+    attention (SUM or MAX over up to 69 rows), n-gram ranges, thresholds, every kind of
+    split (one block, few, the finishing kernel's read-ahead limits, more) -- against
+    the oracle's occurrence lists and draft and, bit for bit, the separate ranking
+    calls' scores and choices."""
+    rng = np.random.default_rng(2024)
+    i32 = dict(dtype=torch.int32, device="cuda")
+    for it in range(60):
+        B = int(rng.integers(1, 9))
+        stride = int(rng.choice([17, 300, 1024, 4096, 8192, 8200, 12000, 16384, 30000]))
+        V = int(rng.choice([1, 2, 5, 50, 1000]))
+        nmin = int(rng.integers(1, 4))
+        nmax = int(rng.integers(nmin, 6))
+        hidden = bool(rng.integers(0, 2))
+        d = int(rng.choice([8, 64, 520, 4096])) if hidden else 0
+        while hidden and B * stride * d > 4e7 and d > 8:
+            d = {4096: 520, 520: 64, 64: 8}[d]
+        R = 0 if hidden else int(rng.integers(1, 70))
+        K = int(rng.integers(1, 40))
+        th = float(rng.choice([-math.inf, 0.0, 0.3]))
+        lo = 1 if stride <= pld.DRAFT_MAX_TOK_STRIDE else -(-stride // pld.DRAFT_MAX_PART)
+        S = int(rng.choice([lo, max(2, lo), max(3, lo), 64, 240, 241, 600, 1024]))
+        toks = rng.integers(0, V, size=(B, stride)).astype(np.int32)
+        lens = rng.integers(1, stride + 1, size=B).astype(np.int32)
+        lens[0] = stride
+        what = f"case {it}: B{B} S{stride} V{V} n{nmin}-{nmax} d{d} R{R} K{K} th{th} split{S}"
+        say("draft random", what)
+        cp, cc, nu = oracle.find(toks, lens, nmin, nmax)
+        ws = draft_workspace(B, S)
+        o = [torch.full((B, stride), -1, **i32), torch.zeros(B, **i32), torch.zeros(B, **i32),
+             torch.zeros(B, **i32), torch.zeros(B, dtype=torch.float32, device="cuda"),
+             torch.zeros((B, K), **i32), torch.zeros(B, **i32)]
+        sc = torch.full((B, stride), 777.0, dtype=torch.float32, device="cuda")
+        if hidden:
+            bits = synth.f32_to_bf16_bits(rng.standard_normal((B, stride, d)).astype(np.float32))
+            hd = d_bf16(bits)
+            pld.pld_draft_hidden(d_i32(toks), d_i32(lens), nmin, nmax, hd, K, *o, threshold=th,
+                                 scores=sc, blocks_per_seq=S, workspace=ws)
+            ref = gpu_rank_hidden(hd, lens, cp, cc, threshold=th)
+        else:
+            A = synth.make_attn(B, R, stride, lens, seed=it)
+            agg = int(rng.integers(0, 2))
+            pld.pld_draft_attn(d_i32(toks), d_i32(lens), nmin, nmax, d_f32(A), K, *o, agg=agg,
+                               threshold=th, scores=sc, blocks_per_seq=S, workspace=ws)
+            ref = gpu_rank_attn(d_f32(A), lens, cp, cc, agg, threshold=th)
+        torch.cuda.synchronize()
+        g = [t.cpu().numpy() for t in o]
+        check_find((g[0], g[1], g[2]), (cp, cc, nu), what)
+        gs = sc.cpu().numpy()
+        for b in range(B):
+            assert np.array_equal(gs[b, :cc[b]], ref[0][b, :cc[b]], equal_nan=True), what
+        assert np.array_equal(g[3], ref[1]), what
+        rd, rl = oracle.emit(toks, lens, g[3], K)
+        assert np.array_equal(g[5], rd) and np.array_equal(g[6], rl), what
+        if ws is not None:
+            assert draft_keys_zero(ws, B), what
+
+
 # ------------------------------------------------ halves and graph replays
 def test_halves_equal_combined_calls():
     """score + select == rank, verify_argmax + verify_accept == verify_greedy, bit for bit."""
