@@ -351,6 +351,54 @@ def test_verify_parity(case):
     check_verify(gpu_verify(zd, draft, L), ref, str(case))
 
 
+def test_verify_random_shapes():
+    """Seeded random shapes of greedy verification -- f32 and bf16 logits, integer
+    rows with ties and signed zeros, draft lengths from -1 to K+1, planted accepted
+    prefixes -- the one-call greedy verification, its halves and the acceptance fused
+    with the commit, each against the oracle (accepted lengths and tokens bit for bit,
+    the rows, lengths and counters of the commit too)."""
+    rng = np.random.default_rng(77)
+    i32 = dict(dtype=torch.int32, device="cuda")
+    for it in range(40):
+        B = int(rng.integers(1, 17))
+        K = int(rng.integers(1, 41))
+        V = int(rng.choice([1, 3, 7, 1000, 32000, 50001]))
+        bf16 = bool(rng.integers(0, 2))
+        integer = bool(rng.integers(0, 2))
+        what = f"case {it}: B{B} K{K} V{V} {'bf16' if bf16 else 'f32'} {'int' if integer else 'normal'}"
+        say("verify random", what)
+        if integer:
+            Z = rng.integers(-2, 3, size=(B, K + 1, V)).astype(np.float32)
+            Z[rng.random(Z.shape) < 0.3] *= -1.0
+        else:
+            Z = rng.standard_normal((B, K + 1, V)).astype(np.float32)
+        L = rng.integers(-1, K + 2, size=B).astype(np.int32)
+        draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+        for b in range(B):
+            for i in range(int(rng.integers(0, K + 1))):
+                Z[b, i, draft[b, i]] = 10.0
+        zbits = synth.f32_to_bf16_bits(Z) if bf16 else Z
+        ref = oracle.verify(zbits, draft, L, bf16=bf16)
+        zd = d_bf16(zbits) if bf16 else d_f32(Z)
+        check_verify(gpu_verify(zd, draft, L), ref, what)
+        # the halves, then the acceptance fused with the commit
+        ws = workspace(B, K)
+        acc, out, cnt = (torch.full((B,), -7, **i32), torch.full((B, K + 1), -7, **i32),
+                         torch.full((B,), -7, **i32))
+        stride = int(rng.integers(1, 3 * (K + 1) + 2))
+        toks = rng.integers(0, 100, size=(B, stride)).astype(np.int32)
+        lens = rng.integers(-1, stride + 2, size=B).astype(np.int32)
+        limit = rng.integers(0, stride + 1, size=B).astype(np.int32)
+        td, ld = d_i32(toks), d_i32(lens)
+        pld.pld_verify_argmax(zd, d_i32(L), ws)
+        pld.pld_accept_commit(d_i32(draft), d_i32(L), acc, out, cnt, td, ld, ws, limit=d_i32(limit))
+        torch.cuda.synchronize()
+        assert int(torch.count_nonzero(ws).item()) == 0, what
+        check_verify((acc.cpu().numpy(), out.cpu().numpy(), cnt.cpu().numpy()), ref, what)
+        wt, wl, _ = oracle.commit(toks, lens, ref[1], ref[2], limit=limit)
+        assert np.array_equal(td.cpu().numpy(), wt) and np.array_equal(ld.cpu().numpy(), wl), what
+
+
 def test_verify_misaligned_row_views():
     """Rows that start off a 16-byte boundary (a view into a padded buffer)."""
     say("verify misaligned")
