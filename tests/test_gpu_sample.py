@@ -83,6 +83,34 @@ def test_verify_sample_parity(case):
         assert got[3][0, 0] == ref[3][0, 0]
 
 
+def test_verify_sample_random_shapes():
+    """Seeded random shapes of sampling verification -- f32 and bf16, batch up to 12,
+    K up to 40 (several rounds of the finishing kernel's waves), vocabularies from 1
+    to 140000, temperatures from 0.2 to 5, draft lengths from -1 to K+1, planted
+    accepted prefixes -- against the oracle, near-tie flips bounded and counted."""
+    rng = np.random.default_rng(99)
+    for it in range(24):
+        B = int(rng.integers(1, 13))
+        K = int(rng.integers(1, 41))
+        V = int(rng.choice([1, 5, 999, 32000, 140000]))
+        bf16 = bool(rng.integers(0, 2))
+        tau = float(rng.choice([0.2, 0.7, 1.0, 1.0, 5.0]))
+        what = f"case {it}: B{B} K{K} V{V} {'bf16' if bf16 else 'f32'} tau{tau}"
+        say("verify_sample random", what)
+        Z = (rng.standard_normal((B, K + 1, V)) * 2.0).astype(np.float32)
+        L = rng.integers(-1, K + 2, size=B).astype(np.int32)
+        draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+        for b in range(B):
+            for i in range(int(rng.integers(0, K + 1))):
+                Z[b, i, draft[b, i]] = 30.0          # all the mass on the draft token
+        U = rng.random((B, K + 1), dtype=np.float32)
+        zbits = synth.f32_to_bf16_bits(Z) if bf16 else Z
+        ref = oracle.verify_sample(zbits, draft, L, tau, U, bf16=bf16)
+        zd = d_bf16(zbits) if bf16 else d_f32(Z)
+        got = gpu_verify_sample(zd, draft, L, tau, U)
+        check_sample(_rows_fn(zbits, bf16), tau, U, draft, L, got, ref, what)
+
+
 def test_verify_sample_exact_rows():
     """Rows whose masses are exact in fp32: every token must equal the oracle's and
     the value the definition gives by hand."""
