@@ -28,6 +28,16 @@ def say(*a):
     sys.stdout.flush()
 
 
+def random_plan(seed, iters):
+    """Seed and case count of a seeded random-shape test: the defaults, unless
+    PLD_RANDOM_SEED_OFFSET (added to the seed) or PLD_RANDOM_ITERS_SCALE (a
+    factor on the count) ask for a wider sweep of new shapes."""
+    import os
+    off = int(os.environ.get("PLD_RANDOM_SEED_OFFSET", "0"))
+    scale = float(os.environ.get("PLD_RANDOM_ITERS_SCALE", "1"))
+    return np.random.default_rng(seed + off), max(1, int(round(iters * scale)))
+
+
 def dev():
     return torch.device("cuda:0")
 

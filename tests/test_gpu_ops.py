@@ -15,7 +15,7 @@ import oracle
 import paper_2412_01447_amd as pld
 import synth
 from gpu_helpers import (check_best, check_find, check_scores, check_verify, d_bf16, d_f32,
-                         draft_keys_zero, draft_workspace,
+                         draft_keys_zero, draft_workspace, random_plan,
                          d_i32, gpu_emit, gpu_find, gpu_rank_attn, gpu_rank_hidden, gpu_verify,
                          say, workspace)
 
@@ -357,9 +357,9 @@ def test_verify_random_shapes():
     prefixes -- the one-call greedy verification, its halves and the acceptance fused
     with the commit, each against the oracle (accepted lengths and tokens bit for bit,
     the rows, lengths and counters of the commit too)."""
-    rng = np.random.default_rng(77)
+    rng, n_cases = random_plan(77, 40)
     i32 = dict(dtype=torch.int32, device="cuda")
-    for it in range(40):
+    for it in range(n_cases):
         B = int(rng.integers(1, 17))
         K = int(rng.integers(1, 41))
         V = int(rng.choice([1, 3, 7, 1000, 32000, 50001]))
@@ -597,9 +597,9 @@ def test_draft_random_shapes():
     split (one block, few, the finishing kernel's read-ahead limits, more) -- against
     the oracle's occurrence lists and draft and, bit for bit, the separate ranking
     calls' scores and choices."""
-    rng = np.random.default_rng(2024)
+    rng, n_cases = random_plan(2024, 60)
     i32 = dict(dtype=torch.int32, device="cuda")
-    for it in range(60):
+    for it in range(n_cases):
         B = int(rng.integers(1, 9))
         stride = int(rng.choice([17, 300, 1024, 4096, 8192, 8200, 12000, 16384, 30000]))
         V = int(rng.choice([1, 2, 5, 50, 1000]))

@@ -16,7 +16,7 @@ import oracle
 import paper_2412_01447_amd as pld
 import synth
 from gpu_helpers import (check_sample, d_bf16, d_f32, d_i32, gpu_verify, gpu_verify_sample,
-                         sample_workspace, say, workspace)
+                         random_plan, sample_workspace, say, workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -88,8 +88,8 @@ def test_verify_sample_random_shapes():
     K up to 40 (several rounds of the finishing kernel's waves), vocabularies from 1
     to 140000, temperatures from 0.2 to 5, draft lengths from -1 to K+1, planted
     accepted prefixes -- against the oracle, near-tie flips bounded and counted."""
-    rng = np.random.default_rng(99)
-    for it in range(24):
+    rng, n_cases = random_plan(99, 24)
+    for it in range(n_cases):
         B = int(rng.integers(1, 13))
         K = int(rng.integers(1, 41))
         V = int(rng.choice([1, 5, 999, 32000, 140000]))
