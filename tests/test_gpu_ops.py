@@ -133,6 +133,34 @@ def test_find_lane31_hits(stride):
                        f"lane31 draft split {split}")
 
 
+def test_find_random_shapes():
+    """Seeded random shapes of the candidate search alone -- ragged lengths (1 to
+    the stride), strides on both sides of the one-block and tiled limits and up to
+    131072, n-gram ranges up to 8, small vocabularies (dense hits) and periodic
+    rows (every position a long match) -- against the oracle's occurrence lists,
+    counts and n used, bit for bit."""
+    rng, n_cases = random_plan(31, 40)
+    for it in range(n_cases):
+        B = int(rng.integers(1, 13))
+        stride = int(rng.choice([1, 2, 63, 64, 65, 4095, 8191, 8192, 8193, 16383, 16384,
+                                 16385, 20000, 65536, 131072]))
+        while B * stride > 1 << 20:
+            B = max(1, B // 2)
+        V = int(rng.choice([1, 2, 3, 17, 1000]))
+        nmin = int(rng.integers(1, 5))
+        nmax = int(rng.integers(nmin, 9))
+        what = f"case {it}: B{B} S{stride} V{V} n{nmin}-{nmax}"
+        say("find random", what)
+        if rng.integers(0, 4) == 0:   # periodic rows
+            period = int(rng.integers(1, 6))
+            toks = np.tile((np.arange(stride) % period).astype(np.int32), (B, 1))
+        else:
+            toks = rng.integers(0, V, size=(B, stride)).astype(np.int32)
+        lens = rng.integers(1, stride + 1, size=B).astype(np.int32)
+        lens[0] = stride
+        check_find(gpu_find(toks, lens, nmin, nmax), oracle.find(toks, lens, nmin, nmax), what)
+
+
 def test_find_planted_ngrams_multi_tile():
     """Long sequences with planted n-gram repeats crossing tile borders."""
     say("find planted multi-tile")
