@@ -306,6 +306,49 @@ def test_rank_attn_parity(R, agg):
     check_best(gbp, gbs, rsc, rbp, rbs, cp, cc, f"attn R={R}")
 
 
+def test_rank_random_shapes():
+    """Seeded random shapes of the separate ranking calls against the oracle --
+    hidden (bf16, d from 8 to 8192, padded rows) and attention (SUM or MAX over 1 to
+    70 rows, padded keys), ragged lengths, dense or sparse candidates, thresholds --
+    scores within the stated tolerance, the choice bit for bit or a counted near tie."""
+    rng, n_cases = random_plan(57, 30)
+    flips = 0
+    for it in range(n_cases):
+        B = int(rng.integers(1, 9))
+        T = int(rng.choice([2, 3, 70, 1000, 5000]))
+        V = int(rng.choice([1, 3, 40, 5000]))
+        hidden = bool(rng.integers(0, 2))
+        th = float(rng.choice([-math.inf, 0.0, 0.2]))
+        toks = rng.integers(0, V, size=(B, T)).astype(np.int32)
+        lens = rng.integers(1, T + 1, size=B).astype(np.int32)
+        lens[0] = T
+        cp, cc, _ = oracle.find(toks, lens, 1, 1)
+        if hidden:
+            d = int(rng.choice([8, 64, 520, 4096, 8192]))
+            while B * T * d > 2e7 and d > 8:
+                d = {8192: 520, 4096: 520, 520: 64, 64: 8}[d]
+            pad = int(rng.choice([0, 8]))
+            what = f"case {it}: hidden B{B} T{T} V{V} d{d} pad{pad} th{th}"
+            say("rank random", what)
+            H = rng.standard_normal((B, T, d + pad)).astype(np.float32)
+            bits = synth.f32_to_bf16_bits(H)
+            rsc, rbp, rbs = oracle.rank_hidden(bits[:, :, :d], lens, cp, cc, threshold=th)
+            gsc, gbp, gbs = gpu_rank_hidden(d_bf16(bits)[:, :, :d], lens, cp, cc, threshold=th)
+        else:
+            R = int(rng.integers(1, 71))
+            agg = int(rng.integers(0, 2))
+            pad = int(rng.choice([0, 5]))
+            what = f"case {it}: attn B{B} T{T} V{V} R{R} agg{agg} pad{pad} th{th}"
+            say("rank random", what)
+            A = rng.random((B, R, T + pad)).astype(np.float32)
+            A /= A.sum(axis=2, keepdims=True)
+            rsc, rbp, rbs = oracle.rank_attn(A[:, :, :T], lens, cp, cc, agg, threshold=th)
+            gsc, gbp, gbs = gpu_rank_attn(d_f32(A)[:, :, :T], lens, cp, cc, agg, threshold=th)
+        check_scores(gsc, rsc, cc, what)
+        flips += check_best(gbp, gbs, rsc, rbp, rbs, cp, cc, what, threshold=th)
+    say("rank random: near-tie flips", flips)
+
+
 def test_rank_attn_strided_keys_and_ties():
     say("rank_attn strided/ties")
     B, R, T, pad = 3, 5, 120, 13
