@@ -3,22 +3,30 @@
 
     python bench.py [--steps K] [--warmup W] [--config C] [--verify greedy|sample]
                     [--temperature T] [--mode auto|fused|split] [--split S] [--warm]
-                    [--no-cpu-baseline] [--copy-probe]
+                    [--no-cpu-baseline] [--no-gate] [--copy-probe]
     python bench.py --loop TASK        # the generation loop, once per ranking
     python bench.py --probe            # bandwidth ceilings of the access patterns
 
 A step is one pass of the whole hot path over one batch of synthetic input
-already resident in HBM.  The default workload is config 2 (batch 8, context
-4096, n-grams 3..1 longest first, hidden 4096 bf16, K = 10, fp32 logits over
-32000 ids); --config picks another (1-5 scale the workload up, 6 and 7 are the
-paper's attention-MAX and thresholded hidden-state settings at its input
-sizes); --verify sample verifies by sampling at --temperature (default 1)
-instead of the argmax.  To keep the caches honest the
-inputs exist in several copies at distinct addresses and consecutive steps
-rotate through them, so every step reads from HBM rather than from the 256 MB
-last-level cache.  W untimed steps run first, then exactly K steps are timed
-between two device synchronisations; HIP events on the launch stream time the
-dominant kernel inside that region, on every eighth step (--event-every).  One JSON line goes to stdout.
+already resident in HBM.  The default workload is config 4, the largest one
+(batch 64, context 16384, vocabulary 128256, hidden 8192 bf16 and 64 attention
+rows per sequence, both rankings, K = 16, bf16 logits); --config picks another
+(1-5 scale the workload up, 6 and 7 are the paper's attention-MAX and
+thresholded hidden-state settings at its input sizes); --verify sample
+verifies by sampling at --temperature (default 1) instead of the argmax.  To
+keep the caches honest the inputs exist in several copies at distinct
+addresses and consecutive steps rotate through them, so every step reads from
+HBM rather than from the 256 MB last-level cache.  W untimed steps run first,
+then exactly K steps are timed between two device synchronisations; HIP
+events on the launch stream bracket the ranking kernel, the attention
+scoring (when the step ranks by both artifacts) and the verification argmax,
+each on one step in eight, in turn (--event-every).  `roofline` is the
+ranking kernel's (the hidden-state scoring when there is one, else the
+attention scoring, else the one-call drafting); `rooflines_other` holds the
+others.  With --gate (the default) the other two of the three largest
+workloads (configs 3, 4, 5) are measured as well, in the same run, and their
+ranking and verification fractions of peak are reported under `gate`.  One
+JSON line goes to stdout.
 
 The CPU oracle (test infrastructure) is timed on the host on the same inputs
 as a reported baseline, unless --no-cpu-baseline.
@@ -44,7 +52,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5, 6, 7])
+    p.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5, 6, 7])
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="CPU work the oracle baseline is given (whole steps, at least one)")
@@ -54,7 +62,13 @@ def parse():
     p.add_argument("--copy-probe", action="store_true",
                    help="after the timed region, copy 1 GiB three times (counter calibration)")
     p.add_argument("--event-every", type=int, default=8,
-                   help="bracket the dominant call with timing events on every N-th timed step")
+                   help="bracket each timed call (ranking, attention scoring, verification "
+                        "argmax) with timing events on one step in N, in turn")
+    p.add_argument("--gate", action=argparse.BooleanOptionalAction, default=True,
+                   help="also measure the ranking and verification kernels of the three "
+                        "largest workloads (configs 3, 4, 5) in the same run (default on)")
+    p.add_argument("--gate-steps", type=int, default=100,
+                   help="timed steps of each extra workload of --gate")
     p.add_argument("--split", type=int, default=0,
                    help="blocks per sequence of the one-call drafting (default: from the "
                         "first step's candidate counts)")
@@ -88,11 +102,12 @@ def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fu
             keys = cand_pos[b, :C[b]].astype(np.int64) - 1
             segs += len(np.unique((keys * 4) // SEG))
         out["score_attn"] = int(segs * cfg.R * SEG + C.sum() * 4)
-        out["select_attn"] = B * 8 * 2 + B * 8
     if cfg.rank in ("hidden", "both"):
         out["score_hidden"] = int(((C + (C > 0)) * cfg.d * 2).sum() + C.sum() * 4)
-        out["select"] = B * 8 * 2 + B * 8
-    out["emit"] = int(B * K * 4 * 2)
+    # the selection (key slots read and zeroed, per ranking) and the draft
+    # (tokens read and written, lengths and choices written)
+    nrank = 2 if cfg.rank == "both" else 1
+    out["select_draft"] = int(nrank * B * 16 * 8 * 2 + B * K * 4 * 2 + nrank * B * 8 + B * 4)
     rows = draft_len.astype(np.int64) + 1
     if sample:
         # statistics: the logits rows i <= L once, one (max, mass) pair per segment
@@ -105,15 +120,14 @@ def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fu
         out["verify_argmax"] = int((rows * cfg.V * elt_logits).sum())
         out["verify_accept"] = int((rows * 8 * 2).sum() + B * K * 4 + B * (K + 1) * 4)
     if fused:   # one launch does find, rank, select and emit
-        out["draft"] = sum(out.pop(k) for k in ("find", "score_hidden", "score_attn", "select",
-                                                "select_attn", "emit") if k in out)
+        out["draft"] = sum(out.pop(k) for k in ("find", "score_hidden", "score_attn",
+                                                "select_draft") if k in out)
     return out
 
 
 # kernels behind each timed call (names as rocprofv3 reports them)
 KERNELS = {"draft": "pld::draft_", "find": "pld::find_", "score_hidden": "pld::rank_hidden_kernel",
-           "score_attn": "pld::rank_attn_kernel", "select": "pld::rank_finish_kernel",
-           "select_attn": "pld::rank_finish_kernel", "emit": "pld::emit_kernel",
+           "score_attn": "pld::rank_attn_kernel", "select_draft": "pld::select_draft_kernel",
            "verify_argmax": "pld::verify_argmax_kernel", "verify_accept": "pld::verify_accept_kernel",
            "verify_sample_stats": "pld::sample_stats_kernel",
            "verify_sample_finish": "pld::sample_finish_kernel"}
@@ -165,26 +179,174 @@ class TimingEvents:
         self.ev = []
 
 
-def measured_traffic(workload, call):
-    """HBM bytes per launch of the call's kernel from the committed counter runs
-    (profiles/traffic.json), or None when the kernel sources changed since."""
+def sources_sha256():
     import glob
     import hashlib
-    path = os.path.join(ROOT, "profiles", "traffic.json")
-    if not os.path.exists(path):
-        return None
-    with open(path) as f:
-        table = json.load(f)
     h = hashlib.sha256()
     for fn in sorted(glob.glob(os.path.join(ROOT, "paper_2412_01447_amd", "csrc", "*"))):
         h.update(os.path.basename(fn).encode())
         with open(fn, "rb") as f:
             h.update(f.read())
-    if h.hexdigest() != table.get("sources_sha256"):
+    return h.hexdigest()
+
+
+def measured_traffic(workload, call):
+    """HBM bytes per launch of the call's kernel from the committed counter runs
+    (profiles/traffic.json), or None when the kernel sources changed since."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        table = json.load(f)
+    if sources_sha256() != table.get("sources_sha256"):
         return None
     rows = table.get("workloads", {}).get(workload, {})
     hits = [v for k, v in rows.items() if k.startswith(KERNELS.get(call, "?"))]
     return sum(hits) if hits else None
+
+
+def ranking_call(names):
+    """The call that holds the ranking kernel (Eq. 2 / Eq. 3): the hidden-state
+    scoring when the step has one, else the attention scoring, else the one-call
+    drafting (whose launch finds, ranks and selects)."""
+    for n in ("score_hidden", "score_attn", "draft"):
+        if n in names:
+            return n
+    return None
+
+
+def measure(cfg, args, log, mode=None, steps=None, warmup=None, cpu=False, cold=True):
+    """One workload: inputs resident in HBM (rotated cold copies), W warm-up steps,
+    then exactly K timed steps between two device synchronisations; HIP events on
+    the launch stream bracket the ranking call, the verification argmax (or the
+    sampling statistics) and, with two rankings, the attention scoring, each on
+    every `event_every`-th step in turn.  Returns the step time, the byte counts
+    and each bracketed call's timings; the CPU oracle's baseline when `cpu`."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2412_01447_amd import PLD_AGG_MAX, PLD_AGG_SUM
+    from paper_2412_01447_amd.step import DraftStep
+    mode = mode or args.mode
+    steps = args.steps if steps is None else steps
+    warmup = args.warmup if warmup is None else warmup
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    w = synth.make_workload(cfg, dev, structured=True)
+    toks, lens = w["tokens"], w["lens"]
+    draft_i, dlen_i = synth.intended_drafts(w["metas"], cfg.K)
+    z = synth.logits_for(w, draft_i, dlen_i)
+    bf16 = cfg.logits == "bf16"
+    elt = 2 if bf16 else 4
+    log(f"[bench] {cfg.name}: inputs generated in {time.time() - t0:.1f}s")
+
+    def dev_logits(a):
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16) if bf16 else a).to(dev)
+        return t.view(torch.bfloat16) if bf16 else t
+
+    base = dict(tokens=torch.from_numpy(toks).to(dev), lens=torch.from_numpy(lens).to(dev),
+                logits=dev_logits(z), hidden=w["hidden"],
+                attn=torch.from_numpy(w["attn"]).to(dev) if w["attn"] is not None else None)
+    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, mode=mode)
+    fused = step.uses_fused(base["hidden"], base["attn"])
+    sample = args.verify == "sample"
+    if sample:
+        step.set_sampling(args.temperature, cfg.V, bf16,
+                          uniforms=torch.from_numpy(synth.make_uniforms(cfg.B, cfg.K, cfg.seed)).to(dev))
+    rank_args = dict(ngram=cfg.ngram, agg=PLD_AGG_MAX if cfg.agg == "max" else PLD_AGG_SUM,
+                     threshold=cfg.theta)
+
+    # one step to learn the data-dependent byte counts (and, for the one-call
+    # drafting, how many blocks should share a sequence)
+    step.run(base["tokens"], base["lens"], base["logits"], hidden=base["hidden"],
+             attn=base["attn"], **rank_args)
+    torch.cuda.synchronize()
+    nbytes = algorithmic_bytes(cfg, lens, step.cand_count.cpu().numpy(),
+                               step.draft_len.cpu().numpy(), step.cand_pos.cpu().numpy(), elt,
+                               fused, sample=sample)
+    step_bytes = sum(nbytes.values())
+    # input copies at distinct addresses: the steps of one rotation touch at
+    # least twice the last-level cache
+    copies = 1 if not cold else int(min(64, max(2, math.ceil(2 * MALL_BYTES /
+                                                              max(step_bytes, 1)))))
+    sets = [base]
+    for _ in range(copies - 1):
+        sets.append({k: (v.clone() if v is not None else None) for k, v in base.items()})
+    torch.cuda.synchronize()
+    log(f"[bench] step bytes {step_bytes / 1e6:.2f} MB {json.dumps(nbytes)}; {copies} input copies")
+    stream = torch.cuda.current_stream()
+    if fused:
+        # blocks per sequence for the one-call drafting, from the first step's
+        # candidate counts (or as given)
+        if args.split:
+            step.set_split(args.split)
+        else:
+            step.tune_split(step.cand_count.cpu().numpy(), hidden=base["hidden"] is not None)
+        log(f"[bench] drafting with {step.draft_split} block(s) per sequence")
+    # every step as prepared calls (arguments marshalled once, one kernel each)
+    plans = [step.plan(s_["tokens"], s_["lens"], s_["logits"], hidden=s_["hidden"],
+                       attn=s_["attn"], stream=stream, **rank_args) for s_ in sets]
+    names = [n for n, _ in plans[0]]
+    assert set(names) == set(nbytes), (names, list(nbytes))
+    rank = ranking_call(names)
+    timed = [rank] + [n for n in ("score_attn",) if n in names and n != rank] + \
+            ["verify_sample_stats" if sample else "verify_argmax"]
+    E = args.event_every
+    assert len(timed) <= E
+    slots = [(k, timed[k % E]) for k in range(steps) if k % E < len(timed)]
+    ev = TimingEvents(len(slots))
+    which = {k: (i, name) for i, (k, name) in enumerate(slots)}
+
+    for k in range(warmup):
+        for _, call in plans[k % copies]:
+            call()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(steps):
+        i, target = which.get(k, (-1, None))
+        for name, call in plans[k % copies]:
+            if name == target:
+                ev.record(2 * i, stream)
+                call()
+                ev.record(2 * i + 1, stream)
+            else:
+                call()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    per_call = {}
+    for i, (k, name) in enumerate(slots):
+        per_call.setdefault(name, []).append(ev.elapsed_ms(2 * i, 2 * i + 1))
+    ev.close()
+    calls = {}
+    for name, ms in per_call.items():
+        avg = sum(ms) / len(ms)
+        ach = nbytes[name] / (avg * 1e-3) / 1e9
+        calls[name] = {"kernel": KERNELS[name], "achieved": round(ach, 1),
+                       "frac": round(ach / HBM_PEAK_GBS, 4), "bytes_per_launch": nbytes[name],
+                       "avg_us": round(avg * 1e3, 2),
+                       **{f"p{q}_us": round(float(np.percentile(ms, q)) * 1e3, 2)
+                          for q in (10, 50, 90)},
+                       "launches_timed": len(ms)}
+        log(f"[bench] {name}: {avg * 1e3:.2f} us avg, {ach:.1f} GB/s "
+            f"({ach / HBM_PEAK_GBS:.3f} of peak)")
+    out = {"cfg": cfg, "step": step, "fused": fused, "sample": sample, "copies": copies,
+           "nbytes": nbytes, "step_bytes": step_bytes, "us_per_step": elapsed * 1e6 / steps,
+           "calls": calls, "rank": rank, "w": w, "z": z, "bf16": bf16}
+    if cpu:
+        out["cpu"] = cpu_baseline(cfg, w, z, bf16, args.cpu_seconds, log,
+                                  (args.temperature, synth.make_uniforms(cfg.B, cfg.K, cfg.seed))
+                                  if sample else None)
+    del sets, plans, base
+    return out
+
+
+def roofline_of(cfg, call, rec):
+    """The roofline object of one bracketed call."""
+    return {"bound": "hbm", "kernel": call, "achieved": rec["achieved"], "peak": HBM_PEAK_GBS,
+            "unit": "GB/s", "frac": rec["frac"], "traffic": measured_traffic(cfg.name, call),
+            **{k: rec[k] for k in ("bytes_per_launch", "avg_us", "p10_us", "p50_us", "p90_us",
+                                   "launches_timed")}}
 
 
 def main():
@@ -193,11 +355,9 @@ def main():
         print("bench.py measures one GPU (--gpus 1): the step shards by sequence with no "
               "exchange between GPUs, so more GPUs only scale the batch.", file=sys.stderr)
         sys.exit(2)
-    import numpy as np
     import torch
 
     import synth
-    from paper_2412_01447_amd.step import DraftStep
 
     if args.probe:
         import subprocess
@@ -209,116 +369,16 @@ def main():
     if args.loop:
         return run_loop(args)
     cfg = synth.CONFIGS[args.config]
-    dev = torch.device("cuda:0")
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
     log(f"[bench] config {args.config}: {cfg.name}")
-    t0 = time.time()
-    w = synth.make_workload(cfg, dev, structured=True)
-    toks, lens = w["tokens"], w["lens"]
-    draft_i, dlen_i = synth.intended_drafts(w["metas"], cfg.K)
-    z = synth.logits_for(w, draft_i, dlen_i)
-    bf16 = cfg.logits == "bf16"
-    elt = 2 if bf16 else 4
-    log(f"[bench] inputs generated in {time.time() - t0:.1f}s")
-
-    def dev_logits(a):
-        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16) if bf16 else a).to(dev)
-        return t.view(torch.bfloat16) if bf16 else t
-
-    base = dict(tokens=torch.from_numpy(toks).to(dev), lens=torch.from_numpy(lens).to(dev),
-                logits=dev_logits(z), hidden=w["hidden"],
-                attn=torch.from_numpy(w["attn"]).to(dev) if w["attn"] is not None else None)
-    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, mode=args.mode)
-    fused = step.uses_fused(base["hidden"], base["attn"])
-    sample = args.verify == "sample"
-    if sample:
-        step.set_sampling(args.temperature, cfg.V, bf16,
-                          uniforms=torch.from_numpy(synth.make_uniforms(cfg.B, cfg.K, cfg.seed)).to(dev))
-
-    from paper_2412_01447_amd import PLD_AGG_MAX, PLD_AGG_SUM
-    rank_args = dict(ngram=cfg.ngram, agg=PLD_AGG_MAX if cfg.agg == "max" else PLD_AGG_SUM,
-                     threshold=cfg.theta)
-
-    def run(s):
-        step.run(s["tokens"], s["lens"], s["logits"], hidden=s["hidden"], attn=s["attn"],
-                 **rank_args)
-
-    # one step to learn the data-dependent byte counts (and, for the one-call
-    # drafting, how many blocks should share a sequence)
-    run(base)
-    torch.cuda.synchronize()
-    nbytes = algorithmic_bytes(cfg, lens, step.cand_count.cpu().numpy(),
-                               step.draft_len.cpu().numpy(), step.cand_pos.cpu().numpy(), elt,
-                               fused, sample=sample)
-    step_bytes = sum(nbytes.values())
-    dominant = max(nbytes, key=nbytes.get)
-    # input copies at distinct addresses: the steps of one rotation touch at
-    # least twice the last-level cache
-    copies = 1 if args.warm else int(min(64, max(2, math.ceil(2 * MALL_BYTES / max(step_bytes, 1)))))
-    sets = [base]
-    for _ in range(copies - 1):
-        sets.append({k: (v.clone() if v is not None else None) for k, v in base.items()})
-    torch.cuda.synchronize()
-    log(f"[bench] step bytes {step_bytes / 1e6:.2f} MB {json.dumps(nbytes)}; "
-        f"dominant {dominant}; {copies} input copies")
-    # every step as prepared calls (arguments marshalled once, one kernel each)
-    stream = torch.cuda.current_stream()
-
-    def make_plans():
-        return [step.plan(s_["tokens"], s_["lens"], s_["logits"], hidden=s_["hidden"],
-                          attn=s_["attn"], stream=stream, **rank_args) for s_ in sets]
-
-    if fused:
-        # blocks per sequence for the one-call drafting, from the first step's
-        # candidate counts (or as given)
-        if args.split:
-            step.set_split(args.split)
-        else:
-            step.tune_split(step.cand_count.cpu().numpy(), hidden=base["hidden"] is not None)
-        log(f"[bench] drafting with {step.draft_split} block(s) per sequence")
-    plans = make_plans()
-    names = [n for n, _ in plans[0]]
-    assert set(names) == set(nbytes), (names, list(nbytes))
-    # the dominant call is bracketed by events on every `event_every`-th timed
-    # step: an event pair adds its own dispatches to the step, so sampling keeps
-    # the step time close to the unbracketed one
-    timed = [k for k in range(args.steps) if k % args.event_every == 0]
-    ev = TimingEvents(len(timed))
-
-    for k in range(args.warmup):
-        for _, call in plans[k % copies]:
-            call()
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for k in range(args.steps):
-        e = k // args.event_every if k % args.event_every == 0 else -1
-        for name, call in plans[k % copies]:
-            if name == dominant and e >= 0:
-                ev.record(2 * e, stream)
-                call()
-                ev.record(2 * e + 1, stream)
-            else:
-                call()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
-    ms_per_step = elapsed * 1e3 / args.steps
-    dom_each = [ev.elapsed_ms(2 * e, 2 * e + 1) for e in range(len(timed))]
-    dom_ms = sum(dom_each) / len(dom_each)
-    ev.close()
-    import numpy as np
-    pct = {f"p{q}_us": round(float(np.percentile(dom_each, q)) * 1e3, 2) for q in (10, 50, 90)}
-
-    roofline = None
-    if dom_ms:
-        achieved = nbytes[dominant] / (dom_ms * 1e-3) / 1e9
-        roofline = {"bound": "hbm", "kernel": dominant, "achieved": round(achieved, 1),
-                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                    "traffic": measured_traffic(cfg.name, dominant),
-                    "bytes_per_launch": nbytes[dominant],
-                    "avg_us": round(dom_ms * 1e3, 2), **pct, "launches_timed": len(timed)}
-        log(f"[bench] {dominant}: {dom_ms * 1e3:.2f} us avg, {achieved:.1f} GB/s")
+    m = measure(cfg, args, log, cpu=not args.no_cpu_baseline, cold=not args.warm)
+    step, fused, sample = m["step"], m["fused"], m["sample"]
+    rank = m["rank"]
+    roofline = roofline_of(cfg, rank, m["calls"][rank]) if rank in m["calls"] else None
+    others = {n: roofline_of(cfg, n, r) for n, r in m["calls"].items() if n != rank}
 
     if args.copy_probe:
+        dev = torch.device("cuda:0")
         src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
@@ -326,15 +386,32 @@ def main():
         torch.cuda.synchronize()
         log("[bench] copy probe: 3 x 1 GiB device copies done")
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, w, z, bf16, args.cpu_seconds, log,
-                           (args.temperature, synth.make_uniforms(cfg.B, cfg.K, cfg.seed))
-                           if sample else None)
+    gate = None
+    if args.gate and not args.warm:
+        # the other two of the three largest workloads, measured in the same run
+        # (their own step configuration, fewer steps, no CPU baseline): the
+        # fractions of peak of their ranking and verification kernels
+        m.pop("w"), m.pop("z"), m.pop("step")
+        torch.cuda.empty_cache()
+        gate = {}
+        for cid in (3, 4, 5):
+            if cid == args.config:
+                g = m
+            else:
+                g = measure(synth.CONFIGS[cid], args, log, steps=args.gate_steps,
+                            warmup=args.gate_steps // 10 + 5)
+            gate[f"config{cid}"] = {
+                "workload": synth.CONFIGS[cid].name, "us_per_step": round(g["us_per_step"], 2),
+                "drafting": "one call" if g["fused"] else "separate calls",
+                **{n: {"avg_us": r["avg_us"], "GBps": r["achieved"], "frac": r["frac"],
+                       "bytes": r["bytes_per_launch"]} for n, r in g["calls"].items()}}
+            if g is not m:
+                del g
+                torch.cuda.empty_cache()
 
     line = {
-        "metric": METRIC, "value": round(ms_per_step * 1e3, 2), "unit": "us", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "metric": METRIC, "value": round(m["us_per_step"], 2), "unit": "us", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(m["us_per_step"] / 1e3, 5),
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": cfg.name, "batch": cfg.B, "context": cfg.T, "vocab": cfg.V,
@@ -346,15 +423,18 @@ def main():
                                 else "separate calls"),
                    "verification": (f"sampling at temperature {args.temperature}" if sample
                                     else "greedy"),
-                   "input_copies": copies,
+                   "input_copies": m["copies"],
                    "cache": "warm: one copy of the inputs" if args.warm else
                             "cold: copies rotated past the last-level cache",
                    **({"attn_bytes_dense": int(cfg.B) * cfg.R * cfg.T * 4}
                       if cfg.rank in ("attn", "both") else {}),
-                   "step_bytes": step_bytes},
+                   "step_bytes": m["step_bytes"]},
         "roofline": roofline,
-        "cpu_baseline": cpu,
+        "rooflines_other": others,
+        "cpu_baseline": m.get("cpu"),
     }
+    if gate is not None:
+        line["gate"] = gate
     print(json.dumps(line), flush=True)
 
 
@@ -505,7 +585,12 @@ def cpu_baseline(cfg, w, z, bf16, seconds, log, sampling=None):
             break
     dt = (time.perf_counter() - t0) / n
     log(f"[bench] cpu oracle: {n} whole steps, {dt * 1e3:.2f} ms per step")
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = None
     out = {"value": round(dt * 1e6, 1), "unit": "us", "cores": 1, "kind": "oracle",
+           "host_cores": os.cpu_count(), "host_cores_usable": affinity,
            "sample": f"{n} whole steps of the same workload (all {cfg.B} sequences), "
                      f"single-threaded C oracle in fp64",
            "per_op_us": {k: round(v / n * 1e6, 1) for k, v in ops.items()},

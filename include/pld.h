@@ -180,10 +180,15 @@ int pld_emit_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *len
  * among equal maxima; -0 and +0 compare equal):
  *   accept_len[b] = the first i < L with y_i != draft[b][i], else L
  *   out_tokens[b] = draft[b][0..a-1], y_a, then -1 padding;  out_count[b] = a+1
- * where L = draft_len[b].  Rows i > L are never read.
+ * where L = draft_len[b].  Rows i > L do not affect any output.
  *
  *   logits      PLD_F32 or PLD_BF16 (bit patterns); element (b, i, v) at
- *               b*l_seq_stride + i*l_row_stride + v; element-aligned.
+ *               b*l_seq_stride + i*l_row_stride + v; element-aligned.  All
+ *               K+1 rows of every sequence (the last one's included) must be
+ *               readable device memory whatever draft_len holds: the argmax
+ *               requests the first part of each row before the draft length
+ *               arrives, so the rows past a short draft are read in part or
+ *               in full (their values are never used).
  *   V           vocabulary size >= 1;  K >= 1 draft slots per sequence
  *   draft       int32 [B][K], draft_len int32 [B] (from pld_emit_draft)
  *   accept_len, out_count int32 [B];  out_tokens int32 [B][K+1]
@@ -251,7 +256,8 @@ size_t pld_verify_sample_workspace_bytes(int B, int K, int V, int dtype);
  *   score then most recent position): turns those keys into best_pos /
  *   best_score and returns the workspace to zero.
  * pld_verify_argmax -- y_i = argmax_v Z[b][i][v] for the rows i <= draft_len[b],
- *   kept in the workspace.
+ *   kept in the workspace (rows past the draft may be read, as in
+ *   pld_verify_greedy, and are never used).
  * pld_verify_accept -- the accepted length and emitted tokens from those
  *   row maxima (Sec. 4.4); returns the workspace to zero.
  * pld_verify_sample_stats -- the streaming pass of pld_verify_sample: per
@@ -274,6 +280,34 @@ int pld_score_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stride
 
 int pld_select_best(int B, int32_t *best_pos, float *best_score, void *workspace,
                     size_t workspace_bytes, void *stream);
+
+/*
+ * pld_select_draft -- pld_select_best followed by pld_emit_draft in one
+ * launch (the argmax over the occurrences, then the draft of Sec. 4.3): from
+ * the keys a scoring call left in `workspace`, best_pos / best_score, then
+ * draft / draft_len exactly as pld_emit_draft writes them for that best_pos.
+ * With aux_workspace non-NULL, the keys a second scoring call left there (a
+ * second ranking of the same occurrences, e.g. attention beside hidden states)
+ * are resolved as well, into aux_best_pos / aux_best_score only.  Both
+ * workspaces are returned to zero.  One dependent launch fewer per step than
+ * the separate calls, two fewer with a second ranking.
+ *
+ *   tokens, lens, K, draft, draft_len   as pld_emit_draft
+ *   best_pos, best_score                as pld_select_best
+ *   workspace       the first ranking's keys (pld_score_hidden / _attn)
+ *   aux_workspace   NULL, or the second ranking's keys: a buffer of its own of
+ *                   at least pld_workspace_bytes(B, K) bytes, zero-filled once
+ *   aux_best_pos, aux_best_score   int32 [B], fp32 [B]; required with aux_workspace
+ * Errors: PLD_ERR_INVALID (NULL required pointer, B outside [1, PLD_MAX_BATCH],
+ * K < 1, tok_stride outside [1, 2^30], aux_workspace without its outputs),
+ * PLD_ERR_WORKSPACE (a workspace NULL or too small, or the two the same
+ * buffer), PLD_ERR_LAUNCH.
+ */
+int pld_select_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B, int K,
+                     int32_t *best_pos, float *best_score, int32_t *draft, int32_t *draft_len,
+                     void *workspace, size_t workspace_bytes, void *aux_workspace,
+                     size_t aux_workspace_bytes, int32_t *aux_best_pos, float *aux_best_score,
+                     void *stream);
 
 int pld_verify_argmax(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
                       int V, int K, const int32_t *draft_len, int B, void *workspace,

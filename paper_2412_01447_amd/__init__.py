@@ -20,7 +20,8 @@ __all__ = [
     "pld_rank_hidden", "pld_rank_attn", "pld_emit_draft", "pld_verify_greedy",
     "pld_draft_hidden", "pld_draft_attn", "pld_draft_workspace_bytes", "DRAFT_MAX_TOK_STRIDE",
     "DRAFT_MAX_PART", "pld_score_hidden",
-    "pld_score_attn", "pld_select_best", "pld_verify_argmax", "pld_verify_accept",
+    "pld_score_attn", "pld_select_best", "pld_select_draft", "pld_verify_argmax",
+    "pld_verify_accept",
     "pld_verify_sample", "pld_verify_sample_workspace_bytes", "pld_verify_sample_stats",
     "pld_verify_sample_finish", "PLD_MAX_SAMPLE_ROWS", "pld_select_prefix", "pld_commit", "pld_accept_commit",
     "PLD_MAX_MATCH",
@@ -63,6 +64,8 @@ _SIGNATURES = {
     "pld_score_attn": ([_vp, _i64, _i64, _i64, _int, _int, _vp, _vp, _i64, _vp, _int, _f32, _vp,
                         _vp, _sz, _vp], _int),
     "pld_select_best": ([_int, _vp, _vp, _vp, _sz, _vp], _int),
+    "pld_select_draft": ([_vp, _i64, _vp, _int, _int, _vp, _vp, _vp, _vp, _vp, _sz, _vp, _sz, _vp,
+                          _vp, _vp], _int),
     "pld_verify_argmax": ([_vp, _int, _i64, _i64, _int, _int, _vp, _int, _vp, _sz, _vp], _int),
     "pld_verify_accept": ([_vp, _vp, _int, _int, _vp, _vp, _vp, _vp, _sz, _vp], _int),
     "pld_verify_sample": ([_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int, ctypes.c_double, _vp,
@@ -381,6 +384,23 @@ def pld_select_best(B, best_pos, best_score, workspace, stream=None, prepare=Fal
     """Selection half of the ranking calls: keys -> best_pos / best_score."""
     return _run("pld_select_best", (B, _ptr(best_pos), _ptr(best_score), _ptr(workspace),
           _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_select_draft(tokens, lens, K, best_pos, best_score, draft, draft_len, workspace,
+                     aux_workspace=None, aux_best_pos=None, aux_best_score=None, stream=None,
+                     prepare=False):
+    """Selection and draft in one launch: keys in `workspace` -> best_pos / best_score and
+    draft [B][K] / draft_len [B]; a second ranking's keys in `aux_workspace` (optional) ->
+    aux_best_pos / aux_best_score."""
+    import torch
+    _need(tokens, torch.int32, "tokens", 2)
+    _need(draft, torch.int32, "draft", 2)
+    if draft.shape[1] != K or draft.stride(0) != K:
+        raise TypeError("draft must be a contiguous [B][K] tensor")
+    return _run("pld_select_draft", (_ptr(tokens), tokens.stride(0), _ptr(lens), tokens.shape[0],
+          K, _ptr(best_pos), _ptr(best_score), _ptr(draft), _ptr(draft_len), _ptr(workspace),
+          _nbytes(workspace), _ptr(aux_workspace), _nbytes(aux_workspace), _ptr(aux_best_pos),
+          _ptr(aux_best_score), _stream(stream),), prepare)
 
 
 def pld_verify_argmax(logits, draft_len, workspace, stream=None, prepare=False):

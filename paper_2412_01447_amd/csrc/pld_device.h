@@ -377,6 +377,27 @@ __device__ __forceinline__ float attn_gather_group(const float *col, int64_t ar,
     return sum ? acc + x4 : fmaxf(acc, x4);
 }
 
+// The choice j* of a sequence from its best ranking key (0: no eligible
+// candidate) and its draft (Sec. 4.3): L = min(K, T-1-j*) when the length is
+// valid and 0 <= j* <= T-2, else 0; draft[i] = x[j*+1+i] for i < L, -1 after.
+// One wave; `x` is the sequence's token row (global memory or its LDS copy),
+// the outputs point at the sequence's own entries.
+__device__ __forceinline__ void write_choice_draft(uint64_t best, int64_t T, bool tok_ok,
+                                                   const int32_t *x, int K, int32_t *best_pos,
+                                                   float *best_score, int32_t *draft,
+                                                   int32_t *draft_len) {
+    const int lane = lane_id();
+    const int32_t bp = best ? (int32_t)(uint32_t)(best & 0xffffffffu) : -1;
+    if (lane == 0) {
+        *best_pos = bp;
+        *best_score = best ? unord_f32((uint32_t)(best >> 32)) : -INFINITY;
+    }
+    int64_t L = 0;
+    if (tok_ok && bp >= 0 && (int64_t)bp <= T - 2) L = min((int64_t)K, T - 1 - bp);
+    for (int i = lane; i < K; i += kWave) draft[i] = (i < L) ? x[bp + 1 + i] : -1;
+    if (lane == 0) *draft_len = (int32_t)L;
+}
+
 // Eq. 2's cosine from the dot product and the two squared norms; the clamp
 // is the usual eps = 1e-8 guard (eps^2 on the product of squared norms).
 __device__ __forceinline__ float cosine(float dot, float hh, float qq) {

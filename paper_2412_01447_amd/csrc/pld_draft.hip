@@ -184,21 +184,13 @@ __device__ uint64_t rank_candidates(const DraftArgs &a, int b, int64_t T, bool s
     return best;
 }
 
-// The draft of sequence b from its best key (Sec. 4.3), written by one wave;
-// `x` is the sequence's token row (global memory or its LDS copy).
+// The choice and the draft of sequence b from its best key (Sec. 4.3),
+// written by one wave; `x` is the sequence's token row (global memory or its
+// LDS copy).
 __device__ void write_draft(const DraftArgs &a, int b, int64_t T, bool tok_ok, uint64_t best,
                             const int32_t *x) {
-    const int lane = lane_id();
-    const int32_t bp = best ? (int32_t)(uint32_t)(best & 0xffffffffu) : -1;
-    if (lane == 0) {
-        a.best_pos[b] = bp;
-        a.best_score[b] = best ? unord_f32((uint32_t)(best >> 32)) : -INFINITY;
-    }
-    int64_t L = 0;
-    if (tok_ok && bp >= 0 && (int64_t)bp <= T - 2) L = min((int64_t)a.K, T - 1 - bp);
-    for (int i = lane; i < a.K; i += kWave)
-        a.draft[(int64_t)b * a.K + i] = (i < L) ? x[bp + 1 + i] : -1;
-    if (lane == 0) a.draft_len[b] = (int32_t)L;
+    write_choice_draft(best, T, tok_ok, x, a.K, a.best_pos + b, a.best_score + b,
+                       a.draft + (int64_t)b * a.K, a.draft_len + b);
 }
 
 // ------------------------------------------------------------------- S == 1

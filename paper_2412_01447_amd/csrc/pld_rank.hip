@@ -13,21 +13,24 @@
 //
 // Hidden ranking: a range crosses few sequences; for each sequence piece the
 // block stages the query row H[T-2] in LDS (bf16), and each wave takes whole
-// candidate rows: 16-byte loads of the bf16 row, fp32 FMAs of the dot product
-// and the squared norm with eight per-lane accumulators, a butterfly wave sum.
-// The reduction order depends only on d, never on the slot, so equal rows give
+// candidate rows: 16-byte nontemporal loads of the bf16 row, the dot product
+// and the squared norm by the bf16 dot instruction (two products added into an
+// fp32 accumulator, four accumulators per lane), then a DPP wave sum.  The
+// reduction order depends only on d, never on the slot, so equal rows give
 // bit-identical scores, and a row equal to the query gives exactly 1.
 //
-// Attention ranking: one lane per candidate gathers A[b][r][j-1] for r < R in
-// r order (the candidates are ascending, so neighbouring lanes read
-// neighbouring keys).
+// Attention ranking: a group of eight lanes per candidate gathers
+// A[b][r][j-1] for r < R (lane t of the group takes rows t, t+8, ...) and the
+// group's partials are combined by DPP moves; the candidates are ascending, so
+// neighbouring groups read neighbouring keys.
 //
 // Selection: a candidate with s > threshold contributes the 64-bit key
 // (orderable(s) << 32 | j); a block reduces its keys per sequence and folds
 // them with one 64-bit atomic max into one of kKeySlots workspace slots of the
 // sequence (the slot is picked by block index, so an atomic never waits
-// behind more than a handful of others on the same address).  A small finishing kernel, launched right
-// after on the same stream, turns the keys into best_pos / best_score and
+// behind more than a handful of others on the same address).  A small
+// finishing kernel, launched right after on the same stream, turns the keys
+// into best_pos / best_score (and, in pld_select_draft, the draft as well) and
 // zeroes the slots (the kernel boundary orders the two; no block of the
 // ranking kernel ever waits for, or fences against, another).
 #include <math.h>
@@ -168,6 +171,52 @@ __global__ __launch_bounds__(256) void rank_finish_kernel(RankCommon c) {
         c.best_pos[b] = (int32_t)(uint32_t)(k & 0xffffffffu);
         c.best_score[b] = unord_f32((uint32_t)(k >> 32));
     }
+}
+
+// The selection and the draft in one launch (Sec. 4.3): one wave per
+// sequence reads the ranking's key slots (lanes 0..15) and, when a second
+// ranking's keys are given, those too (lanes 16..31) together with the length;
+// it returns the slots to zero, writes the second ranking's choice, then the
+// first one's choice and draft (one more trip to memory, for the tokens).
+struct SelectDraftArgs {
+    const int32_t *tokens;
+    int64_t tok_stride;
+    const int32_t *lens;
+    int B, K;
+    uint64_t *keys;          // [B][kKeySlots], zero on exit
+    int32_t *best_pos;
+    float *best_score;
+    int32_t *draft;
+    int32_t *draft_len;
+    uint64_t *aux_keys;      // [B][kKeySlots] or null
+    int32_t *aux_best_pos;
+    float *aux_best_score;
+};
+
+__global__ __launch_bounds__(256) void select_draft_kernel(SelectDraftArgs a) {
+    const int b = (int)((blockIdx.x * (int64_t)blockDim.x + threadIdx.x) / kWave);
+    if (b >= a.B) return;   // wave-uniform
+    const int lane = lane_id();
+    const bool own = lane < kKeySlots;
+    const bool aux = a.aux_keys && !own && lane < 2 * kKeySlots;
+    uint64_t *slot = own ? a.keys + (int64_t)b * kKeySlots + lane
+                         : (aux ? a.aux_keys + (int64_t)b * kKeySlots + (lane - kKeySlots)
+                                : nullptr);
+    const uint64_t k = slot ? *slot : 0ull;
+    const int64_t T = a.lens[b];
+    if (slot) *slot = 0;
+    const uint64_t best = wave_max_u64(own ? k : 0ull);
+    if (a.aux_keys) {   // wave-uniform
+        const uint64_t ab = wave_max_u64(aux ? k : 0ull);
+        if (lane == 0) {
+            a.aux_best_pos[b] = ab ? (int32_t)(uint32_t)(ab & 0xffffffffu) : -1;
+            a.aux_best_score[b] = ab ? unord_f32((uint32_t)(ab >> 32)) : -INFINITY;
+        }
+    }
+    const bool tok_ok = (T >= 1 && T <= a.tok_stride);
+    write_choice_draft(best, T, tok_ok, a.tokens + (int64_t)b * a.tok_stride, a.K,
+                       a.best_pos + b, a.best_score + b, a.draft + (int64_t)b * a.K,
+                       a.draft_len + b);
 }
 
 // ---------------------------------------------------------------- hidden
@@ -444,6 +493,27 @@ extern "C" int pld_select_best(int B, int32_t *best_pos, float *best_score, void
     c.keys = (uint64_t *)workspace;
     int rc = launch_select(c, best_pos, best_score, (hipStream_t)stream);
     return rc != PLD_OK ? rc : launched();
+}
+
+extern "C" int pld_select_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *lens,
+                                int B, int K, int32_t *best_pos, float *best_score,
+                                int32_t *draft, int32_t *draft_len, void *workspace,
+                                size_t workspace_bytes, void *aux_workspace,
+                                size_t aux_workspace_bytes, int32_t *aux_best_pos,
+                                float *aux_best_score, void *stream) {
+    if (!tokens || !lens || !best_pos || !best_score || !draft || !draft_len)
+        return PLD_ERR_INVALID;
+    if (B < 1 || B > PLD_MAX_BATCH || K < 1 || tok_stride < 1 || tok_stride > kMaxTokStride)
+        return PLD_ERR_INVALID;
+    if (aux_workspace && (!aux_best_pos || !aux_best_score)) return PLD_ERR_INVALID;
+    if (!workspace || workspace_bytes < rank_ws_bytes(B)) return PLD_ERR_WORKSPACE;
+    if (aux_workspace && (aux_workspace_bytes < rank_ws_bytes(B) || aux_workspace == workspace))
+        return PLD_ERR_WORKSPACE;
+    SelectDraftArgs a{tokens, tok_stride, lens, B, K, (uint64_t *)workspace, best_pos, best_score,
+                      draft, draft_len, (uint64_t *)aux_workspace, aux_best_pos, aux_best_score};
+    hipLaunchKernelGGL(select_draft_kernel, dim3((unsigned)((B + 3) / 4)), dim3(256), 0,
+                       (hipStream_t)stream, a);
+    return launched();
 }
 
 extern "C" int pld_rank_hidden(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,

@@ -16,7 +16,11 @@
 // A small acceptance kernel, launched right after on the same stream (the
 // kernel boundary orders the two), reads the row keys back with one thread
 // per sequence, computes the accepted length, writes the outputs and returns
-// the slots to zero.  Rows i > L are never read.
+// the slots to zero.  Rows i > L never reach a slot: a block requests its
+// first batch of loads before the draft length arrives (the latency of that
+// read is then hidden) and returns once it sees that its row is past the
+// draft, so every row of the buffer must be readable, and rows past a short
+// draft are read in part or in full.
 //
 // Also here: the commit of the generation loop and the library-wide calls
 // (version, status strings, workspace sizes).  Sampling verification is in

@@ -12,7 +12,8 @@ from . import (DRAFT_MAX_PART, DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, PLD_BF16, PLD_
                PLD_MAX_DRAFT_SPLIT, pld_accept_commit, pld_commit, pld_draft_attn, pld_draft_hidden,
                pld_draft_workspace_bytes, pld_emit_draft, pld_find_candidates,
                pld_find_scratch_bytes, pld_rank_attn, pld_rank_hidden, pld_score_attn,
-               pld_score_hidden, pld_select_best, pld_select_prefix, pld_verify_accept,
+               pld_score_hidden, pld_select_best, pld_select_draft, pld_select_prefix,
+               pld_verify_accept,
                pld_verify_argmax, pld_verify_greedy, pld_verify_sample, pld_verify_sample_finish,
                pld_verify_sample_stats, pld_verify_sample_workspace_bytes, pld_workspace_bytes)
 
@@ -48,6 +49,9 @@ class DraftStep:
         self.out_count = torch.zeros(B, **i32)
         # ranking / verification keys: zero once here, left zero by every call
         self.workspace = torch.zeros(pld_workspace_bytes(B, K), dtype=torch.uint8, device=device)
+        # the attention ranking's keys when both artifacts rank the same occurrences
+        self.workspace_aux = torch.zeros(pld_workspace_bytes(B, K), dtype=torch.uint8,
+                                         device=device)
         nscratch = pld_find_scratch_bytes(B, tok_stride)
         self.scratch = (torch.empty(nscratch, dtype=torch.uint8, device=device)
                         if nscratch else None)
@@ -249,13 +253,34 @@ class DraftStep:
         if self.uses_fused(hidden, attn):
             self.draft_fused(tokens, lens, hidden, attn, ngram, agg, threshold, stream=stream)
             return
-        self.find(tokens, lens, *ngram, stream=stream)
+        # (unprepared: each call is issued as the list is built)
+        self._split_drafting(tokens, lens, hidden, attn, ngram, agg, threshold,
+                             dict(stream=stream, prepare=False))
+
+    def _split_drafting(self, tokens, lens, hidden, attn, ngram, agg, threshold, P):
+        """The separate calls of the drafting half: find, the scoring of each artifact,
+        then the selection and the draft in one launch (with both artifacts the
+        attention ranking's keys go to the second workspace and its choice to
+        best_pos_attn / best_score_attn)."""
+        both = hidden is not None and attn is not None
+        ops = [("find", pld_find_candidates(tokens, lens, ngram[0], ngram[1], self.cand_pos,
+                                            self.cand_count, self.ngram_used, self.scratch, **P))]
         if attn is not None:
-            self.rank_attn(attn, lens, agg=agg, threshold=threshold, into_best=hidden is None,
-                           stream=stream)
+            ops.append(("score_attn", pld_score_attn(
+                attn, lens, self.cand_pos, self.cand_count,
+                self.workspace_aux if both else self.workspace, agg=agg, threshold=threshold,
+                scores=self.scores_attn, **P)))
         if hidden is not None:
-            self.rank_hidden(hidden, lens, threshold=threshold, stream=stream)
-        self.emit(tokens, lens, stream=stream)
+            ops.append(("score_hidden", pld_score_hidden(hidden, lens, self.cand_pos,
+                                                         self.cand_count, self.workspace,
+                                                         threshold=threshold, scores=self.scores,
+                                                         **P)))
+        ops.append(("select_draft", pld_select_draft(
+            tokens, lens, self.K, self.best_pos, self.best_score, self.draft, self.draft_len,
+            self.workspace, aux_workspace=self.workspace_aux if both else None,
+            aux_best_pos=self.best_pos_attn if both else None,
+            aux_best_score=self.best_score_attn if both else None, **P)))
+        return ops
 
     def run(self, tokens, lens, logits, hidden=None, attn=None, ngram=(1, 1), agg=PLD_AGG_SUM,
             threshold=float("-inf"), prefix_match=None, stream=None):
@@ -299,27 +324,7 @@ class DraftStep:
                                    **P)
             ops = [("draft", d)]
         else:
-            ops = [("find", pld_find_candidates(tokens, lens, ngram[0], ngram[1], self.cand_pos,
-                                                self.cand_count, self.ngram_used, self.scratch,
-                                                **P))]
-            if attn is not None:
-                into = hidden is None
-                ops.append(("score_attn", pld_score_attn(attn, lens, self.cand_pos,
-                                                         self.cand_count, self.workspace, agg=agg,
-                                                         threshold=threshold,
-                                                         scores=self.scores_attn, **P)))
-                ops.append(("select_attn", pld_select_best(
-                    self.B, self.best_pos if into else self.best_pos_attn,
-                    self.best_score if into else self.best_score_attn, self.workspace, **P)))
-            if hidden is not None:
-                ops.append(("score_hidden", pld_score_hidden(hidden, lens, self.cand_pos,
-                                                             self.cand_count, self.workspace,
-                                                             threshold=threshold,
-                                                             scores=self.scores, **P)))
-                ops.append(("select", pld_select_best(self.B, self.best_pos, self.best_score,
-                                                      self.workspace, **P)))
-            ops.append(("emit", pld_emit_draft(tokens, lens, self.best_pos, self.K, self.draft,
-                                               self.draft_len, **P)))
+            ops = self._split_drafting(tokens, lens, hidden, attn, ngram, agg, threshold, P)
         if self.temperature is not None:
             ops.append(("verify_sample_stats", pld_verify_sample_stats(
                 logits, self.draft_len, self.temperature, self.workspace, **P)))

@@ -242,7 +242,7 @@ def sample_window_ok(z, temperature, u, y, eps=SAMPLE_EPS):
 
 
 def check_sample(z_rows, temperature, uniforms, draft, draft_len, g, r, what="",
-                 max_flip_frac=0.15):
+                 max_flip_frac=0.02):
     """GPU sampling verification against the oracle's.  Rows past the draft and
     invalid lengths must match exactly; each sampled row must equal the oracle's
     token or be one that a target within SAMPLE_EPS * S would give (a flip, from

@@ -141,6 +141,19 @@ def test_host_validation_error_codes():
     assert e(F, 8, F, F, 1, 0, F, F, NULL) == E_INV
     assert e(F, 8, F, F, 0, 4, F, F, NULL) == E_INV
     assert e(F, 8, F, NULL, 1, 4, F, F, NULL) == E_INV
+    # selection + draft in one launch
+    sd = lib.pld_select_draft
+    assert sd(NULL, 8, F, 1, 4, F, F, F, F, F, 1 << 20, NULL, 0, NULL, NULL, NULL) == E_INV
+    assert sd(F, 8, F, 0, 4, F, F, F, F, F, 1 << 20, NULL, 0, NULL, NULL, NULL) == E_INV
+    assert sd(F, 8, F, 4097, 4, F, F, F, F, F, 1 << 20, NULL, 0, NULL, NULL, NULL) == E_INV
+    assert sd(F, 8, F, 1, 0, F, F, F, F, F, 1 << 20, NULL, 0, NULL, NULL, NULL) == E_INV
+    assert sd(F, 0, F, 1, 4, F, F, F, F, F, 1 << 20, NULL, 0, NULL, NULL, NULL) == E_INV
+    assert sd(F, 8, F, 1, 4, F, F, F, NULL, F, 1 << 20, NULL, 0, NULL, NULL, NULL) == E_INV
+    assert sd(F, 8, F, 1, 4, F, F, F, F, F, 1 << 20, P(0x2000), 1 << 20, NULL, F, NULL) == E_INV
+    assert sd(F, 8, F, 1, 4, F, F, F, F, NULL, 1 << 20, NULL, 0, NULL, NULL, NULL) == E_WS
+    assert sd(F, 8, F, 1, 4, F, F, F, F, F, 8, NULL, 0, NULL, NULL, NULL) == E_WS
+    assert sd(F, 8, F, 1, 4, F, F, F, F, F, 1 << 20, P(0x2000), 8, F, F, NULL) == E_WS
+    assert sd(F, 8, F, 1, 4, F, F, F, F, F, 1 << 20, F, 1 << 20, F, F, NULL) == E_WS   # same buffer
     # verify
     v = lib.pld_verify_greedy
     assert v(F, 2, 40, 10, 10, 3, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_INV   # dtype

@@ -24,10 +24,13 @@ pytestmark = pytest.mark.gpu
 
 # mode: "split" separate calls; "fused" the one-call drafting with blocks per sequence
 # from the candidate counts, as the benchmark tunes it; "fused1" one block per
-# sequence; "fused8" positions split over 8 blocks per sequence
+# sequence; "fused8" positions split over 8 blocks per sequence.  The one-call
+# drafting takes one artifact: on the workload with both it runs on the hidden
+# states alone.
 CASES = [(1, True, "fused"), (1, False, "split"), (2, True, "fused"), (2, False, "fused"),
          (2, True, "split"), (2, True, "fused8"), (3, True, "fused"), (3, False, "split"),
-         (3, False, "fused"), (3, False, "fused1"), (4, True, "split"), (5, True, "split"),
+         (3, False, "fused"), (3, False, "fused1"), (4, True, "split"), (4, False, "split"),
+         (4, True, "fused"), (5, True, "split"),
          (5, False, "split"), (5, True, "fused"), (5, False, "fused"),
          (6, True, "fused"), (6, False, "fused"), (6, False, "split"), (6, True, "fused8"),
          (7, True, "fused"), (7, False, "fused"), (7, False, "split"), (7, False, "fused8")]
@@ -41,6 +44,8 @@ def test_config_step_parity(cid, structured, mode):
     dev = torch.device("cuda:0")
     w = synth.make_workload(cfg, dev, structured=structured)
     toks, lens = w["tokens"], w["lens"]
+    if mode.startswith("fused") and w["hidden"] is not None:
+        w["attn"] = None
     # ---- oracle, stage by stage
     cp, cc, nu = oracle.find(toks, lens, *cfg.ngram)
     ref = {}
@@ -73,6 +78,7 @@ def test_config_step_parity(cid, structured, mode):
     torch.cuda.synchronize()
     g = step.host()
     assert int(torch.count_nonzero(step.workspace).item()) == 0
+    assert int(torch.count_nonzero(step.workspace_aux).item()) == 0
     assert draft_keys_zero(step.draft_ws, cfg.B)
     check_find((g["cand_pos"], g["cand_count"], g["ngram_used"]), (cp, cc, nu), cfg.name)
     flips = 0
@@ -140,7 +146,7 @@ def test_config_verify_sample(cid):
         r = synth.bf16_bits_to_f32(z[b, i]) if bf16 else z[b, i]
         return np.asarray(r, np.float64)
 
-    flips = check_sample(z_rows, 1.0, U, draft, dlen, got, ref, cfg.name, max_flip_frac=0.25)
+    flips = check_sample(z_rows, 1.0, U, draft, dlen, got, ref, cfg.name, max_flip_frac=0.01)
     say("  sampled-row flips:", flips, " accept lengths:",
         np.bincount(got[0][got[0] >= 0], minlength=cfg.K + 1).tolist())
     del step, zd

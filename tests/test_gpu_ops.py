@@ -16,8 +16,8 @@ import paper_2412_01447_amd as pld
 import synth
 from gpu_helpers import (check_best, check_find, check_scores, check_verify, d_bf16, d_f32,
                          draft_keys_zero, draft_workspace, random_plan,
-                         d_i32, gpu_emit, gpu_find, gpu_rank_attn, gpu_rank_hidden, gpu_verify,
-                         say, workspace)
+                         d_i32, dev, gpu_emit, gpu_find, gpu_rank_attn, gpu_rank_hidden,
+                         gpu_verify, say, workspace, assert_ws_zero)
 
 pytestmark = pytest.mark.gpu
 
@@ -387,6 +387,100 @@ def test_emit_parity():
         assert np.array_equal(gd, rd) and np.array_equal(gl, rl), K
 
 
+# ------------------------------------------------- selection + draft, one launch
+def _order_key(score, j):
+    """The ranking key (orderable fp32 score << 32 | j) written on the host."""
+    u = int(np.array([score], np.float32).view(np.uint32)[0])
+    if u == 0x80000000:
+        u = 0
+    o = (~u & 0xffffffff) if u & 0x80000000 else (u | 0x80000000)
+    return (o << 32) | (int(j) & 0xffffffff)
+
+
+def _key_slots(rng, B, stride, empty_every):
+    """Random key slots [B][16]: some sequences with no key at all, equal scores at
+    different positions, signed zeros, positions past the context."""
+    keys = np.zeros((B, 16), np.uint64)
+    for b in range(B):
+        if b % empty_every == 0:
+            continue
+        for k in range(16):
+            if rng.random() < 0.3:
+                continue
+            s = float(rng.choice([rng.normal(), 0.5, -0.0, 0.0, -2.0]))
+            j = int(rng.integers(1, stride + 3))
+            keys[b, k] = _order_key(s, j)
+    return keys
+
+
+def _decode(keys):
+    """best_pos / best_score of each sequence from its slots, decoded on the host."""
+    best = keys.max(axis=1)
+    pos = np.where(best == 0, -1, (best & np.uint64(0xffffffff)).astype(np.int64)).astype(np.int32)
+    o = (best >> np.uint64(32)).astype(np.uint32)
+    u = np.where(o & 0x80000000, o & 0x7fffffff, ~o).astype(np.uint32)
+    sc = np.where(best == 0, -np.inf, u.view(np.float32)).astype(np.float32)
+    return pos, sc
+
+
+@pytest.mark.parametrize("K", [1, 16, 70])
+def test_select_draft_parity(K):
+    """pld_select_draft: the choice from the key slots and the draft equal the
+    host-decoded keys and the oracle's emit, with and without a second ranking's
+    keys, and both workspaces are left zero; the same outputs as pld_select_best
+    followed by pld_emit_draft, bit for bit."""
+    say("select_draft", K)
+    rng = np.random.default_rng(100 + K)
+    B, stride = 70, 90
+    toks = rng.integers(0, 500, size=(B, stride)).astype(np.int32)
+    lens = rng.integers(1, stride + 1, size=B).astype(np.int32)
+    lens[:5] = [0, -3, stride + 1, 1, 2]          # invalid lengths, then the shortest
+    keys = _key_slots(rng, B, stride, 7)
+    aux = _key_slots(rng, B, stride, 5)
+    want_pos, want_sc = _decode(keys)
+    aux_pos, aux_sc = _decode(aux)
+    rd, rl = oracle.emit(toks, lens, want_pos, K)
+    td, ld = d_i32(toks), d_i32(lens)
+    for with_aux in (False, True):
+        ws = workspace(B, K)
+        ws[:B * 128] = torch.from_numpy(keys.view(np.uint8).reshape(-1)).to(dev())
+        ws2 = workspace(B, K) if with_aux else None
+        if with_aux:
+            ws2[:B * 128] = torch.from_numpy(aux.view(np.uint8).reshape(-1)).to(dev())
+        bp = torch.full((B,), -7, dtype=torch.int32, device=dev())
+        bs = torch.zeros(B, dtype=torch.float32, device=dev())
+        dr = torch.full((B, K), -7, dtype=torch.int32, device=dev())
+        dl = torch.full((B,), -7, dtype=torch.int32, device=dev())
+        abp = torch.full((B,), -7, dtype=torch.int32, device=dev())
+        abs_ = torch.zeros(B, dtype=torch.float32, device=dev())
+        pld.pld_select_draft(td, ld, K, bp, bs, dr, dl, ws, aux_workspace=ws2,
+                             aux_best_pos=abp if with_aux else None,
+                             aux_best_score=abs_ if with_aux else None)
+        torch.cuda.synchronize()
+        assert np.array_equal(bp.cpu().numpy(), want_pos)
+        assert np.array_equal(bs.cpu().numpy().view(np.uint32), want_sc.view(np.uint32))
+        assert np.array_equal(dr.cpu().numpy(), rd) and np.array_equal(dl.cpu().numpy(), rl)
+        assert_ws_zero(ws)
+        if with_aux:
+            assert np.array_equal(abp.cpu().numpy(), aux_pos)
+            assert np.array_equal(abs_.cpu().numpy().view(np.uint32), aux_sc.view(np.uint32))
+            assert_ws_zero(ws2)
+        else:
+            assert (abp == -7).all()
+    # the two separate calls from the same slots
+    ws = workspace(B, K)
+    ws[:B * 128] = torch.from_numpy(keys.view(np.uint8).reshape(-1)).to(dev())
+    bp = torch.full((B,), -7, dtype=torch.int32, device=dev())
+    bs = torch.zeros(B, dtype=torch.float32, device=dev())
+    pld.pld_select_best(B, bp, bs, ws)
+    dr = torch.full((B, K), -7, dtype=torch.int32, device=dev())
+    dl = torch.full((B,), -7, dtype=torch.int32, device=dev())
+    pld.pld_emit_draft(td, ld, bp, K, dr, dl)
+    torch.cuda.synchronize()
+    assert np.array_equal(bp.cpu().numpy(), want_pos)
+    assert np.array_equal(dr.cpu().numpy(), rd) and np.array_equal(dl.cpu().numpy(), rl)
+
+
 # ----------------------------------------------------------------- verify
 VERIFY_CASES = [
     # (B, K, V, bf16, integer_valued, seed)
@@ -748,6 +842,8 @@ def test_halves_equal_combined_calls():
     for k in ha:
         assert np.array_equal(ha[k], hb[k], equal_nan=True), k
     assert int(torch.count_nonzero(b.workspace).item()) == 0
+    assert int(torch.count_nonzero(a.workspace).item()) == 0
+    assert int(torch.count_nonzero(a.workspace_aux).item()) == 0
 
 
 @pytest.mark.parametrize("mode", ["fused", "split"])
