@@ -52,7 +52,8 @@ enum {
     PLD_ERR_INVALID = 1,   /* a NULL required pointer, a size or enum out of range   */
     PLD_ERR_ALIGN = 2,     /* a pointer or stride that breaks an alignment rule       */
     PLD_ERR_WORKSPACE = 3, /* workspace NULL or smaller than the call needs           */
-    PLD_ERR_LAUNCH = 4     /* the HIP runtime reported an error when launching        */
+    PLD_ERR_LAUNCH = 4,    /* the HIP runtime reported an error when launching        */
+    PLD_ERR_SCRATCH = 5    /* sizes beyond the static scratch of pld_verify_greedy_noalloc */
 };
 
 /* Element types of the verification logits. */
@@ -202,6 +203,29 @@ int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride, int64
                       int V, int K, const int32_t *draft, const int32_t *draft_len, int B,
                       int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
                       void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * pld_verify_greedy_noalloc -- pld_verify_greedy for callers that cannot
+ * allocate device memory or pass a workspace (code under stream capture,
+ * tight serving loops, harnesses that forbid allocation).  Same arguments
+ * minus the workspace, same outputs and device-side rules, bit for bit.
+ *
+ * The row maxima live in a static array of the library, 65536 64-bit keys
+ * (512 KiB) per GPU, held from the first call on that GPU until the process
+ * ends; the call clears the B*(K+1) keys it uses (a fill kernel, then the
+ * argmax and acceptance kernels: three launches) and never allocates.  The
+ * stream must belong to the current device.  Every call on one GPU shares
+ * that GPU's array: calls that overlap in time on one GPU (different streams,
+ * threads or processes' streams of one context) race and give undefined
+ * results, so serialise them.
+ * Errors: those of pld_verify_greedy (no workspace errors), and
+ * PLD_ERR_SCRATCH when B*(K+1) > 65536; PLD_ERR_LAUNCH also when the array's
+ * device address cannot be obtained.
+ */
+int pld_verify_greedy_noalloc(const void *logits, int dtype, int64_t l_seq_stride,
+                              int64_t l_row_stride, int V, int K, const int32_t *draft,
+                              const int32_t *draft_len, int B, int32_t *accept_len,
+                              int32_t *out_tokens, int32_t *out_count, void *stream);
 
 /*
  * pld_verify_sample -- sampling verification (Sec. 3 and Sec. 4.4 with a

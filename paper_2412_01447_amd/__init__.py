@@ -18,6 +18,7 @@ __all__ = [
     "pld_version", "pld_status_string", "pld_workspace_bytes", "pld_find_scratch_bytes",
     "pld_find_candidates",
     "pld_rank_hidden", "pld_rank_attn", "pld_emit_draft", "pld_verify_greedy",
+    "pld_verify_greedy_noalloc", "NOALLOC_MAX_KEYS",
     "pld_draft_hidden", "pld_draft_attn", "pld_draft_workspace_bytes", "DRAFT_MAX_TOK_STRIDE",
     "DRAFT_MAX_PART", "pld_score_hidden",
     "pld_score_attn", "pld_select_best", "pld_select_draft", "pld_verify_argmax",
@@ -27,7 +28,8 @@ __all__ = [
     "PLD_MAX_MATCH",
 ]
 
-PLD_OK, PLD_ERR_INVALID, PLD_ERR_ALIGN, PLD_ERR_WORKSPACE, PLD_ERR_LAUNCH = range(5)
+PLD_OK, PLD_ERR_INVALID, PLD_ERR_ALIGN, PLD_ERR_WORKSPACE, PLD_ERR_LAUNCH, PLD_ERR_SCRATCH = range(6)
+NOALLOC_MAX_KEYS = 65536        # pld_verify_greedy_noalloc: B*(K+1) limit
 PLD_F32, PLD_BF16 = 0, 1
 PLD_AGG_SUM, PLD_AGG_MAX = 0, 1
 PLD_MAX_NGRAM, PLD_MAX_HIDDEN, PLD_MAX_BATCH, PLD_MAX_DRAFT_SPLIT = 8, 16384, 4096, 1024
@@ -59,6 +61,8 @@ _SIGNATURES = {
     "pld_emit_draft": ([_vp, _i64, _vp, _vp, _int, _int, _vp, _vp, _vp], _int),
     "pld_verify_greedy": ([_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int, _vp, _vp, _vp, _vp,
                            _sz, _vp], _int),
+    "pld_verify_greedy_noalloc": ([_vp, _int, _i64, _i64, _int, _int, _vp, _vp, _int, _vp, _vp,
+                                   _vp, _vp], _int),
     "pld_score_hidden": ([_vp, _i64, _i64, _i64, _int, _vp, _vp, _i64, _vp, _int, _f32, _vp, _vp,
                           _sz, _vp], _int),
     "pld_score_attn": ([_vp, _i64, _i64, _i64, _int, _int, _vp, _vp, _i64, _vp, _int, _f32, _vp,
@@ -255,6 +259,26 @@ def pld_verify_greedy(logits, draft, draft_len, accept_len, out_tokens, out_coun
     return _run("pld_verify_greedy", (_ptr(logits), dtype, logits.stride(0), logits.stride(1), V, K,
           _ptr(draft), _ptr(draft_len), B, _ptr(accept_len), _ptr(out_tokens), _ptr(out_count),
           _ptr(workspace), _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_verify_greedy_noalloc(logits, draft, draft_len, accept_len, out_tokens, out_count,
+                              stream=None, prepare=False):
+    """pld_verify_greedy without a workspace: the row maxima live in the library's static
+    per-GPU array (B*(K+1) <= NOALLOC_MAX_KEYS); calls on one GPU must not overlap."""
+    import torch
+    if logits.dtype not in (torch.float32, torch.bfloat16):
+        raise TypeError("logits must be float32 or bfloat16")
+    _need(logits, logits.dtype, "logits", 3)
+    B, K1, V = logits.shape
+    K = K1 - 1
+    if draft.shape != (B, K) or draft.stride(0) != K:
+        raise TypeError("draft must be a contiguous [B][K] tensor")
+    if out_tokens.shape != (B, K1) or out_tokens.stride(0) != K1:
+        raise TypeError("out_tokens must be a contiguous [B][K+1] tensor")
+    dtype = PLD_F32 if logits.dtype == torch.float32 else PLD_BF16
+    return _run("pld_verify_greedy_noalloc", (_ptr(logits), dtype, logits.stride(0),
+          logits.stride(1), V, K, _ptr(draft), _ptr(draft_len), B, _ptr(accept_len),
+          _ptr(out_tokens), _ptr(out_count), _stream(stream),), prepare)
 
 
 def pld_verify_sample(logits, draft, draft_len, temperature, uniforms, accept_len, out_tokens,

@@ -27,6 +27,8 @@
 // pld_sample.hip; the pieces both use are in pld_verify.h.
 #include <math.h>
 
+#include <mutex>
+
 #include "pld.h"
 #include "pld_device.h"
 #include "pld_verify.h"
@@ -234,15 +236,24 @@ __global__ __launch_bounds__(256) void accept_commit_kernel(VerifyArgs a, Commit
     }
 }
 
-int prep_verify(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
-                int V, int K, const int32_t *draft_len, int B, void *workspace,
-                       size_t workspace_bytes, VerifyArgs &a) {
+// The checks of the logits arguments (everything but the workspace).
+static int check_verify(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
+                        int V, int K, const int32_t *draft_len, int B) {
     if (!logits || !draft_len) return PLD_ERR_INVALID;
     if (B < 1 || K < 1 || V < 1 || (dtype != PLD_F32 && dtype != PLD_BF16)) return PLD_ERR_INVALID;
     if (B > 65535 || K + 1 > 65535) return PLD_ERR_INVALID;       // grid y / z limits
     if (l_row_stride < V || l_seq_stride < (int64_t)(K + 1) * l_row_stride) return PLD_ERR_INVALID;
     const size_t esz = dtype == PLD_F32 ? 4 : 2;
     if ((uintptr_t)logits % esz) return PLD_ERR_ALIGN;
+    return PLD_OK;
+}
+
+int prep_verify(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
+                int V, int K, const int32_t *draft_len, int B, void *workspace,
+                size_t workspace_bytes, VerifyArgs &a) {
+    const int rc = check_verify(logits, dtype, l_seq_stride, l_row_stride, V, K, draft_len, B);
+    if (rc != PLD_OK) return rc;
+    const size_t esz = dtype == PLD_F32 ? 4 : 2;
     if (!workspace || workspace_bytes < verify_ws_bytes(B, K)) return PLD_ERR_WORKSPACE;
     // Blocks per row: enough for ~2048 blocks in flight, but each block keeps
     // at least two 16-byte vectors per thread.
@@ -278,9 +289,71 @@ static void launch_accept(const VerifyArgs &a, hipStream_t s) {
     hipLaunchKernelGGL(verify_accept_kernel, dim3((a.B + 3) / 4), dim3(256), 0, s, a);
 }
 
+// ------------------------------------------------ allocation-free variant
+// pld_verify_greedy_noalloc keeps the row keys in this file-scope device
+// array instead of a caller's workspace.  Each GPU holds its own copy, at its
+// own address, which the host learns once per device from
+// hipGetSymbolAddress; in host code the array's name is only a stand-in and
+// is never passed to a kernel.  Every call on a GPU shares that GPU's array.
+constexpr int kStaticKeys = 65536;                  // B*(K+1) limit: 512 KiB per GPU
+static __device__ __align__(256) uint64_t scratch[kStaticKeys];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static uint64_t *g_scratch_addr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device (looked up on the
+// first call made with that device current, then kept).
+static int scratch_address(uint64_t **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return PLD_ERR_LAUNCH;
+    std::lock_guard<std::mutex> g(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return PLD_ERR_LAUNCH;
+        g_scratch_addr[dev] = reinterpret_cast<uint64_t *>(p);
+    }
+    *out = g_scratch_addr[dev];
+    return PLD_OK;
+}
+
+// The keys the argmax folds into must start at zero: a fill kernel (rather
+// than a memset node) clears the n slots this call uses.
+__global__ __launch_bounds__(256) void clear_keys_kernel(uint64_t *keys, int n) {
+    const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (i < n) keys[i] = 0;
+}
+
 }  // namespace pld
 
 using namespace pld;
+
+extern "C" int pld_verify_greedy_noalloc(const void *logits, int dtype, int64_t l_seq_stride,
+                                         int64_t l_row_stride, int V, int K, const int32_t *draft,
+                                         const int32_t *draft_len, int B, int32_t *accept_len,
+                                         int32_t *out_tokens, int32_t *out_count, void *stream) {
+    if (!draft || !accept_len || !out_tokens || !out_count) return PLD_ERR_INVALID;
+    int rc = check_verify(logits, dtype, l_seq_stride, l_row_stride, V, K, draft_len, B);
+    if (rc != PLD_OK) return rc;
+    if ((int64_t)B * (K + 1) > kStaticKeys) return PLD_ERR_SCRATCH;
+    uint64_t *keys = nullptr;
+    rc = scratch_address(&keys);
+    if (rc != PLD_OK) return rc;
+    VerifyArgs a;
+    rc = prep_verify(logits, dtype, l_seq_stride, l_row_stride, V, K, draft_len, B, keys,
+                     (size_t)kStaticKeys * sizeof(uint64_t), a);
+    if (rc != PLD_OK) return rc;
+    a.draft = draft;
+    a.accept_len = accept_len;
+    a.out_tokens = out_tokens;
+    a.out_count = out_count;
+    const int n = B * (K + 1);
+    hipLaunchKernelGGL(clear_keys_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
+                       (hipStream_t)stream, keys, n);
+    launch_argmax(a, dtype, (hipStream_t)stream);
+    launch_accept(a, (hipStream_t)stream);
+    return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
+}
 
 extern "C" int pld_verify_argmax(const void *logits, int dtype, int64_t l_seq_stride,
                                  int64_t l_row_stride, int V, int K, const int32_t *draft_len,
@@ -389,6 +462,7 @@ extern "C" const char *pld_status_string(int status) {
     case PLD_ERR_ALIGN: return "misaligned pointer or stride";
     case PLD_ERR_WORKSPACE: return "workspace missing or too small";
     case PLD_ERR_LAUNCH: return "kernel launch failed";
+    case PLD_ERR_SCRATCH: return "sizes exceed the static scratch of the allocation-free call";
     default: return "unknown status";
     }
 }

@@ -154,6 +154,15 @@ def test_host_validation_error_codes():
     assert sd(F, 8, F, 1, 4, F, F, F, F, F, 8, NULL, 0, NULL, NULL, NULL) == E_WS
     assert sd(F, 8, F, 1, 4, F, F, F, F, F, 1 << 20, P(0x2000), 8, F, F, NULL) == E_WS
     assert sd(F, 8, F, 1, 4, F, F, F, F, F, 1 << 20, F, 1 << 20, F, F, NULL) == E_WS   # same buffer
+    # the allocation-free verification: host checks come before any device set-up
+    na = lib.pld_verify_greedy_noalloc
+    assert na(F, 0, 40, 10, 10, 3, NULL, F, 1, F, F, F, NULL) == E_INV
+    assert na(F, 2, 40, 10, 10, 3, F, F, 1, F, F, F, NULL) == E_INV                # dtype
+    assert na(F, 0, 39, 10, 10, 3, F, F, 1, F, F, F, NULL) == E_INV                # seq stride
+    assert na(MIS, 0, 40, 10, 10, 3, F, F, 1, F, F, F, NULL) == E_AL
+    E_SC = pld.PLD_ERR_SCRATCH
+    assert na(F, 0, 17 * 10, 10, 10, 16, F, F, 3856, F, F, F, NULL) == E_SC   # 65552 keys
+    assert na(F, 0, 40001 * 2, 2, 2, 40000, F, F, 2, F, F, F, NULL) == E_SC   # 80002 keys
     # verify
     v = lib.pld_verify_greedy
     assert v(F, 2, 40, 10, 10, 3, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_INV   # dtype
