@@ -312,6 +312,20 @@ __device__ __forceinline__ void row_dot(const uint4 *row, const uint4 *q, int nc
     finish_row(ad, an, dot, nrm);
 }
 
+// The query row's squared norm from its LDS copy, in row_dot's order (lane l:
+// chunks l, l+64, ..., pair p into acc[p]) with one chunk in hand at a time,
+// so that it costs few registers; the same bits as row_dot(q, q).
+__device__ __forceinline__ float query_norm(const uint4 *q, int nch) {
+    float ad[4] = {0.f, 0.f, 0.f, 0.f}, an[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int ch = lane_id(); ch < nch; ch += kWave) {
+        const uint4 v = q[ch];
+        accum_chunk(v, v, ad, an);
+    }
+    float dot, nrm;
+    finish_row(ad, an, dot, nrm);
+    return nrm;
+}
+
 // G rows of width nch <= 64 * (16 / G) chunks, all their loads requested at
 // once; a row whose pointer is null is skipped (its results are 0).
 template <int G>
@@ -339,6 +353,64 @@ __device__ __forceinline__ void rows_dot(const uint4 *const (&rows)[G], const ui
             }
         }
         finish_row(ad, an, dot[g], nrm[g]);
+    }
+}
+
+// Rows streamed through a two-deep pipeline of pieces.  A piece is 64 kU
+// chunks of 8 bf16 (kU 16-byte loads per lane, lane l taking chunks l, l+64,
+// ... of the piece; 4 KB for kU = 4); a row is kPieces pieces.  The callers
+// split a row in two (kPieces = 2: kU = 4 for d = 4096, 8 for d = 8192), the
+// fastest of the piece sizes measured for both widths.
+// The wave keeps the loads of the next piece in flight while it reduces the
+// current one, so its memory queue never drains between rows the way a
+// load-all-then-wait round does.  The accumulation order is row_dot's (lane l
+// visits its chunks l, l+64, l+128, ... in order, pair p of a chunk into
+// acc[p]), so a row gives the same bits here as through row_dot / rows_dot.
+// `row(k)` gives the k-th row (k < n) of this wave, or null for an unusable
+// one (its results are reported as not valid); `done(k, valid, dot, nrm)` runs
+// in every lane when row k is complete, in order of k.
+template <int kPieces, int kU, class RowPtr, class Done>
+__device__ __forceinline__ void stream_rows(int n, RowPtr row, const uint4 *q, Done done) {
+    constexpr int kPiece = kU * kWave;    // chunks per piece (kU 16-byte loads per lane)
+    const int lane = lane_id();
+    const int total = n * kPieces;
+    uint4 buf[2][kU];
+    float ad[4] = {0.f, 0.f, 0.f, 0.f}, an[4] = {0.f, 0.f, 0.f, 0.f};
+    auto issue = [&](int slot, int pc) {
+        const uint4 *r = row(pc / kPieces);
+        if (r) {
+            const uint4 *src = r + (pc % kPieces) * kPiece + lane;
+#pragma unroll
+            for (int u = 0; u < kU; ++u) buf[slot][u] = ld_stream(src + u * kWave);
+        }
+    };
+    auto consume = [&](int slot, int pc) {
+        const int k = pc / kPieces, p = pc % kPieces;
+        const bool ok = row(k) != nullptr;
+        if (p == 0) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) ad[i] = an[i] = 0.f;
+        }
+        if (ok) {
+            const uint4 *qq = q + p * kPiece + lane;
+#pragma unroll
+            for (int u = 0; u < kU; ++u) accum_chunk(buf[slot][u], qq[u * kWave], ad, an);
+        }
+        if (p == kPieces - 1) {
+            float dot, nrm;
+            finish_row(ad, an, dot, nrm);
+            done(k, ok, dot, nrm);
+        }
+    };
+    if (total > 0) issue(0, 0);
+    if (total > 1) issue(1, 1);
+    for (int pc = 0; pc < total; pc += 2) {
+        consume(0, pc);
+        if (pc + 2 < total) issue(0, pc + 2);
+        if (pc + 1 < total) {
+            consume(1, pc + 1);
+            if (pc + 3 < total) issue(1, pc + 3);
+        }
     }
 }
 

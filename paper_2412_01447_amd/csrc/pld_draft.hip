@@ -134,11 +134,38 @@ __device__ void draft_score_rows(const DraftArgs &a, int b, int64_t T, bool seq_
     }
 }
 
+// The same for rows of d = 1024 * kU, streamed through stream_rows' two-deep
+// pipeline, two pieces per row (the same bits as draft_score_rows).
+template <int kU>
+__device__ void draft_score_rows_stream(const DraftArgs &a, int b, int64_t T, bool seq_ok,
+                                        const uint16_t *Hb, const uint4 *q_s, float qq,
+                                        const int32_t *s_cand, int first, int step, int total,
+                                        int64_t out0, uint64_t &best) {
+    const int lane = lane_id();
+    const int n = total > first ? (total - first + step - 1) / step : 0;
+    auto row = [&](int k) -> const uint4 * {
+        const int32_t j = s_cand[first + k * step];
+        const bool ok = seq_ok && j >= 1 && (int64_t)j <= T - 2;
+        return ok ? reinterpret_cast<const uint4 *>(Hb + (int64_t)(j - 1) * a.hr) : nullptr;
+    };
+    stream_rows<2, kU>(n, row, q_s, [&](int k, bool ok, float dot, float nrm) {
+        float s = __builtin_nanf("");
+        if (ok) {
+            s = cosine(dot, nrm, qq);
+            if (s > a.threshold) {
+                const uint64_t key = rank_key(s, s_cand[first + k * step]);
+                best = key > best ? key : best;
+            }
+        }
+        if (a.scores && lane == 0) a.scores[(int64_t)b * a.cap + out0 + first + k * step] = s;
+    });
+}
+
 // The block's share of the ranking (Eq. 2 / Eq. 3) over the list s_cand of
 // `total` candidates: list slots w, w + kWaves, ... per wave (hidden), or one
 // slot per group of kGatherLanes lanes (attention).  Returns the block's best key in every thread;
 // `s_q` holds the query row (hidden), `s_key` is kWaves words of LDS.
-template <bool kHidden, int kWaves>
+template <bool kHidden, int kWaves, int kU>
 __device__ uint64_t rank_candidates(const DraftArgs &a, int b, int64_t T, bool seq_ok,
                                     const int32_t *s_cand, int total, int64_t out0,
                                     const uint4 *s_q, uint64_t *s_key) {
@@ -148,9 +175,11 @@ __device__ uint64_t rank_candidates(const DraftArgs &a, int b, int64_t T, bool s
     if constexpr (kHidden) {
         const uint16_t *Hb = a.hidden + (int64_t)b * a.hs;
         const int nch = a.d / 8;
-        float qdot = 0.f, qq = 0.f;
-        if (seq_ok) row_dot<false>(s_q, s_q, nch, qdot, qq);
-        if (nch <= 4 * kWave)
+        const float qq = seq_ok ? query_norm(s_q, nch) : 0.f;
+        if constexpr (kU > 0)
+            draft_score_rows_stream<kU>(a, b, T, seq_ok, Hb, s_q, qq, s_cand, w, kWaves,
+                                             total, out0, best);
+        else if (nch <= 4 * kWave)
             draft_score_rows<4>(a, b, T, seq_ok, Hb, s_q, qq, s_cand, w, kWaves, total, out0, best);
         else if (nch <= 8 * kWave)
             draft_score_rows<2>(a, b, T, seq_ok, Hb, s_q, qq, s_cand, w, kWaves, total, out0, best);
@@ -194,7 +223,7 @@ __device__ void write_draft(const DraftArgs &a, int b, int64_t T, bool tok_ok, u
 }
 
 // ------------------------------------------------------------------- S == 1
-template <bool kHidden>
+template <bool kHidden, int kU>
 __global__ __launch_bounds__(kFindWavesFused * kWave) void draft_kernel(DraftArgs a) {
     constexpr int kWaves = kFindWavesFused;
     static_assert(kFindFusedMax == kWaves * kWave * kLanePos, "one pass per block");
@@ -266,7 +295,8 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void draft_kernel(DraftArg
     }
     uint64_t best = 0;
     if (total > 0)   // block-uniform
-        best = rank_candidates<kHidden, kWaves>(a, b, T, seq_ok, s_list, total, 0, s_q, s_key);
+        best = rank_candidates<kHidden, kWaves, kU>(a, b, T, seq_ok, s_list, total, 0, s_q,
+                                                         s_key);
     if (w == 0) write_draft(a, b, T, tok_ok, best, s_buf);
 }
 
@@ -370,7 +400,7 @@ __device__ int part_n(const DraftArgs &a, int b, int *s_tot) {
 // that small slices leave room for many blocks per CU.
 static size_t part_tok_bytes(int64_t P) { return align_up((size_t)(P + 8) * 4, 16); }
 
-template <bool kHidden, int kWaves>
+template <bool kHidden, int kWaves, int kU>
 __global__ __launch_bounds__(kWaves * kWave) void draft_part_kernel(DraftArgs a) {
     constexpr int kPasses = PartShape<kWaves>::kPasses, kPass = PartShape<kWaves>::kPass;
     extern __shared__ uint4 s_dyn[];
@@ -435,7 +465,7 @@ __global__ __launch_bounds__(kWaves * kWave) void draft_part_kernel(DraftArgs a)
                   out, start[t]);
     __syncthreads();
     const uint64_t best =
-        rank_candidates<kHidden, kWaves>(a, b, T, seq_ok, s_x, total, lo, s_q, s_key);
+        rank_candidates<kHidden, kWaves, kU>(a, b, T, seq_ok, s_x, total, lo, s_q, s_key);
     if (threadIdx.x == 0 && best)
         atomicMax((unsigned long long *)&a.keys[(int64_t)b * kKeySlots + (s % kKeySlots)],
                   (unsigned long long)best);
@@ -671,12 +701,12 @@ static DraftArgs make_draft(const int32_t *tokens, int64_t tok_stride, const int
     return a;
 }
 
-template <bool kHidden>
-static void launch_draft(const DraftArgs &a, hipStream_t s) {
+template <bool kHidden, int kU>
+static void launch_draft_as(const DraftArgs &a, hipStream_t s) {
     const size_t lds = kHidden ? (size_t)(a.d / 8) * sizeof(uint4) : 0;
     if (a.S == 1) {
-        hipLaunchKernelGGL(draft_kernel<kHidden>, dim3(1, a.B), dim3(kFindWavesFused * kWave),
-                           lds, s, a);
+        hipLaunchKernelGGL((draft_kernel<kHidden, kU>), dim3(1, a.B),
+                           dim3(kFindWavesFused * kWave), lds, s, a);
         return;
     }
     if (a.nmin < a.nmax)
@@ -684,12 +714,23 @@ static void launch_draft(const DraftArgs &a, hipStream_t s) {
     // blocks of 8 waves when the grid is small (more rows in flight per block),
     // of 4 otherwise (more blocks resident per CU); the results are the same
     if ((int64_t)a.B * a.S <= kFewBlocks)
-        hipLaunchKernelGGL((draft_part_kernel<kHidden, kPartWavesFew>), dim3(a.S, a.B),
+        hipLaunchKernelGGL((draft_part_kernel<kHidden, kPartWavesFew, kU>), dim3(a.S, a.B),
                            dim3(kPartWavesFew * kWave), part_tok_bytes(a.P) + lds, s, a);
     else
-        hipLaunchKernelGGL((draft_part_kernel<kHidden, kPartWaves>), dim3(a.S, a.B),
+        hipLaunchKernelGGL((draft_part_kernel<kHidden, kPartWaves, kU>), dim3(a.S, a.B),
                            dim3(kPartWaves * kWave), part_tok_bytes(a.P) + lds, s, a);
     hipLaunchKernelGGL(draft_finish_part_kernel, dim3(a.B), dim3(kFinishThreads), 0, s, a);
+}
+
+// Hidden rows of d = 4096 or 8192 take the streaming pipeline (a kernel of
+// their own, so each keeps only the registers its path needs).
+template <bool kHidden>
+static void launch_draft(const DraftArgs &a, hipStream_t s) {
+    if constexpr (kHidden) {
+        if (a.d == 4096) return launch_draft_as<true, 4>(a, s);
+        if (a.d == 8192) return launch_draft_as<true, 8>(a, s);
+    }
+    launch_draft_as<kHidden, 0>(a, s);
 }
 
 }  // namespace pld

@@ -85,9 +85,11 @@ __device__ __forceinline__ uint32_t clamped_count(const RankCommon &c, int b) {
     return (n >= 0 && (int64_t)n <= c.cap) ? (uint32_t)n : 0u;
 }
 
+template <int kThreads = kRankThreads>
 __device__ void candidate_prefix(const RankCommon &c, uint32_t *pre, int32_t *s_lens = nullptr) {
-    __shared__ uint32_t s_wave[kRankWaves];
-    const int per = (c.B + kRankThreads - 1) / kRankThreads;
+    constexpr int kWaves = kThreads / kWave;
+    __shared__ uint32_t s_wave[kWaves];
+    const int per = (c.B + kThreads - 1) / kThreads;
     const int b0 = threadIdx.x * per;
     const int b1 = min(b0 + per, c.B);
     uint32_t sum = 0;
@@ -110,7 +112,7 @@ __device__ void candidate_prefix(const RankCommon &c, uint32_t *pre, int32_t *s_
     }
     if (threadIdx.x == 0) {
         uint32_t t = 0;
-        for (int i = 0; i < kRankWaves; ++i) t += s_wave[i];
+        for (int i = 0; i < kWaves; ++i) t += s_wave[i];
         pre[c.B] = t;
     }
     __syncthreads();
@@ -225,20 +227,20 @@ __global__ __launch_bounds__(256) void select_draft_kernel(SelectDraftArgs a) {
 // to 64 rows with one load (the first batch, jv0, comes in prefetched), then
 // scores G rows at a time with all their loads in flight.  `best` collects the
 // wave's best key.
-template <int G>
+template <int G, int kW>
 __device__ void score_rows(const RankHiddenArgs &a, int b, int64_t T, bool seq_ok,
                            const uint16_t *Hb, const uint4 *q_s, float qq, uint32_t first,
                            uint32_t end, uint32_t seq_start, int32_t jv0, uint64_t &best) {
     const RankCommon &c = a.c;
     const int lane = lane_id();
     const int nch = a.d / 8;
-    const uint32_t n = end > first ? (end - first + kRankWaves - 1) / kRankWaves : 0;
+    const uint32_t n = end > first ? (end - first + kW - 1) / kW : 0;
     for (uint32_t base = 0; base < n; base += kWave) {
         const uint32_t nb = min((uint32_t)kWave, n - base);
         const uint32_t mine = base + lane;
         int32_t jv = jv0;   // the first batch was requested with the query row
         if (base > 0 && mine < n)
-            jv = c.cand_pos[(int64_t)b * c.cap + (first + mine * kRankWaves - seq_start)];
+            jv = c.cand_pos[(int64_t)b * c.cap + (first + mine * kW - seq_start)];
         for (uint32_t r = 0; r < nb; r += G) {
             const uint4 *rows[G];
             int32_t js[G];
@@ -268,21 +270,61 @@ __device__ void score_rows(const RankHiddenArgs &a, int b, int64_t T, bool seq_o
                 }
                 if (c.scores && lane == 0)
                     c.scores[(int64_t)b * c.cap +
-                             (first + (base + r + g) * kRankWaves - seq_start)] = s;
+                             (first + (base + r + g) * kW - seq_start)] = s;
             }
         }
     }
 }
 
-__global__ __launch_bounds__(kRankThreads) void rank_hidden_kernel(RankHiddenArgs a) {
+// The same for rows of d = 1024 * kU: the wave's rows stream through
+// stream_rows' two-deep pipeline, two pieces per row (same bits as score_rows).
+template <int kU, int kW>
+__device__ void score_rows_stream(const RankHiddenArgs &a, int b, int64_t T, bool seq_ok,
+                                  const uint16_t *Hb, const uint4 *q_s, float qq, uint32_t first,
+                                  uint32_t end, uint32_t seq_start, int32_t jv0, uint64_t &best) {
+    const RankCommon &c = a.c;
+    const int lane = lane_id();
+    const uint32_t n = end > first ? (end - first + kW - 1) / kW : 0;
+    for (uint32_t base = 0; base < n; base += kWave) {
+        const uint32_t nb = min((uint32_t)kWave, n - base);
+        const uint32_t mine = base + lane;
+        int32_t jv = jv0;   // the first batch was requested with the query row
+        if (base > 0 && mine < n)
+            jv = c.cand_pos[(int64_t)b * c.cap + (first + mine * kW - seq_start)];
+        auto row = [&](int k) -> const uint4 * {
+            const int32_t j = __builtin_amdgcn_readlane(jv, k);
+            const bool ok = seq_ok && j >= 1 && (int64_t)j <= T - 2;
+            return ok ? reinterpret_cast<const uint4 *>(Hb + (int64_t)(j - 1) * a.hr) : nullptr;
+        };
+        stream_rows<2, kU>((int)nb, row, q_s,
+                                            [&](int k, bool ok, float dot, float nrm) {
+            float s = __builtin_nanf("");
+            if (ok) {
+                s = cosine(dot, nrm, qq);
+                if (s > c.threshold) {
+                    const uint64_t key = rank_key(s, __builtin_amdgcn_readlane(jv, k));
+                    best = key > best ? key : best;
+                }
+            }
+            if (c.scores && lane == 0)
+                c.scores[(int64_t)b * c.cap + (first + (base + k) * kW - seq_start)] = s;
+        });
+    }
+}
+
+// kU > 0: rows of d = 1024 * kU through the streaming pipeline; 0: any d
+// through score_rows (one instantiation per path keeps each kernel's register
+// count to what its path needs).
+template <int kU, int kW>
+__global__ __launch_bounds__(kW * kWave) void rank_hidden_kernel(RankHiddenArgs a) {
     extern __shared__ uint4 smem[];
-    __shared__ uint64_t s_best[kRankWaves];
+    __shared__ uint64_t s_best[kW];
     const RankCommon &c = a.c;
     const int nch = a.d / 8;
     uint4 *q_s = smem;                                         // nch chunks of 8 bf16
     uint32_t *pre = reinterpret_cast<uint32_t *>(smem + nch);  // B + 1
     int32_t *lens = reinterpret_cast<int32_t *>(pre + c.B + 1); // B
-    candidate_prefix(c, pre, lens);
+    candidate_prefix<kW * kWave>(c, pre, lens);
     uint32_t lo0, hi;
     block_share(pre[c.B], blockIdx.x, lo0, hi);
     const int w = threadIdx.x / kWave;
@@ -298,26 +340,28 @@ __global__ __launch_bounds__(kRankThreads) void rank_hidden_kernel(RankHiddenArg
         const uint16_t *Hb = a.hidden + (int64_t)b * a.hs;
         // the wave's first 64 candidate positions and the query row travel together
         const uint32_t first = lo + w;
-        const uint32_t nw = seg_hi > first ? (seg_hi - first + kRankWaves - 1) / kRankWaves : 0;
+        const uint32_t nw = seg_hi > first ? (seg_hi - first + kW - 1) / kW : 0;
         const int32_t jv0 = (uint32_t)lane < nw
-            ? c.cand_pos[(int64_t)b * c.cap + (first + (uint32_t)lane * kRankWaves - pre[b])] : 0;
+            ? c.cand_pos[(int64_t)b * c.cap + (first + (uint32_t)lane * kW - pre[b])] : 0;
         if (seq_ok) copy_to_lds(reinterpret_cast<const uint4 *>(Hb + (T - 2) * a.hr), q_s, nch);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
-        float qdot = 0.f, qq = 0.f;
-        if (seq_ok) row_dot<false>(q_s, q_s, nch, qdot, qq);
+        const float qq = seq_ok ? query_norm(q_s, nch) : 0.f;
         uint64_t best = 0;
-        if (nch <= 4 * kWave)
-            score_rows<4>(a, b, T, seq_ok, Hb, q_s, qq, first, seg_hi, pre[b], jv0, best);
+        if constexpr (kU > 0)
+            score_rows_stream<kU, kW>(a, b, T, seq_ok, Hb, q_s, qq, first, seg_hi, pre[b], jv0,
+                                       best);
+        else if (nch <= 4 * kWave)
+            score_rows<4, kW>(a, b, T, seq_ok, Hb, q_s, qq, first, seg_hi, pre[b], jv0, best);
         else if (nch <= 8 * kWave)
-            score_rows<2>(a, b, T, seq_ok, Hb, q_s, qq, first, seg_hi, pre[b], jv0, best);
+            score_rows<2, kW>(a, b, T, seq_ok, Hb, q_s, qq, first, seg_hi, pre[b], jv0, best);
         else
-            score_rows<1>(a, b, T, seq_ok, Hb, q_s, qq, first, seg_hi, pre[b], jv0, best);
+            score_rows<1, kW>(a, b, T, seq_ok, Hb, q_s, qq, first, seg_hi, pre[b], jv0, best);
         if (lane == 0) s_best[w] = best;
         __syncthreads();                                       // also: q_s is restaged next
         if (threadIdx.x == 0) {
             uint64_t k = s_best[0];
-            for (int i = 1; i < kRankWaves; ++i) k = s_best[i] > k ? s_best[i] : k;
+            for (int i = 1; i < kW; ++i) k = s_best[i] > k ? s_best[i] : k;
             if (k)
                 atomicMax((unsigned long long *)&c.keys[(int64_t)b * kKeySlots +
                                                         (blockIdx.x % kKeySlots)],
@@ -431,11 +475,21 @@ static int prep_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stri
 
 // The ranking grids are persistent: as many blocks as fit on the device at
 // once, each taking an equal contiguous share of the flattened candidates.
+template <int kU, int kW>
+static void launch_hidden_as(const RankHiddenArgs &a, size_t lds, hipStream_t s) {
+    const void *k = reinterpret_cast<const void *>(&rank_hidden_kernel<kU, kW>);
+    const int grid = resident_blocks(k, kW * kWave, lds) * PLD_RANK_OVERSUB;
+    hipLaunchKernelGGL((rank_hidden_kernel<kU, kW>), dim3(grid), dim3(kW * kWave), lds, s, a);
+}
+
 static void launch_hidden(const RankHiddenArgs &a, hipStream_t s) {
     const size_t lds = (size_t)(a.d / 8) * sizeof(uint4) + (size_t)(2 * a.c.B + 1) * sizeof(uint32_t);
-    const int grid = resident_blocks(reinterpret_cast<const void *>(&rank_hidden_kernel),
-                                     kRankThreads, lds) * PLD_RANK_OVERSUB;
-    hipLaunchKernelGGL(rank_hidden_kernel, dim3(grid), dim3(kRankThreads), lds, s, a);
+    if (a.d == 4096)
+        launch_hidden_as<4, kRankWaves>(a, lds, s);
+    else if (a.d == 8192)
+        launch_hidden_as<8, kRankWaves>(a, lds, s);
+    else
+        launch_hidden_as<0, kRankWaves>(a, lds, s);
 }
 
 static void launch_attn(const RankAttnArgs &a, hipStream_t s) {

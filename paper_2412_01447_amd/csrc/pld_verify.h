@@ -20,9 +20,14 @@ namespace pld {
 #define PLD_VERIFY_TARGET_BLOCKS 2048    // split-row kernel: blocks to aim for
 #endif
 
+#ifndef PLD_ARGMAX_UNROLL
+#define PLD_ARGMAX_UNROLL 11         // 16-byte loads per thread per batch of the argmax
+#endif
+
 constexpr int kVerifyThreads = 256;
 constexpr int kVerifyWaves = kVerifyThreads / kWave;
-constexpr int kVerifyUnroll = PLD_VERIFY_UNROLL;
+constexpr int kVerifyUnroll = PLD_VERIFY_UNROLL;   // sampling statistics (its segment size)
+constexpr int kArgmaxUnroll = PLD_ARGMAX_UNROLL;
 
 struct VerifyArgs {
     const void *logits;

@@ -55,9 +55,9 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArg
     // The first batch of this thread's vectors is requested together with the
     // draft length (every row of the buffer exists, so the loads are in
     // bounds); a row past the draft then returns without reading further.
-    uint4 r[kVerifyUnroll];
+    uint4 r[kArgmaxUnroll];
 #pragma unroll
-    for (int u = 0; u < kVerifyUnroll; ++u) {
+    for (int u = 0; u < kArgmaxUnroll; ++u) {
         const int64_t vi = my_v + (int64_t)u * kVerifyThreads;
         if (vi < v1) r[u] = ld_stream(vec + vi);
     }
@@ -81,16 +81,16 @@ __global__ __launch_bounds__(kVerifyThreads) void verify_argmax_kernel(VerifyArg
         const float f = E::get(row, threadIdx.x);
         if (f > best) best = f;
     }
-    for (int64_t vb = my_v; vb < v1; vb += (int64_t)kVerifyThreads * kVerifyUnroll) {
+    for (int64_t vb = my_v; vb < v1; vb += (int64_t)kVerifyThreads * kArgmaxUnroll) {
         if (vb != my_v) {
 #pragma unroll
-            for (int u = 0; u < kVerifyUnroll; ++u) {
+            for (int u = 0; u < kArgmaxUnroll; ++u) {
                 const int64_t vi = vb + (int64_t)u * kVerifyThreads;
                 if (vi < v1) r[u] = ld_stream(vec + vi);
             }
         }
 #pragma unroll
-        for (int u = 0; u < kVerifyUnroll; ++u) {
+        for (int u = 0; u < kArgmaxUnroll; ++u) {
             const int64_t vi = vb + (int64_t)u * kVerifyThreads;
             if (vi < v1) {
                 float f[P];
@@ -255,11 +255,21 @@ int prep_verify(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_r
     if (rc != PLD_OK) return rc;
     const size_t esz = dtype == PLD_F32 ? 4 : 2;
     if (!workspace || workspace_bytes < verify_ws_bytes(B, K)) return PLD_ERR_WORKSPACE;
-    // Blocks per row: enough for ~2048 blocks in flight, but each block keeps
-    // at least two 16-byte vectors per thread.
+    // Blocks per row.  When every block can take its share of a row in one
+    // batch of loads with the whole grid resident at once, as many blocks per
+    // row as fit on the GPU together (a grid a little larger than what is
+    // resident would run its last blocks in a second round, one whole block
+    // duration later); otherwise, for rows that need several batches per
+    // thread anyway, about PLD_VERIFY_TARGET_BLOCKS blocks in all.  Each
+    // block keeps at least two 16-byte vectors per thread.
     const int64_t rows = (int64_t)B * (K + 1);
     const int64_t nvec = (int64_t)V * esz / 16;
+    const void *kern = dtype == PLD_F32
+        ? reinterpret_cast<const void *>(&verify_argmax_kernel<0>)
+        : reinterpret_cast<const void *>(&verify_argmax_kernel<1>);
+    const int64_t fit = resident_blocks(kern, kVerifyThreads, 0) / rows;
     int64_t S = (PLD_VERIFY_TARGET_BLOCKS + rows - 1) / rows;
+    if (fit >= 1 && (nvec + fit - 1) / fit <= (int64_t)kArgmaxUnroll * kVerifyThreads) S = fit;
     const int64_t smax = nvec / (2 * kVerifyThreads);
     if (S > smax) S = smax;
     if (S < 1) S = 1;
