@@ -25,8 +25,10 @@ ranking kernel's (the hidden-state scoring when there is one, else the
 attention scoring, else the one-call drafting); `rooflines_other` holds the
 others.  With --gate (the default) the other two of the three largest
 workloads (configs 3, 4, 5) are measured as well, in the same run, and their
-ranking and verification fractions of peak are reported under `gate`.  One
-JSON line goes to stdout.
+ranking and verification fractions of peak are reported under `gate` (configs
+3 and 5 both as their steps run -- the one-call drafting -- and with the
+separate calls, where the ranking kernel is a launch of its own).  One JSON
+line goes to stdout.
 
 The CPU oracle (test infrastructure) is timed on the host on the same inputs
 as a reported baseline, unless --no-cpu-baseline.
@@ -390,17 +392,21 @@ def main():
     if args.gate and not args.warm:
         # the other two of the three largest workloads, measured in the same run
         # (their own step configuration, fewer steps, no CPU baseline): the
-        # fractions of peak of their ranking and verification kernels
+        # fractions of peak of their ranking and verification kernels.  Their
+        # steps draft with the one-call drafting, whose launch also finds the
+        # occurrences and is followed by its finishing launch; each is also
+        # run with the separate calls, where the ranking kernel is timed alone.
         m.pop("w"), m.pop("z"), m.pop("step")
         torch.cuda.empty_cache()
         gate = {}
-        for cid in (3, 4, 5):
-            if cid == args.config:
+        runs = [(3, None), (3, "split"), (4, None), (5, None), (5, "split")]
+        for cid, mode in runs:
+            if cid == args.config and mode is None:
                 g = m
             else:
-                g = measure(synth.CONFIGS[cid], args, log, steps=args.gate_steps,
+                g = measure(synth.CONFIGS[cid], args, log, mode=mode, steps=args.gate_steps,
                             warmup=args.gate_steps // 10 + 5)
-            gate[f"config{cid}"] = {
+            gate[f"config{cid}" + ("_separate_calls" if mode == "split" else "")] = {
                 "workload": synth.CONFIGS[cid].name, "us_per_step": round(g["us_per_step"], 2),
                 "drafting": "one call" if g["fused"] else "separate calls",
                 **{n: {"avg_us": r["avg_us"], "GBps": r["achieved"], "frac": r["frac"],

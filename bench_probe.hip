@@ -12,6 +12,8 @@
 //   columns  one 4-byte value from each of 64 rows 64 KB apart per lane, for
 //            285 random columns of each of 64 sequences (the attention gathers
 //            of the b64 workload); bytes counted as distinct 128-byte lines
+//   gather_b32_tripsN  the attention gathers of the b32 x 8192 workload (~10 MB
+//            of distinct lines) behind N = 1, 2 or 3 dependent trips to memory
 //   strideS  4M 4-byte reads S bytes apart (S = 32 .. 512), consecutive lanes
 //            on consecutive addresses: the time per read shows the granule the
 //            memory system fetches for scattered 4-byte loads
@@ -84,6 +86,47 @@ __global__ __launch_bounds__(256) void columns_kernel(const float *buf, int R, i
         for (int u = 0; u < 32; ++u) acc += v[u];
     }
     if (acc == 12345.f) sink[i] = acc;
+}
+
+// The attention gathers of the b32 x 8192 workload (40 rows of 8192 keys per
+// sequence, ~80 candidate columns each, ~10 MB of distinct 128-byte lines),
+// with kTrips dependent trips to memory in the launch: 1 -- the columns are
+// computed in registers; 2 -- read from a list first (the positions); 3 -- a
+// per-sequence count read before the list (the counts, then the positions).
+// A group of 8 lanes per column, lane t reading rows t, t+8, ... as the
+// ranking kernels do.  The launch time against the bytes gives the fastest a
+// single launch of this dependency structure can read them.
+__device__ __forceinline__ int hashed_column(int s, int k, int N) {
+    unsigned h = (unsigned)(s * 131071 + k * 8191 + 12345) * 2654435761u;
+    return (int)((h >> 7) % (unsigned)(N - 1));
+}
+
+template <int kTrips>
+__global__ __launch_bounds__(256) void gather_kernel(const float *buf, int R, int N, const int *col,
+                                                     const int *count, int C, int S, float *sink) {
+    const int g = (int)((blockIdx.x * blockDim.x + threadIdx.x) >> 3);
+    const int t = threadIdx.x & 7;
+    if (g >= S * C) return;
+    const int s = g / C, k = g % C;
+    int c;
+    if constexpr (kTrips == 1) {
+        c = hashed_column(s, k, N);
+    } else if constexpr (kTrips == 2) {
+        c = col[g];
+    } else {
+        const int n = count[s];
+        c = k < n ? col[g] : 0;
+    }
+    const float *p = buf + (size_t)s * R * N + c;
+    float v[8], acc = 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+        const int r = t + 8 * u;
+        v[u] = r < R ? p[(size_t)r * N] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
+    if (acc == 12345.f) sink[g] = acc;
 }
 
 __global__ __launch_bounds__(256) void strided_kernel(const float *p, size_t stride, float *sink) {
@@ -194,6 +237,47 @@ int main() {
                                reinterpret_cast<float *>(sink));
         }, nsets);
         report("columns", (double)lines * R * 128, us);
+    }
+    {   // the b32 x 8192 attention gathers: 1, 2 and 3 dependent trips per launch
+        const int S = 32, R = 40, N = 8192, C = 80;
+        const size_t n = (size_t)S * R * N;   // 42 MB per copy; 8 copies rotate past the LLC
+        std::vector<int> h((size_t)S * C), cnt(S, C);
+        size_t lines = 0;
+        for (int s = 0; s < S; ++s) {
+            std::vector<int> lk;
+            for (int k = 0; k < C; ++k) {
+                const unsigned hh = (unsigned)(s * 131071 + k * 8191 + 12345) * 2654435761u;
+                h[(size_t)s * C + k] = (int)((hh >> 7) % (unsigned)(N - 1));
+                lk.push_back(h[(size_t)s * C + k] / 32);
+            }
+            std::sort(lk.begin(), lk.end());
+            lines += (size_t)(std::unique(lk.begin(), lk.end()) - lk.begin());
+        }
+        int *dcnt;
+        CK(hipMalloc(&dcnt, S * sizeof(int)));
+        CK(hipMemcpy(didx, h.data(), h.size() * sizeof(int), hipMemcpyHostToDevice));
+        CK(hipMemcpy(dcnt, cnt.data(), S * sizeof(int), hipMemcpyHostToDevice));
+        const float *fb = reinterpret_cast<const float *>(buf);
+        const unsigned blocks = (unsigned)((S * C * 8 + 255) / 256);
+        for (int trips = 1; trips <= 3; ++trips) {
+            const double us = time_us([&](int r) {
+                const float *src = fb + (size_t)r * n;
+                float *sk = reinterpret_cast<float *>(sink);
+                if (trips == 1)
+                    hipLaunchKernelGGL(gather_kernel<1>, dim3(blocks), dim3(256), 0, 0, src, R, N,
+                                       didx, dcnt, C, S, sk);
+                else if (trips == 2)
+                    hipLaunchKernelGGL(gather_kernel<2>, dim3(blocks), dim3(256), 0, 0, src, R, N,
+                                       didx, dcnt, C, S, sk);
+                else
+                    hipLaunchKernelGGL(gather_kernel<3>, dim3(blocks), dim3(256), 0, 0, src, R, N,
+                                       didx, dcnt, C, S, sk);
+            }, 8);
+            char name[32];
+            std::snprintf(name, sizeof(name), "gather_b32_trips%d", trips);
+            report(name, (double)lines * R * 128, us);
+        }
+        CK(hipFree(dcnt));
     }
     for (int stride : {32, 64, 128, 256, 512}) {   // 4M reads, spans of 128 MB to 2 GB
         const size_t reads = (size_t)1 << 22, threads = reads / 8;

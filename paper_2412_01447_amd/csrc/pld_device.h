@@ -22,7 +22,10 @@ constexpr int kFindTile = 2048;          // positions per block, multi-block fin
 constexpr int kFindWavesTiled = 4;       // 256 threads, 512 positions per wave
 constexpr int kFindWavesFused = 16;      // 1024 threads, one block per sequence
 constexpr int kFindFusedMax = kFindWavesFused * 512;  // tok_stride <= 8192: fused path
-constexpr int kFindFusedPasses = 2;   // the one-block search takes tok_stride <= 16384
+#ifndef PLD_FIND_FUSED_PASSES
+#define PLD_FIND_FUSED_PASSES 2
+#endif
+constexpr int kFindFusedPasses = PLD_FIND_FUSED_PASSES;   // one-block search: tok_stride <= 16384
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 

@@ -118,9 +118,9 @@ __device__ void candidate_prefix(const RankCommon &c, uint32_t *pre, int32_t *s_
     __syncthreads();
 }
 
-// Block k's share [lo, hi) of n items split evenly over the grid (32-bit).
-__device__ __forceinline__ void block_share(uint32_t n, uint32_t k, uint32_t &lo, uint32_t &hi) {
-    const uint32_t g = gridDim.x;
+// Block k's share [lo, hi) of n items split evenly over g blocks (32-bit).
+__device__ __forceinline__ void block_share(uint32_t n, uint32_t k, uint32_t &lo, uint32_t &hi,
+                                            uint32_t g) {
     const uint32_t q = n / g, r = n % g;
     lo = k * q + min(k, r);
     hi = lo + q + (k < r ? 1u : 0u);
@@ -134,11 +134,12 @@ __device__ __forceinline__ void block_share(uint32_t n, uint32_t k, uint32_t &lo
 // lines stay in one L2) while the runs of all XCDs interleave along the list
 // (every XCD sees the same mix of cheap and costly candidates; one contiguous
 // eighth per XCD was measured slower).  Blocks past the last whole group of
-// 8m keep their own index.  A permutation: the results do not depend on it.
+// 8m of the first g blocks keep their own index.  A permutation of [0, g)
+// (and of the blocks past it): the results do not depend on it.
 constexpr uint32_t kXcds = 8, kXcdRun = 16;
-__device__ __forceinline__ uint32_t xcd_run_index(uint32_t k) {
+__device__ __forceinline__ uint32_t xcd_run_index(uint32_t k, uint32_t g) {
     const uint32_t group = kXcds * kXcdRun;
-    if (k >= gridDim.x / group * group) return k;
+    if (k >= g / group * group) return k;
     const uint32_t x = k % kXcds, i = k / kXcds;
     return (i / kXcdRun) * group + x * kXcdRun + i % kXcdRun;
 }
@@ -326,7 +327,7 @@ __global__ __launch_bounds__(kW * kWave) void rank_hidden_kernel(RankHiddenArgs 
     int32_t *lens = reinterpret_cast<int32_t *>(pre + c.B + 1); // B
     candidate_prefix<kW * kWave>(c, pre, lens);
     uint32_t lo0, hi;
-    block_share(pre[c.B], blockIdx.x, lo0, hi);
+    block_share(pre[c.B], blockIdx.x, lo0, hi, gridDim.x);
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     if (lo0 >= hi) return;   // block-uniform: nothing to score
@@ -372,14 +373,29 @@ __global__ __launch_bounds__(kW * kWave) void rank_hidden_kernel(RankHiddenArgs 
 }
 
 // ------------------------------------------------------------------ attn
+#ifndef PLD_ATTN_MIN_SHARE
+#define PLD_ATTN_MIN_SHARE 8         // candidates per active attention block (tuning builds)
+#endif
+constexpr uint32_t kAttnMinShare = PLD_ATTN_MIN_SHARE;
+// Only as many blocks as give every block at least kAttnMinShare candidates
+// (a wave's pass: one per lane group) take shares; the rest return after the
+// prefix.  With few candidates in all, a share per resident block would leave
+// most blocks with one or two candidates, each paying the whole prologue
+// (measured: 9.5 -> 7.5 us on 32 x 8192 with 40 rows; 8 per block was faster
+// than 16 or 32, and the 64 x 16384 workload, with more candidates than
+// 8 per resident block, keeps every block).
 __global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a) {
     __shared__ uint32_t pre[PLD_MAX_BATCH + 1];
     const RankCommon &c = a.c;
     candidate_prefix(c, pre);
-    uint32_t lo, hi;
-    block_share(pre[c.B], xcd_run_index(blockIdx.x), lo, hi);
     // a group of kGatherLanes lanes per candidate
     constexpr uint32_t kPerPass = kRankThreads / kGatherLanes;
+    const uint32_t total = pre[c.B];
+    const uint32_t active = min(gridDim.x, (total + kAttnMinShare - 1) / kAttnMinShare);
+    const uint32_t k = xcd_run_index(blockIdx.x, active);
+    if (k >= active) return;   // block-uniform
+    uint32_t lo, hi;
+    block_share(total, k, lo, hi, active);
     for (uint32_t base = lo; base < hi; base += kPerPass) {
         const uint32_t i = base + threadIdx.x / kGatherLanes;
         const bool active = i < hi;
