@@ -24,9 +24,10 @@ workloads (arXiv 2412.01447, Sec. 5.1: outputs that copy spans of their input):
 * uniforms -- the draws of sampling verification, U[0, 1) fp32 [B][K+1].
 * decoding tasks (DECODE_TASKS) -- for the multi-step loop: target sequences
   (the token generator's output, whose last quarter is the continuation to
-  generate), hidden states that embed each position's last few tokens, and a
-  stand-in target model whose greedy choice at every position is the target
-  token, so that greedy decoding reproduces the target whatever the drafts.
+  generate; or sectioned documents copied with edits), hidden states that embed each
+  position's last few tokens (a decaying window), and a stand-in target model
+  whose greedy choice at every position is the target token, so that greedy
+  decoding reproduces the target whatever the drafts.
 
 Seeds are numpy SeedSequence([seed, b, stream]) per sequence and stream, so a
 sequence can be regenerated alone.
@@ -45,6 +46,8 @@ STREAM_HIDDEN = 5
 STREAM_UNIFORMS = 6
 STREAM_CONTEXT = 7
 STREAM_MODEL = 8
+STREAM_EDIT = 9
+STREAM_SECTIONS = 10
 
 
 @dataclasses.dataclass(frozen=True)
@@ -347,7 +350,9 @@ class DecodeTask:
     """A multi-step decoding run: B target sequences of length T whose last
     quarter is generated step by step, starting from the first three quarters
     (the prompt); a stated fraction of the generated part copies spans of the
-    prompt (input-guided generation, Sec. 5.1)."""
+    prompt (input-guided generation, Sec. 5.1), or, for a sectioned task
+    (header > 0), the prompt is a run of sections and the generated part an
+    edited copy of consecutive ones (span then gives the body lengths)."""
     name: str
     B: int
     T: int
@@ -361,6 +366,8 @@ class DecodeTask:
     window: int = 4       # hidden state of position p: decaying sum over x[p-window+1 .. p]
     decay: float = 0.5
     noise: float = 0.25
+    edit_rate: float = 0.0   # sectioned tasks: chance that a copied token is replaced
+    header: int = 0          # > 0: a sectioned task (make_sections) with a header this long
 
 
 DECODE_TASKS = {
@@ -370,7 +377,54 @@ DECODE_TASKS = {
     # a batch of eight, longer contexts, K = 16
     "b8_t4096_copy50_k16": DecodeTask("b8_t4096_copy50_k16", 8, 4096, 32000, 1.1, 0.5, (8, 64),
                                       4096, 16, 22),
+    # Sectioned documents copied with edits, the situation of the Fig. 3
+    # caption.  The input is a run of sections that all start with the same
+    # 8-token header (as functions or lines of code start alike) followed by
+    # 24-56 Zipf tokens; the output copies consecutive sections from a random
+    # one, one copied token in ten replaced (an edit).  The hidden states carry
+    # a decaying window of the last 32 tokens.  After an edit, the drafter has
+    # to find its place again: the last tokens, often header tokens, occur in
+    # every section, and prompt lookup takes the earliest of the equally long
+    # matches, while the hidden state still resembles the one at the true source.
+    "b1_t1024_sections_edit10_k10": DecodeTask("b1_t1024_sections_edit10_k10", 1, 1024, 32000,
+                                               1.1, 0.0, (24, 56), 4096, 10, 23, window=32,
+                                               decay=0.85, edit_rate=0.1, header=8),
+    "b8_t4096_sections_edit10_k16": DecodeTask("b8_t4096_sections_edit10_k16", 8, 4096, 32000,
+                                               1.1, 0.0, (24, 56), 4096, 16, 24, window=32,
+                                               decay=0.85, edit_rate=0.1, header=8),
 }
+
+
+def make_sections(task: "DecodeTask") -> np.ndarray:
+    """Targets [B][T] of a sectioned task: the first T - T/4 tokens are sections
+    (the header, then a body of task.span[0]..task.span[1] Zipf tokens); the last
+    T/4 copy consecutive sections from a random one, with each copied token
+    replaced by a fresh Zipf token with probability task.edit_rate."""
+    cdf = zipf_cdf(task.V, task.zipf_s)
+    T = task.T
+    P = T - T // 4
+    out = np.zeros((task.B, T), np.int32)
+    for b in range(task.B):
+        rng = rng_for(task.seed, b, STREAM_SECTIONS)
+        header = zipf_tokens(rng, task.header, cdf)
+        starts, x = [], []
+        while len(x) < P:
+            starts.append(len(x))
+            body = int(rng.integers(task.span[0], task.span[1] + 1))
+            x.extend(header.tolist())
+            x.extend(zipf_tokens(rng, body, cdf).tolist())
+        x = x[:P]
+        edit = rng_for(task.seed, b, STREAM_EDIT)
+        src = starts[int(rng.integers(0, max(1, len(starts) - 8)))]
+        gen = []
+        while len(gen) < T - P:
+            t = x[src % P]
+            if edit.random() < task.edit_rate:
+                t = int(zipf_tokens(edit, 1, cdf)[0])
+            gen.append(t)
+            src += 1
+        out[b] = np.array(x + gen, np.int32)
+    return out
 
 
 def make_context_hidden(tokens: np.ndarray, d: int, seed: int, window: int = 4,
@@ -398,8 +452,11 @@ def make_context_hidden(tokens: np.ndarray, d: int, seed: int, window: int = 4,
 def make_decode_task(task: DecodeTask, device="cpu"):
     """Targets (host int32 [B][T]), the prompt length per sequence (host int32),
     and the loop's hidden states (device bf16 [B][T][d])."""
-    toks, lens, metas = make_tokens(task.B, task.T, task.V, task.zipf_s, task.plant_frac,
-                                    task.span, task.seed)
+    if task.header > 0:
+        toks, metas = make_sections(task), None
+    else:
+        toks, lens, metas = make_tokens(task.B, task.T, task.V, task.zipf_s, task.plant_frac,
+                                        task.span, task.seed)
     start = np.full(task.B, task.T - task.T // 4, np.int32)
     hidden = make_context_hidden(toks, task.d, task.seed, task.window, task.decay, task.noise,
                                  device)

@@ -173,7 +173,11 @@ LOOPS = [("b1_t1024_copy60_k10", "hidden", None, (1, 1)),
          ("b1_t1024_copy60_k10", "prefix", 3, (1, 3)),
          ("b1_t1024_copy60_k10", "prefix", 64, (1, 1)),
          ("b8_t4096_copy50_k16", "hidden", None, (1, 1)),
-         ("b8_t4096_copy50_k16", "prefix", 3, (1, 3))]
+         ("b8_t4096_copy50_k16", "prefix", 3, (1, 3)),
+         ("b1_t1024_sections_edit10_k10", "hidden", None, (1, 1)),
+         ("b1_t1024_sections_edit10_k10", "prefix", 3, (1, 3)),
+         ("b8_t4096_sections_edit10_k16", "hidden", None, (1, 1)),
+         ("b8_t4096_sections_edit10_k16", "prefix", 64, (1, 1))]
 
 
 @pytest.mark.parametrize("task_name,ranking,max_match,ngram", LOOPS,
