@@ -69,7 +69,7 @@ def parse():
     p.add_argument("--gate", action=argparse.BooleanOptionalAction, default=True,
                    help="also measure the ranking and verification kernels of the three "
                         "largest workloads (configs 3, 4, 5) in the same run (default on)")
-    p.add_argument("--gate-steps", type=int, default=100,
+    p.add_argument("--gate-steps", type=int, default=200,
                    help="timed steps of each extra workload of --gate")
     p.add_argument("--split", type=int, default=0,
                    help="blocks per sequence of the one-call drafting (default: from the "
@@ -405,12 +405,13 @@ def main():
                 g = m
             else:
                 g = measure(synth.CONFIGS[cid], args, log, mode=mode, steps=args.gate_steps,
-                            warmup=args.gate_steps // 10 + 5)
+                            warmup=args.warmup)
             gate[f"config{cid}" + ("_separate_calls" if mode == "split" else "")] = {
                 "workload": synth.CONFIGS[cid].name, "us_per_step": round(g["us_per_step"], 2),
                 "drafting": "one call" if g["fused"] else "separate calls",
-                **{n: {"avg_us": r["avg_us"], "GBps": r["achieved"], "frac": r["frac"],
-                       "bytes": r["bytes_per_launch"]} for n, r in g["calls"].items()}}
+                **{n: {"avg_us": r["avg_us"], "p50_us": r["p50_us"], "GBps": r["achieved"],
+                       "frac": r["frac"], "bytes": r["bytes_per_launch"]}
+                   for n, r in g["calls"].items()}}
             if g is not m:
                 del g
                 torch.cuda.empty_cache()
