@@ -2,7 +2,7 @@
 """Benchmark of the PLD+ drafting step (find -> rank -> emit -> verify) on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--config C] [--verify greedy|sample]
-                    [--temperature T] [--mode auto|fused|split] [--split S] [--warm]
+                    [--temperature T] [--mode auto|fused|split|split_sep] [--split S] [--warm]
                     [--no-cpu-baseline] [--no-gate] [--copy-probe]
     python bench.py --loop TASK        # the generation loop, once per ranking
     python bench.py --probe            # bandwidth ceilings of the access patterns
@@ -19,15 +19,17 @@ addresses and consecutive steps rotate through them, so every step reads from
 HBM rather than from the 256 MB last-level cache.  W untimed steps run first,
 then exactly K steps are timed between two device synchronisations; HIP
 events on the launch stream bracket the ranking kernel, the attention
-scoring (when the step ranks by both artifacts) and the verification argmax,
-each on one step in eight, in turn (--event-every).  `roofline` is the
-ranking kernel's (the hidden-state scoring when there is one, else the
-attention scoring, else the one-call drafting); `rooflines_other` holds the
-others.  With --gate (the default) the other two of the three largest
+scoring (when the step ranks by both artifacts in launches of their own) and
+the verification argmax, each on one step in eight, in turn (--event-every).
+`roofline` is the ranking kernel's (both scorings in one launch when the step
+ranks by both artifacts, else the hidden-state scoring when there is one, else
+the attention scoring, else the one-call drafting); `rooflines_other` holds
+the others.  With --gate (the default) the other two of the three largest
 workloads (configs 3, 4, 5) are measured as well, in the same run, and their
 ranking and verification fractions of peak are reported under `gate` (configs
 3 and 5 both as their steps run -- the one-call drafting -- and with the
-separate calls, where the ranking kernel is a launch of its own).  One JSON
+separate calls, where the ranking kernel is a launch of its own; config 4 also
+with its two scorings in launches of their own).  One JSON
 line goes to stdout.
 
 The CPU oracle (test infrastructure) is timed on the host on the same inputs
@@ -74,8 +76,10 @@ def parse():
     p.add_argument("--split", type=int, default=0,
                    help="blocks per sequence of the one-call drafting (default: from the "
                         "first step's candidate counts)")
-    p.add_argument("--mode", choices=["auto", "fused", "split"], default="auto",
-                   help="drafting: one-launch call (fused), separate calls (split), or auto")
+    p.add_argument("--mode", choices=["auto", "fused", "split", "split_sep"], default="auto",
+                   help="drafting: one-launch call (fused), separate calls (split; with both "
+                        "artifacts the two scorings share a launch), separate calls with each "
+                        "scoring in a launch of its own (split_sep), or auto")
     p.add_argument("--verify", choices=["greedy", "sample"], default="greedy",
                    help="verification: argmax (greedy) or sampling at --temperature")
     p.add_argument("--temperature", type=float, default=1.0)
@@ -129,6 +133,7 @@ def algorithmic_bytes(cfg, lens, cand_count, draft_len, cand_pos, elt_logits, fu
 
 # kernels behind each timed call (names as rocprofv3 reports them)
 KERNELS = {"draft": "pld::draft_", "find": "pld::find_", "score_hidden": "pld::rank_hidden_kernel",
+           "score_both": "pld::rank_both_kernel",
            "score_attn": "pld::rank_attn_kernel", "select_draft": "pld::select_draft_kernel",
            "verify_argmax": "pld::verify_argmax_kernel", "verify_accept": "pld::verify_accept_kernel",
            "verify_sample_stats": "pld::sample_stats_kernel",
@@ -207,11 +212,20 @@ def measured_traffic(workload, call):
     return sum(hits) if hits else None
 
 
+def drafting_label(m):
+    """How a measured step drafted."""
+    if m["fused"]:
+        return f"one call, {m['draft_split']} block(s) per sequence"
+    if "score_both" in m["calls"]:
+        return "separate calls, both scorings in one launch"
+    return "separate calls"
+
+
 def ranking_call(names):
     """The call that holds the ranking kernel (Eq. 2 / Eq. 3): the hidden-state
     scoring when the step has one, else the attention scoring, else the one-call
     drafting (whose launch finds, ranks and selects)."""
-    for n in ("score_hidden", "score_attn", "draft"):
+    for n in ("score_both", "score_hidden", "score_attn", "draft"):
         if n in names:
             return n
     return None
@@ -250,7 +264,8 @@ def measure(cfg, args, log, mode=None, steps=None, warmup=None, cpu=False, cold=
     base = dict(tokens=torch.from_numpy(toks).to(dev), lens=torch.from_numpy(lens).to(dev),
                 logits=dev_logits(z), hidden=w["hidden"],
                 attn=torch.from_numpy(w["attn"]).to(dev) if w["attn"] is not None else None)
-    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, mode=mode)
+    step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, mode="split" if mode == "split_sep" else mode,
+                     rank_both=mode != "split_sep")
     fused = step.uses_fused(base["hidden"], base["attn"])
     sample = args.verify == "sample"
     if sample:
@@ -290,6 +305,8 @@ def measure(cfg, args, log, mode=None, steps=None, warmup=None, cpu=False, cold=
     plans = [step.plan(s_["tokens"], s_["lens"], s_["logits"], hidden=s_["hidden"],
                        attn=s_["attn"], stream=stream, **rank_args) for s_ in sets]
     names = [n for n, _ in plans[0]]
+    if "score_both" in names:   # both scorings in one launch
+        nbytes["score_both"] = nbytes.pop("score_hidden") + nbytes.pop("score_attn")
     assert set(names) == set(nbytes), (names, list(nbytes))
     rank = ranking_call(names)
     timed = [rank] + [n for n in ("score_attn",) if n in names and n != rank] + \
@@ -334,7 +351,8 @@ def measure(cfg, args, log, mode=None, steps=None, warmup=None, cpu=False, cold=
             f"({ach / HBM_PEAK_GBS:.3f} of peak)")
     out = {"cfg": cfg, "step": step, "fused": fused, "sample": sample, "copies": copies,
            "nbytes": nbytes, "step_bytes": step_bytes, "us_per_step": elapsed * 1e6 / steps,
-           "calls": calls, "rank": rank, "w": w, "z": z, "bf16": bf16}
+           "calls": calls, "rank": rank, "w": w, "z": z, "bf16": bf16,
+           "draft_split": step.draft_split}
     if cpu:
         out["cpu"] = cpu_baseline(cfg, w, z, bf16, args.cpu_seconds, log,
                                   (args.temperature, synth.make_uniforms(cfg.B, cfg.K, cfg.seed))
@@ -399,16 +417,17 @@ def main():
         m.pop("w"), m.pop("z"), m.pop("step")
         torch.cuda.empty_cache()
         gate = {}
-        runs = [(3, None), (3, "split"), (4, None), (5, None), (5, "split")]
+        runs = [(3, None), (3, "split"), (4, None), (4, "split_sep"), (5, None), (5, "split")]
         for cid, mode in runs:
             if cid == args.config and mode is None:
                 g = m
             else:
                 g = measure(synth.CONFIGS[cid], args, log, mode=mode, steps=args.gate_steps,
                             warmup=args.warmup)
-            gate[f"config{cid}" + ("_separate_calls" if mode == "split" else "")] = {
+            suffix = {"split": "_separate_calls", "split_sep": "_separate_rankings"}
+            gate[f"config{cid}" + suffix.get(mode, "")] = {
                 "workload": synth.CONFIGS[cid].name, "us_per_step": round(g["us_per_step"], 2),
-                "drafting": "one call" if g["fused"] else "separate calls",
+                "drafting": drafting_label(g),
                 **{n: {"avg_us": r["avg_us"], "p50_us": r["p50_us"], "GBps": r["achieved"],
                        "frac": r["frac"], "bytes": r["bytes_per_launch"]}
                    for n, r in g["calls"].items()}}
@@ -426,8 +445,7 @@ def main():
                    "attn_rows": cfg.R, "attn_aggregation": cfg.agg, "threshold": cfg.theta,
                    "K": cfg.K, "logits": cfg.logits,
                    "inputs": "hidden bf16, attention f32, tokens int32",
-                   "drafting": (f"one call, {step.draft_split} block(s) per sequence" if fused
-                                else "separate calls"),
+                   "drafting": drafting_label(m),
                    "verification": (f"sampling at temperature {args.temperature}" if sample
                                     else "greedy"),
                    "input_copies": m["copies"],

@@ -302,6 +302,32 @@ int pld_score_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stride
                    const int32_t *cand_count, int B, float threshold, float *scores,
                    void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * pld_score_both -- pld_score_hidden and pld_score_attn of the same occurrences
+ * in one launch (Eq. 2 and Eq. 3 side by side, as when both artifacts rank one
+ * candidate list): part of the grid gathers attention weights while the rest
+ * streams hidden rows, so the gathers overlap the stream instead of following
+ * it.  Scores and keys equal those of the two separate calls bit for bit.
+ *
+ *   hidden ... d       as pld_score_hidden
+ *   attn ... agg       as pld_score_attn
+ *   lens, cand_pos, cap, cand_count, B   the one candidate list both rank
+ *   threshold_h, threshold_a   each ranking's threshold
+ *   scores_h, scores_a         each ranking's scores, [B][cap] fp32 (may be NULL)
+ *   workspace_h, workspace_a   each ranking's keys: two distinct workspaces
+ *                   (the rules above); pld_select_draft with workspace_h and
+ *                   aux_workspace = workspace_a resolves both
+ * Errors: those of the two separate calls, checked in that order, and
+ * PLD_ERR_WORKSPACE when the two workspaces are the same buffer.
+ */
+int pld_score_both(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
+                   int64_t n_rows, int d, const float *attn, int64_t a_seq_stride,
+                   int64_t a_row_stride, int64_t n_keys, int R, int agg, const int32_t *lens,
+                   const int32_t *cand_pos, int64_t cap, const int32_t *cand_count, int B,
+                   float threshold_h, float threshold_a, float *scores_h, float *scores_a,
+                   void *workspace_h, size_t workspace_h_bytes, void *workspace_a,
+                   size_t workspace_a_bytes, void *stream);
+
 int pld_select_best(int B, int32_t *best_pos, float *best_score, void *workspace,
                     size_t workspace_bytes, void *stream);
 

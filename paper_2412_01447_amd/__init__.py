@@ -20,7 +20,7 @@ __all__ = [
     "pld_rank_hidden", "pld_rank_attn", "pld_emit_draft", "pld_verify_greedy",
     "pld_verify_greedy_noalloc", "NOALLOC_MAX_KEYS",
     "pld_draft_hidden", "pld_draft_attn", "pld_draft_workspace_bytes", "DRAFT_MAX_TOK_STRIDE",
-    "DRAFT_MAX_PART", "pld_score_hidden",
+    "DRAFT_MAX_PART", "pld_score_hidden", "pld_score_both",
     "pld_score_attn", "pld_select_best", "pld_select_draft", "pld_verify_argmax",
     "pld_verify_accept",
     "pld_verify_sample", "pld_verify_sample_workspace_bytes", "pld_verify_sample_stats",
@@ -67,6 +67,8 @@ _SIGNATURES = {
                           _sz, _vp], _int),
     "pld_score_attn": ([_vp, _i64, _i64, _i64, _int, _int, _vp, _vp, _i64, _vp, _int, _f32, _vp,
                         _vp, _sz, _vp], _int),
+    "pld_score_both": ([_vp, _i64, _i64, _i64, _int, _vp, _i64, _i64, _i64, _int, _int, _vp, _vp,
+                        _i64, _vp, _int, _f32, _f32, _vp, _vp, _vp, _sz, _vp, _sz, _vp], _int),
     "pld_select_best": ([_int, _vp, _vp, _vp, _sz, _vp], _int),
     "pld_select_draft": ([_vp, _i64, _vp, _int, _int, _vp, _vp, _vp, _vp, _vp, _sz, _vp, _sz, _vp,
                           _vp, _vp], _int),
@@ -402,6 +404,25 @@ def pld_score_attn(attn, lens, cand_pos, cand_count, workspace, agg=PLD_AGG_SUM,
     return _run("pld_score_attn", (_ptr(attn), attn.stride(0), attn.stride(1), n_keys, R, int(agg),
           _ptr(lens), _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), B, float(threshold),
           _ptr(scores), _ptr(workspace), _nbytes(workspace), _stream(stream),), prepare)
+
+
+def pld_score_both(hidden, attn, lens, cand_pos, cand_count, workspace_h, workspace_a,
+                   agg=PLD_AGG_SUM, threshold_h=float("-inf"), threshold_a=float("-inf"),
+                   scores_h=None, scores_a=None, stream=None, prepare=False):
+    """pld_score_hidden and pld_score_attn of the same occurrences in one launch."""
+    import torch
+    _need(hidden, torch.bfloat16, "hidden", 3)
+    _need(attn, torch.float32, "attn", 3)
+    _need(cand_pos, torch.int32, "cand_pos", 2)
+    B, n_rows, d = hidden.shape
+    _, R, n_keys = attn.shape
+    return _run("pld_score_both", (
+        _ptr(hidden), hidden.stride(0), hidden.stride(1), n_rows, d,
+        _ptr(attn), attn.stride(0), attn.stride(1), n_keys, R, int(agg),
+        _ptr(lens), _ptr(cand_pos), cand_pos.stride(0), _ptr(cand_count), B,
+        float(threshold_h), float(threshold_a), _ptr(scores_h), _ptr(scores_a),
+        _ptr(workspace_h), _nbytes(workspace_h), _ptr(workspace_a), _nbytes(workspace_a),
+        _stream(stream)), prepare)
 
 
 def pld_select_best(B, best_pos, best_score, workspace, stream=None, prepare=False):

@@ -313,13 +313,12 @@ __device__ void score_rows_stream(const RankHiddenArgs &a, int b, int64_t T, boo
     }
 }
 
-// kU > 0: rows of d = 1024 * kU through the streaming pipeline; 0: any d
-// through score_rows (one instantiation per path keeps each kernel's register
-// count to what its path needs).
+// Block k of g of the hidden-state ranking (its share of the flattened
+// list).  smem: the query row (d/8 chunks), then pre (B + 1) and the lengths
+// (B); s_best: kW words.
 template <int kU, int kW>
-__global__ __launch_bounds__(kW * kWave) void rank_hidden_kernel(RankHiddenArgs a) {
-    extern __shared__ uint4 smem[];
-    __shared__ uint64_t s_best[kW];
+__device__ void hidden_block(const RankHiddenArgs &a, uint32_t k, uint32_t g, uint4 *smem,
+                             uint64_t *s_best) {
     const RankCommon &c = a.c;
     const int nch = a.d / 8;
     uint4 *q_s = smem;                                         // nch chunks of 8 bf16
@@ -327,7 +326,7 @@ __global__ __launch_bounds__(kW * kWave) void rank_hidden_kernel(RankHiddenArgs 
     int32_t *lens = reinterpret_cast<int32_t *>(pre + c.B + 1); // B
     candidate_prefix<kW * kWave>(c, pre, lens);
     uint32_t lo0, hi;
-    block_share(pre[c.B], blockIdx.x, lo0, hi, gridDim.x);
+    block_share(pre[c.B], k, lo0, hi, g);
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     if (lo0 >= hi) return;   // block-uniform: nothing to score
@@ -361,15 +360,24 @@ __global__ __launch_bounds__(kW * kWave) void rank_hidden_kernel(RankHiddenArgs 
         if (lane == 0) s_best[w] = best;
         __syncthreads();                                       // also: q_s is restaged next
         if (threadIdx.x == 0) {
-            uint64_t k = s_best[0];
-            for (int i = 1; i < kW; ++i) k = s_best[i] > k ? s_best[i] : k;
-            if (k)
-                atomicMax((unsigned long long *)&c.keys[(int64_t)b * kKeySlots +
-                                                        (blockIdx.x % kKeySlots)],
-                          (unsigned long long)k);
+            uint64_t m = s_best[0];
+            for (int i = 1; i < kW; ++i) m = s_best[i] > m ? s_best[i] : m;
+            if (m)
+                atomicMax((unsigned long long *)&c.keys[(int64_t)b * kKeySlots + (k % kKeySlots)],
+                          (unsigned long long)m);
         }
         lo = seg_hi;
     }
+}
+
+// kU > 0: rows of d = 1024 * kU through the streaming pipeline; 0: any d
+// through score_rows (one instantiation per path keeps each kernel's register
+// count to what its path needs).
+template <int kU, int kW>
+__global__ __launch_bounds__(kW * kWave) void rank_hidden_kernel(RankHiddenArgs a) {
+    extern __shared__ uint4 smem[];
+    __shared__ uint64_t s_best[kW];
+    hidden_block<kU, kW>(a, blockIdx.x, gridDim.x, smem, s_best);
 }
 
 // ------------------------------------------------------------------ attn
@@ -384,15 +392,15 @@ constexpr uint32_t kAttnMinShare = PLD_ATTN_MIN_SHARE;
 // (measured: 9.5 -> 7.5 us on 32 x 8192 with 40 rows; 8 per block was faster
 // than 16 or 32, and the 64 x 16384 workload, with more candidates than
 // 8 per resident block, keeps every block).
-__global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a) {
-    __shared__ uint32_t pre[PLD_MAX_BATCH + 1];
+// Block blk of g of the attention ranking; pre: B + 1 words of LDS.
+__device__ void attn_block(const RankAttnArgs &a, uint32_t blk, uint32_t g, uint32_t *pre) {
     const RankCommon &c = a.c;
     candidate_prefix(c, pre);
     // a group of kGatherLanes lanes per candidate
     constexpr uint32_t kPerPass = kRankThreads / kGatherLanes;
     const uint32_t total = pre[c.B];
-    const uint32_t active = min(gridDim.x, (total + kAttnMinShare - 1) / kAttnMinShare);
-    const uint32_t k = xcd_run_index(blockIdx.x, active);
+    const uint32_t active = min(g, (total + kAttnMinShare - 1) / kAttnMinShare);
+    const uint32_t k = xcd_run_index(blk, active);
     if (k >= active) return;   // block-uniform
     uint32_t lo, hi;
     block_share(total, k, lo, hi, active);
@@ -415,7 +423,7 @@ __global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a)
         // one atomic per wave when all its lanes share a sequence
         const int b0 = __shfl(b, 0);
         const bool same = __ballot(active && b != b0) == 0ull;
-        const int slot = (int)((blockIdx.x * kRankWaves + threadIdx.x / kWave) % kKeySlots);
+        const int slot = (int)((blk * kRankWaves + threadIdx.x / kWave) % kKeySlots);
         if (same) {
             uint64_t m = wave_max_u64(key);
             if (lane_id() == 0 && m)
@@ -426,6 +434,28 @@ __global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a)
                       (unsigned long long)key);
         }
     }
+}
+
+__global__ __launch_bounds__(kRankThreads) void rank_attn_kernel(RankAttnArgs a) {
+    __shared__ uint32_t pre[PLD_MAX_BATCH + 1];
+    attn_block(a, blockIdx.x, gridDim.x, pre);
+}
+
+// Both rankings of the same occurrences in one launch: blocks [0, ga) rank
+// by attention, blocks [ga, grid) by hidden states, each group over its own
+// shares as the separate kernels would (the same scores and keys, bit for
+// bit).  The attention gathers then overlap the stream of hidden rows instead
+// of following it in a launch of their own.  ga is a multiple of 8, so the
+// attention blocks' XCD runs line up with the hardware's round-robin.
+template <int kU>
+__global__ __launch_bounds__(kRankThreads) void rank_both_kernel(RankHiddenArgs h, RankAttnArgs t,
+                                                                 uint32_t ga) {
+    extern __shared__ uint4 smem[];
+    __shared__ uint64_t s_best[kRankWaves];
+    if (blockIdx.x < ga)   // block-uniform
+        attn_block(t, blockIdx.x, ga, reinterpret_cast<uint32_t *>(smem));
+    else
+        hidden_block<kU, kRankWaves>(h, blockIdx.x - ga, gridDim.x - ga, smem, s_best);
 }
 
 static RankCommon make_common(const int32_t *lens, const int32_t *cand_pos, int64_t cap,
@@ -508,6 +538,33 @@ static void launch_hidden(const RankHiddenArgs &a, hipStream_t s) {
         launch_hidden_as<0, kRankWaves>(a, lds, s);
 }
 
+#ifndef PLD_BOTH_ATTN_PERMILLE
+#define PLD_BOTH_ATTN_PERMILLE 200   // rank_both_kernel: the share of the grid ranking by attention
+#endif
+
+// The grid of the combined ranking is the resident blocks; an eighth of them
+// (a multiple of 8) rank by attention, the rest by hidden states.
+template <int kU>
+static void launch_both_as(const RankHiddenArgs &h, const RankAttnArgs &t, size_t lds,
+                           hipStream_t s) {
+    const void *k = reinterpret_cast<const void *>(&rank_both_kernel<kU>);
+    const int grid = resident_blocks(k, kRankThreads, lds);
+    uint32_t ga = (uint32_t)((int64_t)grid * PLD_BOTH_ATTN_PERMILLE / 1000) / 8 * 8;
+    if (ga < 8) ga = 8;
+    const unsigned total = (unsigned)(grid > (int)ga ? grid : (int)ga + 8);
+    hipLaunchKernelGGL((rank_both_kernel<kU>), dim3(total), dim3(kRankThreads), lds, s, h, t, ga);
+}
+
+static void launch_both(const RankHiddenArgs &h, const RankAttnArgs &t, hipStream_t s) {
+    const size_t lds = (size_t)(h.d / 8) * sizeof(uint4) + (size_t)(2 * h.c.B + 1) * sizeof(uint32_t);
+    if (h.d == 4096)
+        launch_both_as<4>(h, t, lds, s);
+    else if (h.d == 8192)
+        launch_both_as<8>(h, t, lds, s);
+    else
+        launch_both_as<0>(h, t, lds, s);
+}
+
 static void launch_attn(const RankAttnArgs &a, hipStream_t s) {
     const int grid = resident_blocks(reinterpret_cast<const void *>(&rank_attn_kernel),
                                      kRankThreads, 0) * PLD_RANK_OVERSUB;
@@ -551,6 +608,27 @@ extern "C" int pld_score_attn(const float *attn, int64_t a_seq_stride, int64_t a
                        cand_count, B, threshold, scores, workspace, workspace_bytes, a);
     if (rc != PLD_OK) return rc;
     launch_attn(a, (hipStream_t)stream);
+    return launched();
+}
+
+extern "C" int pld_score_both(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
+                              int64_t n_rows, int d, const float *attn, int64_t a_seq_stride,
+                              int64_t a_row_stride, int64_t n_keys, int R, int agg,
+                              const int32_t *lens, const int32_t *cand_pos, int64_t cap,
+                              const int32_t *cand_count, int B, float threshold_h,
+                              float threshold_a, float *scores_h, float *scores_a,
+                              void *workspace_h, size_t workspace_h_bytes, void *workspace_a,
+                              size_t workspace_a_bytes, void *stream) {
+    RankHiddenArgs h;
+    int rc = prep_hidden(hidden, h_seq_stride, h_row_stride, n_rows, d, lens, cand_pos, cap,
+                         cand_count, B, threshold_h, scores_h, workspace_h, workspace_h_bytes, h);
+    if (rc != PLD_OK) return rc;
+    RankAttnArgs t;
+    rc = prep_attn(attn, a_seq_stride, a_row_stride, n_keys, R, agg, lens, cand_pos, cap,
+                   cand_count, B, threshold_a, scores_a, workspace_a, workspace_a_bytes, t);
+    if (rc != PLD_OK) return rc;
+    if (workspace_a == workspace_h) return PLD_ERR_WORKSPACE;
+    launch_both(h, t, (hipStream_t)stream);
     return launched();
 }
 

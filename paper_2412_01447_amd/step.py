@@ -12,7 +12,7 @@ from . import (DRAFT_MAX_PART, DRAFT_MAX_TOK_STRIDE, PLD_AGG_SUM, PLD_BF16, PLD_
                PLD_MAX_DRAFT_SPLIT, pld_accept_commit, pld_commit, pld_draft_attn, pld_draft_hidden,
                pld_draft_workspace_bytes, pld_emit_draft, pld_find_candidates,
                pld_find_scratch_bytes, pld_rank_attn, pld_rank_hidden, pld_score_attn,
-               pld_score_hidden, pld_select_best, pld_select_draft, pld_select_prefix,
+               pld_score_both, pld_score_hidden, pld_select_best, pld_select_draft, pld_select_prefix,
                pld_verify_accept,
                pld_verify_argmax, pld_verify_greedy, pld_verify_sample, pld_verify_sample_finish,
                pld_verify_sample_stats, pld_verify_sample_workspace_bytes, pld_workspace_bytes)
@@ -22,13 +22,17 @@ class DraftStep:
     """mode: "split" runs the separate calls (find, rank, emit), "fused" the one-call
     drafting (one ranking artifact), "auto" the one-call drafting when there is one
     ranking artifact and the separate calls otherwise.  draft_split is the one-call
-    drafting's blocks per sequence (1: one block owns a sequence, tok_stride <= 8192)."""
+    drafting's blocks per sequence (1: one block owns a sequence, tok_stride <= 8192).
+    rank_both: with both artifacts, the two scorings share one launch (pld_score_both)
+    instead of two (the same scores and choices)."""
 
     def __init__(self, B, tok_stride, K, device="cuda", cap=None, keep_scores=False, mode="auto",
-                 draft_split=1):
+                 draft_split=1, rank_both=True):
         if mode not in ("auto", "fused", "split"):
             raise ValueError(mode)
         self.B, self.tok_stride, self.K, self.mode = B, tok_stride, K, mode
+        # with both artifacts, both scorings in one launch (pld_score_both)
+        self.rank_both = bool(rank_both)
         cap = tok_stride if cap is None else cap
         self.device = device
         i32 = dict(dtype=torch.int32, device=device)
@@ -261,20 +265,25 @@ class DraftStep:
         """The separate calls of the drafting half: find, the scoring of each artifact,
         then the selection and the draft in one launch (with both artifacts the
         attention ranking's keys go to the second workspace and its choice to
-        best_pos_attn / best_score_attn)."""
+        best_pos_attn / best_score_attn; with rank_both the two scorings are one launch)."""
         both = hidden is not None and attn is not None
         ops = [("find", pld_find_candidates(tokens, lens, ngram[0], ngram[1], self.cand_pos,
                                             self.cand_count, self.ngram_used, self.scratch, **P))]
-        if attn is not None:
-            ops.append(("score_attn", pld_score_attn(
-                attn, lens, self.cand_pos, self.cand_count,
-                self.workspace_aux if both else self.workspace, agg=agg, threshold=threshold,
-                scores=self.scores_attn, **P)))
-        if hidden is not None:
-            ops.append(("score_hidden", pld_score_hidden(hidden, lens, self.cand_pos,
-                                                         self.cand_count, self.workspace,
-                                                         threshold=threshold, scores=self.scores,
-                                                         **P)))
+        if both and self.rank_both:
+            ops.append(("score_both", pld_score_both(
+                hidden, attn, lens, self.cand_pos, self.cand_count, self.workspace,
+                self.workspace_aux, agg=agg, threshold_h=threshold, threshold_a=threshold,
+                scores_h=self.scores, scores_a=self.scores_attn, **P)))
+        else:
+            if attn is not None:
+                ops.append(("score_attn", pld_score_attn(
+                    attn, lens, self.cand_pos, self.cand_count,
+                    self.workspace_aux if both else self.workspace, agg=agg,
+                    threshold=threshold, scores=self.scores_attn, **P)))
+            if hidden is not None:
+                ops.append(("score_hidden", pld_score_hidden(
+                    hidden, lens, self.cand_pos, self.cand_count, self.workspace,
+                    threshold=threshold, scores=self.scores, **P)))
         ops.append(("select_draft", pld_select_draft(
             tokens, lens, self.K, self.best_pos, self.best_score, self.draft, self.draft_len,
             self.workspace, aux_workspace=self.workspace_aux if both else None,

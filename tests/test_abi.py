@@ -136,6 +136,23 @@ def test_host_validation_error_codes():
     assert a(F, 64, 8, 0, 1, 0, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
     assert a(MIS, 64, 8, 8, 1, 0, F, F, 8, F, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_AL
     assert a(F, 64, 8, 8, 1, 0, F, F, 8, NULL, 1, INF, NULL, F, F, F, 1 << 20, NULL) == E_INV
+    # both scorings in one launch: each half's checks, then distinct workspaces
+    sb = lib.pld_score_both
+    W2 = P(0x2000)
+
+    def both(hidden=F, hr=8, d=8, attn=F, R=1, agg=0, ws_a=W2, ws_a_bytes=1 << 20):
+        return sb(hidden, 64, hr, 8, d, attn, 64, 8, 8, R, agg, F, F, 8, F, 1, INF, INF,
+                  NULL, NULL, F, 1 << 20, ws_a, ws_a_bytes, NULL)
+    assert both(hidden=NULL) == E_INV
+    assert both(d=12) == E_INV
+    assert both(hidden=MIS) == E_AL
+    assert both(hr=12) == E_AL
+    assert both(R=0) == E_INV
+    assert both(agg=2) == E_INV
+    assert both(attn=MIS) == E_AL
+    assert both(ws_a=NULL) == E_WS
+    assert both(ws_a_bytes=7) == E_WS
+    assert both(ws_a=F) == E_WS                                           # same buffer
     # emit
     e = lib.pld_emit_draft
     assert e(F, 8, F, F, 1, 0, F, F, NULL) == E_INV

@@ -22,14 +22,16 @@ from paper_2412_01447_amd.step import DraftStep
 
 pytestmark = pytest.mark.gpu
 
-# mode: "split" separate calls; "fused" the one-call drafting with blocks per sequence
+# mode: "split" separate calls (with both artifacts, the two scorings in one launch);
+# "split_sep" the same with the two scorings in launches of their own; "fused" the
+# one-call drafting with blocks per sequence
 # from the candidate counts, as the benchmark tunes it; "fused1" one block per
 # sequence; "fused8" positions split over 8 blocks per sequence.  The one-call
 # drafting takes one artifact: on the workload with both it runs on the hidden
 # states alone.
 CASES = [(1, True, "fused"), (1, False, "split"), (2, True, "fused"), (2, False, "fused"),
          (2, True, "split"), (2, True, "fused8"), (3, True, "fused"), (3, False, "split"),
-         (3, False, "fused"), (3, False, "fused1"), (4, True, "split"), (4, False, "split"),
+         (3, False, "fused"), (3, False, "fused1"), (4, True, "split"), (4, False, "split"), (4, False, "split_sep"),
          (4, True, "fused"), (5, True, "split"),
          (5, False, "split"), (5, True, "fused"), (5, False, "fused"),
          (6, True, "fused"), (6, False, "fused"), (6, False, "split"), (6, True, "fused8"),
@@ -65,7 +67,8 @@ def test_config_step_parity(cid, structured, mode):
         rver[0].tolist()[:16])
     # ---- GPU step, as the benchmark launches it
     step = DraftStep(cfg.B, cfg.T, cfg.K, device=dev, keep_scores=True,
-                     mode="fused" if mode.startswith("fused") else mode)
+                     mode="fused" if mode.startswith("fused") else "split",
+                     rank_both=mode != "split_sep")
     if mode == "fused":     # blocks per sequence from the candidate counts, as the bench does
         say("  blocks per sequence:", step.tune_split(cc, hidden=w["hidden"] is not None))
     elif mode == "fused8":

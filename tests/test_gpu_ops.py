@@ -349,6 +349,74 @@ def test_rank_random_shapes():
     say("rank random: near-tie flips", flips)
 
 
+def test_score_both_equals_separate_calls():
+    """pld_score_both against pld_score_hidden + pld_score_attn on the same
+    candidate lists, over seeded random shapes (d on each hidden path: 8, 520,
+    4096, 8192; 1 to 70 attention rows, SUM or MAX; ragged and empty sequences;
+    each ranking's own threshold): scores and choices bit for bit, both
+    workspaces left zero, and the choices against the oracle."""
+    rng, n_cases = random_plan(83, 16)
+    flips = 0
+    for it in range(n_cases):
+        B = int(rng.choice([1, 3, 8, 64]))
+        T = int(rng.choice([2, 70, 1000, 3000]))
+        V = int(rng.choice([3, 40, 5000]))
+        d = int(rng.choice([8, 520, 4096, 8192]))
+        while B * T * d > 2e7 and d > 8:
+            d = {8192: 4096, 4096: 520, 520: 8}[d]
+        R = int(rng.integers(1, 71))
+        agg = int(rng.integers(0, 2))
+        th_h = float(rng.choice([-math.inf, 0.0, 2.0]))
+        th_a = float(rng.choice([-math.inf, 0.001, 2.0]))
+        what = f"case {it}: B{B} T{T} V{V} d{d} R{R} agg{agg} th{th_h}/{th_a}"
+        say("score both", what)
+        toks = rng.integers(0, V, size=(B, T)).astype(np.int32)
+        lens = rng.integers(1, T + 1, size=B).astype(np.int32)
+        lens[0] = T
+        if B > 2:
+            lens[1] = 1                               # no candidates
+        cp, cc, _ = oracle.find(toks, lens, 1, 1)
+        bits = synth.f32_to_bf16_bits(rng.standard_normal((B, T, d)).astype(np.float32))
+        A = rng.random((B, R, T)).astype(np.float32)
+        A /= A.sum(axis=2, keepdims=True)
+        hd, ad, ld, cpd, ccd = d_bf16(bits), d_f32(A), d_i32(lens), d_i32(cp), d_i32(cc)
+        out = {}
+        for how in ("separate", "both"):
+            ws = [workspace(B, 1), workspace(B, 1)]
+            sc = [torch.full(cp.shape, 12345.0, dtype=torch.float32, device=dev()) for _ in ws]
+            if how == "separate":
+                pld.pld_score_hidden(hd, ld, cpd, ccd, ws[0], threshold=th_h, scores=sc[0])
+                pld.pld_score_attn(ad, ld, cpd, ccd, ws[1], agg=agg, threshold=th_a,
+                                   scores=sc[1])
+            else:
+                pld.pld_score_both(hd, ad, ld, cpd, ccd, ws[0], ws[1], agg=agg,
+                                   threshold_h=th_h, threshold_a=th_a, scores_h=sc[0],
+                                   scores_a=sc[1])
+            res = []
+            for w_, s_ in zip(ws, sc):
+                bp = torch.full((B,), -7, dtype=torch.int32, device=dev())
+                bs = torch.zeros(B, dtype=torch.float32, device=dev())
+                pld.pld_select_best(B, bp, bs, w_)
+                res.append((s_.cpu().numpy(), bp.cpu().numpy(), bs.cpu().numpy()))
+            torch.cuda.synchronize()
+            for w_ in ws:
+                assert_ws_zero(w_)
+            out[how] = res
+        for (a_sc, a_bp, a_bs), (b_sc, b_bp, b_bs) in zip(out["separate"], out["both"]):
+            assert np.array_equal(a_sc, b_sc, equal_nan=True), what
+            assert np.array_equal(a_bp, b_bp) and np.array_equal(a_bs, b_bs), what
+        ref_h = oracle.rank_hidden(bits, lens, cp, cc, threshold=th_h)
+        ref_a = oracle.rank_attn(A, lens, cp, cc, agg, threshold=th_a)
+        for (g_sc, g_bp, g_bs), (r_sc, r_bp, r_bs), name in zip(out["both"], (ref_h, ref_a),
+                                                               ("hidden", "attn")):
+            check_scores(g_sc, r_sc, cc, what + " " + name)
+            flips += check_best(g_bp, g_bs, r_sc, r_bp, r_bs, cp, cc, what + " " + name,
+                                threshold=th_h if name == "hidden" else th_a)
+        del hd, ad
+        torch.cuda.empty_cache()
+    say("score both: near-tie flips", flips)
+
+
 def test_rank_attn_strided_keys_and_ties():
     say("rank_attn strided/ties")
     B, R, T, pad = 3, 5, 120, 13
