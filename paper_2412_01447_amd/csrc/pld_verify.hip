@@ -9,7 +9,7 @@
 // The argmax is a streaming read of the logits, so the kernel is shaped for
 // HBM: every row is split across S blocks (S picked on the host so that a few
 // thousand blocks are in flight), each thread issues 16-byte loads (4 fp32 or
-// 8 bf16) unrolled eight deep, keeps the first maximum of its own elements,
+// 8 bf16) in batches of PLD_ARGMAX_UNROLL, keeps the first maximum of its own elements,
 // and the wave / block reduce the 64-bit key (orderable(value) << 32 |
 // ~index), whose maximum is the highest value with the lowest index.  A block
 // folds its key into the row's workspace slot with one 64-bit atomic max.

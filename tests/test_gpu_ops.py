@@ -663,6 +663,35 @@ def test_verify_all_equal_rows_and_negative_infinity():
     check_verify(gpu_verify(d_f32(Z), draft, L), ref, "degenerate")
 
 
+@pytest.mark.parametrize("B,K,V,bf16", [(200, 16, 5000, False), (1, 16, 128256, True),
+                                         (3, 70, 32000, False)])
+def test_verify_one_launch_repeated_calls(B, K, V, bf16):
+    """Greedy verification on one workspace over calls in a row with changing
+    draft lengths, invalid ones included, at 1 to over a hundred blocks per
+    row: every call against the oracle and the workspace zero after each."""
+    say("verify one launch", B, K, V, bf16)
+    rng = np.random.default_rng(B * 1000 + K)
+    ws = workspace(B, K)
+    Z = rng.standard_normal((B, K + 1, V)).astype(np.float32)
+    draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+    for b in range(B):   # accepted prefixes of every length
+        for i in range(int(rng.integers(0, K + 1))):
+            Z[b, i, draft[b, i]] = 10.0
+    zbits = synth.f32_to_bf16_bits(Z) if bf16 else Z
+    zd = d_bf16(zbits) if bf16 else d_f32(Z)
+    for call in range(4):
+        L = rng.integers(0, K + 1, size=B).astype(np.int32)
+        if call == 1:
+            L[:] = K
+        if call == 2:
+            L[0] = -1
+            L[-1] = K + 1 if B > 1 else 0
+        if call == 3:
+            L[:] = 0
+        ref = oracle.verify(zbits, draft, L, bf16=bf16)
+        check_verify(gpu_verify(zd, draft, L, ws=ws), ref, f"call {call}")
+
+
 def test_workspace_shared_across_calls_and_determinism():
     """One workspace serves every call in turn and is zero after each; repeated
     calls give bit-identical results."""
