@@ -5,7 +5,8 @@
 // last-level cache, so no repetition is served from it.  One JSON line per
 // pattern on stdout; times are means over batches of back-to-back launches.
 //
-//   stream   block-contiguous 16-byte loads over 1 GiB (8 per thread in flight)
+//   stream   block-contiguous 16-byte loads over 1 GiB (8 per thread in flight);
+//            stream_279mb / stream_68mb the same at the verification logits sizes
 //   rows8k   random 8 KB rows, 106 MB per launch (the hidden rows of the b4 x
 //            131072 workload), 2 rows of 8 loads per wave in flight
 //   rows16k  random 16 KB rows, 380 MB per launch (the b64 x 16384 workload)
@@ -183,14 +184,19 @@ int main() {
     v4u *sink;
     CK(hipMalloc(&sink, (size_t)1 << 24));
 
-    {   // stream: 1 GiB per launch at 8 rotating offsets
-        const size_t chunk = (size_t)1 << 30;
+    // stream: 1 GiB per launch at 8 rotating offsets; then the same at the
+    // logits sizes of the verification kernels (279 MB: b64 x 17 rows x 128256
+    // bf16; 68 MB: b32 x 17 x 32000 fp32 and b4 x 33 x 128256 bf16), where the
+    // launch's ramp-up and drain weigh more
+    for (const size_t chunk : {(size_t)1 << 30, (size_t)279 << 20, (size_t)68 << 20}) {
         const size_t per = chunk / 16 / ((size_t)cus * 8) / 2048 * 2048;   // whole rounds
         const double us = time_us([&](int r) {
             hipLaunchKernelGGL(stream_kernel, dim3(cus * 8), dim3(256), 0, 0,
-                               buf + (size_t)r * (chunk / 16), per, sink);
+                               buf + (size_t)r * (((size_t)1 << 30) / 16), per, sink);
         }, 8);
-        report("stream", (double)per * 16 * cus * 8, us);
+        report(chunk == ((size_t)1 << 30) ? "stream" : chunk == ((size_t)279 << 20) ? "stream_279mb"
+                                                                                  : "stream_68mb",
+               (double)per * 16 * cus * 8, us);
     }
     std::mt19937_64 rng(7);
     const int nsets = 8;

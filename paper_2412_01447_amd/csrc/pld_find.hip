@@ -9,8 +9,9 @@
 // ngram_max] with a non-zero count wins, and its occurrences are compacted in
 // ascending order.
 //
-// The tokens a block needs are first copied to LDS with independent loads, so
-// the backwards comparisons never wait on a chain of global loads.  Each lane
+// The tokens a block needs are first copied to LDS with independent loads
+// (straight into LDS, with the length, in the one-block form), so the
+// backwards comparisons never wait on a chain of global loads.  Each lane
 // then takes 8 consecutive positions: it reads the 16 tokens around them with
 // four aligned 16-byte LDS loads and builds, per n, an 8-bit hit mask from
 // register compares -- no branch per comparison, 512 positions per wave
@@ -54,7 +55,17 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
+    // the whole token row (tok_stride fits the LDS copy) is requested with
+    // the length instead of after it: positions past T - 2 are never
+    // compared, so the tokens past the length do no harm
     const int64_t T = a.lens[b];
+    if (((uintptr_t)x & 15) == 0 && (a.tok_stride & 3) == 0)
+        copy_to_lds(reinterpret_cast<const uint4 *>(x), reinterpret_cast<uint4 *>(s_x),
+                    (int)(a.tok_stride / 4));
+    else
+        stage_tokens(x, 0, a.tok_stride, s_x);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
     if (T < 1 || T > a.tok_stride) {
         if (threadIdx.x == 0) {
             a.cand_count[b] = 0;
@@ -62,8 +73,6 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
         }
         return;
     }
-    stage_tokens(x, 0, T, s_x);
-    __syncthreads();
     const Query q = load_query(s_x, T, a.nmax);
     uint64_t hits[kPasses];
 #pragma unroll
