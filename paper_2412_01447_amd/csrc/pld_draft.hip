@@ -413,17 +413,21 @@ __global__ __launch_bounds__(kWaves * kWave) void draft_part_kernel(DraftArgs a)
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
-    const int64_t T = a.lens[b];
     const int64_t lo = (int64_t)s * a.P;
-    if (!(T >= 1 && T <= a.tok_stride)) return;   // the finishing kernel reports it
-    if (lo > T - 2) {                              // no position of this block can match
-        if (threadIdx.x == 0) a.hcount[(int64_t)b * a.S + s] = 0;
-        return;
-    }
-    const bool seq_ok = kHidden ? (T >= 2 && T - 2 < a.n_rows) : (T >= 2);
+    // the slice's tokens are requested with the length, not after it (the
+    // slice lies inside the token row whatever the length)
     const int64_t s0 = lo >= 8 ? lo - 8 : 0;
     const int64_t s1 = (lo + a.P < a.tok_stride) ? lo + a.P : a.tok_stride;
     stage_part(x, s0, s1, s_x);
+    const int64_t T = a.lens[b];
+    if (!(T >= 1 && T <= a.tok_stride) || lo > T - 2) {   // block-uniform
+        __builtin_amdgcn_s_waitcnt(0);                   // the copy lands before the block ends
+        // an invalid length is reported by the finishing kernel; otherwise no
+        // position of this block can match
+        if (T >= 1 && T <= a.tok_stride && threadIdx.x == 0) a.hcount[(int64_t)b * a.S + s] = 0;
+        return;
+    }
+    const bool seq_ok = kHidden ? (T >= 2 && T - 2 < a.n_rows) : (T >= 2);
     if (kHidden && seq_ok)
         copy_to_lds(reinterpret_cast<const uint4 *>(a.hidden + (int64_t)b * a.hs + (T - 2) * a.hr),
                     const_cast<uint4 *>(s_q), a.d / 8);
