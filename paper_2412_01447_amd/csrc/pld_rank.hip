@@ -24,6 +24,12 @@
 // group's partials are combined by DPP moves; the candidates are ascending, so
 // neighbouring groups read neighbouring keys.
 //
+// Both rankings of one candidate list (pld_score_both) share one grid: a
+// fifth of the resident blocks run the attention blocks' code over the
+// attention shares while the rest run the hidden blocks' code over theirs, so
+// the scattered attention gathers overlap the stream of hidden rows instead of
+// following it in a launch of their own.
+//
 // Selection: a candidate with s > threshold contributes the 64-bit key
 // (orderable(s) << 32 | j); a block reduces its keys per sequence and folds
 // them with one 64-bit atomic max into one of kKeySlots workspace slots of the

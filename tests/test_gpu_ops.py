@@ -943,34 +943,40 @@ def test_halves_equal_combined_calls():
     assert int(torch.count_nonzero(a.workspace_aux).item()) == 0
 
 
-@pytest.mark.parametrize("mode", ["fused", "split"])
+@pytest.mark.parametrize("mode", ["fused", "split", "both"])
 def test_graph_replays_match_eager(mode):
     """The step captured in a HIP graph gives the eager result on every replay,
-    with eager work and synchronisations between the replays."""
+    with eager work and synchronisations between the replays ("both": the two
+    artifacts ranked side by side, both scorings in one launch)."""
     say("graph replay", mode)
     from paper_2412_01447_amd.step import DraftStep
-    cfg = synth.Config("t", 5, 6000, 400, 1.1, 0.3, (8, 32), (1, 3), 512, "hidden", 0, 10, "f32", 41)
+    both = mode == "both"
+    cfg = synth.Config("t", 5, 6000, 400, 1.1, 0.3, (8, 32), (1, 3), 512,
+                       "both" if both else "hidden", 9 if both else 0, 10, "f32", 41)
     w = synth.make_workload(cfg, "cuda", structured=True)
     toks, lens = d_i32(w["tokens"]), d_i32(w["lens"])
+    attn = d_f32(w["attn"]) if both else None
     dr, dl = synth.intended_drafts(w["metas"], cfg.K)
     z = d_f32(synth.logits_for(w, dr, dl))
-    eager = DraftStep(cfg.B, cfg.T, cfg.K, device="cuda", keep_scores=True, mode=mode)
-    eager.run(toks, lens, z, hidden=w["hidden"], ngram=cfg.ngram)
+    smode = "split" if both else mode
+    eager = DraftStep(cfg.B, cfg.T, cfg.K, device="cuda", keep_scores=True, mode=smode)
+    eager.run(toks, lens, z, hidden=w["hidden"], attn=attn, ngram=cfg.ngram)
     torch.cuda.synchronize()
     want = eager.host()
-    st = DraftStep(cfg.B, cfg.T, cfg.K, device="cuda", keep_scores=True, mode=mode)
+    st = DraftStep(cfg.B, cfg.T, cfg.K, device="cuda", keep_scores=True, mode=smode)
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
-        st.run(toks, lens, z, hidden=w["hidden"], ngram=cfg.ngram)
+        st.run(toks, lens, z, hidden=w["hidden"], attn=attn, ngram=cfg.ngram)
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        st.run(toks, lens, z, hidden=w["hidden"], ngram=cfg.ngram)
+        st.run(toks, lens, z, hidden=w["hidden"], attn=attn, ngram=cfg.ngram)
     for rep in range(4):
-        for t in (st.cand_count, st.best_pos, st.draft, st.out_tokens):  # scribble, replay
-            t.fill_(-9)
+        scribble = [st.cand_count, st.best_pos, st.draft, st.out_tokens]
+        for t in scribble + ([st.best_pos_attn] if both else []):
+            t.fill_(-9)   # scribble, replay
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
@@ -978,7 +984,8 @@ def test_graph_replays_match_eager(mode):
         for k in want:
             assert np.array_equal(got[k], want[k], equal_nan=True), (rep, k)
         assert int(torch.count_nonzero(st.workspace).item()) == 0
-        eager.run(toks, lens, z, hidden=w["hidden"], ngram=cfg.ngram)   # eager work between
+        assert int(torch.count_nonzero(st.workspace_aux).item()) == 0
+        eager.run(toks, lens, z, hidden=w["hidden"], attn=attn, ngram=cfg.ngram)
         torch.cuda.synchronize()
 
 
