@@ -67,7 +67,9 @@ enum { PLD_AGG_SUM = 0, PLD_AGG_MAX = 1 };
 #define PLD_MAX_HIDDEN 16384    /* d <= 16384 (the query row is staged in LDS)       */
 #define PLD_MAX_BATCH 4096      /* B <= 4096 for the ranking calls                   */
 
-/* Version of this ABI (major * 10000 + minor * 100 + patch). */
+/* Version of this ABI (major * 10000 + minor * 100 + patch); pld_version()
+ * returns the library's, which equals PLD_ABI_VERSION for a matching build. */
+#define PLD_ABI_VERSION 200
 int pld_version(void);
 
 /* A static, human-readable name for a status code. */

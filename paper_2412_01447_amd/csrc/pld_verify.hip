@@ -463,7 +463,7 @@ extern "C" int pld_commit(int32_t *tokens, int64_t tok_stride, int32_t *lens,
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;
 }
 
-extern "C" int pld_version(void) { return 100; }
+extern "C" int pld_version(void) { return PLD_ABI_VERSION; }
 
 extern "C" const char *pld_status_string(int status) {
     switch (status) {

@@ -51,8 +51,21 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(pld, n), f"binding lacks {n}"
 
 
+def test_header_compiles_as_c_and_cpp(tmp_path):
+    """include/pld.h is self-contained: it compiles alone as strict C99 and as C++17."""
+    inc = os.path.join(ROOT, "include")
+    src = tmp_path / "use.c"
+    src.write_text('#include "pld.h"\nint main(void) { return pld_version() == PLD_ABI_VERSION ? 0 : 1; }\n')
+    for cc, std in (("gcc", "-std=c99"), ("g++", "-std=c++17")):
+        r = subprocess.run([cc, std, "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only",
+                            "-x", "c" if cc == "gcc" else "c++", "-I", inc, str(src)],
+                           capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
+
+
 def test_status_strings_and_version():
-    assert pld.pld_version() >= 100
+    m = re.search(r"#define PLD_ABI_VERSION (\d+)", open(HEADER).read())
+    assert m and pld.pld_version() == int(m.group(1))
     assert pld.pld_status_string(0) == "ok"
     assert "workspace" in pld.pld_status_string(3)
     assert pld.pld_status_string(99) == "unknown status"
