@@ -320,7 +320,8 @@ int pld_score_attn(const float *attn, int64_t a_seq_stride, int64_t a_row_stride
  *                   (the rules above); pld_select_draft with workspace_h and
  *                   aux_workspace = workspace_a resolves both
  * Errors: those of the two separate calls, checked in that order, and
- * PLD_ERR_WORKSPACE when the two workspaces are the same buffer.
+ * PLD_ERR_WORKSPACE when the key regions of the two workspaces (the first
+ * 128 * B bytes of each) overlap.
  */
 int pld_score_both(const uint16_t *hidden, int64_t h_seq_stride, int64_t h_row_stride,
                    int64_t n_rows, int d, const float *attn, int64_t a_seq_stride,
@@ -352,8 +353,8 @@ int pld_select_best(int B, int32_t *best_pos, float *best_score, void *workspace
  *   aux_best_pos, aux_best_score   int32 [B], fp32 [B]; required with aux_workspace
  * Errors: PLD_ERR_INVALID (NULL required pointer, B outside [1, PLD_MAX_BATCH],
  * K < 1, tok_stride outside [1, 2^30], aux_workspace without its outputs),
- * PLD_ERR_WORKSPACE (a workspace NULL or too small, or the two the same
- * buffer), PLD_ERR_LAUNCH.
+ * PLD_ERR_WORKSPACE (a workspace NULL or too small, or the key regions of the
+ * two, the first 128 * B bytes of each, overlapping), PLD_ERR_LAUNCH.
  */
 int pld_select_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *lens, int B, int K,
                      int32_t *best_pos, float *best_score, int32_t *draft, int32_t *draft_len,

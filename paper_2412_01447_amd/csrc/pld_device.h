@@ -29,6 +29,12 @@ constexpr int kFindFusedPasses = PLD_FIND_FUSED_PASSES;   // one-block search: t
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// Whether the byte ranges [p, p + np) and [q, q + nq) share a byte.
+inline bool ranges_overlap(const void *p, size_t np, const void *q, size_t nq) {
+    const uintptr_t a = (uintptr_t)p, b = (uintptr_t)q;
+    return a < b + nq && b < a + np;
+}
+
 // Blocks of `kernel` that fit on the current device at once (CUs x resident
 // blocks per CU): the grid of the persistent kernels, whose equal contiguous
 // work ranges then finish in a single round.  Cached per device, kernel and

@@ -585,6 +585,9 @@ static int launch_select(RankCommon c, int32_t *best_pos, float *best_score, hip
     return PLD_OK;
 }
 
+// The bytes of a workspace that hold the ranking keys of B sequences.
+static size_t key_bytes(int B) { return (size_t)B * kKeySlots * sizeof(uint64_t); }
+
 static int launched() { return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH; }
 
 }  // namespace pld
@@ -633,7 +636,8 @@ extern "C" int pld_score_both(const uint16_t *hidden, int64_t h_seq_stride, int6
     rc = prep_attn(attn, a_seq_stride, a_row_stride, n_keys, R, agg, lens, cand_pos, cap,
                    cand_count, B, threshold_a, scores_a, workspace_a, workspace_a_bytes, t);
     if (rc != PLD_OK) return rc;
-    if (workspace_a == workspace_h) return PLD_ERR_WORKSPACE;
+    if (ranges_overlap(workspace_h, key_bytes(B), workspace_a, key_bytes(B)))
+        return PLD_ERR_WORKSPACE;
     launch_both(h, t, (hipStream_t)stream);
     return launched();
 }
@@ -661,7 +665,8 @@ extern "C" int pld_select_draft(const int32_t *tokens, int64_t tok_stride, const
         return PLD_ERR_INVALID;
     if (aux_workspace && (!aux_best_pos || !aux_best_score)) return PLD_ERR_INVALID;
     if (!workspace || workspace_bytes < rank_ws_bytes(B)) return PLD_ERR_WORKSPACE;
-    if (aux_workspace && (aux_workspace_bytes < rank_ws_bytes(B) || aux_workspace == workspace))
+    if (aux_workspace && (aux_workspace_bytes < rank_ws_bytes(B) ||
+                          ranges_overlap(workspace, key_bytes(B), aux_workspace, key_bytes(B))))
         return PLD_ERR_WORKSPACE;
     SelectDraftArgs a{tokens, tok_stride, lens, B, K, (uint64_t *)workspace, best_pos, best_score,
                       draft, draft_len, (uint64_t *)aux_workspace, aux_best_pos, aux_best_score};

@@ -166,6 +166,8 @@ def test_host_validation_error_codes():
     assert both(ws_a=NULL) == E_WS
     assert both(ws_a_bytes=7) == E_WS
     assert both(ws_a=F) == E_WS                                           # same buffer
+    assert both(ws_a=P(0x1000 + 127)) == E_WS                             # keys overlap (B = 1)
+    assert both(ws_a=P(0x1000 - 127)) == E_WS
     # emit
     e = lib.pld_emit_draft
     assert e(F, 8, F, F, 1, 0, F, F, NULL) == E_INV
@@ -184,6 +186,7 @@ def test_host_validation_error_codes():
     assert sd(F, 8, F, 1, 4, F, F, F, F, F, 8, NULL, 0, NULL, NULL, NULL) == E_WS
     assert sd(F, 8, F, 1, 4, F, F, F, F, F, 1 << 20, P(0x2000), 8, F, F, NULL) == E_WS
     assert sd(F, 8, F, 1, 4, F, F, F, F, F, 1 << 20, F, 1 << 20, F, F, NULL) == E_WS   # same buffer
+    assert sd(F, 8, F, 1, 4, F, F, F, F, F, 1 << 20, P(0x1000 + 64), 1 << 20, F, F, NULL) == E_WS
     # the allocation-free verification: host checks come before any device set-up
     na = lib.pld_verify_greedy_noalloc
     assert na(F, 0, 40, 10, 10, 3, NULL, F, 1, F, F, F, NULL) == E_INV
