@@ -183,7 +183,9 @@ int pld_emit_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *len
  * among equal maxima; -0 and +0 compare equal):
  *   accept_len[b] = the first i < L with y_i != draft[b][i], else L
  *   out_tokens[b] = draft[b][0..a-1], y_a, then -1 padding;  out_count[b] = a+1
- * where L = draft_len[b].  Rows i > L do not affect any output.
+ * where L = draft_len[b].  Rows i > L do not affect any output.  NaN
+ * logits are outside the contract (a row holding one gets an unspecified
+ * y_i).
  *
  *   logits      PLD_F32 or PLD_BF16 (bit patterns); element (b, i, v) at
  *               b*l_seq_stride + i*l_row_stride + v; element-aligned.  All

@@ -43,6 +43,16 @@ struct VerifyArgs {
     uint64_t *keys;      // [B][K+1], zero on entry
 };
 
+// The largest of n values by the NaN-propagating maximum (three inputs per
+// instruction on gfx950; -0 < +0, which only decides which zero is kept).
+template <int n>
+__device__ __forceinline__ float vmax_of(const float (&f)[n]) {
+    float m = f[0];
+#pragma unroll
+    for (int e = 1; e < n; ++e) m = __builtin_elementwise_maximum(m, f[e]);
+    return m;
+}
+
 template <int kBf16>
 struct Elem;
 template <>
@@ -55,6 +65,11 @@ struct Elem<0> {
         o[1] = __uint_as_float(v.y);
         o[2] = __uint_as_float(v.z);
         o[3] = __uint_as_float(v.w);
+    }
+    __device__ static float vmax(const uint4 &v) {
+        float o[4];
+        unpack(v, o);
+        return vmax_of(o);
     }
 };
 template <>
@@ -73,6 +88,11 @@ struct Elem<1> {
         o[5] = bf16_hi(v.z);
         o[6] = bf16_lo(v.w);
         o[7] = bf16_hi(v.w);
+    }
+    __device__ static float vmax(const uint4 &v) {
+        float o[8];
+        unpack(v, o);
+        return vmax_of(o);
     }
 };
 
