@@ -4,7 +4,8 @@
 // selection of the best occurrence, and the draft span (Sec. 4.3).
 //
 // S == 1 (tok_stride <= 8192): one 1024-thread block owns a sequence.  It
-//   copies the token row and the query row into LDS, finds the occurrences,
+//   copies the token row and the query row into LDS, finds the occurrences
+//   (the one-block search of the find call, listing them in LDS as well),
 //   scores them with the same per-row routines as the separate ranking calls
 //   (bit-identical scores), selects, and writes the draft -- one launch.
 // S  > 1: the positions are partitioned.  Block s of a sequence owns the
@@ -226,7 +227,6 @@ __device__ void write_draft(const DraftArgs &a, int b, int64_t T, bool tok_ok, u
 template <bool kHidden, int kU>
 __global__ __launch_bounds__(kFindWavesFused * kWave) void draft_kernel(DraftArgs a) {
     constexpr int kWaves = kFindWavesFused;
-    static_assert(kFindFusedMax == kWaves * kWave * kLanePos, "one pass per block");
     __shared__ __align__(16) int32_t s_buf[kFindFusedMax];   // the tokens
     __shared__ int32_t s_list[kFindFusedMax];                // the occurrence list
     extern __shared__ uint4 s_q[];                           // query row H[T-2] (hidden)
@@ -234,7 +234,6 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void draft_kernel(DraftArg
     __shared__ uint64_t s_key[kWaves];
     const int b = blockIdx.y;
     const int w = threadIdx.x / kWave;
-    const int lane = lane_id();
     const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
 
     // the token row straight into LDS when it is 16-byte aligned (it does not
@@ -253,41 +252,12 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void draft_kernel(DraftArg
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    // ---- occurrences (Eq. 1), longest n first: one pass, 8 positions a lane
+    // ---- occurrences (Eq. 1), longest n first, listed in LDS and in cand_pos
     int n_used = -1, total = 0;
-    if (tok_ok) {
-        const Query q = load_query(s_buf, T, a.nmax);
-        const int64_t base = (int64_t)threadIdx.x * kLanePos;
-        const uint64_t hits = lane_hits(s_buf, 0, T, base, q, a.nmax);
-        int cnt[kMaxNgram];
-#pragma unroll
-        for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
-        count_levels(hits, a.nmax, cnt);
-#pragma unroll
-        for (int k = 0; k < kMaxNgram; ++k) {
-            if (k < a.nmax) {   // uniform
-                const int t = wave_sum_i32(cnt[k]);
-                if (lane == 0) s_lvl[w][k] = t;
-            }
-        }
-        __syncthreads();
-        n_used = 0;
-        for (int n = a.nmax; n >= a.nmin; --n) {
-            int t = 0;
-            for (int i = 0; i < kWaves; ++i) t += s_lvl[i][n - 1];
-            if (t > 0) {
-                n_used = n;
-                total = t;
-                break;
-            }
-        }
-        if (n_used > 0) {   // block-uniform; the ascending list
-            int64_t run = 0;
-            for (int i = 0; i < w; ++i) run += s_lvl[i][n_used - 1];
-            emit_bits(level_bits(hits, n_used), base, s_list, a.cand_pos + (int64_t)b * a.cap,
-                      run);
-            __syncthreads();
-        }
+    if (tok_ok) {   // block-uniform
+        n_used = block_search<kWaves, kFindFusedMax / (kWaves * kWave)>(
+            s_buf, T, a.nmin, a.nmax, s_lvl, a.cand_pos + (int64_t)b * a.cap, s_list, total);
+        if (n_used > 0) __syncthreads();   // the list in LDS is complete
     }
     if (threadIdx.x == 0) {
         a.cand_count[b] = total;

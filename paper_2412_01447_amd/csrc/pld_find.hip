@@ -11,16 +11,18 @@
 //
 // The tokens a block needs are first copied to LDS with independent loads
 // (straight into LDS, with the length, in the one-block form), so the
-// backwards comparisons never wait on a chain of global loads.  Each lane
-// then takes 8 consecutive positions: it reads the 16 tokens around them with
-// four aligned 16-byte LDS loads and builds, per n, an 8-bit hit mask from
-// register compares -- no branch per comparison, 512 positions per wave
-// pass.  Compaction is an exclusive wave scan of the lanes' hit counts plus
-// the per-wave and per-block counts.  Sequences up to 16384 tokens take one
-// 1024-thread block each (count, pick n, compact, in one kernel);
-// longer ones split into kFindTile-position blocks: a count kernel writes
-// per-tile counts to the scratch buffer, and the compaction kernel derives
-// its tile's output offset from the counts of the tiles before it.
+// backwards comparisons never wait on a chain of global loads.  Sequences up
+// to 16384 tokens take one 1024-thread block each (count, pick n, compact, in
+// one kernel): the block searches in groups of 64 positions, one per lane,
+// each group's hits a 64-bit compare mask (block_search), because on the one
+// CU that holds a sequence the number of instructions per position sets the
+// time.  Longer ones split into kFindTile-position blocks in which each lane
+// takes 8 consecutive positions, reads the 16 tokens around them with four
+// aligned 16-byte LDS loads and builds, per n, an 8-bit hit mask from
+// register compares; a count kernel writes per-tile counts to the scratch
+// buffer, and the compaction kernel derives its tile's output offset from the
+// counts of the tiles before it (an exclusive wave scan of the lanes' hit
+// counts plus the per-wave and per-tile counts).
 #include "pld.h"
 #include "pld_device.h"
 #include "pld_match.h"
@@ -43,17 +45,14 @@ struct FindArgs {
 
 // ---------------------------------------------------------------- fused
 // One 1024-thread block per sequence, tok_stride <= kPasses * kFindFusedMax:
-// every lane takes 8 positions per pass, a pass covers 8192 positions, and
-// all the tokens sit in LDS (64 KB for two passes).
-static_assert(kFindFusedMax == kFindWavesFused * kWave * kLanePos, "8192 positions per pass");
-
+// the whole row sits in LDS (64 KB for two passes' worth, 16384 tokens) and
+// block_search takes it in groups of 64 positions, kPasses * 8 per wave.
 template <int kPasses>
 __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(FindArgs a) {
+    constexpr int G = kPasses * kFindFusedMax / (kFindWavesFused * kWave);
     __shared__ __align__(16) int32_t s_x[kPasses * kFindFusedMax];
-    __shared__ int s_lvl[kPasses][kFindWavesFused][kMaxNgram];
+    __shared__ int s_lvl[kFindWavesFused][kMaxNgram];
     const int b = blockIdx.x;
-    const int w = threadIdx.x / kWave;
-    const int lane = lane_id();
     const int32_t *x = a.tokens + (int64_t)b * a.tok_stride;
     // the whole token row (tok_stride fits the LDS copy) is requested with
     // the length instead of after it: positions past T - 2 are never
@@ -73,50 +72,10 @@ __global__ __launch_bounds__(kFindWavesFused * kWave) void find_fused_kernel(Fin
         }
         return;
     }
-    const Query q = load_query(s_x, T, a.nmax);
-    uint64_t hits[kPasses];
-#pragma unroll
-    for (int t = 0; t < kPasses; ++t) {
-        const int64_t base = (int64_t)t * kFindFusedMax + (int64_t)threadIdx.x * kLanePos;
-        hits[t] = lane_hits(s_x, 0, T, base, q, a.nmax);
-        int cnt[kMaxNgram];
-#pragma unroll
-        for (int k = 0; k < kMaxNgram; ++k) cnt[k] = 0;
-        count_levels(hits[t], a.nmax, cnt);
-#pragma unroll
-        for (int k = 0; k < kMaxNgram; ++k) {
-            if (k < a.nmax) {   // uniform
-                const int c = wave_sum_i32(cnt[k]);
-                if (lane == 0) s_lvl[t][w][k] = c;
-            }
-        }
-    }
-    __syncthreads();
-    // the longest n with an occurrence (every thread, same answer)
-    int n_used = 0, total = 0;
-    for (int n = a.nmax; n >= a.nmin; --n) {
-        int c = 0;
-        for (int t = 0; t < kPasses; ++t)
-            for (int i = 0; i < kFindWavesFused; ++i) c += s_lvl[t][i][n - 1];
-        if (c > 0) {
-            n_used = n;
-            total = c;
-            break;
-        }
-    }
-    if (n_used > 0) {   // ascending: pass, then wave, then lane
-        int64_t run = 0;
-#pragma unroll
-        for (int t = 0; t < kPasses; ++t) {
-            int64_t r = run;
-            for (int i = 0; i < kFindWavesFused; ++i) {
-                if (i < w) r += s_lvl[t][i][n_used - 1];
-                run += s_lvl[t][i][n_used - 1];
-            }
-            const int64_t base = (int64_t)t * kFindFusedMax + (int64_t)threadIdx.x * kLanePos;
-            emit_bits(level_bits(hits[t], n_used), base, a.cand_pos + (int64_t)b * a.cap, nullptr, r);
-        }
-    }
+    int total;
+    const int n_used = block_search<kFindWavesFused, G>(s_x, T, a.nmin, a.nmax, s_lvl,
+                                                        a.cand_pos + (int64_t)b * a.cap, nullptr,
+                                                        total);
     if (threadIdx.x == 0) {
         a.cand_count[b] = total;
         a.ngram_used[b] = n_used;

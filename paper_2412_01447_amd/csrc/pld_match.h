@@ -104,6 +104,130 @@ __device__ __forceinline__ uint64_t lane_hits(const int32_t *s, int64_t s0, int6
     return out;
 }
 
+// ------------------------------------------------------------- block search
+// Writes the positions p0 + l of the set bits l of the wave-uniform mask m to
+// out[run ...] (and out2[run ...] when given) in ascending order; returns run
+// plus the number of bits.  The mask becomes the execution mask of the
+// stores; an entry's byte offset fits in 32 bits (fewer than 2^30 positions
+// per row).
+__device__ __forceinline__ int emit_group(uint64_t m, int p0, int32_t *out, int32_t *out2,
+                                          int run) {
+    if (__builtin_amdgcn_inverse_ballot_w64(m)) {
+        const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+            (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        const uint32_t off = ((uint32_t)run + below) << 2;
+        const int32_t p = p0 + lane_id();
+        *reinterpret_cast<int32_t *>(reinterpret_cast<char *>(out) + off) = p;
+        if (out2) *reinterpret_cast<int32_t *>(reinterpret_cast<char *>(out2) + off) = p;
+    }
+    return run + (int)__popcll(m);
+}
+
+// Occurrence search of a whole row by one block of kW waves (Eq. 1 with
+// n-gram queries tried longest first).  The row is in LDS: s_x[p] = x[p] for
+// p < kW * G * 64 (tokens past the length do no harm: positions past T-2 are
+// masked).  Wave w takes the positions [w * G * 64, (w + 1) * G * 64) in
+// groups of 64, one position per lane, and keeps one 64-bit mask per group:
+// level 0 is one vector compare of the tokens against x[T-1] (and, in the
+// group that crosses T-2, one more against the position); level k keeps the
+// bits whose x[p-k] equals x[T-1-k], all groups of a level at once, while any
+// bit is left.  On the single CU that searches a sequence the pass costs a
+// few instructions per 64 positions and level.  Returns n (0: no occurrence)
+// and the count; with n > 0 the occurrences are written in ascending order
+// to out (and out2 when given).  s_lvl: kW x kMaxNgram ints of LDS.  Call
+// with T in [1, kW * G * 64], from the whole block.
+template <int kW, int G>
+__device__ __forceinline__ int block_search(const int32_t *s_x, int64_t T, int nmin, int nmax,
+                                            int (*s_lvl)[kMaxNgram], int32_t *out, int32_t *out2,
+                                            int &total) {
+    const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x / kWave);
+    const int lane = lane_id();
+    const int w0 = w * G * kWave;
+    const int hi = (int)T - 2;             // occurrences lie in [1, T-2]
+    const int pl = w0 + lane;              // the lane's position in group 0
+    const bool some = w0 <= hi;            // uniform: the wave has positions to test
+    // level 0
+    uint64_t m0[G];
+#pragma unroll
+    for (int i = 0; i < G; ++i) m0[i] = 0ull;
+    if (some) {
+        const int32_t q0 = s_x[T - 1];
+        int32_t t[G];
+#pragma unroll
+        for (int i = 0; i < G; ++i) t[i] = s_x[pl + i * kWave];
+        if (w0 + G * kWave - 1 <= hi) {    // every position of the wave is below T-1
+#pragma unroll
+            for (int i = 0; i < G; ++i) m0[i] = __ballot(t[i] == q0);
+        } else {
+#pragma unroll
+            for (int i = 0; i < G; ++i) m0[i] = __ballot(t[i] == q0) & __ballot(pl <= hi - i * kWave);
+        }
+        if (w == 0) m0[0] &= ~1ull;        // position 0 is never an occurrence
+    }
+    // The masks of level `upto` (at most nmax - 1) from level 0, level by
+    // level; `count(k, c)` gets each level's count.  A non-empty level k-1
+    // holds a position p <= T-2 with p >= k-1, so x[T-1-k] exists.
+    auto levels = [&](uint64_t (&m)[G], int upto, auto count) {
+        for (int k = 1; k <= upto; ++k) {
+            uint64_t any = 0ull;
+#pragma unroll
+            for (int i = 0; i < G; ++i) any |= m[i];
+            if (!any) break;   // uniform
+            const int32_t qk = s_x[T - 1 - k];
+            int32_t t[G];
+#pragma unroll
+            for (int i = 0; i < G; ++i) t[i] = s_x[max(pl + i * kWave - k, 0)];
+#pragma unroll
+            for (int i = 0; i < G; ++i) m[i] &= __ballot(t[i] == qk);
+            if (w == 0) m[0] &= ~0ull << k;   // x[p-k] exists only from p = k on
+            int c = 0;
+#pragma unroll
+            for (int i = 0; i < G; ++i) c += (int)__popcll(m[i]);
+            count(k, c);
+        }
+    };
+    {
+        int c0 = 0;
+#pragma unroll
+        for (int i = 0; i < G; ++i) c0 += (int)__popcll(m0[i]);
+        if (lane == 0) {
+            s_lvl[w][0] = c0;
+#pragma unroll
+            for (int k = 1; k < kMaxNgram; ++k) s_lvl[w][k] = 0;
+        }
+        if (nmax > 1 && some) {   // uniform
+            uint64_t m[G];
+#pragma unroll
+            for (int i = 0; i < G; ++i) m[i] = m0[i];
+            levels(m, nmax - 1, [&](int k, int c) {
+                if (lane == 0) s_lvl[w][k] = c;
+            });
+        }
+    }
+    __syncthreads();
+    // the longest n with an occurrence, and this wave's offset in the list:
+    // lane i < kW holds wave i's count of the level
+    int n_used = 0, run = 0;
+    total = 0;
+    for (int n = nmax; n >= nmin; --n) {
+        const int c = lane < kW ? s_lvl[lane][n - 1] : 0;
+        int t;
+        const int ex = wave_excl_scan(c, t);
+        if (t > 0) {   // uniform
+            n_used = n;
+            total = t;
+            run = __builtin_amdgcn_readlane(ex, w);
+            break;
+        }
+    }
+    if (n_used > 0 && some) {   // uniform; ascending: wave, then group, then lane
+        if (n_used > 1) levels(m0, n_used - 1, [](int, int) {});
+#pragma unroll
+        for (int i = 0; i < G; ++i) run = emit_group(m0[i], w0 + i * kWave, out, out2, run);
+    }
+    return n_used;
+}
+
 __device__ __forceinline__ uint32_t level_bits(uint64_t hits, int n) {
     return (uint32_t)(hits >> (8 * (n - 1))) & 0xffu;
 }
