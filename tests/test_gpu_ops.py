@@ -161,6 +161,49 @@ def test_find_random_shapes():
         check_find(gpu_find(toks, lens, nmin, nmax), oracle.find(toks, lens, nmin, nmax), what)
 
 
+@pytest.mark.parametrize("stride", [8192, 16384])
+def test_find_group_and_wave_borders(stride):
+    """The one-block search takes 64 positions per compare mask and a run of
+    groups per wave (8 groups of 64 for rows up to 8192 tokens, 16 up to
+    16384): occurrences of 1- to 8-grams planted so that their windows end on
+    either side of every group border of the first waves and of every wave
+    border, with the length ending inside, on and past a group; the find call
+    and the one-call drafting with one block against the oracle, bit for bit."""
+    say("find group/wave borders", stride)
+    rng = np.random.default_rng(stride)
+    per_wave = stride // 16
+    B = 4
+    toks = rng.integers(1000, 30000, size=(B, stride)).astype(np.int32)
+    lens = np.array([stride, stride - 1, stride - 63, stride - 64 - 17], np.int32)
+    ends = set()
+    for g in range(1, 3 * per_wave // 64):
+        ends.update((64 * g - 1, 64 * g))
+    for w in range(1, 16):
+        ends.update((w * per_wave - 1, w * per_wave, w * per_wave + 7))
+    for b in range(B):
+        T = int(lens[b])
+        q = toks[b, T - 8:T].copy()
+        for e in sorted(ends):
+            if 8 <= e <= T - 9:
+                n = 1 + (e % 8)                  # a window of n tokens ending at e
+                toks[b, e - n + 1:e + 1] = q[8 - n:]
+    for nmin, nmax in ((1, 1), (1, 8), (3, 5), (8, 8)):
+        ref = oracle.find(toks, lens, nmin, nmax)
+        check_find(gpu_find(toks, lens, nmin, nmax), ref, f"borders {stride} n{nmin}-{nmax}")
+        if stride <= pld.DRAFT_MAX_TOK_STRIDE:
+            i32 = dict(dtype=torch.int32, device="cuda")
+            K = 4
+            A = synth.make_attn(B, 2, stride, lens, seed=3)
+            o = [torch.full((B, stride), -1, **i32), torch.zeros(B, **i32), torch.zeros(B, **i32),
+                 torch.zeros(B, **i32), torch.zeros(B, dtype=torch.float32, device="cuda"),
+                 torch.zeros((B, K), **i32), torch.zeros(B, **i32)]
+            pld.pld_draft_attn(d_i32(toks), d_i32(lens), nmin, nmax, d_f32(A), K, *o,
+                               blocks_per_seq=1, workspace=draft_workspace(B, 1))
+            torch.cuda.synchronize()
+            check_find((o[0].cpu().numpy(), o[1].cpu().numpy(), o[2].cpu().numpy()), ref,
+                       f"borders draft {stride} n{nmin}-{nmax}")
+
+
 def test_find_planted_ngrams_multi_tile():
     """Long sequences with planted n-gram repeats crossing tile borders."""
     say("find planted multi-tile")
