@@ -250,8 +250,11 @@ int pld_verify_greedy_noalloc(const void *logits, int dtype, int64_t l_seq_strid
  *                past the draft (all -1 when draft_len is out of range)
  *   workspace    at least pld_verify_sample_workspace_bytes(B, K, V, dtype)
  *                bytes, zero-filled once like every workspace; its first
- *                pld_workspace_bytes(B, K) bytes are left zero by the call and
- *                the rest is per-call statistics, rewritten each time.
+ *                pld_workspace_bytes(B, K) bytes are left zero by the call,
+ *                then come per-call statistics, B counters that every call
+ *                leaves zero (K+1 > 16: the blocks that share a sequence's
+ *                rows count themselves done there, the last one accepting)
+ *                and the tokens those blocks hand over, rewritten each time.
  * Arithmetic: the masses are fp32 (2^((z - m) * log2(e)/tau)) and are summed
  * per 512-vector segment of the row, then over the segments; a row of -inf
  * gives y = 0, and where rounding leaves no element past the target the last

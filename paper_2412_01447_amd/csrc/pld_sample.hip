@@ -45,6 +45,9 @@ struct SampleArgs {
     int32_t *out_count;
     int32_t *row_sample;   // [B][K+1] or null
     float2 *stats;         // [B][K+1][nseg_max]: (segment maximum, mass relative to it)
+    int parts;             // finishing blocks per sequence (rows split between them)
+    int32_t *tickets;      // [B], zero on entry and exit: the parts that are done
+    int32_t *tokens;       // [B][K+1]: the parts' tokens, handed to the last part
 };
 
 __host__ __device__ __forceinline__ int seg_count(int nvec) {
@@ -310,31 +313,62 @@ __device__ __forceinline__ int sample_row(const SampleArgs &a, int b, int i, con
 template <int kBf16>
 __global__ __launch_bounds__(kFinishWaves *kWave) void sample_finish_kernel(SampleArgs a) {
     extern __shared__ int32_t s_y[];   // [K+1]
-    const int b = blockIdx.x, K = a.K;
+    __shared__ int s_last;
+    const int part = blockIdx.x, b = blockIdx.y, K = a.K;
     const int w = (int)threadIdx.x / kWave, lane = lane_id();
-    const int nw = (int)blockDim.x / kWave;   // min(16, K+1) waves
+    const int nw = (int)blockDim.x / kWave;   // rows of this part per round
+    // This part's rows: [r0, r1), with the parts taking consecutive runs of at
+    // most 16 rows, so that every row of the sequence is in its first round.
+    const int per = (K + 1 + a.parts - 1) / a.parts;
+    const int r0 = part * per, r1 = min(r0 + per, K + 1);
     // The first row's inputs and (wave 0) the draft are requested together with
     // the length: every row's statistics and draws exist whatever the length.
     RowInputs next{};
-    if (w <= K) next = load_row_inputs<kBf16>(a, b, w);
+    if (r0 + w < r1) next = load_row_inputs<kBf16>(a, b, r0 + w);
     const int32_t *dr = a.draft + (int64_t)b * K;
     const int32_t d0 = (w == 0 && lane < K) ? dr[lane] : -1;
     const int L = a.draft_len[b];
     const bool ok = L >= 0 && L <= K;   // block-uniform
     int32_t *rs = a.row_sample ? a.row_sample + (int64_t)b * (K + 1) : nullptr;
+    int32_t *tok = a.tokens + (int64_t)b * (K + 1);
     if (ok) {
-        for (int i = w; i <= L; i += nw) {
+        for (int i = r0 + w; i < r1 && i <= L; i += nw) {
             const RowInputs in = next;
-            if (i + nw <= L) next = load_row_inputs<kBf16>(a, b, i + nw);
+            if (i + nw < r1 && i + nw <= L) next = load_row_inputs<kBf16>(a, b, i + nw);
             const int y = sample_row<kBf16>(a, b, i, in);
             if (lane == 0) {
-                s_y[i] = y;
+                if (a.parts == 1) {
+                    s_y[i] = y;
+                } else {
+                    // handed over by an atomic, whose return is waited for: the
+                    // exchange is complete before this part counts itself done
+                    const int prev = atomicExch(tok + i, y);
+                    asm volatile("" ::"v"(prev));   // the returned value must arrive here
+                    __builtin_amdgcn_s_waitcnt(0);
+                }
                 if (rs) rs[i] = y;
             }
         }
     }
     if (rs)
-        for (int i = (ok ? L + 1 : 0) + (int)threadIdx.x; i <= K; i += (int)blockDim.x) rs[i] = -1;
+        for (int i = max(r0, ok ? L + 1 : 0) + (int)threadIdx.x; i < r1; i += (int)blockDim.x)
+            rs[i] = -1;
+    if (a.parts > 1) {
+        // The last part to finish runs the acceptance.  The tokens travel by
+        // atomics only (no cache maintenance): every part's exchanges have
+        // completed before its count, and the last part reads them after its
+        // own count, with atomics as well.
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            const int done = atomicAdd(a.tickets + b, 1);
+            s_last = done == a.parts - 1;
+            if (s_last) atomicExch(a.tickets + b, 0);   // zero again for the next call
+        }
+        __syncthreads();
+        if (!s_last) return;   // block-uniform
+        if (ok)
+            for (int i = (int)threadIdx.x; i <= L; i += (int)blockDim.x) s_y[i] = atomicAdd(tok + i, 0);
+    }
     __syncthreads();
     if (w == 0) {
         auto lds_token = [&](int r) { return (ok && r <= L) ? s_y[r] : -1; };
@@ -348,10 +382,15 @@ __global__ __launch_bounds__(kFinishWaves *kWave) void sample_finish_kernel(Samp
 static int sample_nseg_max(int V, int dtype) {
     return seg_count(V / (dtype == PLD_F32 ? 4 : 8));   // a row has at most V / P whole vectors
 }
-static size_t sample_ws_bytes(int B, int K, int V, int dtype) {
-    return common_ws_bytes(B, K) +
-           align_up((size_t)B * (size_t)(K + 1) * (size_t)sample_nseg_max(V, dtype) * sizeof(float2),
+static size_t sample_stats_bytes(int B, int K, int V, int dtype) {
+    return align_up((size_t)B * (size_t)(K + 1) * (size_t)sample_nseg_max(V, dtype) * sizeof(float2),
                     256);
+}
+// [the shared zero-invariant part | statistics | tickets (zero-invariant) | tokens]
+static size_t sample_ws_bytes(int B, int K, int V, int dtype) {
+    return common_ws_bytes(B, K) + sample_stats_bytes(B, K, V, dtype) +
+           align_up((size_t)B * sizeof(int32_t), 256) +
+           align_up((size_t)B * (size_t)(K + 1) * sizeof(int32_t), 256);
 }
 
 // The sampling calls' arguments: those of prep_verify plus the temperature,
@@ -378,7 +417,13 @@ static int prep_sample(const void *logits, int dtype, int64_t l_seq_stride, int6
     a.nseg_max = sample_nseg_max(V, dtype);
     a.k = (float)kd;
     a.draft_len = draft_len;
-    a.stats = reinterpret_cast<float2 *>(static_cast<char *>(workspace) + common_ws_bytes(B, K));
+    char *ws = static_cast<char *>(workspace);
+    a.stats = reinterpret_cast<float2 *>(ws + common_ws_bytes(B, K));
+    a.tickets = reinterpret_cast<int32_t *>(ws + common_ws_bytes(B, K) +
+                                            sample_stats_bytes(B, K, V, dtype));
+    a.tokens = a.tickets + align_up((size_t)B * sizeof(int32_t), 256) / sizeof(int32_t);
+    // finishing parts: every row of a sequence in the first round of a part's waves
+    a.parts = (K + 1 + kFinishWaves - 1) / kFinishWaves;
     // Statistics blocks per row: about PLD_VERIFY_TARGET_BLOCKS in all, and
     // no more waves per row than the row has segments.
     const int64_t rows = (int64_t)B * (K + 1);
@@ -416,11 +461,12 @@ static void launch_stats(const SampleArgs &a, int dtype, hipStream_t s) {
 
 static void launch_finish(const SampleArgs &a, int dtype, hipStream_t s) {
     const size_t lds = (size_t)(a.K + 1) * sizeof(int32_t);
-    const dim3 block((unsigned)(kWave * (a.K + 1 < kFinishWaves ? a.K + 1 : kFinishWaves)));
+    const int per = (a.K + 1 + a.parts - 1) / a.parts;   // <= kFinishWaves
+    const dim3 grid((unsigned)a.parts, (unsigned)a.B), block((unsigned)(kWave * per));
     if (dtype == PLD_F32)
-        hipLaunchKernelGGL(sample_finish_kernel<0>, dim3((unsigned)a.B), block, lds, s, a);
+        hipLaunchKernelGGL(sample_finish_kernel<0>, grid, block, lds, s, a);
     else
-        hipLaunchKernelGGL(sample_finish_kernel<1>, dim3((unsigned)a.B), block, lds, s, a);
+        hipLaunchKernelGGL(sample_finish_kernel<1>, grid, block, lds, s, a);
 }
 
 }  // namespace pld
