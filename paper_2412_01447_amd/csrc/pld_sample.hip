@@ -5,9 +5,9 @@
 // uniform u: the first v whose cumulative mass exceeds u times the row's
 // total.  One streaming pass writes, per 512-vector segment of a row, the
 // segment maximum and the segment's mass relative to it; a finishing kernel
-// (one block per sequence, one wave per row) combines the segment masses,
+// (one wave per row, up to 16 rows per block) combines the segment masses,
 // finds the segment the target falls in, re-reads only that segment (1/nseg of
-// the row) to find the token, and runs the acceptance on the tokens from LDS.
+// the row) to find the token, and runs the acceptance on the row tokens.
 #include <float.h>
 #include <math.h>
 
@@ -111,8 +111,9 @@ __device__ __forceinline__ float seg_weight(float2 st, float M, float k) {
     return st.x > -INFINITY ? st.y * rel_mass(st.x, M, k) : 0.f;
 }
 
-// The rows' tokens and the acceptance, one block per sequence of
-// min(16, K+1) waves.  A wave takes a row i <= L (then i + waves, ...):
+// The rows' tokens and the acceptance.  A sequence's K+1 rows are split over
+// ceil((K+1)/16) blocks (parts) of at most 16 waves, so that every row is in
+// the first round of its block's waves; a wave takes a row i <= L:
 //  1. the row maximum M over the segment maxima, the segment masses rescaled
 //     to M and their inclusive scan (64 segments per round, rounds chained in
 //     one fixed order, so the last cumulative value is the total S bit for
@@ -125,8 +126,14 @@ __device__ __forceinline__ float seg_weight(float2 st, float M, float k) {
 //  3. the first element whose cumulative mass exceeds the target, found by a
 //     ballot and a walk through one vector's elements.
 // Where rounding leaves no crossing, the last element with mass is taken, so
-// the token always has nonzero fp32 probability.  The tokens go to LDS; after
-// a barrier one wave runs the acceptance.
+// the token always has nonzero fp32 probability.  With one part the tokens go
+// to LDS and, after a barrier, one wave runs the acceptance.  With several,
+// each token goes to the workspace by an atomic exchange whose return is
+// waited for, each part then counts itself done with one atomic add on the
+// sequence's counter, and the part that brings it to the number of parts
+// reads the tokens back by atomics, returns the counter to zero and runs the
+// acceptance: the tokens travel through atomics only, so no part writes back
+// or invalidates a cache.
 constexpr int kFinishWaves = 16;
 constexpr int kFinishMaxRows = PLD_MAX_SAMPLE_ROWS;   // K+1 limit (the row tokens live in LDS)
 
