@@ -150,6 +150,32 @@ def test_verify_sample_exact_rows():
             assert np.array_equal(g, r), f"{dt} {name}: {g} vs {r}"
 
 
+
+@pytest.mark.parametrize("K", [15, 16, 31, 32, 47, 48])
+def test_verify_sample_finish_block_borders(K):
+    """The finishing kernel splits a sequence's K+1 rows over ceil((K+1)/16)
+    blocks, the last to finish accepting: K+1 at and around multiples of 16,
+    draft lengths that end a block's share exactly or one row into the next,
+    leave blocks without rows, or are invalid; three calls in a row on one
+    workspace (its hand-off counters must be zero again for each next call)."""
+    say("verify_sample finish borders", K)
+    B, V = 8, 1001
+    rng = np.random.default_rng(700 + K)
+    ws = sample_workspace(B, K, V, False)
+    for call in range(3):
+        Z = (rng.standard_normal((B, K + 1, V)) * 2.0).astype(np.float32)
+        L = np.array([-1, 0, 15, min(16, K), K - 1, K, K + 1, int(rng.integers(0, K + 1))],
+                     np.int32)
+        rng.shuffle(L)
+        draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+        for b in range(B):
+            for i in range(int(rng.integers(0, K + 1))):
+                Z[b, i, draft[b, i]] = 30.0          # all the mass on the draft token
+        U = rng.random((B, K + 1), dtype=np.float32)
+        ref = oracle.verify_sample(Z, draft, L, 1.0, U)
+        got = gpu_verify_sample(d_f32(Z), draft, L, 1.0, U, ws=ws)
+        check_sample(_rows_fn(Z, False), 1.0, U, draft, L, got, ref, f"K{K} call {call}")
+
 @pytest.mark.parametrize("V,scale,bf16", [(37, 1.0, False), (37, 2.0, True), (3000, 3.0, False)])
 def test_verify_sample_stratified_counts(V, scale, bf16):
     """One logits row repeated over N = 2B rows with uniforms (j + 1/2) / N: the
