@@ -128,11 +128,11 @@ __device__ __forceinline__ int emit_group(uint64_t m, int p0, int32_t *out, int3
 // p < kW * G * 64 (tokens past the length do no harm: positions past T-2 are
 // masked).  Wave w takes the positions [w * G * 64, (w + 1) * G * 64) in
 // groups of 64, one position per lane, and keeps one 64-bit mask per group:
-// level 0 is one vector compare of the tokens against x[T-1] (and, in the
-// group that crosses T-2, one more against the position); level k keeps the
-// bits whose x[p-k] equals x[T-1-k], all groups of a level at once, while any
-// bit is left.  On the single CU that searches a sequence the pass costs a
-// few instructions per 64 positions and level.  Returns n (0: no occurrence)
+// level 0 is one vector compare of the tokens against x[T-1] (and, in each
+// group of the wave whose positions reach past T-2, one more against the
+// position); level k keeps the bits whose x[p-k] equals x[T-1-k], all groups
+// of a level at once, while any bit is left.  On the single CU that searches
+// a sequence the pass costs a few instructions per 64 positions and level.  Returns n (0: no occurrence)
 // and the count; with n > 0 the occurrences are written in ascending order
 // to out (and out2 when given).  s_lvl: kW x kMaxNgram ints of LDS.  Call
 // with T in [1, kW * G * 64], from the whole block.

@@ -7,16 +7,18 @@
 // accepted draft prefix followed by y_a.
 //
 // The argmax is a streaming read of the logits, so the kernel is shaped for
-// HBM: every row is split across S blocks (S picked on the host so that a few
-// thousand blocks are in flight), each thread issues 16-byte loads (4 fp32 or
-// 8 bf16) in batches of PLD_ARGMAX_UNROLL, keeps the first maximum of its own elements,
-// and the wave / block reduce the 64-bit key (orderable(value) << 32 |
-// ~index), whose maximum is the highest value with the lowest index.  A block
-// folds its key into the row's workspace slot with one 64-bit atomic max.
-// A small acceptance kernel, launched right after on the same stream (the
-// kernel boundary orders the two), reads the row keys back with one thread
-// per sequence, computes the accepted length, writes the outputs and returns
-// the slots to zero.  Rows i > L never reach a slot: a block requests its
+// HBM: every row is split across S blocks (picked on the host: as many per
+// row as are resident together when each block's share then fits one batch
+// of loads, otherwise about PLD_VERIFY_TARGET_BLOCKS blocks in all), each
+// thread issues 16-byte loads (4 fp32 or 8 bf16) in batches of
+// PLD_ARGMAX_UNROLL, keeps the first maximum of its own elements, and the
+// wave / block reduce the 64-bit key (orderable(value) << 32 | ~index), whose
+// maximum is the highest value with the lowest index.  A block folds its key
+// into the row's workspace slot with one 64-bit atomic max.  A small
+// acceptance kernel, launched right after on the same stream (the kernel
+// boundary orders the two), reads the row keys back with one wave per
+// sequence (a lane per row), computes the accepted length, writes the outputs
+// and returns the slots to zero.  Rows i > L never reach a slot: a block requests its
 // first batch of loads before the draft length arrives (the latency of that
 // read is then hidden) and returns once it sees that its row is past the
 // draft, so every row of the buffer must be readable, and rows past a short
