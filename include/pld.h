@@ -85,7 +85,9 @@ size_t pld_workspace_bytes(int B, int K);
 /*
  * Bytes of scratch pld_find_candidates needs for batch B and token stride
  * tok_stride: 0 up to tok_stride = 16384 (one block per sequence), else the
- * per-tile occurrence counts.  Returns 0 when an argument is out of range.
+ * per-tile occurrence counts of every n (2048 positions per tile), and past
+ * 256 tiles (524288 tokens) also each tile's output offset and each
+ * sequence's chosen n and count.  Returns 0 when an argument is out of range.
  */
 size_t pld_find_scratch_bytes(int B, int64_t tok_stride);
 

@@ -70,11 +70,22 @@ inline int resident_blocks(const void *kernel, int threads, size_t dyn_lds) {
     return blocks;
 }
 
-// Scratch of the multi-block find: per-tile occurrence counts of every n.
+// Tiles per sequence up to which each compaction block sums the per-tile
+// counts itself (a few KB per block); past it a scan launch gives every tile
+// its offset, so the work grows with the tiles, not with their square.
+constexpr int kFindScanTiles = 256;
+
+// Scratch of the multi-block find: per-tile occurrence counts of every n;
+// past kFindScanTiles tiles also the per-tile offsets of the chosen n and
+// each sequence's (n, count).
 inline size_t find_scratch_bytes(int B, int64_t tok_stride) {
     if (tok_stride <= kFindFusedPasses * kFindFusedMax) return 0;   // the one-block search
     const int64_t ntiles = (tok_stride + kFindTile - 1) / kFindTile;
-    return align_up((size_t)B * (size_t)ntiles * 8 * sizeof(int32_t), 256);
+    size_t bytes = align_up((size_t)B * (size_t)ntiles * 8 * sizeof(int32_t), 256);
+    if (ntiles > kFindScanTiles)
+        bytes += align_up((size_t)B * (size_t)ntiles * sizeof(int32_t), 256) +
+                 align_up((size_t)B * 2 * sizeof(int32_t), 256);
+    return bytes;
 }
 // Workspace of the ranking and verification calls: 64-bit keys that must be
 // zero when a call starts and that the call leaves zero.  The ranking keys of

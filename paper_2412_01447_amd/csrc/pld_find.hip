@@ -22,7 +22,11 @@
 // register compares; a count kernel writes per-tile counts to the scratch
 // buffer, and the compaction kernel derives its tile's output offset from the
 // counts of the tiles before it (an exclusive wave scan of the lanes' hit
-// counts plus the per-wave and per-tile counts).
+// counts plus the per-wave and per-tile counts).  Up to kFindScanTiles tiles
+// per sequence each compaction block sums those counts itself; past that a
+// scan launch between the two writes every tile's offset once, so a row of
+// 2^30 tokens (524288 tiles) costs reads in proportion to its tiles, not to
+// their square.
 #include "pld.h"
 #include "pld_device.h"
 #include "pld_match.h"
@@ -40,6 +44,8 @@ struct FindArgs {
     int32_t *cand_count;
     int32_t *ngram_used;
     int32_t *tile_counts;   // [B][ntiles][8], scratch
+    int32_t *tile_off;      // [B][ntiles], scratch (ntiles > kFindScanTiles; else null)
+    int32_t *seq_n;         // [B][2]: the chosen n and its count (likewise)
     int ntiles;
 };
 
@@ -131,6 +137,68 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_count_kernel(Fin
     }
 }
 
+// Long rows (more than kFindScanTiles tiles): one 1024-thread block per
+// sequence sums every level's per-tile counts, picks the longest n with an
+// occurrence, and writes each tile's exclusive prefix of that level's counts
+// (tiles in order, 1024 per round, a wave scan and the waves' totals) and the
+// sequence's (n, count).  The compaction blocks then read their own offset.
+__global__ __launch_bounds__(kFindWavesFused * kWave) void find_scan_kernel(FindArgs a) {
+    __shared__ int s_tot[kMaxNgram];
+    __shared__ int s_w[kFindWavesFused];
+    const int b = blockIdx.x;
+    const int w = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const int64_t T = a.lens[b];
+    if (T < 1 || T > a.tok_stride) return;   // block-uniform; the compaction reports it
+    const int32_t *tc = a.tile_counts + (int64_t)b * a.ntiles * kMaxNgram;
+    if (threadIdx.x < kMaxNgram) s_tot[threadIdx.x] = 0;
+    __syncthreads();
+    {
+        int tot[kMaxNgram];
+#pragma unroll
+        for (int k = 0; k < kMaxNgram; ++k) tot[k] = 0;
+        for (int t = threadIdx.x; t < a.ntiles; t += blockDim.x) {
+#pragma unroll
+            for (int k = 0; k < kMaxNgram; ++k) tot[k] += tc[(int64_t)t * kMaxNgram + k];
+        }
+#pragma unroll
+        for (int k = 0; k < kMaxNgram; ++k) {
+            const int v = wave_sum_i32(tot[k]);
+            if (lane == 0 && v) atomicAdd(&s_tot[k], v);
+        }
+    }
+    __syncthreads();
+    int n_used = 0;
+    for (int n = a.nmax; n >= a.nmin; --n) {
+        if (s_tot[n - 1] > 0) {
+            n_used = n;
+            break;
+        }
+    }
+    int32_t *off = a.tile_off + (int64_t)b * a.ntiles;
+    int carry = 0;
+    for (int t0 = 0; n_used > 0 && t0 < a.ntiles; t0 += (int)blockDim.x) {   // block-uniform
+        const int t = t0 + (int)threadIdx.x;
+        const int c = t < a.ntiles ? tc[(int64_t)t * kMaxNgram + n_used - 1] : 0;
+        int wt;
+        const int ex = wave_excl_scan(c, wt);
+        if (lane == 0) s_w[w] = wt;
+        __syncthreads();
+        int before = carry, all = 0;
+        for (int i = 0; i < kFindWavesFused; ++i) {
+            if (i < w) before += s_w[i];
+            all += s_w[i];
+        }
+        if (t < a.ntiles) off[t] = before + ex;
+        carry += all;
+        __syncthreads();   // s_w is written again in the next round
+    }
+    if (threadIdx.x == 0) {
+        a.seq_n[2 * b] = n_used;
+        a.seq_n[2 * b + 1] = n_used > 0 ? s_tot[n_used - 1] : 0;
+    }
+}
+
 __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_compact_kernel(FindArgs a) {
     __shared__ __align__(16) int32_t s_x[kFindTile + kHalo];
     __shared__ int s_tot[kMaxNgram];
@@ -154,7 +222,15 @@ __global__ __launch_bounds__(kFindWavesTiled * kWave) void find_compact_kernel(F
         s_pre[threadIdx.x] = 0;
     }
     __syncthreads();
-    {
+    if (a.tile_off) {   // uniform: the scan launch wrote n, its count and this tile's offset
+        if (threadIdx.x == 0) {
+            const int n = a.seq_n[2 * b];
+            if (n > 0) {
+                s_tot[n - 1] = a.seq_n[2 * b + 1];
+                s_pre[n - 1] = a.tile_off[(int64_t)b * a.ntiles + tile];
+            }
+        }
+    } else {
         // totals over all tiles, and over the tiles before this one
         int tot[kMaxNgram], pre[kMaxNgram];
 #pragma unroll
@@ -245,8 +321,17 @@ extern "C" int pld_find_candidates(const int32_t *tokens, int64_t tok_stride, co
     } else {
         if (!scratch || scratch_bytes < find_scratch_bytes(B, tok_stride)) return PLD_ERR_WORKSPACE;
         a.tile_counts = (int32_t *)scratch;
+        a.tile_off = nullptr;
+        a.seq_n = nullptr;
+        if (a.ntiles > kFindScanTiles) {
+            char *p = (char *)scratch + align_up((size_t)B * a.ntiles * 8 * sizeof(int32_t), 256);
+            a.tile_off = (int32_t *)p;
+            a.seq_n = (int32_t *)(p + align_up((size_t)B * a.ntiles * sizeof(int32_t), 256));
+        }
         dim3 grid(a.ntiles, B);
         hipLaunchKernelGGL(find_count_kernel, grid, dim3(kFindWavesTiled * kWave), 0, s, a);
+        if (a.tile_off)
+            hipLaunchKernelGGL(find_scan_kernel, dim3(B), dim3(kFindWavesFused * kWave), 0, s, a);
         hipLaunchKernelGGL(find_compact_kernel, grid, dim3(kFindWavesTiled * kWave), 0, s, a);
     }
     return hipGetLastError() == hipSuccess ? PLD_OK : PLD_ERR_LAUNCH;

@@ -85,6 +85,11 @@ def test_workspace_and_scratch_bytes():
     assert pld.pld_find_scratch_bytes(8, 16385) >= 8 * 9 * 8 * 4
     assert pld.pld_find_scratch_bytes(4, 131072) >= 4 * 64 * 8 * 4
     assert pld.pld_find_scratch_bytes(0, 9000) == 0
+    # past 256 tiles (524288 tokens) also a per-tile offset and each sequence's (n, count)
+    assert pld.pld_find_scratch_bytes(2, 256 * 2048) == 2 * 256 * 8 * 4
+    assert pld.pld_find_scratch_bytes(2, 256 * 2048 + 1) >= 2 * 257 * (8 + 1) * 4 + 2 * 2 * 4
+    assert pld.pld_find_scratch_bytes(3, 1 << 30) >= 3 * (1 << 19) * (8 + 1) * 4 + 3 * 2 * 4
+    assert pld.pld_find_scratch_bytes(3, (1 << 30) + 1) == 0
     # one-call drafting: none for one block per sequence; key slots, per-block
     # counts and per-block per-n counts for split positions
     assert pld.pld_draft_workspace_bytes(8, 1) == 0

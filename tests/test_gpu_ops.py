@@ -17,7 +17,7 @@ import synth
 from gpu_helpers import (check_best, check_find, check_scores, check_verify, d_bf16, d_f32,
                          draft_keys_zero, draft_workspace, random_plan,
                          d_i32, dev, gpu_emit, gpu_find, gpu_rank_attn, gpu_rank_hidden,
-                         gpu_verify, say, workspace, assert_ws_zero)
+                         gpu_verify, say, scratch, workspace, assert_ws_zero)
 
 pytestmark = pytest.mark.gpu
 
@@ -77,6 +77,9 @@ FIND_CASES = [
     (4, 16384, 1, 1, 1, 14), (4, 16385, 3, 1, 2, 15),
     (5, 20000, 3, 1, 3, 8), (4, 70000, 1000, 1, 2, 9),
     (3, 131072, 2, 8, 8, 10), (3, 50000, 1, 1, 1, 11),
+    # 256 tiles: each compaction block sums the tile counts; 257 and more: the scan launch
+    (3, 524288, 3, 1, 3, 16), (3, 524289, 3, 1, 3, 17), (4, 2000003, 2, 1, 8, 18),
+    (3, 1048576, 5000, 1, 2, 19),
 ]
 
 
@@ -159,6 +162,48 @@ def test_find_random_shapes():
         lens = rng.integers(1, stride + 1, size=B).astype(np.int32)
         lens[0] = stride
         check_find(gpu_find(toks, lens, nmin, nmax), oracle.find(toks, lens, nmin, nmax), what)
+
+
+def test_find_and_emit_at_the_largest_stride():
+    """tok_stride = 2^30, the largest the calls accept (positions are int32): two
+    sequences, 2^31 tokens (8 GiB) in all, occurrences planted at the start, the
+    middle and the end of each row, so the tiled search (524288 tiles per row,
+    offsets from the scan launch) and the draft of the last occurrence, which
+    reaches the context end, run at the far end of the index ranges.  Only the
+    listed prefix of the outputs is copied back."""
+    import torch
+    S = 1 << 30
+    say("find at the largest stride", S)
+    toks = np.zeros((2, S), np.int32)
+    lens = np.array([S, S - 11], np.int32)
+    # sequence 0: the query 2-gram (5, 7) ends at 1, 2^29 + 3 and T - 3; lone 7s elsewhere
+    for j in (1, (1 << 29) + 3, S - 3, S - 1):
+        toks[0, j - 1], toks[0, j] = 5, 7
+    toks[0, [100, S - 100]] = 7
+    # sequence 1: the last token 9 follows a 0, as do its earlier copies
+    T1 = int(lens[1])
+    toks[1, [12345, 1 << 28, T1 - 20, T1 - 1]] = 9
+    cp_ref, cc_ref, nu_ref = oracle.find(toks, lens, 1, 2)
+    assert list(cc_ref) == [3, 3] and list(nu_ref) == [2, 2]
+    K = 8
+    best = np.array([cp_ref[0, 2], cp_ref[1, 2]], np.int32)   # the last occurrence of each
+    dr_ref, dl_ref = oracle.emit(toks, lens, best, K)
+    say("oracle done; copying the tokens")
+    t = torch.from_numpy(toks).to(dev())
+    del toks
+    l = d_i32(lens)
+    cp = torch.full((2, S), -1, dtype=torch.int32, device=dev())
+    cc = torch.full((2,), -7, dtype=torch.int32, device=dev())
+    nu = torch.full((2,), -7, dtype=torch.int32, device=dev())
+    pld.pld_find_candidates(t, l, 1, 2, cp, cc, nu, scratch(2, S))
+    dr = torch.full((2, K), -7, dtype=torch.int32, device=dev())
+    dl = torch.full((2,), -7, dtype=torch.int32, device=dev())
+    pld.pld_emit_draft(t, l, d_i32(best), K, dr, dl)
+    torch.cuda.synchronize()
+    assert list(cc.cpu().numpy()) == [3, 3] and list(nu.cpu().numpy()) == [2, 2]
+    assert np.array_equal(cp[:, :3].cpu().numpy(), cp_ref[:, :3])
+    assert np.array_equal(dr.cpu().numpy(), dr_ref) and np.array_equal(dl.cpu().numpy(), dl_ref)
+    assert list(dl_ref) == [2, 8]
 
 
 @pytest.mark.parametrize("stride", [8192, 16384])
