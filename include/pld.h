@@ -407,6 +407,10 @@ int pld_verify_sample_finish(const void *logits, int dtype, int64_t l_seq_stride
  *                 [0, T-2]; entries past cand_count are not written
  * Device-side rules: a count outside [0, cap] counts as 0; a sequence with
  * T < 2 or T > tok_stride gets best_pos = -1, best_score = -inf.
+ * Cost: one 256-thread block per sequence, one trip to memory per 16 matched
+ * tokens of a candidate, so a sequence takes about cand_count / 256 rounds
+ * of ceil(m / 16) trips: made for the lists of a decoding step (thousands of
+ * candidates), not for lists of millions.
  * Errors: PLD_ERR_INVALID (NULL, B outside [1, 65535], tok_stride or cap out
  * of range, bad max_match), PLD_ERR_LAUNCH.
  */
