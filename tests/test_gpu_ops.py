@@ -291,6 +291,52 @@ def test_rank_hidden_parity(d):
     say("near-tie flips", flips)
 
 
+def test_rank_at_the_largest_batch_and_width():
+    """B = PLD_MAX_BATCH sequences with hidden rows of the largest width
+    (PLD_MAX_HIDDEN): every ranking block holds the per-sequence prefix of all
+    4096 lists and a 32 KB query row in LDS at once.  Short rows over a
+    3-token vocabulary give 0 to 5 occurrences per sequence, empty lists
+    included; both rankings and both in one launch, against the oracle."""
+    B, T, d, R = pld.PLD_MAX_BATCH, 8, pld.PLD_MAX_HIDDEN, 5
+    say("rank at the largest batch and width", B, d)
+    rng = np.random.default_rng(4096)
+    toks = rng.integers(0, 3, size=(B, T)).astype(np.int32)
+    lens = rng.integers(1, T + 1, size=B).astype(np.int32)
+    bits = synth.f32_to_bf16_bits(rng.standard_normal((B, T, d), dtype=np.float32))
+    attn = rng.random((B, R, T), dtype=np.float32)
+    cp, cc, nu = oracle.find(toks, lens, 1, 1)
+    assert (cc == 0).any() and cc.max() >= 5
+    hd, ad = d_bf16(bits), d_f32(attn)
+    rsc, rbp, rbs = oracle.rank_hidden(bits, lens, cp, cc)
+    gsc, gbp, gbs = gpu_rank_hidden(hd, lens, cp, cc)
+    check_scores(gsc, rsc, cc, "largest batch and width")
+    flips = check_best(gbp, gbs, rsc, rbp, rbs, cp, cc, "largest batch and width")
+    asc, abp, abs_ = oracle.rank_attn(attn, lens, cp, cc, oracle.AGG_SUM)
+    gasc, gabp, gabs = gpu_rank_attn(ad, lens, cp, cc, pld.PLD_AGG_SUM)
+    check_scores(gasc, asc, cc, "largest batch, attention")
+    flips += check_best(gabp, gabs, asc, abp, abs_, cp, cc, "largest batch, attention")
+    # both scorings in one launch: the same scores bit for bit, the same keys
+    wh, wa = workspace(B, 1), workspace(B, 1)
+    sh = torch.zeros((B, T), dtype=torch.float32, device=dev())
+    sa = torch.zeros((B, T), dtype=torch.float32, device=dev())
+    dl, dcp, dcc = d_i32(lens), d_i32(cp), d_i32(cc)
+    pld.pld_score_both(hd, ad, dl, dcp, dcc, wh, wa, agg=pld.PLD_AGG_SUM, scores_h=sh, scores_a=sa)
+    bp = torch.full((2, B), -7, dtype=torch.int32, device=dev())
+    bs = torch.zeros((2, B), dtype=torch.float32, device=dev())
+    pld.pld_select_best(B, bp[0], bs[0], wh)
+    pld.pld_select_best(B, bp[1], bs[1], wa)
+    torch.cuda.synchronize()
+    assert_ws_zero(wh)
+    assert_ws_zero(wa)
+    both_h, both_a = sh.cpu().numpy(), sa.cpu().numpy()
+    for b in range(B):
+        n = int(cc[b])
+        assert np.array_equal(both_h[b, :n].view(np.uint32), gsc[b, :n].view(np.uint32)), b
+        assert np.array_equal(both_a[b, :n].view(np.uint32), gasc[b, :n].view(np.uint32)), b
+    assert np.array_equal(bp[0].cpu().numpy(), gbp) and np.array_equal(bp[1].cpu().numpy(), gabp)
+    say("near-tie flips", flips)
+
+
 def test_rank_hidden_strided_rows_and_threshold():
     say("rank_hidden strided")
     B, T, d, pad = 4, 200, 256, 24
@@ -670,6 +716,28 @@ def test_verify_parity(case):
     ref = oracle.verify(zbits, draft, L, bf16=bf16)
     zd = d_bf16(zbits) if bf16 else d_f32(Z)
     check_verify(gpu_verify(zd, draft, L), ref, str(case))
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_verify_at_the_largest_draft(bf16):
+    """K + 1 = 65535 rows per sequence, the most the argmax launch's second grid
+    dimension holds: a full acceptance (K + 1 tokens), a first mismatch deep in
+    the rows, a draft accepted to its length, and an empty draft, against the
+    oracle; the workspace is left zero."""
+    B, K, V = 4, 65534, 5
+    say("verify at the largest draft", K, "bf16" if bf16 else "f32")
+    rng = np.random.default_rng(65534)
+    Z = rng.standard_normal((B, K + 1, V)).astype(np.float32)
+    draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+    L = np.array([K, K, 40000, 0], np.int32)
+    for b, upto in ((0, K), (1, 50000), (2, 40000)):
+        Z[b, np.arange(upto), draft[b, :upto]] = 10.0
+    Z[1, 50000, draft[1, 50000]] = -10.0          # a sure mismatch at row 50000
+    zbits = synth.f32_to_bf16_bits(Z) if bf16 else Z
+    ref = oracle.verify(zbits, draft, L, bf16=bf16)
+    assert list(ref[0]) == [K, 50000, 40000, 0] and ref[2][0] == K + 1
+    got = gpu_verify(d_bf16(zbits) if bf16 else d_f32(Z), draft, L)
+    check_verify(got, ref, f"K={K}")
 
 
 def test_verify_random_shapes():

@@ -176,6 +176,26 @@ def test_verify_sample_finish_block_borders(K):
         got = gpu_verify_sample(d_f32(Z), draft, L, 1.0, U, ws=ws)
         check_sample(_rows_fn(Z, False), 1.0, U, draft, L, got, ref, f"K{K} call {call}")
 
+
+def test_verify_sample_at_the_most_rows():
+    """K + 1 = PLD_MAX_SAMPLE_ROWS rows per sequence: 1024 finishing blocks per
+    sequence hand their tokens to the last one.  A full acceptance, a draft
+    accepted in part, and an invalid length, against the oracle."""
+    B, V = 3, 7
+    K = pld.PLD_MAX_SAMPLE_ROWS - 1
+    say("verify_sample at the most rows", K + 1)
+    rng = np.random.default_rng(16383)
+    Z = (rng.standard_normal((B, K + 1, V)) * 2.0).astype(np.float32)
+    draft = rng.integers(0, V, size=(B, K)).astype(np.int32)
+    L = np.array([K, 9000, -1], np.int32)
+    for b, upto in ((0, K), (1, 5000)):
+        Z[b, np.arange(upto), draft[b, :upto]] = 30.0   # all the mass on the draft token
+    U = rng.random((B, K + 1), dtype=np.float32)
+    ref = oracle.verify_sample(Z, draft, L, 1.0, U)
+    assert ref[0][0] == K and ref[0][1] >= 5000
+    got = gpu_verify_sample(d_f32(Z), draft, L, 1.0, U)
+    check_sample(_rows_fn(Z, False), 1.0, U, draft, L, got, ref, "the most rows")
+
 @pytest.mark.parametrize("V,scale,bf16", [(37, 1.0, False), (37, 2.0, True), (3000, 3.0, False)])
 def test_verify_sample_stratified_counts(V, scale, bf16):
     """One logits row repeated over N = 2B rows with uniforms (j + 1/2) / N: the
