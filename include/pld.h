@@ -201,9 +201,9 @@ int pld_emit_draft(const int32_t *tokens, int64_t tok_stride, const int32_t *len
  *   accept_len, out_count int32 [B];  out_tokens int32 [B][K+1]
  * Device-side rule: draft_len outside [0, K] gives accept_len = -1,
  * out_count = 0 and out_tokens all -1.
- * Errors: PLD_ERR_INVALID (NULL, B < 1, K < 1, V < 1, bad dtype, strides
- * smaller than a row / K+1 rows), PLD_ERR_ALIGN, PLD_ERR_WORKSPACE,
- * PLD_ERR_LAUNCH.
+ * Errors: PLD_ERR_INVALID (NULL, B outside [1, 65535], K outside [1, 65534],
+ * V < 1, bad dtype, strides smaller than a row / K+1 rows), PLD_ERR_ALIGN,
+ * PLD_ERR_WORKSPACE, PLD_ERR_LAUNCH.
  */
 int pld_verify_greedy(const void *logits, int dtype, int64_t l_seq_stride, int64_t l_row_stride,
                       int V, int K, const int32_t *draft, const int32_t *draft_len, int B,
@@ -436,8 +436,8 @@ int pld_select_prefix(const int32_t *tokens, int64_t tok_stride, const int32_t *
  *   stats      int64 [B][2] or NULL, accumulated
  * Device-side rule: a sequence with T outside [0, cap] or out_count outside
  * [0, K+1] is left unchanged.
- * Errors: PLD_ERR_INVALID (NULL, B < 1, K < 1, tok_stride out of range),
- * PLD_ERR_LAUNCH.
+ * Errors: PLD_ERR_INVALID (NULL, B outside [1, 65535], K outside [1, 65534]
+ * (the verification calls' limits), tok_stride out of range), PLD_ERR_LAUNCH.
  */
 int pld_commit(int32_t *tokens, int64_t tok_stride, int32_t *lens, const int32_t *limit,
                const int32_t *out_tokens, const int32_t *out_count, int B, int K,

@@ -96,7 +96,7 @@ inline size_t rank_ws_bytes(int B) {
     return align_up((size_t)B * kKeySlots * sizeof(uint64_t), 256);
 }
 inline size_t verify_ws_bytes(int B, int K) {
-    return align_up((size_t)B * (size_t)(K + 1) * sizeof(uint64_t), 256);
+    return align_up((size_t)B * ((size_t)K + 1) * sizeof(uint64_t), 256);
 }
 
 // ---------------------------------------------------------------- keys

@@ -390,14 +390,14 @@ static int sample_nseg_max(int V, int dtype) {
     return seg_count(V / (dtype == PLD_F32 ? 4 : 8));   // a row has at most V / P whole vectors
 }
 static size_t sample_stats_bytes(int B, int K, int V, int dtype) {
-    return align_up((size_t)B * (size_t)(K + 1) * (size_t)sample_nseg_max(V, dtype) * sizeof(float2),
+    return align_up((size_t)B * ((size_t)K + 1) * (size_t)sample_nseg_max(V, dtype) * sizeof(float2),
                     256);
 }
 // [the shared zero-invariant part | statistics | tickets (zero-invariant) | tokens]
 static size_t sample_ws_bytes(int B, int K, int V, int dtype) {
     return common_ws_bytes(B, K) + sample_stats_bytes(B, K, V, dtype) +
            align_up((size_t)B * sizeof(int32_t), 256) +
-           align_up((size_t)B * (size_t)(K + 1) * sizeof(int32_t), 256);
+           align_up((size_t)B * ((size_t)K + 1) * sizeof(int32_t), 256);
 }
 
 // The sampling calls' arguments: those of prep_verify plus the temperature,
@@ -412,7 +412,7 @@ static int prep_sample(const void *logits, int dtype, int64_t l_seq_stride, int6
     if (!(temperature > 0.0) || !(temperature <= DBL_MAX)) return PLD_ERR_INVALID;
     const double kd = 1.4426950408889634 / temperature;
     if (!(kd <= FLT_MAX)) return PLD_ERR_INVALID;
-    if (K + 1 > kFinishMaxRows) return PLD_ERR_INVALID;
+    if (K > kFinishMaxRows - 1) return PLD_ERR_INVALID;
     if (workspace_bytes < sample_ws_bytes(B, K, V, dtype)) return PLD_ERR_WORKSPACE;
     a = SampleArgs{};
     a.logits = logits;

@@ -257,7 +257,7 @@ static int check_verify(const void *logits, int dtype, int64_t l_seq_stride, int
                         int V, int K, const int32_t *draft_len, int B) {
     if (!logits || !draft_len) return PLD_ERR_INVALID;
     if (B < 1 || K < 1 || V < 1 || (dtype != PLD_F32 && dtype != PLD_BF16)) return PLD_ERR_INVALID;
-    if (B > 65535 || K + 1 > 65535) return PLD_ERR_INVALID;       // grid y / z limits
+    if (B > 65535 || K > 65534) return PLD_ERR_INVALID;           // grid y / z limits
     if (l_row_stride < V || l_seq_stride < (int64_t)(K + 1) * l_row_stride) return PLD_ERR_INVALID;
     const size_t esz = dtype == PLD_F32 ? 4 : 2;
     if ((uintptr_t)logits % esz) return PLD_ERR_ALIGN;
@@ -361,7 +361,7 @@ extern "C" int pld_verify_greedy_noalloc(const void *logits, int dtype, int64_t 
     if (!draft || !accept_len || !out_tokens || !out_count) return PLD_ERR_INVALID;
     int rc = check_verify(logits, dtype, l_seq_stride, l_row_stride, V, K, draft_len, B);
     if (rc != PLD_OK) return rc;
-    if ((int64_t)B * (K + 1) > kStaticKeys) return PLD_ERR_SCRATCH;
+    if ((int64_t)B * ((int64_t)K + 1) > kStaticKeys) return PLD_ERR_SCRATCH;
     uint64_t *keys = nullptr;
     rc = scratch_address(&keys);
     if (rc != PLD_OK) return rc;
@@ -396,7 +396,7 @@ extern "C" int pld_verify_accept(const int32_t *draft, const int32_t *draft_len,
                                  int32_t *accept_len, int32_t *out_tokens, int32_t *out_count,
                                  void *workspace, size_t workspace_bytes, void *stream) {
     if (!draft || !draft_len || !accept_len || !out_tokens || !out_count) return PLD_ERR_INVALID;
-    if (B < 1 || K < 1 || B > 65535 || K + 1 > 65535) return PLD_ERR_INVALID;
+    if (B < 1 || K < 1 || B > 65535 || K > 65534) return PLD_ERR_INVALID;
     if (!workspace || workspace_bytes < verify_ws_bytes(B, K)) return PLD_ERR_WORKSPACE;
     VerifyArgs a{};
     a.K = K;
@@ -450,7 +450,7 @@ extern "C" int pld_accept_commit(const int32_t *draft, const int32_t *draft_len,
                                  size_t workspace_bytes, void *stream) {
     if (!draft || !draft_len || !accept_len || !out_tokens || !out_count || !tokens || !lens)
         return PLD_ERR_INVALID;
-    if (B < 1 || K < 1 || B > 65535 || K + 1 > 65535) return PLD_ERR_INVALID;
+    if (B < 1 || K < 1 || B > 65535 || K > 65534) return PLD_ERR_INVALID;
     if (tok_stride < 1 || tok_stride > kMaxTokStride) return PLD_ERR_INVALID;
     if (!workspace || workspace_bytes < verify_ws_bytes(B, K)) return PLD_ERR_WORKSPACE;
     VerifyArgs a{};
@@ -472,7 +472,8 @@ extern "C" int pld_commit(int32_t *tokens, int64_t tok_stride, int32_t *lens,
                           const int32_t *limit, const int32_t *out_tokens,
                           const int32_t *out_count, int B, int K, int64_t *stats, void *stream) {
     if (!tokens || !lens || !out_tokens || !out_count) return PLD_ERR_INVALID;
-    if (B < 1 || K < 1 || tok_stride < 1 || tok_stride > kMaxTokStride) return PLD_ERR_INVALID;
+    if (B < 1 || B > 65535 || K < 1 || K > 65534) return PLD_ERR_INVALID;
+    if (tok_stride < 1 || tok_stride > kMaxTokStride) return PLD_ERR_INVALID;
     hipLaunchKernelGGL(commit_kernel, dim3((unsigned)((B + 3) / 4)), dim3(256), 0,
                        (hipStream_t)stream, tokens, tok_stride, lens, limit, out_tokens,
                        out_count, B, K, stats);

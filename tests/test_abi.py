@@ -79,6 +79,8 @@ def test_workspace_and_scratch_bytes():
     assert pld.pld_workspace_bytes(64, 32) >= pld.pld_workspace_bytes(64, 16)
     assert pld.pld_workspace_bytes(64, 16) >= 64 * 17 * 8      # verify keys: B*(K+1) u64
     assert pld.pld_workspace_bytes(4096, 1) >= 4096 * 8        # ranking keys: B u64
+    assert pld.pld_workspace_bytes(1, 2**31 - 1) == 8 << 31     # K + 1 counted without overflow
+    assert pld.pld_verify_sample_workspace_bytes(1, 2**31 - 1, 10, pld.PLD_F32) > 8 << 31
     # find: no scratch up to 16384 tokens (one block per sequence), per-tile counts beyond
     assert pld.pld_find_scratch_bytes(8, 8192) == 0
     assert pld.pld_find_scratch_bytes(8, 16384) == 0
@@ -210,6 +212,9 @@ def test_host_validation_error_codes():
     assert v(F, 0, 39, 10, 10, 3, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_INV   # seq stride
     assert v(MIS, 0, 40, 10, 10, 3, F, F, 1, F, F, F, F, 1 << 20, NULL) == E_AL  # fp32 alignment
     assert v(F, 0, 40, 10, 10, 3, F, F, 1, F, F, F, F, 8, NULL) == E_WS
+    # K + 1 rows must fit the launch's second grid dimension (65535), also at the int limit
+    for k in (65535, 2**31 - 1):
+        assert v(F, 0, (k + 1) * 10, 10, 10, k, F, F, 1, F, F, F, F, 1 << 40, NULL) == E_INV, k
     assert v(F, 0, 40, 10, 10, 3, F, F, 1, F, F, F, NULL, 1 << 20, NULL) == E_WS
 
 
@@ -261,6 +266,7 @@ def test_verify_sample_host_validation():
     assert call(K=0) == E_INV
     assert call(K=pld.PLD_MAX_SAMPLE_ROWS, u_stride=pld.PLD_MAX_SAMPLE_ROWS + 1,
                 ws_bytes=1 << 40) == E_INV
+    assert call(K=2**31 - 1, u_stride=2**31, ws_bytes=1 << 62) == E_INV
     # the two halves check the same things
     st = lib.pld_verify_sample_stats
     assert st(F, pld.PLD_F32, (K + 1) * V, V, V, K, F, B, 0.0, F, need, NULL) == E_INV
@@ -287,6 +293,9 @@ def test_prefix_and_commit_host_validation():
     assert cm(F, 100, F, NULL, F, F, 0, 4, NULL, NULL) == E_INV
     assert cm(F, 100, F, NULL, F, F, 2, 0, NULL, NULL) == E_INV
     assert cm(F, 0, F, NULL, F, F, 2, 4, NULL, NULL) == E_INV
+    assert cm(F, 100, F, NULL, F, F, 65536, 4, NULL, NULL) == E_INV
+    assert cm(F, 100, F, NULL, F, F, 2, 65535, NULL, NULL) == E_INV
+    assert cm(F, 100, F, NULL, F, F, 2, 2**31 - 1, NULL, NULL) == E_INV
     # the acceptance with the commit: the union of the two calls' checks
     ac = lib.pld_accept_commit
     ws_n = pld.pld_workspace_bytes(2, 4)
