@@ -172,14 +172,16 @@ class DraftStep:
     def tune_split(self, cand_count, hidden=True):
         """Blocks per sequence for the one-call drafting from observed candidate
         counts (e.g. the previous step's).  Short contexts with short lists keep
-        one block per sequence (one launch).  Otherwise, for hidden-state ranking,
-        about 32 rows per block of the longest list and at least 512 blocks in
-        all (the library gives grids of up to 512 blocks 8 waves each, two per
-        CU); for attention ranking, about 32 gathers per block; and at least 64
-        positions per block."""
+        one block per sequence (one launch): up to 32 hidden rows or 256
+        attention gathers in the longest list (past 32 rows of 8 KB, spreading
+        them over more CUs repays the finishing launch).  Otherwise, for
+        hidden-state ranking, about 32 rows per block of the longest list and at
+        least 512 blocks in all (the library gives grids of up to 512 blocks 8
+        waves each, two per CU); for attention ranking, about 32 gathers per
+        block; and at least 64 positions per block."""
         import math
         mx = int(max(int(c) for c in cand_count)) if len(cand_count) else 0
-        small = 64 if hidden else 256
+        small = 32 if hidden else 256
         if self.tok_stride <= DRAFT_MAX_TOK_STRIDE and mx <= small:
             return self.set_split(1)
         if hidden:

@@ -319,8 +319,8 @@ def test_split_rule():
     than the stride needs (8192 positions at most per block)."""
     from paper_2412_01447_amd.step import DraftStep
     s = DraftStep(8, 4096, 10, device="cpu")
-    assert s.tune_split([2, 64], hidden=True) == 1
-    assert s.tune_split([65], hidden=True) == 64          # 512 // 8
+    assert s.tune_split([2, 32], hidden=True) == 1
+    assert s.tune_split([33], hidden=True) == 64          # 512 // 8
     assert s.tune_split([480, 3], hidden=True) == 64
     assert s.tune_split([3000], hidden=True) == 64        # ceil(3000/32) capped at 4096/64
     assert s.tune_split([256], hidden=False) == 1
@@ -330,7 +330,8 @@ def test_split_rule():
     assert big.tune_split([8000], hidden=True) == 250             # ceil(8000/32)
     assert big.tune_split([10], hidden=False) == 16               # 131072 / 8192 positions
     one = DraftStep(1, 1024, 10, device="cpu")
-    assert one.tune_split([42], hidden=True) == 1
+    assert one.tune_split([32], hidden=True) == 1
+    assert one.tune_split([42], hidden=True) == 16                # 1024 / 64 positions
     assert one.tune_split([100], hidden=True) == 16               # 1024 / 64 positions
     att = DraftStep(32, 8192, 16, device="cpu")
     assert att.tune_split([1181, 7], hidden=False) == 37
